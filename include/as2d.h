@@ -1,0 +1,182 @@
+/*
+ * as2d.h - C ABI of the MI355X (gfx950) target verification library.
+ *
+ * The library runs the target side of AS2D's decoding loop (arXiv
+ * 2609.37617): a decoder-only target model, prefilled with audio
+ * embeddings and instruction tokens, verifies a known root token plus k
+ * drafted candidates in one forward pass and commits the longest prefix of
+ * candidates equal to its own greedy tokens, followed by its correction
+ * (Section 4.2 "Target verification"; Appendix C.2 "Verification and state
+ * repair").  Rejected cache entries are dropped by shortening the logical
+ * KV length; nothing is copied.
+ *
+ * Conventions for every call:
+ *   - Return value: AS2D_OK (0) or a negative AS2D_E* code.  Outputs are
+ *     written only on success; as2d_last_error() then holds a message.
+ *   - Host pointers are owned by the caller and only read (or written, for
+ *     outputs) during the call; the library copies what it keeps.
+ *   - All device memory (packed weights, KV cache slots, scratch) is owned
+ *     by the library and released by as2d_free().
+ *   - A context is used by one host thread at a time.
+ *   - Token ids are int32 in [0, vocab).
+ *
+ * Model: pre-RMSNorm decoder layers with grouped-query attention (query
+ * head h reads KV head floor(h * n_kv / n_q)), rotary position embedding
+ * (rotate-half pairs (i, i + d/2), angle pos * theta^(-2i/d)), optional QKV
+ * bias, SwiGLU MLP, final RMSNorm and an untied LM head.  The greedy token
+ * is the arg-max logit, ties to the lowest token id (the deterministic
+ * tie-break of Appendix C.4, Eq. reference-transition).
+ */
+#ifndef AS2D_H
+#define AS2D_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  AS2D_OK = 0,
+  AS2D_EINVAL = -1,    /* bad argument: k, token id, request id, rollback length, null pointer */
+  AS2D_ECAPACITY = -2, /* the request's KV slot cannot hold the new rows */
+  AS2D_ESTATE = -3,    /* verify/decode on a request that has not been prefilled */
+  AS2D_EHIP = -4,      /* HIP runtime error */
+  AS2D_ENUMERIC = -5,  /* non-finite logits: no token can be chosen */
+  AS2D_ENOMEM = -6     /* device or pinned host allocation failed */
+};
+
+enum { AS2D_F32 = 0, AS2D_BF16 = 1 };
+
+typedef struct as2d_ctx as2d_ctx;
+
+typedef struct {
+  int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, vocab;
+  float rope_theta, rms_eps;
+  int32_t dtype;    /* AS2D_F32 or AS2D_BF16: weights, GEMM operands and KV cache */
+  int32_t qkv_bias; /* 0 or 1 */
+  int32_t max_requests, max_kv_len, max_k; /* KV slots, positions per slot, candidates per call */
+} as2d_config;
+
+typedef struct {
+  int32_t accepted_len;     /* a in [0, k]: candidates committed */
+  int32_t correction_token; /* target's greedy token after root + a candidates; the next root */
+  int32_t kv_len;           /* positions now in the KV cache: previous kv_len + a + 1 */
+  int32_t committed;        /* tokens committed since prefill (first root excluded) */
+} as2d_verify_out;
+
+/*
+ * Load a model and create a context.
+ *
+ * host_tensors: n_tensors pointers in this canonical order
+ *   embed [vocab][hidden]
+ *   per layer l = 0..n_layers-1:
+ *     attn_norm [hidden], wq [n_q*d][hidden], wk [n_kv*d][hidden], wv [n_kv*d][hidden],
+ *     (qkv_bias only) bq [n_q*d], bk [n_kv*d], bv [n_kv*d],
+ *     wo [hidden][n_q*d], mlp_norm [hidden],
+ *     w_gate [ffn][hidden], w_up [ffn][hidden], w_down [hidden][ffn]
+ *   final_norm [hidden], lm_head [vocab][hidden]
+ * Matrices and the embedding are row-major in cfg->dtype (bf16 as uint16
+ * bit patterns); norm gains and biases are float32.
+ * Shape requirements: head_dim 64 or 128, n_q divisible by n_kv, hidden a
+ * multiple of 128, ffn a multiple of 64, vocab a multiple of 128,
+ * max_k <= 31.
+ * hip_stream: the hipStream_t all work is ordered on (NULL: the library
+ * creates its own).  The weights are repacked on the device into the tile
+ * order the GEMM kernels stream.
+ */
+int as2d_load_weights(const as2d_config* cfg, const void* const* host_tensors, int32_t n_tensors,
+                      void* hip_stream, as2d_ctx** out);
+
+/*
+ * Prefill request slot `req` (Appendix A.1: the prepared audio KV and the
+ * instruction give the initial decoding state; Appendix C.2).
+ * audio_emb: [n_audio][hidden] in cfg->dtype, used directly as hidden
+ * states at positions 0..n_audio-1; instr_tokens: n_instr token ids at the
+ * following positions.  n_audio + n_instr >= 1 and <= max_kv_len.
+ * On success *first_token is the greedy token after the prefix (the first
+ * root, not yet in the cache) and *kv_len = n_audio + n_instr.
+ * Re-prefilling a slot discards its previous state.
+ */
+int as2d_prefill_kv(as2d_ctx* ctx, int32_t req, const void* audio_emb, int32_t n_audio,
+                    const int32_t* instr_tokens, int32_t n_instr, int32_t* first_token,
+                    int32_t* kv_len);
+
+/*
+ * One verification call (Section 4.2; Appendix C.2): the pending root and
+ * cands[0..k) are processed at positions kv_len..kv_len+k in one forward
+ * pass; accepted_len is the length of the longest candidate prefix equal
+ * to the target's greedy tokens and correction_token the greedy token that
+ * follows it (a bonus token when all k match).  The root and the accepted
+ * candidates stay in the cache; the correction becomes the pending root.
+ * 0 <= k <= max_k; kv_len + k + 1 <= max_kv_len (else AS2D_ECAPACITY).
+ */
+int as2d_verify(as2d_ctx* ctx, int32_t req, const int32_t* cands, int32_t k, as2d_verify_out* out);
+
+/* Target-only (K1) step: as2d_verify with k = 0 (Appendix C.2). */
+int as2d_decode_one(as2d_ctx* ctx, int32_t req, as2d_verify_out* out);
+
+/*
+ * Verification calls of n distinct requests in one fused forward pass.
+ * reqs[i], ks[i] as in as2d_verify; cands_flat holds the requests'
+ * candidates back to back (sum of ks entries).  Each request's rows attend
+ * only to its own cache slot.  outs[i] receives request i's result.
+ * sum(ks[i] + 1) <= max_requests * (max_k + 1).
+ */
+int as2d_verify_batch(as2d_ctx* ctx, int32_t n, const int32_t* reqs, const int32_t* cands_flat,
+                      const int32_t* ks, as2d_verify_out* outs);
+
+/* ---- test and inspection hooks (not on the timed path) ---------------- */
+
+/* When on, later calls also write the float32 logits of every processed
+ * row (off by default). */
+int as2d_set_keep_logits(as2d_ctx* ctx, int32_t on);
+
+/* Logits of the rows of `req`'s last verify/decode call (needs
+ * keep_logits): host[max_rows][vocab]; *n_rows receives the row count
+ * (k + 1).  After a prefill, the logits of the last prefix row. */
+int as2d_get_logits(as2d_ctx* ctx, int32_t req, float* host, int32_t max_rows, int32_t* n_rows);
+
+/* Greedy token of every row of `req`'s last call: host[max_rows]. */
+int as2d_get_row_tokens(as2d_ctx* ctx, int32_t req, int32_t* host, int32_t max_rows, int32_t* n_rows);
+
+/* Return `req` to an earlier committed state: prefix length <= kv_len <=
+ * current kv_len; root becomes the pending root.  Cache rows past kv_len
+ * are ignored and overwritten by later calls. */
+int as2d_rollback(as2d_ctx* ctx, int32_t req, int32_t kv_len, int32_t root);
+
+/* Current state of `req`: kv_len, pending root and committed count. */
+int as2d_get_state(as2d_ctx* ctx, int32_t req, int32_t* kv_len, int32_t* root, int32_t* committed);
+
+/* Copy positions 0..n_tok-1 of one layer's cache: host_k, host_v
+ * [n_kv][n_tok][head_dim] in cfg->dtype (K after rotation). */
+int as2d_read_kv(as2d_ctx* ctx, int32_t req, int32_t layer, void* host_k, void* host_v, int32_t n_tok);
+
+/* Mark a slot free (its state is discarded). */
+int as2d_release_request(as2d_ctx* ctx, int32_t req);
+
+/*
+ * Per-kernel timing with HIP events on the library's stream.  When on,
+ * each launch of the step is bracketed by events and its duration is
+ * accumulated per kernel kind; this serialises nothing but adds event
+ * records between launches.  as2d_timing_read fills up to max entries of
+ * names (each up to 31 chars + NUL, 32 bytes per entry), total
+ * milliseconds and launch counts, and returns the number of kinds.
+ */
+int as2d_set_timing(as2d_ctx* ctx, int32_t on);
+int as2d_timing_read(as2d_ctx* ctx, char* names, double* total_ms, int64_t* counts, int32_t max);
+int as2d_timing_reset(as2d_ctx* ctx);
+
+/* Algorithmic HBM bytes of one forward pass of `rows` rows whose
+ * requests hold `kv_keys` attended positions in total per layer
+ * (weights streamed once, embedding rows, KV read and append). */
+int64_t as2d_step_bytes(const as2d_ctx* ctx, int32_t rows, int64_t kv_keys);
+
+void as2d_free(as2d_ctx* ctx);
+const char* as2d_last_error(const as2d_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AS2D_H */

@@ -1,0 +1,225 @@
+"""ctypes binding of libas2d.so (include/as2d.h).
+
+Argument marshalling only: every step of the verification path runs in the
+library's HIP kernels.  Importing this module does not touch the GPU;
+loading the library fails loudly if it has not been built.
+"""
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libas2d.so")
+
+OK, EINVAL, ECAPACITY, ESTATE, EHIP, ENUMERIC, ENOMEM = 0, -1, -2, -3, -4, -5, -6
+F32, BF16 = 0, 1
+
+# Every symbol include/as2d.h declares.
+EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_one",
+           "as2d_verify_batch", "as2d_set_keep_logits", "as2d_get_logits", "as2d_get_row_tokens",
+           "as2d_rollback", "as2d_get_state", "as2d_read_kv", "as2d_release_request",
+           "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_step_bytes",
+           "as2d_free", "as2d_last_error"]
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("qkv_bias", ctypes.c_int32),
+                ("max_requests", ctypes.c_int32), ("max_kv_len", ctypes.c_int32),
+                ("max_k", ctypes.c_int32)]
+
+
+class VerifyOut(ctypes.Structure):
+    _fields_ = [("accepted_len", ctypes.c_int32), ("correction_token", ctypes.c_int32),
+                ("kv_len", ctypes.c_int32), ("committed", ctypes.c_int32)]
+
+    def as_dict(self):
+        return dict(accepted_len=self.accepted_len, correction_token=self.correction_token,
+                    kv_len=self.kv_len, committed=self.committed)
+
+
+class As2dError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"as2d error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libas2d.so; raises if it is missing (no fallback path exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is not built; run __graft_entry__.build() "
+                                f"or python paper_2609_37617_amd/build.py")
+    lib = ctypes.CDLL(path)
+    lib.as2d_load_weights.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(_P), _I, _P,
+                                      ctypes.POINTER(_P)]
+    lib.as2d_prefill_kv.argtypes = [_P, _I, _P, _I, _P, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
+    lib.as2d_verify.argtypes = [_P, _I, _P, _I, ctypes.POINTER(VerifyOut)]
+    lib.as2d_decode_one.argtypes = [_P, _I, ctypes.POINTER(VerifyOut)]
+    lib.as2d_verify_batch.argtypes = [_P, _I, _P, _P, _P, _P]
+    lib.as2d_set_keep_logits.argtypes = [_P, _I]
+    lib.as2d_get_logits.argtypes = [_P, _I, _P, _I, ctypes.POINTER(_I)]
+    lib.as2d_get_row_tokens.argtypes = [_P, _I, _P, _I, ctypes.POINTER(_I)]
+    lib.as2d_rollback.argtypes = [_P, _I, _I, _I]
+    lib.as2d_get_state.argtypes = [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]
+    lib.as2d_read_kv.argtypes = [_P, _I, _I, _P, _P, _I]
+    lib.as2d_release_request.argtypes = [_P, _I]
+    lib.as2d_set_timing.argtypes = [_P, _I]
+    lib.as2d_timing_read.argtypes = [_P, _P, _P, _P, _I]
+    lib.as2d_timing_reset.argtypes = [_P]
+    lib.as2d_step_bytes.argtypes = [_P, _I, ctypes.c_int64]
+    lib.as2d_step_bytes.restype = ctypes.c_int64
+    lib.as2d_free.argtypes = [_P]
+    lib.as2d_free.restype = None
+    lib.as2d_last_error.argtypes = [_P]
+    lib.as2d_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name not in ("as2d_free", "as2d_last_error", "as2d_step_bytes"):
+            getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+class Model:
+    """One library context: a loaded target model with its KV slots."""
+
+    def __init__(self, shape, tensors: Sequence[np.ndarray], max_requests: int = 1,
+                 max_kv_len: int = 1024, max_k: int = 8, stream: Optional[int] = None):
+        """shape: workload.configs.ModelShape; tensors: the canonical list
+        in the 'device' format of workload.gen.make_weights."""
+        self.lib = load_library()
+        self.shape = shape
+        cfg = Config(shape.n_layers, shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                     shape.ffn, shape.vocab, shape.rope_theta, shape.rms_eps, shape.dtype,
+                     int(shape.qkv_bias), max_requests, max_kv_len, max_k)
+        self.cfg = cfg
+        self._keep = [np.ascontiguousarray(t) for t in tensors]
+        arr = (_P * len(self._keep))(*[_ptr(t) for t in self._keep])
+        ctx = _P()
+        rc = self.lib.as2d_load_weights(ctypes.byref(cfg), arr, len(self._keep), stream, ctypes.byref(ctx))
+        self._keep = None
+        if rc != OK:
+            raise As2dError(rc, "as2d_load_weights failed (see argument checks in include/as2d.h)")
+        self.ctx = ctx
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            self.lib.as2d_free(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, rc):
+        if rc != OK:
+            raise As2dError(rc, self.lib.as2d_last_error(self.ctx).decode())
+
+    def call(self, name, *args):
+        """Raw call returning the status code (for error-path tests)."""
+        return getattr(self.lib, name)(self.ctx, *args)
+
+    def prefill(self, req: int, audio: np.ndarray, instr: Sequence[int]):
+        audio = np.ascontiguousarray(audio)
+        instr = np.ascontiguousarray(instr, dtype=np.int32)
+        first, kv = _I(), _I()
+        n_audio = audio.shape[0] if audio.size else 0
+        self._check(self.lib.as2d_prefill_kv(self.ctx, req, _ptr(audio) if n_audio else None, n_audio,
+                                             _ptr(instr) if len(instr) else None, len(instr),
+                                             ctypes.byref(first), ctypes.byref(kv)))
+        return first.value, kv.value
+
+    def verify(self, req: int, cands: Sequence[int], k: Optional[int] = None) -> dict:
+        c = np.ascontiguousarray(cands, dtype=np.int32)
+        k = len(c) if k is None else k
+        out = VerifyOut()
+        self._check(self.lib.as2d_verify(self.ctx, req, _ptr(c) if c.size else None, k, ctypes.byref(out)))
+        return out.as_dict()
+
+    def decode_one(self, req: int) -> dict:
+        out = VerifyOut()
+        self._check(self.lib.as2d_decode_one(self.ctx, req, ctypes.byref(out)))
+        return out.as_dict()
+
+    def verify_batch(self, reqs: Sequence[int], cands: Sequence[Sequence[int]]) -> List[dict]:
+        n = len(reqs)
+        r = np.ascontiguousarray(reqs, dtype=np.int32)
+        ks = np.array([len(c) for c in cands], dtype=np.int32)
+        flat = np.ascontiguousarray(np.concatenate([np.asarray(c, dtype=np.int32) for c in cands])
+                                    if ks.sum() else np.zeros(1, np.int32), dtype=np.int32)
+        outs = (VerifyOut * n)()
+        self._check(self.lib.as2d_verify_batch(self.ctx, n, _ptr(r), _ptr(flat), _ptr(ks), outs))
+        return [o.as_dict() for o in outs]
+
+    def set_keep_logits(self, on: bool):
+        self._check(self.lib.as2d_set_keep_logits(self.ctx, int(on)))
+
+    def logits(self, req: int, max_rows: int = 32) -> np.ndarray:
+        buf = np.empty((max_rows, self.shape.vocab), dtype=np.float32)
+        n = _I()
+        self._check(self.lib.as2d_get_logits(self.ctx, req, _ptr(buf), max_rows, ctypes.byref(n)))
+        return buf[:n.value].copy()
+
+    def row_tokens(self, req: int, max_rows: int = 32) -> List[int]:
+        buf = np.empty(max_rows, dtype=np.int32)
+        n = _I()
+        self._check(self.lib.as2d_get_row_tokens(self.ctx, req, _ptr(buf), max_rows, ctypes.byref(n)))
+        return [int(t) for t in buf[:n.value]]
+
+    def rollback(self, req: int, kv_len: int, root: int):
+        self._check(self.lib.as2d_rollback(self.ctx, req, kv_len, root))
+
+    def state(self, req: int):
+        kv, root, com = _I(), _I(), _I()
+        self._check(self.lib.as2d_get_state(self.ctx, req, ctypes.byref(kv), ctypes.byref(root),
+                                            ctypes.byref(com)))
+        return kv.value, root.value, com.value
+
+    def read_kv(self, req: int, layer: int, n_tok: int):
+        s = self.shape
+        dt = np.uint16 if s.dtype == BF16 else np.float32
+        k = np.empty((s.n_kv_heads, n_tok, s.head_dim), dtype=dt)
+        v = np.empty_like(k)
+        self._check(self.lib.as2d_read_kv(self.ctx, req, layer, _ptr(k), _ptr(v), n_tok))
+        return k, v
+
+    def release(self, req: int):
+        self._check(self.lib.as2d_release_request(self.ctx, req))
+
+    def set_timing(self, on: bool):
+        self._check(self.lib.as2d_set_timing(self.ctx, int(on)))
+
+    def timing_reset(self):
+        self._check(self.lib.as2d_timing_reset(self.ctx))
+
+    def timing(self) -> dict:
+        names = ctypes.create_string_buffer(32 * 16)
+        ms = (ctypes.c_double * 16)()
+        cnt = (ctypes.c_int64 * 16)()
+        n = self.lib.as2d_timing_read(self.ctx, names, ms, cnt, 16)
+        out = {}
+        for i in range(n):
+            nm = names.raw[32 * i:32 * i + 32].split(b"\0")[0].decode()
+            out[nm] = (ms[i], cnt[i])
+        return out
+
+    def step_bytes(self, rows: int, kv_keys: int) -> int:
+        return int(self.lib.as2d_step_bytes(self.ctx, rows, kv_keys))

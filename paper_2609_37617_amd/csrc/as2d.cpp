@@ -1,0 +1,796 @@
+// C ABI of the target verification library (include/as2d.h): context and
+// request state, weight packing at load time, and the step driver that
+// launches the gfx950 kernels of kernels.hip on one HIP stream.
+#include "../../include/as2d.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace as2d;
+
+namespace {
+
+struct GemmPlan {
+  int N = 0, K = 0, KT = 0, groups = 0, KS = 1, ktps = 0;
+};
+
+struct LayerW {
+  uint4 *qkv = nullptr, *o = nullptr, *gu = nullptr, *down = nullptr;
+  float *bias = nullptr, *g_attn = nullptr, *g_mlp = nullptr;
+};
+
+struct ReqState {
+  int active = 0, kv_len = 0, prefix_len = 0, root = -1;
+  int last_row_start = 0, last_rows = 0;
+  int last_logits = 0;  // logits of the last call are in the device buffer
+};
+
+enum Kind { K_EMBED, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_LM, K_FINISH, K_COUNT };
+const char* kKindNames[K_COUNT] = {"embed", "gemm_qkv", "attention", "gemm_o",
+                                   "gemm_gate_up", "gemm_down", "gemm_lm_head", "finish"};
+
+}  // namespace
+
+struct as2d_ctx {
+  as2d_config cfg{};
+  bool bf16 = true;
+  int es = 2;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  std::string err;
+  std::vector<void*> allocs;
+
+  void* embed = nullptr;
+  std::vector<LayerW> layers;
+  float* g_final = nullptr;
+  uint4* lm = nullptr;
+  GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
+
+  void *kc = nullptr, *vc = nullptr;
+  long long slot_stride = 0, layer_stride = 0;
+
+  float *x = nullptr, *q = nullptr, *logits = nullptr, *sumsq = nullptr, *amax_val = nullptr;
+  float *part = nullptr, *pacc = nullptr, *pml = nullptr, *rope_cs = nullptr;
+  int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr;
+  void *attn = nullptr, *hbuf = nullptr, *audio = nullptr;
+  size_t audio_cap = 0;
+  int n_chunks_cap = 0;
+  int max_rows = 0;
+
+  RowDesc* d_rows = nullptr;
+  ReqDesc* d_reqs = nullptr;  // [2 * max_requests]: attention requests, then finish requests
+  StepOut* d_out = nullptr;
+  RowDesc* h_rows = nullptr;
+  ReqDesc* h_reqs = nullptr;
+  StepOut* h_out = nullptr;
+  int* h_tok = nullptr;
+
+  std::vector<ReqState> reqs;
+  int keep_logits = 0;
+
+  int timing = 0;
+  double t_ms[K_COUNT] = {};
+  long long t_n[K_COUNT] = {};
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<std::pair<int, int>> ev_used;  // (kind, first event index)
+};
+
+namespace {
+
+int fail(as2d_ctx* c, int code, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+  }
+  return code;
+}
+
+#define HIP_TRY(c, expr)                                                                    \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail(c, e_ == hipErrorOutOfMemory ? AS2D_ENOMEM : AS2D_EHIP, "%s: %s (%s:%d)", \
+                  #expr, hipGetErrorString(e_), __FILE__, __LINE__);                        \
+  } while (0)
+
+template <typename P>
+int dalloc(as2d_ctx* c, P** p, size_t bytes) {
+  void* v = nullptr;
+  hipError_t e = hipMalloc(&v, bytes ? bytes : 16);
+  if (e != hipSuccess) return fail(c, AS2D_ENOMEM, "hipMalloc(%zu): %s", bytes, hipGetErrorString(e));
+  c->allocs.push_back(v);
+  *p = static_cast<P*>(v);
+  return AS2D_OK;
+}
+
+GemmPlan make_plan(int N, int K, int KE, int target_wgs) {
+  GemmPlan p;
+  p.N = N;
+  p.K = K;
+  p.KT = K / KE;
+  p.groups = N / kGroupCols;
+  int ks = (int)std::lround((double)target_wgs / p.groups);
+  ks = std::max(1, std::min(ks, std::max(1, p.KT / 4)));
+  p.ktps = (p.KT + ks - 1) / ks;
+  p.KS = (p.KT + p.ktps - 1) / p.ktps;
+  return p;
+}
+
+int env_int(const char* name, int def) {
+  const char* v = getenv(name);
+  return v && *v ? atoi(v) : def;
+}
+
+// Event-bracketed launch accounting (as2d_set_timing).
+hipEvent_t ev_get(as2d_ctx* c, size_t i) {
+  while (c->ev_pool.size() <= i) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->ev_pool.push_back(e);
+  }
+  return c->ev_pool[i];
+}
+
+struct Timed {
+  as2d_ctx* c;
+  int kind;
+  Timed(as2d_ctx* c_, int k) : c(c_), kind(k) {
+    if (c->timing) {
+      size_t i = c->ev_used.size() * 2;
+      hipEvent_t e = ev_get(c, i);
+      ev_get(c, i + 1);
+      if (e) hipEventRecord(e, c->stream);
+    }
+  }
+  ~Timed() {
+    if (c->timing) {
+      size_t i = c->ev_used.size() * 2;
+      hipEvent_t e = ev_get(c, i + 1);
+      if (e) hipEventRecord(e, c->stream);
+      c->ev_used.push_back({kind, (int)i});
+    }
+  }
+};
+
+void timing_collect(as2d_ctx* c) {
+  if (!c->timing) return;
+  for (auto& u : c->ev_used) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, c->ev_pool[u.second], c->ev_pool[u.second + 1]) == hipSuccess) {
+      c->t_ms[u.first] += ms;
+      c->t_n[u.first] += 1;
+    }
+  }
+  c->ev_used.clear();
+}
+
+int check_req(as2d_ctx* c, int req) {
+  if (!c) return AS2D_EINVAL;
+  if (req < 0 || req >= c->cfg.max_requests) return fail(c, AS2D_EINVAL, "request id %d out of range", req);
+  return AS2D_OK;
+}
+
+GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
+  GemmArgs a{};
+  a.W = W;
+  a.N = pl.N;
+  a.K = pl.K;
+  a.KT = pl.KT;
+  a.KS = pl.KS;
+  a.ktps = pl.ktps;
+  a.M = M;
+  a.MT = (M + 15) / 16;
+  a.sumsq = c->sumsq;
+  a.n_norm_groups = c->cfg.hidden / kGroupCols;
+  a.eps = c->cfg.rms_eps;
+  a.part = c->part;
+  a.counters = c->counters;
+  a.rows = c->d_rows;
+  return a;
+}
+
+// One forward pass over the rows and requests already in h_rows / h_reqs:
+// n_att attention requests (h_reqs[0..n_att)), n_fin finish requests
+// (h_reqs[max_requests..max_requests+n_fin)); with_head = run the LM head
+// and verification.
+int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
+  const as2d_config& g = c->cfg;
+  hipStream_t s = c->stream;
+  const bool bf = c->bf16;
+  const int mr = g.max_requests;
+  HIP_TRY(c, hipMemcpyAsync(c->d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(c->d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
+  int max_chunks = 1;
+  for (int r = 0; r < n_att; ++r) {
+    const int nk = c->h_reqs[r].L0 + c->h_reqs[r].W;
+    max_chunks = std::max(max_chunks, (nk + kAttnChunk - 1) / kAttnChunk);
+  }
+  if (max_chunks > c->n_chunks_cap) return fail(c, AS2D_ECAPACITY, "attention chunks %d > %d", max_chunks, c->n_chunks_cap);
+
+  {
+    Timed t(c, K_EMBED);
+    HIP_TRY(c, launch_embed(bf, c->d_rows, M, c->embed, c->audio, g.hidden, c->x, c->sumsq, s));
+  }
+  const int H = g.hidden, d = g.head_dim;
+  for (int l = 0; l < g.n_layers; ++l) {
+    const LayerW& w = c->layers[l];
+    void* kc = (char*)c->kc + (size_t)l * c->layer_stride * c->es;
+    void* vc = (char*)c->vc + (size_t)l * c->layer_stride * c->es;
+    {
+      GemmArgs a = base_args(c, c->p_qkv, w.qkv, M);
+      a.A = c->x;
+      a.gain = w.g_attn;
+      a.bias = w.bias;
+      a.q_out = c->q;
+      a.k_cache = kc;
+      a.v_cache = vc;
+      a.slot_stride = c->slot_stride;
+      a.kv_cap = g.max_kv_len;
+      a.n_q = g.n_q_heads;
+      a.n_kv = g.n_kv_heads;
+      a.head_dim = d;
+      a.rope_cs = c->rope_cs;
+      Timed t(c, K_QKV);
+      HIP_TRY(c, launch_gemm(bf, A_NORM, EPI_QKV, a, s));
+    }
+    {
+      AttnArgs a{};
+      a.q = c->q;
+      a.k_cache = kc;
+      a.v_cache = vc;
+      a.slot_stride = c->slot_stride;
+      a.kv_cap = g.max_kv_len;
+      a.rows = c->d_rows;
+      a.reqs = c->d_reqs;
+      a.n_q = g.n_q_heads;
+      a.n_kv = g.n_kv_heads;
+      a.head_dim = d;
+      a.scale = 1.0f / std::sqrt((float)d);
+      a.pacc = c->pacc;
+      a.pml = c->pml;
+      a.n_chunks_cap = c->n_chunks_cap;
+      a.out = c->attn;
+      a.M = M;
+      Timed t(c, K_ATTN);
+      HIP_TRY(c, launch_attention(bf, a, n_att, max_chunks, s));
+    }
+    {
+      GemmArgs a = base_args(c, c->p_o, w.o, M);
+      a.A = c->attn;
+      a.x = c->x;
+      a.sumsq_out = c->sumsq;
+      Timed t(c, K_O);
+      HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_RESID, a, s));
+    }
+    {
+      GemmArgs a = base_args(c, c->p_gu, w.gu, M);
+      a.A = c->x;
+      a.gain = w.g_mlp;
+      a.h_out = c->hbuf;
+      Timed t(c, K_GU);
+      HIP_TRY(c, launch_gemm(bf, A_NORM, EPI_SWIGLU, a, s));
+    }
+    {
+      GemmArgs a = base_args(c, c->p_down, w.down, M);
+      a.A = c->hbuf;
+      a.x = c->x;
+      a.sumsq_out = c->sumsq;
+      Timed t(c, K_DOWN);
+      HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_RESID, a, s));
+    }
+  }
+  if (with_head) {
+    {
+      GemmArgs a = base_args(c, c->p_lm, c->lm, M);
+      a.A = c->x;
+      a.gain = c->g_final;
+      a.logits = c->keep_logits ? c->logits : nullptr;
+      a.amax_val = c->amax_val;
+      a.amax_idx = c->amax_idx;
+      Timed t(c, K_LM);
+      HIP_TRY(c, launch_gemm(bf, A_NORM, EPI_ARGMAX, a, s));
+    }
+    {
+      Timed t(c, K_FINISH);
+      HIP_TRY(c, launch_finish(c->d_rows, c->d_reqs + mr, n_fin, c->amax_val, c->amax_idx,
+                               g.vocab / kGroupCols, c->row_tok, c->d_out, s));
+    }
+    HIP_TRY(c, hipMemcpyAsync(c->h_out, c->d_out, sizeof(StepOut) * n_fin, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipMemcpyAsync(c->h_tok, c->row_tok, sizeof(int) * M, hipMemcpyDeviceToHost, s));
+  }
+  HIP_TRY(c, hipStreamSynchronize(s));
+  timing_collect(c);
+  return AS2D_OK;
+}
+
+int upload_matrix(as2d_ctx* c, void* tmp, const void* host, size_t rows, size_t cols) {
+  HIP_TRY(c, hipMemcpyAsync(tmp, host, rows * cols * c->es, hipMemcpyHostToDevice, c->stream));
+  return AS2D_OK;
+}
+
+int pack(as2d_ctx* c, uint4** out, const void* tmp, int N, int K, int remap, int F) {
+  int rc = dalloc(c, out, (size_t)N * K * c->es);
+  if (rc) return rc;
+  HIP_TRY(c, launch_pack(c->bf16, tmp, *out, N, K, remap, F, c->stream));
+  return AS2D_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+
+extern "C" {
+
+const char* as2d_last_error(const as2d_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+void as2d_free(as2d_ctx* c) {
+  if (!c) return;
+  if (c->stream) hipStreamSynchronize(c->stream);
+  for (void* p : c->allocs) hipFree(p);
+  if (c->h_rows) hipHostFree(c->h_rows);
+  if (c->h_reqs) hipHostFree(c->h_reqs);
+  if (c->h_out) hipHostFree(c->h_out);
+  if (c->h_tok) hipHostFree(c->h_tok);
+  for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
+  if (c->own_stream && c->stream) hipStreamDestroy(c->stream);
+  delete c;
+}
+
+int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n_tensors,
+                      void* hip_stream, as2d_ctx** out) {
+  if (!cfg || !host || !out) return AS2D_EINVAL;
+  *out = nullptr;
+  const as2d_config g = *cfg;
+  auto c = new as2d_ctx();
+  auto bad = [&](const char* msg) {
+    as2d_free(c);
+    (void)msg;
+    return AS2D_EINVAL;
+  };
+  if (g.n_layers < 1 || g.hidden % 128 || g.ffn % 64 || g.vocab % 128 || g.vocab <= 0)
+    return bad("shape: need n_layers >= 1, hidden % 128 == 0, ffn % 64 == 0, vocab % 128 == 0");
+  if (g.head_dim != 64 && g.head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (g.n_q_heads < 1 || g.n_kv_heads < 1 || g.n_q_heads % g.n_kv_heads)
+    return bad("n_q_heads must be a positive multiple of n_kv_heads");
+  if (((g.n_q_heads + 2 * g.n_kv_heads) * g.head_dim) % 128 || (g.n_q_heads * g.head_dim) % 128)
+    return bad("attention widths must be multiples of 128");
+  if (g.dtype != AS2D_F32 && g.dtype != AS2D_BF16) return bad("dtype must be AS2D_F32 or AS2D_BF16");
+  if (g.max_requests < 1 || g.max_kv_len < 2 || g.max_k < 0 || g.max_k > 31)
+    return bad("capacity: max_requests >= 1, max_kv_len >= 2, 0 <= max_k <= 31");
+  if (!(g.rms_eps >= 0.f) || !(g.rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0 required");
+  const int per_layer = g.qkv_bias ? 12 : 9;
+  if (n_tensors != 1 + per_layer * g.n_layers + 2) return bad("wrong tensor count for this config");
+  for (int i = 0; i < n_tensors; ++i)
+    if (!host[i]) return bad("null tensor pointer");
+
+  c->cfg = g;
+  c->bf16 = g.dtype == AS2D_BF16;
+  c->es = c->bf16 ? 2 : 4;
+  const int KE = c->bf16 ? 32 : 16;
+  const int H = g.hidden, F = g.ffn, V = g.vocab, d = g.head_dim;
+  const int nq = g.n_q_heads, nkv = g.n_kv_heads;
+  const int qkv_n = (nq + 2 * nkv) * d;
+  int rc;
+  // inside `run` errors return their code; the caller frees the context
+#define CK(x)                      \
+  do {                             \
+    if ((rc = (x)) != 0) return rc; \
+  } while (0)
+
+  if (hip_stream) {
+    c->stream = (hipStream_t)hip_stream;
+  } else {
+    if (hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking) != hipSuccess) {
+      as2d_free(c);
+      return AS2D_EHIP;
+    }
+    c->own_stream = true;
+  }
+  if (H % KE || (nq * d) % KE || F % KE) return bad("inner dimensions must be multiples of the k-step");
+
+  // GEMM plans: k-splits depend on the matrix shape only
+  const int target = env_int("AS2D_TARGET_WGS", 512);
+  c->p_qkv = make_plan(qkv_n, H, KE, target);
+  c->p_o = make_plan(H, nq * d, KE, target);
+  c->p_gu = make_plan(2 * F, H, KE, target);
+  c->p_down = make_plan(H, F, KE, target);
+  c->p_lm = make_plan(V, H, KE, target);
+
+  // temporary device buffer for raw matrices before packing (largest matrix)
+  size_t tmp_elems = std::max({(size_t)V * H, (size_t)qkv_n * H, (size_t)2 * F * H, (size_t)H * F});
+  void* tmp = nullptr;
+  if (hipMalloc(&tmp, tmp_elems * c->es) != hipSuccess) {
+    fail(c, AS2D_ENOMEM, "staging buffer");
+    as2d_free(c);
+    return AS2D_ENOMEM;
+  }
+  auto run = [&]() -> int {
+    int ti = 0;
+    int rc = 0;
+    CK(dalloc(c, &c->embed, (size_t)V * H * c->es));
+    HIP_TRY(c, hipMemcpyAsync(c->embed, host[ti++], (size_t)V * H * c->es, hipMemcpyHostToDevice, c->stream));
+    c->layers.resize(g.n_layers);
+    for (int l = 0; l < g.n_layers; ++l) {
+      LayerW& w = c->layers[l];
+      CK(dalloc(c, &w.g_attn, H * 4));
+      HIP_TRY(c, hipMemcpyAsync(w.g_attn, host[ti++], H * 4, hipMemcpyHostToDevice, c->stream));
+      // q, k, v rows stacked into one [qkv_n][H] matrix
+      char* t = (char*)tmp;
+      HIP_TRY(c, hipMemcpyAsync(t, host[ti++], (size_t)nq * d * H * c->es, hipMemcpyHostToDevice, c->stream));
+      t += (size_t)nq * d * H * c->es;
+      HIP_TRY(c, hipMemcpyAsync(t, host[ti++], (size_t)nkv * d * H * c->es, hipMemcpyHostToDevice, c->stream));
+      t += (size_t)nkv * d * H * c->es;
+      HIP_TRY(c, hipMemcpyAsync(t, host[ti++], (size_t)nkv * d * H * c->es, hipMemcpyHostToDevice, c->stream));
+      CK(pack(c, &w.qkv, tmp, qkv_n, H, 0, 0));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+      if (g.qkv_bias) {
+        CK(dalloc(c, &w.bias, qkv_n * 4));
+        HIP_TRY(c, hipMemcpyAsync(w.bias, host[ti++], nq * d * 4, hipMemcpyHostToDevice, c->stream));
+        HIP_TRY(c, hipMemcpyAsync(w.bias + nq * d, host[ti++], nkv * d * 4, hipMemcpyHostToDevice, c->stream));
+        HIP_TRY(c, hipMemcpyAsync(w.bias + (nq + nkv) * d, host[ti++], nkv * d * 4, hipMemcpyHostToDevice, c->stream));
+      }
+      CK(upload_matrix(c, tmp, host[ti++], H, nq * d));
+      CK(pack(c, &w.o, tmp, H, nq * d, 0, 0));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+      CK(dalloc(c, &w.g_mlp, H * 4));
+      HIP_TRY(c, hipMemcpyAsync(w.g_mlp, host[ti++], H * 4, hipMemcpyHostToDevice, c->stream));
+      CK(upload_matrix(c, tmp, host[ti++], F, H));
+      CK(upload_matrix(c, (char*)tmp + (size_t)F * H * c->es, host[ti++], F, H));
+      CK(pack(c, &w.gu, tmp, 2 * F, H, 1, F));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+      CK(upload_matrix(c, tmp, host[ti++], H, F));
+      CK(pack(c, &w.down, tmp, H, F, 0, 0));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+    }
+    CK(dalloc(c, &c->g_final, H * 4));
+    HIP_TRY(c, hipMemcpyAsync(c->g_final, host[ti++], H * 4, hipMemcpyHostToDevice, c->stream));
+    CK(upload_matrix(c, tmp, host[ti++], V, H));
+    CK(pack(c, &c->lm, tmp, V, H, 0, 0));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    return AS2D_OK;
+  };
+  rc = run();
+  hipFree(tmp);
+  if (rc == 0) rc = [&]() -> int {
+    int rc = 0;
+
+  // KV cache: [slot][layer][kv_head][pos][d]
+  c->layer_stride = (long long)nkv * g.max_kv_len * d;
+  c->slot_stride = c->layer_stride * g.n_layers;
+  const size_t kv_bytes = (size_t)c->slot_stride * g.max_requests * c->es;
+  CK(dalloc(c, &c->kc, kv_bytes));
+  CK(dalloc(c, &c->vc, kv_bytes));
+
+  // activations and scratch, sized for the largest pass
+  c->max_rows = std::min(kMaxRows, std::max(g.max_requests * (g.max_k + 1), 64));
+  const int MR = kMaxRows;
+  c->n_chunks_cap = (g.max_kv_len + kAttnChunk - 1) / kAttnChunk;
+  CK(dalloc(c, &c->x, (size_t)MR * H * 4));
+  CK(dalloc(c, &c->q, (size_t)MR * nq * d * 4));
+  CK(dalloc(c, &c->attn, (size_t)MR * nq * d * c->es));
+  CK(dalloc(c, &c->hbuf, (size_t)MR * F * c->es));
+  CK(dalloc(c, &c->logits, (size_t)MR * V * 4));
+  CK(dalloc(c, &c->sumsq, (size_t)(H / 128) * MR * 4));
+  CK(dalloc(c, &c->amax_val, (size_t)(V / 128) * MR * 4));
+  CK(dalloc(c, &c->amax_idx, (size_t)(V / 128) * MR * 4));
+  CK(dalloc(c, &c->row_tok, (size_t)MR * 4));
+  size_t part_elems = 0;
+  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
+    if (p->KS > 1) part_elems = std::max(part_elems, (size_t)p->KS * MR * p->N);
+  CK(dalloc(c, &c->part, part_elems * 4));
+  CK(dalloc(c, &c->counters, 8192 * 4));
+  HIP_TRY(c, hipMemsetAsync(c->counters, 0, 8192 * 4, c->stream));
+  CK(dalloc(c, &c->pacc, (size_t)c->n_chunks_cap * MR * nq * d * 4));
+  CK(dalloc(c, &c->pml, (size_t)c->n_chunks_cap * MR * nq * 2 * 4));
+  CK(dalloc(c, &c->d_rows, sizeof(RowDesc) * MR));
+  CK(dalloc(c, &c->d_reqs, sizeof(ReqDesc) * 2 * g.max_requests));
+  CK(dalloc(c, &c->d_out, sizeof(StepOut) * g.max_requests));
+
+  // rotary table, evaluated in double precision: [pos][i] -> (cos, sin)
+  {
+    const int half = d / 2;
+    std::vector<float> cs((size_t)g.max_kv_len * half * 2);
+    for (int pos = 0; pos < g.max_kv_len; ++pos)
+      for (int i = 0; i < half; ++i) {
+        const double ang = (double)pos * std::pow((double)g.rope_theta, -2.0 * i / d);
+        cs[((size_t)pos * half + i) * 2] = (float)std::cos(ang);
+        cs[((size_t)pos * half + i) * 2 + 1] = (float)std::sin(ang);
+      }
+    CK(dalloc(c, &c->rope_cs, cs.size() * 4));
+    HIP_TRY(c, hipMemcpy(c->rope_cs, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
+  }
+  if (hipHostMalloc((void**)&c->h_rows, sizeof(RowDesc) * MR, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_reqs, sizeof(ReqDesc) * 2 * g.max_requests, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_out, sizeof(StepOut) * g.max_requests, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_tok, sizeof(int) * MR, 0) != hipSuccess) {
+    return fail(c, AS2D_ENOMEM, "pinned host buffers");
+  }
+  memset(c->h_reqs, 0, sizeof(ReqDesc) * 2 * g.max_requests);
+  c->reqs.assign(g.max_requests, ReqState());
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return AS2D_OK;
+  }();
+  if (rc) {
+    as2d_free(c);
+    return rc;
+  }
+  *out = c;
+  return AS2D_OK;
+#undef CK
+}
+
+int as2d_prefill_kv(as2d_ctx* c, int32_t req, const void* audio, int32_t n_audio,
+                    const int32_t* instr, int32_t n_instr, int32_t* first_token, int32_t* kv_len) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  const as2d_config& g = c->cfg;
+  if (n_audio < 0 || n_instr < 0 || n_audio + n_instr < 1 || (n_audio && !audio) || (n_instr && !instr) ||
+      !first_token || !kv_len)
+    return fail(c, AS2D_EINVAL, "prefill: bad arguments");
+  const int total = n_audio + n_instr;
+  if (total > g.max_kv_len) return fail(c, AS2D_ECAPACITY, "prefill: %d rows > max_kv_len %d", total, g.max_kv_len);
+  for (int i = 0; i < n_instr; ++i)
+    if (instr[i] < 0 || instr[i] >= g.vocab) return fail(c, AS2D_EINVAL, "prefill: token id %d out of range", instr[i]);
+  ReqState& st = c->reqs[req];
+  st = ReqState();
+  if (n_audio) {
+    const size_t bytes = (size_t)n_audio * g.hidden * c->es;
+    if (bytes > c->audio_cap) {
+      if (c->audio) {
+        HIP_TRY(c, hipStreamSynchronize(c->stream));
+        auto it = std::find(c->allocs.begin(), c->allocs.end(), c->audio);
+        if (it != c->allocs.end()) c->allocs.erase(it);
+        hipFree(c->audio);
+        c->audio = nullptr;
+        c->audio_cap = 0;
+      }
+      if ((rc = dalloc(c, &c->audio, bytes))) return rc;
+      c->audio_cap = bytes;
+    }
+    HIP_TRY(c, hipMemcpyAsync(c->audio, audio, bytes, hipMemcpyHostToDevice, c->stream));
+  }
+  const int chunk = c->max_rows;
+  const int mr = g.max_requests;
+  for (int r0 = 0; r0 < total; r0 += chunk) {
+    const int M = std::min(chunk, total - r0);
+    for (int i = 0; i < M; ++i) {
+      const int p = r0 + i;
+      RowDesc rd{};
+      rd.token = p < n_audio ? -1 : instr[p - n_audio];
+      rd.src = p < n_audio ? p : 0;
+      rd.pos = p;
+      rd.slot = req;
+      rd.cmp = -1;
+      c->h_rows[i] = rd;
+    }
+    c->h_reqs[0] = ReqDesc{0, M, r0, req};
+    const bool last = r0 + M == total;
+    c->h_reqs[mr] = ReqDesc{M - 1, 1, r0 + M - 1, req};
+    if ((rc = run_forward(c, M, 1, 1, last))) return rc;
+    if (last) {
+      if (c->h_out[0].nan_flag) return fail(c, AS2D_ENUMERIC, "prefill: non-finite logits");
+      st.root = c->h_out[0].correction;
+      st.last_row_start = M - 1;
+      st.last_rows = 1;
+      st.last_logits = c->keep_logits;
+    }
+  }
+  st.active = 1;
+  st.kv_len = st.prefix_len = total;
+  *first_token = st.root;
+  *kv_len = total;
+  return AS2D_OK;
+}
+
+int as2d_verify_batch(as2d_ctx* c, int32_t n, const int32_t* reqs, const int32_t* cands,
+                      const int32_t* ks, as2d_verify_out* outs) {
+  if (!c) return AS2D_EINVAL;
+  const as2d_config& g = c->cfg;
+  if (n < 1 || n > g.max_requests || !reqs || !ks || !outs) return fail(c, AS2D_EINVAL, "verify: bad arguments");
+  int M = 0, off = 0;
+  const int mr = g.max_requests;
+  for (int r = 0; r < n; ++r) {
+    int rc = check_req(c, reqs[r]);
+    if (rc) return rc;
+    for (int q = 0; q < r; ++q)
+      if (reqs[q] == reqs[r]) return fail(c, AS2D_EINVAL, "verify: request %d listed twice", reqs[r]);
+    const ReqState& st = c->reqs[reqs[r]];
+    if (!st.active) return fail(c, AS2D_ESTATE, "verify: request %d has not been prefilled", reqs[r]);
+    const int k = ks[r];
+    if (k < 0 || k > g.max_k) return fail(c, AS2D_EINVAL, "verify: k=%d outside [0, %d]", k, g.max_k);
+    if (k && !cands) return fail(c, AS2D_EINVAL, "verify: null candidates");
+    for (int i = 0; i < k; ++i)
+      if (cands[off + i] < 0 || cands[off + i] >= g.vocab)
+        return fail(c, AS2D_EINVAL, "verify: candidate id %d out of range", cands[off + i]);
+    if (st.kv_len + k + 1 > g.max_kv_len)
+      return fail(c, AS2D_ECAPACITY, "verify: request %d needs %d positions > %d", reqs[r], st.kv_len + k + 1, g.max_kv_len);
+    M += k + 1;
+    off += k;
+  }
+  if (M > kMaxRows) return fail(c, AS2D_EINVAL, "verify: %d rows exceed %d", M, kMaxRows);
+  int row = 0;
+  off = 0;
+  for (int r = 0; r < n; ++r) {
+    const ReqState& st = c->reqs[reqs[r]];
+    const int k = ks[r];
+    for (int i = 0; i <= k; ++i) {
+      RowDesc rd{};
+      rd.token = i == 0 ? st.root : cands[off + i - 1];
+      rd.src = 0;
+      rd.pos = st.kv_len + i;
+      rd.slot = reqs[r];
+      rd.cmp = i < k ? cands[off + i] : -1;
+      c->h_rows[row + i] = rd;
+    }
+    c->h_reqs[r] = ReqDesc{row, k + 1, st.kv_len, reqs[r]};
+    c->h_reqs[mr + r] = c->h_reqs[r];
+    row += k + 1;
+    off += k;
+  }
+  int rc = run_forward(c, M, n, n, true);
+  if (rc) return rc;
+  for (int r = 0; r < n; ++r)
+    if (c->h_out[r].nan_flag) return fail(c, AS2D_ENUMERIC, "verify: non-finite logits (request %d)", reqs[r]);
+  for (int r = 0; r < n; ++r) {
+    ReqState& st = c->reqs[reqs[r]];
+    const StepOut& o = c->h_out[r];
+    st.kv_len += o.accepted + 1;
+    st.root = o.correction;
+    st.last_row_start = c->h_reqs[r].row_start;
+    st.last_rows = ks[r] + 1;
+    st.last_logits = c->keep_logits;
+    outs[r].accepted_len = o.accepted;
+    outs[r].correction_token = o.correction;
+    outs[r].kv_len = st.kv_len;
+    outs[r].committed = st.kv_len - st.prefix_len;
+  }
+  // other requests' last-call rows are no longer in the device buffers
+  for (int q = 0; q < g.max_requests; ++q) {
+    bool in = false;
+    for (int r = 0; r < n; ++r) in |= reqs[r] == q;
+    if (!in) c->reqs[q].last_logits = 0, c->reqs[q].last_rows = 0;
+  }
+  return AS2D_OK;
+}
+
+int as2d_verify(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k, as2d_verify_out* out) {
+  return as2d_verify_batch(c, 1, &req, cands, &k, out);
+}
+
+int as2d_decode_one(as2d_ctx* c, int32_t req, as2d_verify_out* out) {
+  const int32_t k = 0;
+  return as2d_verify_batch(c, 1, &req, nullptr, &k, out);
+}
+
+int as2d_set_keep_logits(as2d_ctx* c, int32_t on) {
+  if (!c) return AS2D_EINVAL;
+  c->keep_logits = on ? 1 : 0;
+  return AS2D_OK;
+}
+
+int as2d_get_logits(as2d_ctx* c, int32_t req, float* host, int32_t max_rows, int32_t* n_rows) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  const ReqState& st = c->reqs[req];
+  if (!host || !n_rows) return fail(c, AS2D_EINVAL, "get_logits: null pointer");
+  if (!st.last_logits || !st.last_rows) return fail(c, AS2D_ESTATE, "get_logits: no logits kept for request %d", req);
+  if (max_rows < st.last_rows) return fail(c, AS2D_EINVAL, "get_logits: need %d rows", st.last_rows);
+  HIP_TRY(c, hipMemcpy(host, c->logits + (size_t)st.last_row_start * c->cfg.vocab,
+                       (size_t)st.last_rows * c->cfg.vocab * 4, hipMemcpyDeviceToHost));
+  *n_rows = st.last_rows;
+  return AS2D_OK;
+}
+
+int as2d_get_row_tokens(as2d_ctx* c, int32_t req, int32_t* host, int32_t max_rows, int32_t* n_rows) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  const ReqState& st = c->reqs[req];
+  if (!host || !n_rows) return fail(c, AS2D_EINVAL, "get_row_tokens: null pointer");
+  if (!st.last_rows) return fail(c, AS2D_ESTATE, "get_row_tokens: no rows for request %d", req);
+  if (max_rows < st.last_rows) return fail(c, AS2D_EINVAL, "get_row_tokens: need %d rows", st.last_rows);
+  memcpy(host, c->h_tok + st.last_row_start, sizeof(int) * st.last_rows);
+  *n_rows = st.last_rows;
+  return AS2D_OK;
+}
+
+int as2d_rollback(as2d_ctx* c, int32_t req, int32_t kv_len, int32_t root) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  ReqState& st = c->reqs[req];
+  if (!st.active) return fail(c, AS2D_ESTATE, "rollback: request %d has not been prefilled", req);
+  if (kv_len < st.prefix_len || kv_len > st.kv_len)
+    return fail(c, AS2D_EINVAL, "rollback: kv_len %d outside [%d, %d]", kv_len, st.prefix_len, st.kv_len);
+  if (root < 0 || root >= c->cfg.vocab) return fail(c, AS2D_EINVAL, "rollback: root id out of range");
+  st.kv_len = kv_len;
+  st.root = root;
+  st.last_rows = 0;
+  st.last_logits = 0;
+  return AS2D_OK;
+}
+
+int as2d_get_state(as2d_ctx* c, int32_t req, int32_t* kv_len, int32_t* root, int32_t* committed) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  const ReqState& st = c->reqs[req];
+  if (!st.active) return fail(c, AS2D_ESTATE, "request %d has not been prefilled", req);
+  if (kv_len) *kv_len = st.kv_len;
+  if (root) *root = st.root;
+  if (committed) *committed = st.kv_len - st.prefix_len;
+  return AS2D_OK;
+}
+
+int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* host_v, int32_t n_tok) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  const as2d_config& g = c->cfg;
+  if (layer < 0 || layer >= g.n_layers || n_tok < 0 || n_tok > g.max_kv_len || !host_k || !host_v)
+    return fail(c, AS2D_EINVAL, "read_kv: bad arguments");
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const size_t row = (size_t)g.head_dim * c->es;
+  for (int h = 0; h < g.n_kv_heads; ++h) {
+    const size_t src = ((size_t)req * c->slot_stride + (size_t)layer * c->layer_stride +
+                        (size_t)h * g.max_kv_len * g.head_dim) * c->es;
+    HIP_TRY(c, hipMemcpy((char*)host_k + h * n_tok * row, (char*)c->kc + src, n_tok * row, hipMemcpyDeviceToHost));
+    HIP_TRY(c, hipMemcpy((char*)host_v + h * n_tok * row, (char*)c->vc + src, n_tok * row, hipMemcpyDeviceToHost));
+  }
+  return AS2D_OK;
+}
+
+int as2d_release_request(as2d_ctx* c, int32_t req) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  c->reqs[req] = ReqState();
+  return AS2D_OK;
+}
+
+int as2d_set_timing(as2d_ctx* c, int32_t on) {
+  if (!c) return AS2D_EINVAL;
+  c->timing = on ? 1 : 0;
+  return AS2D_OK;
+}
+
+int as2d_timing_reset(as2d_ctx* c) {
+  if (!c) return AS2D_EINVAL;
+  for (int k = 0; k < K_COUNT; ++k) c->t_ms[k] = 0, c->t_n[k] = 0;
+  return AS2D_OK;
+}
+
+int as2d_timing_read(as2d_ctx* c, char* names, double* total_ms, int64_t* counts, int32_t max) {
+  if (!c || !names || !total_ms || !counts) return AS2D_EINVAL;
+  const int n = std::min<int>(max, K_COUNT);
+  for (int k = 0; k < n; ++k) {
+    snprintf(names + 32 * k, 32, "%s", kKindNames[k]);
+    total_ms[k] = c->t_ms[k];
+    counts[k] = c->t_n[k];
+  }
+  return n;
+}
+
+int64_t as2d_step_bytes(const as2d_ctx* c, int32_t rows, int64_t kv_keys) {
+  if (!c) return -1;
+  const as2d_config& g = c->cfg;
+  const int64_t H = g.hidden, F = g.ffn, V = g.vocab, d = g.head_dim;
+  const int64_t nq = g.n_q_heads, nkv = g.n_kv_heads;
+  const int64_t per_layer = H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F;
+  int64_t b = c->es * (g.n_layers * per_layer + V * H);  // weights, streamed once
+  b += c->es * rows * H;                                 // embedding rows
+  b += c->es * g.n_layers * 2 * nkv * d * (kv_keys + rows);  // KV read + append
+  return b;
+}
+
+}  // extern "C"

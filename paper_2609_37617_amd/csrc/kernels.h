@@ -1,0 +1,99 @@
+// Internal interface between the C ABI (as2d.cpp) and the gfx950 kernels
+// (kernels.hip).  Not installed; the public interface is include/as2d.h.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace as2d {
+
+// GEMM tiling shared by the packer and the GEMM kernels.
+constexpr int kWaves = 4;               // waves per workgroup
+constexpr int kTilesPerWave = 2;        // 16-column tiles per wave
+constexpr int kGroupCols = kWaves * kTilesPerWave * 16;   // 128 columns per workgroup
+constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
+constexpr int kMaxRows = kMaxMTiles * 16;
+constexpr int kAttnChunk = 64;          // keys per attention split
+
+// One processed row of a forward pass.
+struct RowDesc {
+  int32_t token;   // embedding row, or -1: take audio staging row `src`
+  int32_t src;     // audio staging row
+  int32_t pos;     // position (also the KV cache row it writes)
+  int32_t slot;    // KV cache slot of its request
+  int32_t cmp;     // candidate its greedy token is compared with (-1: none)
+  int32_t pad[3];
+};
+
+// One request of a forward pass: rows [row_start, row_start + W).
+struct ReqDesc {
+  int32_t row_start, W, L0, slot;
+};
+
+struct StepOut {
+  int32_t accepted, correction, nan_flag, pad;
+};
+
+enum AMode { A_PLAIN = 0, A_NORM = 1 };
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_ARGMAX = 3 };
+
+struct GemmArgs {
+  const uint4* W;        // packed weight tiles
+  int N, K, KT, KS, ktps;
+  int M, MT;
+  // A operand
+  const void* A;         // A_PLAIN: element type [M][K]; A_NORM: float [M][K] (residual x)
+  const float* sumsq;    // A_NORM: per-row sum-of-squares partials [n_norm_groups][kMaxRows]
+  int n_norm_groups;
+  const float* gain;     // A_NORM: RMSNorm gain [K]
+  float eps;
+  // split-K scratch
+  float* part;           // [KS][M][N]
+  int* counters;         // one per column group, zero between launches
+  // epilogue
+  const RowDesc* rows;
+  const float* bias;     // EPI_QKV (may be null)
+  float* q_out;          // EPI_QKV: [M][n_q*d]
+  void* k_cache;         // EPI_QKV: this layer's K cache, slot stride `slot_stride`
+  void* v_cache;
+  long long slot_stride; // elements between slots
+  int kv_cap;            // positions per slot
+  int n_q, n_kv, head_dim;
+  const float* rope_cs;  // [kv_cap][head_dim/2][2] (cos, sin)
+  float* x;              // EPI_RESID: residual [M][N] updated in place
+  float* sumsq_out;      // EPI_RESID: [N/128][kMaxRows]
+  void* h_out;           // EPI_SWIGLU: element type [M][N/2]
+  float* logits;         // EPI_ARGMAX: optional [M][N]
+  float* amax_val;       // EPI_ARGMAX: [N/128][kMaxRows]
+  int* amax_idx;
+};
+
+struct AttnArgs {
+  const float* q;        // [M][n_q*d]
+  const void* k_cache;   // this layer
+  const void* v_cache;
+  long long slot_stride;
+  int kv_cap;
+  const RowDesc* rows;
+  const ReqDesc* reqs;
+  int n_q, n_kv, head_dim;
+  float scale;
+  float* pacc;           // [n_chunks_cap][kMaxRows][n_q][d]
+  float* pml;            // [n_chunks_cap][kMaxRows][n_q][2]
+  int n_chunks_cap;
+  void* out;             // element type [M][n_q*d]
+  int M;
+};
+
+// Launchers (all asynchronous on `s`).  `bf16` selects the element type:
+// true: bf16 stored as uint16 bit patterns; false: float32.
+hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int remap_gate_up,
+                       int F, hipStream_t s);
+hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed, const void* audio,
+                        int H, float* x, float* sumsq, hipStream_t s);
+hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStream_t s);
+hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s);
+hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, const float* amax_val,
+                         const int* amax_idx, int n_groups, int* row_tok, StepOut* out, hipStream_t s);
+int gemm_lds_bytes(bool bf16, int MT, int chunk_kt);
+
+}  // namespace as2d

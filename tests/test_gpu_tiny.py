@@ -1,0 +1,202 @@
+"""GPU parity on the tiny shapes: the HIP path against the oracle through
+prefill and verification rounds, plus the exactness properties on the GPU
+itself (batched verification equals sequential decoding bit for bit)."""
+import numpy as np
+import pytest
+
+from tests.harness import (Stats, compare_kv, logit_tol, make_pair, parity_round, prefix, restore,
+                           snapshot)
+from workload import TINY, TINY_BF16, gen, workload
+from workload.gen import CandidateSource
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [TINY, TINY_BF16]
+
+
+@pytest.fixture(scope="module", params=SHAPES, ids=lambda s: s.name)
+def pair(request):
+    om, gpu = make_pair(request.param, seed=0, max_requests=4, max_kv_len=512, max_k=31)
+    gpu.set_keep_logits(True)
+    yield request.param, om, gpu
+    gpu.close()
+
+
+def test_tiny_workload_rounds(pair):
+    """Config of the tiny decoder: 128 audio rows + 16 instruction tokens,
+    32 rounds of k=4 candidates corrupted with p=0.3."""
+    shape, om, gpu = pair
+    wl = workload(0)
+    rq = wl.requests[0]
+    a_or, a_dev, instr = prefix(shape, rq.n_audio, rq.n_instr)
+    f_o, L_o = om.prefill(a_or, instr)
+    f_g, L_g = gpu.prefill(0, a_dev, instr)
+    assert L_g == L_o == rq.n_audio + rq.n_instr
+    lg = gpu.logits(0)
+    assert np.max(np.abs(lg[0] - om.last_logits[0])) <= logit_tol(shape)
+    assert f_g == f_o
+    snap = snapshot(om)
+    y = om.target_only(rq.reply_len)          # the greedy reference stream y_0..y_N
+    restore(om, snap)
+    src = CandidateSource(y, shape.vocab, rq.p, seed=0)
+    st = Stats()
+    n = 0
+    for _ in range(rq.max_rounds):
+        k = min(rq.k, rq.reply_len - n - 1)
+        if k < 0:
+            break
+        r = parity_round(om, gpu, 0, src.block(n, k), k, logit_tol(shape), st)
+        n += r["accepted_len"] + 1
+    assert st.rounds == rq.max_rounds
+    assert gpu.state(0)[0] == om.kv_len
+    for l in range(shape.n_layers):
+        compare_kv(om, gpu, 0, l, om.kv_len, 1e-5 if shape.dtype == 0 else 2e-2)
+    print(f"{shape.name}: rounds={st.rounds} committed={st.committed} near_ties={st.near_ties} "
+          f"max_logit_err={st.max_err:.3g}")
+
+
+def _prefilled(gpu, shape, req=0, n_audio=70, n_instr=5, seed=3):
+    _, a_dev, instr = prefix(shape, n_audio, n_instr, seed=seed, req=req)
+    first, L = gpu.prefill(req, a_dev, instr)
+    return first, L
+
+
+@pytest.mark.parametrize("k", [1, 4, 8, 16, 31])
+def test_verify_is_bitwise_sequential_decoding(pair, k):
+    """Pathwise equivalence (Appendix C.4) holds exactly on the GPU: the
+    verify call over root + k candidates reproduces the logits of k + 1
+    target-only steps bit for bit, and accepts all k."""
+    shape, _, gpu = pair
+    first, L = _prefilled(gpu, shape)
+    seq_tok, seq_logits = [], []
+    for _ in range(k + 1):
+        r = gpu.decode_one(0)
+        seq_logits.append(gpu.logits(0)[0])
+        seq_tok.append(r["correction_token"])
+    gpu.rollback(0, L, first)
+    r = gpu.verify(0, seq_tok[:k])
+    assert r["accepted_len"] == k and r["correction_token"] == seq_tok[k]
+    assert r["kv_len"] == L + k + 1 and r["committed"] == k + 1
+    assert np.array_equal(gpu.logits(0), np.stack(seq_logits))
+
+
+def test_wrong_first_candidate(pair):
+    shape, _, gpu = pair
+    first, L = _prefilled(gpu, shape, seed=4)
+    t1 = gpu.decode_one(0)["correction_token"]
+    gpu.rollback(0, L, first)
+    r = gpu.verify(0, [(t1 + 1) % shape.vocab, 5, 6])
+    assert (r["accepted_len"], r["correction_token"], r["kv_len"]) == (0, t1, L + 1)
+
+
+@pytest.mark.parametrize("mode", ["random", "corrupted", "all-wrong"])
+def test_proposals_never_change_the_output(pair, mode):
+    """Proposition (Appendix C.4) on the GPU: any proposal stream commits
+    exactly the target-only token stream."""
+    shape, _, gpu = pair
+    first, L = _prefilled(gpu, shape, seed=5)
+    n = 40
+    y = [first] + [gpu.decode_one(0)["correction_token"] for _ in range(n)]
+    gpu.rollback(0, L, first)
+    rng = np.random.default_rng(11)
+    out = [first]
+    while len(out) <= n:
+        k = min(int(rng.integers(0, 9)), n - len(out))
+        true = y[len(out):len(out) + k]
+        if mode == "random":
+            c = [int(t) for t in rng.integers(0, shape.vocab, k)]
+        elif mode == "all-wrong":
+            c = [(t + 1) % shape.vocab for t in true]
+        else:
+            c = [t if rng.random() > 0.3 else int(rng.integers(0, shape.vocab)) for t in true]
+        r = gpu.verify(0, c)
+        out += c[:r["accepted_len"]] + [r["correction_token"]]
+    assert out[:n + 1] == y
+
+
+def test_incremental_kv_equals_fresh_prefill(pair):
+    """Commit-and-repair (Appendix C.4, requirement 2): after rounds with
+    rejections, the retained cache equals a fresh prefill of the committed
+    prefix, bit for bit, and decoding continues identically."""
+    shape, _, gpu = pair
+    a_or, a_dev, instr = prefix(shape, 60, 4, seed=6)
+    first, L = gpu.prefill(0, a_dev, instr)
+    rng = np.random.default_rng(6)
+    committed = [first]
+    for _ in range(8):
+        c = [int(t) for t in rng.integers(0, shape.vocab, 3)]
+        r = gpu.verify(0, c)
+        committed += c[:r["accepted_len"]] + [r["correction_token"]]
+    kv, root, _ = gpu.state(0)
+    processed = np.array(list(instr) + committed[:-1], dtype=np.int32)
+    first2, kv2 = gpu.prefill(1, a_dev, processed)
+    assert kv2 == kv and first2 == root
+    for l in range(shape.n_layers):
+        k1, v1 = gpu.read_kv(0, l, kv)
+        k2, v2 = gpu.read_kv(1, l, kv)
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    assert gpu.decode_one(0)["correction_token"] == gpu.decode_one(1)["correction_token"]
+
+
+def test_batch_equals_single_requests(pair):
+    """A fused multi-request pass gives each request exactly its
+    single-request result (ragged prefixes, k in {0, 4, 8})."""
+    shape, _, gpu = pair
+    lens = [(70, 5), (129, 3), (33, 1)]
+    ks = [4, 0, 8]
+    states = []
+    for r, (na, ni) in enumerate(lens):
+        states.append(_prefilled(gpu, shape, req=r, n_audio=na, n_instr=ni, seed=7))
+    rng = np.random.default_rng(7)
+    cands = [[int(t) for t in rng.integers(0, shape.vocab, k)] for k in ks]
+    single = []
+    for r in range(3):
+        single.append((gpu.verify(r, cands[r]), gpu.logits(r)))
+        gpu.rollback(r, states[r][1], states[r][0])
+    outs = gpu.verify_batch([0, 1, 2], cands)
+    for r in range(3):
+        assert outs[r] == single[r][0]
+        assert np.array_equal(gpu.logits(r), single[r][1])
+
+
+def test_error_paths(pair):
+    from paper_2609_37617_amd.as2d import (As2dError, ECAPACITY, EINVAL, ESTATE)
+    shape, _, gpu = pair
+    gpu.release(3)
+    with pytest.raises(As2dError) as e:
+        gpu.verify(3, [1, 2])
+    assert e.value.code == ESTATE
+    first, L = _prefilled(gpu, shape, req=2, n_audio=500, n_instr=4)
+    before = gpu.state(2)
+    for bad, code in [(lambda: gpu.verify(2, [1] * 32), EINVAL),          # k > max_k
+                      (lambda: gpu.verify(2, [shape.vocab]), EINVAL),       # token id out of range
+                      (lambda: gpu.verify(2, [-1]), EINVAL),
+                      (lambda: gpu.verify(2, [1] * 8), ECAPACITY),          # 504 + 9 > 512
+                      (lambda: gpu.verify(7, [1]), EINVAL),                 # request id
+                      (lambda: gpu.rollback(2, L + 1, 0), EINVAL),          # beyond kv_len
+                      (lambda: gpu.rollback(2, L - 1, 0), EINVAL),          # into the prefix
+                      (lambda: gpu.verify_batch([2, 2], [[1], [2]]), EINVAL)]:
+        with pytest.raises(As2dError) as e:
+            bad()
+        assert e.value.code == code
+        assert gpu.state(2) == before
+    r = gpu.verify(2, [1] * 7)                                             # 504 + 8 = 512 fits
+    assert r["kv_len"] <= 512
+
+
+def test_non_finite_logits_are_reported():
+    """A NaN planted in the LM head makes the arg-max undefined: the call
+    returns AS2D_ENUMERIC and the request state is unchanged."""
+    from paper_2609_37617_amd import as2d
+    from tests.harness import ensure_built
+    ensure_built()
+    shape = TINY
+    dev = gen.make_weights(shape, 0, fmt="device")
+    dev[-1] = dev[-1].copy()
+    dev[-1][17, 3] = np.nan
+    gpu = as2d.Model(shape, dev, max_requests=1, max_kv_len=256, max_k=4)
+    _, a_dev, instr = prefix(shape, 20, 2)
+    with pytest.raises(as2d.As2dError) as e:
+        gpu.prefill(0, a_dev, instr)
+    assert e.value.code == as2d.ENUMERIC
+    gpu.close()
