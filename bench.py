@@ -1,0 +1,291 @@
+#!/usr/bin/env python3
+"""Throughput of the target verification step on one MI355X.
+
+A step is one verification call (Section 4.2; Appendix C.2): one forward
+pass of the 7B-shaped target over the pending root and k candidates against
+the prefilled audio + instruction + committed KV cache, greedy acceptance,
+correction and KV rollback.  The default workload is the Qwen2-7B-shaped
+decoder (28 layers, hidden 3584, 28/4 heads, FFN 18944, vocab 152064, bf16,
+random weights) with a 750-row audio + 32-token instruction prefix, a
+256-token reply verified at k = 8 with candidate corruption p = 0.3.
+
+Printed: one JSON line with committed tokens/s (`value`), ms per step, the
+step's algorithmic HBM bandwidth and its fraction of the 8 TB/s peak, the
+roofline of the dominant kernel (gate/up GEMM) from HIP events on the
+library's stream, and the float64 CPU oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from workload import configs as wc            # noqa: E402
+from workload import gen                      # noqa: E402
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "committed tokens/sec and verify-step HBM GB/s (% peak), 7B-shape k=8, 1 GPU"
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, help="index of workload.configs.workload")
+    ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--p", type=float, default=None)
+    ap.add_argument("--layers", type=int, default=None, help="(tuning only) override layer count")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one device-to-device copy of this many MiB (a plain copy kernel "
+                         "of known size, for scaling hardware byte counters)")
+    return ap.parse_args()
+
+
+def traffic_from_profiles():
+    """HBM bytes per gate/up launch from committed rocprofv3 counter
+    summaries, if present (profiles/gemm_gate_up_7b_k8_pmc.json)."""
+    p = os.path.join(PROFILES, "gemm_gate_up_7b_k8_pmc.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+        if d.get("kernel_source_sha") != kernel_source_sha():
+            return None
+        return d.get("traffic_bytes_per_launch")
+    except Exception:
+        return None
+
+
+def kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h"):
+        h.update(open(os.path.join(ROOT, "paper_2609_37617_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(shape, n_audio, n_instr, k, mean_committed, seed=0):
+    """The float64 oracle on a bounded sample of the same workload: prefix
+    of n_audio + n_instr rows through the first 2 of the layers (setup, not
+    timed), then one verify step of k candidates through those 2 layers and
+    the LM head (timed), scaled to all layers."""
+    from oracle import OracleModel
+    n_sample = 2
+    sub = shape.with_layers(n_sample)
+    t0 = time.time()
+    w = gen.weights_dict(sub, gen.make_weights(sub, seed))
+    om = OracleModel(sub, w)
+    audio = gen.audio_embeddings(sub, n_audio, seed)
+    instr = gen.instruction_tokens(sub, n_instr, seed)
+    om.prefill(audio, instr)
+    setup = time.time() - t0
+    cands = gen.uniform_int(gen.stream_key(seed, "bench-cpu-cands"), shape.vocab, k)
+    x = om.embed_tokens([om.root] + list(cands))
+    t0 = time.perf_counter()
+    L0 = om.kv_len
+    # layers only (logits of no row), then the LM head on all k + 1 rows
+    om.forward(x, L0, logit_rows=np.array([], dtype=np.int64))
+    t_layers = time.perf_counter() - t0
+    om.kv_len = L0
+    t0 = time.perf_counter()
+    om.verify(cands, k)
+    t_full = time.perf_counter() - t0
+    t_head = max(t_full - t_layers, 0.0)
+    t_step = t_layers * shape.n_layers / n_sample + t_head
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    threads = int(os.environ.get("OPENBLAS_NUM_THREADS", os.environ.get("OMP_NUM_THREADS", cores)))
+    return {"value": mean_committed / t_step, "unit": "tokens/s", "cores": min(cores, threads),
+            "kind": "oracle",
+            "sample": (f"one k={k} verify step of the {shape.name} workload ({n_audio}+{n_instr} prefix) "
+                       f"through {n_sample} of {shape.n_layers} layers plus the LM head, float64 numpy; "
+                       f"layer time scaled x{shape.n_layers}/{n_sample}; committed per step taken from "
+                       f"the GPU run ({mean_committed:.2f}); setup {setup:.1f}s untimed"),
+            "step_seconds": t_step}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+    from paper_2609_37617_amd import as2d
+    if not os.path.exists(as2d.LIB_PATH):
+        from paper_2609_37617_amd import build
+        build.build()
+    wl = wc.workload(args.workload)
+    shape = wl.shape if args.layers is None else wl.shape.with_layers(args.layers)
+    reqs = wl.requests
+    if args.k is not None or args.p is not None:
+        reqs = [wc.Request(r.n_audio, r.n_instr, r.reply_len, args.k if args.k is not None else r.k,
+                           args.p if args.p is not None else r.p) for r in reqs]
+    max_k = max(max(r.k for r in reqs), 1)
+    max_kv = max(r.n_audio + r.n_instr + r.reply_len for r in reqs) + max_k + 2
+    max_kv = (max_kv + 63) // 64 * 64
+    log(f"[bench] workload {wl.name}: {len(reqs)} request(s), shape {shape.name} L={shape.n_layers}")
+    t0 = time.time()
+    dev = gen.make_weights(shape, wl.seed, fmt="device")
+    log(f"[bench] weights generated in {time.time() - t0:.1f}s")
+    t0 = time.time()
+    model = as2d.Model(shape, dev, max_requests=len(reqs), max_kv_len=max_kv, max_k=max_k)
+    del dev
+    log(f"[bench] weights loaded and packed in {time.time() - t0:.1f}s")
+
+    # prefill every request; reference streams from target-only decoding
+    srcs, starts = [], []
+    for i, r in enumerate(reqs):
+        audio = gen.audio_embeddings(shape, r.n_audio, wl.seed, i, fmt="device")
+        instr = gen.instruction_tokens(shape, r.n_instr, wl.seed, i)
+        t0 = time.time()
+        first, L = model.prefill(i, audio, instr)
+        y = [first] + [model.decode_one(i)["correction_token"] for _ in range(r.reply_len)]
+        model.rollback(i, L, first)
+        starts.append((L, first))
+        srcs.append(gen.CandidateSource(y, shape.vocab, r.p, seed=wl.seed, req=i))
+        log(f"[bench] request {i}: prefix {L} rows, reference stream {r.reply_len} tokens "
+            f"({time.time() - t0:.1f}s)")
+
+    done = [0] * len(reqs)        # committed tokens of the current reply pass
+
+    def step():
+        """One verification call over every request with reply left (one
+        fused pass for several requests); returns tokens committed."""
+        ids, cands = [], []
+        for i, r in enumerate(reqs):
+            if done[i] >= r.reply_len:
+                continue
+            k = min(r.k, r.reply_len - done[i] - 1)
+            ids.append(i)
+            cands.append(srcs[i].block(done[i], k))
+        if not ids:
+            for i in range(len(reqs)):
+                model.rollback(i, *starts[i])
+                done[i] = 0
+            return step()
+        outs = model.verify_batch(ids, cands) if len(ids) > 1 else [model.verify(ids[0], cands[0])]
+        got = 0
+        for i, c, o in zip(ids, cands, outs):
+            assert c[:o["accepted_len"]] == srcs[i].ref[done[i] + 1:done[i] + 1 + o["accepted_len"]].tolist()
+            done[i] += o["accepted_len"] + 1
+            got += o["accepted_len"] + 1
+        return got, sum(len(c) + 1 for c in cands), sum(model.state(i)[0] for i in ids)
+
+    if args.calib_copy_mib:
+        import torch
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {args.calib_copy_mib} MiB read + {args.calib_copy_mib} MiB written")
+        del src, dst
+    for _ in range(args.warmup):
+        step()
+    try:
+        import torch
+        sync = torch.cuda.synchronize if torch.cuda.is_available() else (lambda: None)
+    except Exception:
+        sync = lambda: None
+    sync()
+    committed = rows = kvsum = 0
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        c, w, kv = step()
+        committed += c
+        rows += w
+        kvsum += kv
+    sync()
+    elapsed = time.perf_counter() - t0
+    ms = elapsed * 1e3 / args.steps
+    mean_rows = rows / args.steps
+    mean_kv = kvsum / args.steps
+    step_bytes = model.step_bytes(int(round(mean_rows)), int(mean_kv))
+    gbps = step_bytes / (elapsed / args.steps) / 1e9
+    log(f"[bench] {args.steps} steps in {elapsed:.3f}s: {ms:.3f} ms/step, {committed / elapsed:.1f} tok/s, "
+        f"{gbps:.0f} GB/s ({gbps / PEAK_HBM_GBPS:.1%} of peak)")
+
+    roof = None
+    kernel_ms = {}
+    if not args.no_kernel_timing:
+        model.set_timing(True)
+        model.timing_reset()
+        n_t = max(10, args.steps // 2)
+        sync()
+        t1 = time.perf_counter()
+        for _ in range(n_t):
+            step()
+        sync()
+        t_evt = (time.perf_counter() - t1) * 1e3 / n_t
+        model.set_timing(False)
+        for name, (tot, cnt) in model.timing().items():
+            if cnt:
+                kernel_ms[name] = {"avg_us": tot * 1e3 / cnt, "launches": cnt, "total_ms_per_step": tot / n_t}
+        gu = kernel_ms.get("gemm_gate_up")
+        if gu:
+            gu_bytes = 2 * shape.ffn * shape.hidden * (2 if shape.dtype == wc.BF16 else 4)
+            achieved = gu_bytes / (gu["avg_us"] * 1e-6) / 1e9
+            traffic = traffic_from_profiles()
+            roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                    "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
+                    "kernel": "gemm_gate_up", "bytes_per_launch": gu_bytes,
+                    "avg_launch_us": round(gu["avg_us"], 2), "ms_per_step_with_events": round(t_evt, 3)}
+        log("[bench] per-kernel: " + ", ".join(f"{k} {v['avg_us']:.1f}us x{v['launches'] // n_t}"
+                                               for k, v in kernel_ms.items()))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        r0 = reqs[0]
+        t0 = time.time()
+        cpu = cpu_baseline(shape, r0.n_audio, r0.n_instr, r0.k, committed / args.steps)
+        log(f"[bench] cpu baseline {cpu['value']:.3f} tok/s ({time.time() - t0:.1f}s)")
+
+    r0 = reqs[0]
+    out = {
+        "metric": METRIC,
+        "value": round(committed / elapsed, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if shape.dtype == wc.BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": shape.n_layers, "hidden": shape.hidden,
+                   "ffn": shape.ffn, "vocab": shape.vocab, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}",
+                   "requests": len(reqs), "prefix": r0.n_audio + r0.n_instr, "reply_tokens": r0.reply_len,
+                   "k": r0.k, "p": r0.p},
+        "verify_steps_per_s": round(args.steps / elapsed, 2),
+        "mean_committed_per_step": round(committed / args.steps, 3),
+        "step_hbm_bytes": step_bytes,
+        "step_hbm_gbps": round(gbps, 1),
+        "step_hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernels": {k: round(v["avg_us"], 2) for k, v in kernel_ms.items()},
+    }
+    print(json.dumps(out), flush=True)
+    model.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -17,6 +17,10 @@
  *     outputs) during the call; the library copies what it keeps.
  *   - All device memory (packed weights, KV cache slots, scratch) is owned
  *     by the library and released by as2d_free().
+ *   - Number formats: weights are stored in cfg->dtype; the residual
+ *     stream, KV cache, softmax and accumulators are float32, and bf16
+ *     models multiply activations into the weights as bf16 (hi, lo) pairs,
+ *     i.e. to about 17 significant bits.
  *   - A context is used by one host thread at a time.
  *   - Token ids are int32 in [0, vocab).
  *
@@ -80,7 +84,7 @@ typedef struct {
  * bit patterns); norm gains and biases are float32.
  * Shape requirements: head_dim 64 or 128, n_q divisible by n_kv, hidden a
  * multiple of 128, ffn a multiple of 64, vocab a multiple of 128,
- * max_k <= 31.
+ * max_k <= 31, max_kv_len <= 32768, hidden <= 8192.
  * hip_stream: the hipStream_t all work is ordered on (NULL: the library
  * creates its own).  The weights are repacked on the device into the tile
  * order the GEMM kernels stream.
@@ -140,6 +144,11 @@ int as2d_get_logits(as2d_ctx* ctx, int32_t req, float* host, int32_t max_rows, i
 /* Greedy token of every row of `req`'s last call: host[max_rows]. */
 int as2d_get_row_tokens(as2d_ctx* ctx, int32_t req, int32_t* host, int32_t max_rows, int32_t* n_rows);
 
+/* Verification passes are captured once per (rows, requests, keep_logits)
+ * into a HIP graph and replayed (on by default); off runs every kernel
+ * launch eagerly.  Results are identical either way. */
+int as2d_set_graphs(as2d_ctx* ctx, int32_t on);
+
 /* Return `req` to an earlier committed state: prefix length <= kv_len <=
  * current kv_len; root becomes the pending root.  Cache rows past kv_len
  * are ignored and overwritten by later calls. */
@@ -149,7 +158,8 @@ int as2d_rollback(as2d_ctx* ctx, int32_t req, int32_t kv_len, int32_t root);
 int as2d_get_state(as2d_ctx* ctx, int32_t req, int32_t* kv_len, int32_t* root, int32_t* committed);
 
 /* Copy positions 0..n_tok-1 of one layer's cache: host_k, host_v
- * [n_kv][n_tok][head_dim] in cfg->dtype (K after rotation). */
+ * [n_kv][n_tok][head_dim] float32 (K after rotation).  The cache is
+ * float32 for every model dtype. */
 int as2d_read_kv(as2d_ctx* ctx, int32_t req, int32_t layer, void* host_k, void* host_v, int32_t n_tok);
 
 /* Mark a slot free (its state is discarded). */

@@ -31,9 +31,29 @@ Section 5.1): pre-RMSNorm, grouped-query attention with rotary position
 embedding (rotate-half convention), SwiGLU MLP, untied LM head.  The paper
 does not spell these layers out; they are the standard definitions.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 F64 = np.float64
+
+
+def to_f64(a):
+    """float64 copy of an array (a plain cast, done in row blocks on
+    several threads because the matrices are large)."""
+    a = np.asarray(a)
+    if a.dtype == F64:
+        return a
+    out = np.empty(a.shape, dtype=F64)
+    if a.ndim == 0 or a.shape[0] < 64:
+        out[...] = a
+        return out
+    n = min(16, os.cpu_count() or 1)
+    edges = np.linspace(0, a.shape[0], n + 1).astype(int)
+    with ThreadPoolExecutor(n) as ex:
+        list(ex.map(lambda i: np.copyto(out[edges[i]:edges[i + 1]], a[edges[i]:edges[i + 1]]), range(n)))
+    return out
 
 
 def rms_norm(x, gain, eps):
@@ -128,15 +148,15 @@ class OracleModel:
         w = weights
         L = shape.n_layers
         self.embed = w[("embed", -1)]                    # gathered rows are upcast on use
-        self.lm_head = np.asarray(w[("lm_head", -1)], dtype=F64)
-        self.final_norm = np.asarray(w[("final_norm", -1)], dtype=F64)
+        self.lm_head = to_f64(w[("lm_head", -1)])
+        self.final_norm = to_f64(w[("final_norm", -1)])
         self.layers = []
         for l in range(L):
             lw = {}
             for name in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down"):
-                lw[name] = np.asarray(w[(name, l)], dtype=F64)
+                lw[name] = to_f64(w[(name, l)])
             for name in ("bq", "bk", "bv"):
-                lw[name] = np.asarray(w[(name, l)], dtype=F64) if shape.qkv_bias else None
+                lw[name] = to_f64(w[(name, l)]) if shape.qkv_bias else None
             self.layers.append(lw)
         self.reset()
 

@@ -20,7 +20,7 @@ F32, BF16 = 0, 1
 EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_one",
            "as2d_verify_batch", "as2d_set_keep_logits", "as2d_get_logits", "as2d_get_row_tokens",
            "as2d_rollback", "as2d_get_state", "as2d_read_kv", "as2d_release_request",
-           "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_step_bytes",
+           "as2d_set_graphs", "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_step_bytes",
            "as2d_free", "as2d_last_error"]
 
 
@@ -76,6 +76,7 @@ def load_library(path: str = LIB_PATH):
     lib.as2d_get_state.argtypes = [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]
     lib.as2d_read_kv.argtypes = [_P, _I, _I, _P, _P, _I]
     lib.as2d_release_request.argtypes = [_P, _I]
+    lib.as2d_set_graphs.argtypes = [_P, _I]
     lib.as2d_set_timing.argtypes = [_P, _I]
     lib.as2d_timing_read.argtypes = [_P, _P, _P, _P, _I]
     lib.as2d_timing_reset.argtypes = [_P]
@@ -195,14 +196,16 @@ class Model:
 
     def read_kv(self, req: int, layer: int, n_tok: int):
         s = self.shape
-        dt = np.uint16 if s.dtype == BF16 else np.float32
-        k = np.empty((s.n_kv_heads, n_tok, s.head_dim), dtype=dt)
+        k = np.empty((s.n_kv_heads, n_tok, s.head_dim), dtype=np.float32)
         v = np.empty_like(k)
         self._check(self.lib.as2d_read_kv(self.ctx, req, layer, _ptr(k), _ptr(v), n_tok))
         return k, v
 
     def release(self, req: int):
         self._check(self.lib.as2d_release_request(self.ctx, req))
+
+    def set_graphs(self, on: bool):
+        self._check(self.lib.as2d_set_graphs(self.ctx, int(on)))
 
     def set_timing(self, on: bool):
         self._check(self.lib.as2d_set_timing(self.ctx, int(on)))

@@ -11,7 +11,9 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "kernels.h"
@@ -56,13 +58,15 @@ struct as2d_ctx {
   uint4* lm = nullptr;
   GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
 
-  void *kc = nullptr, *vc = nullptr;
+  float *kc = nullptr, *vc = nullptr;  // float32 KV cache
   long long slot_stride = 0, layer_stride = 0;
 
   float *x = nullptr, *q = nullptr, *logits = nullptr, *sumsq = nullptr, *amax_val = nullptr;
   float *part = nullptr, *pacc = nullptr, *pml = nullptr, *rope_cs = nullptr;
-  int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr;
-  void *attn = nullptr, *hbuf = nullptr, *audio = nullptr;
+  int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr, *row_bad = nullptr;
+  int* fin_counters = nullptr;
+  void *xg = nullptr, *attn = nullptr, *hbuf = nullptr, *audio = nullptr;  // activation planes
+  long long xg_plane = 0, attn_plane = 0, h_plane = 0;
   size_t audio_cap = 0;
   int n_chunks_cap = 0;
   int max_rows = 0;
@@ -77,6 +81,10 @@ struct as2d_ctx {
 
   std::vector<ReqState> reqs;
   int keep_logits = 0;
+
+  // captured verify passes: (rows, requests, keep_logits) -> executable graph
+  int use_graphs = 1;
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
 
   int timing = 0;
   double t_ms[K_COUNT] = {};
@@ -124,7 +132,7 @@ GemmPlan make_plan(int N, int K, int KE, int target_wgs) {
   p.KT = K / KE;
   p.groups = N / kGroupCols;
   int ks = (int)std::lround((double)target_wgs / p.groups);
-  ks = std::max(1, std::min(ks, std::max(1, p.KT / 4)));
+  ks = std::max(1, std::min({ks, std::max(1, p.KT / 4), kMaxSplits}));
   p.ktps = (p.KT + ks - 1) / ks;
   p.KS = (p.KT + p.ktps - 1) / p.ktps;
   return p;
@@ -196,6 +204,7 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   a.MT = (M + 15) / 16;
   a.sumsq = c->sumsq;
   a.n_norm_groups = c->cfg.hidden / kGroupCols;
+  a.a_plane = 0;
   a.eps = c->cfg.rms_eps;
   a.part = c->part;
   a.counters = c->counters;
@@ -203,37 +212,31 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   return a;
 }
 
-// One forward pass over the rows and requests already in h_rows / h_reqs:
-// n_att attention requests (h_reqs[0..n_att)), n_fin finish requests
-// (h_reqs[max_requests..max_requests+n_fin)); with_head = run the LM head
-// and verification.
-int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
+// Kernel launches of one forward pass over the rows and requests in the
+// device descriptors: n_att attention requests (d_reqs[0..n_att)), n_fin
+// finish requests (d_reqs[max_requests..)) covering fin_rows rows;
+// with_head = run the LM head and verification.  max_chunks bounds the
+// attention key chunks (chunks past a request's keys exit at once).
+int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool with_head, int max_chunks) {
   const as2d_config& g = c->cfg;
   hipStream_t s = c->stream;
   const bool bf = c->bf16;
   const int mr = g.max_requests;
-  HIP_TRY(c, hipMemcpyAsync(c->d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
-  HIP_TRY(c, hipMemcpyAsync(c->d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
-  int max_chunks = 1;
-  for (int r = 0; r < n_att; ++r) {
-    const int nk = c->h_reqs[r].L0 + c->h_reqs[r].W;
-    max_chunks = std::max(max_chunks, (nk + kAttnChunk - 1) / kAttnChunk);
-  }
-  if (max_chunks > c->n_chunks_cap) return fail(c, AS2D_ECAPACITY, "attention chunks %d > %d", max_chunks, c->n_chunks_cap);
-
   {
     Timed t(c, K_EMBED);
-    HIP_TRY(c, launch_embed(bf, c->d_rows, M, c->embed, c->audio, g.hidden, c->x, c->sumsq, s));
+    HIP_TRY(c, launch_embed(bf, c->d_rows, M, c->embed, c->audio, g.hidden, c->layers[0].g_attn, c->x,
+                            c->sumsq, c->xg, c->xg_plane, s));
   }
-  const int H = g.hidden, d = g.head_dim;
+  const int d = g.head_dim;
   for (int l = 0; l < g.n_layers; ++l) {
     const LayerW& w = c->layers[l];
-    void* kc = (char*)c->kc + (size_t)l * c->layer_stride * c->es;
-    void* vc = (char*)c->vc + (size_t)l * c->layer_stride * c->es;
+    float* kc = c->kc + (size_t)l * c->layer_stride;
+    float* vc = c->vc + (size_t)l * c->layer_stride;
+    const float* g_next = l + 1 < g.n_layers ? c->layers[l + 1].g_attn : c->g_final;
     {
       GemmArgs a = base_args(c, c->p_qkv, w.qkv, M);
-      a.A = c->x;
-      a.gain = w.g_attn;
+      a.A = c->xg;
+      a.a_plane = c->xg_plane;
       a.bias = w.bias;
       a.q_out = c->q;
       a.k_cache = kc;
@@ -264,6 +267,7 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
       a.pml = c->pml;
       a.n_chunks_cap = c->n_chunks_cap;
       a.out = c->attn;
+      a.out_plane = c->attn_plane;
       a.M = M;
       Timed t(c, K_ATTN);
       HIP_TRY(c, launch_attention(bf, a, n_att, max_chunks, s));
@@ -271,24 +275,33 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
     {
       GemmArgs a = base_args(c, c->p_o, w.o, M);
       a.A = c->attn;
+      a.a_plane = c->attn_plane;
       a.x = c->x;
       a.sumsq_out = c->sumsq;
+      a.gain_next = w.g_mlp;
+      a.out = c->xg;
+      a.out_plane = c->xg_plane;
       Timed t(c, K_O);
       HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_RESID, a, s));
     }
     {
       GemmArgs a = base_args(c, c->p_gu, w.gu, M);
-      a.A = c->x;
-      a.gain = w.g_mlp;
-      a.h_out = c->hbuf;
+      a.A = c->xg;
+      a.a_plane = c->xg_plane;
+      a.out = c->hbuf;
+      a.out_plane = c->h_plane;
       Timed t(c, K_GU);
       HIP_TRY(c, launch_gemm(bf, A_NORM, EPI_SWIGLU, a, s));
     }
     {
       GemmArgs a = base_args(c, c->p_down, w.down, M);
       a.A = c->hbuf;
+      a.a_plane = c->h_plane;
       a.x = c->x;
       a.sumsq_out = c->sumsq;
+      a.gain_next = g_next;
+      a.out = c->xg;
+      a.out_plane = c->xg_plane;
       Timed t(c, K_DOWN);
       HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_RESID, a, s));
     }
@@ -296,8 +309,8 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
   if (with_head) {
     {
       GemmArgs a = base_args(c, c->p_lm, c->lm, M);
-      a.A = c->x;
-      a.gain = c->g_final;
+      a.A = c->xg;
+      a.a_plane = c->xg_plane;
       a.logits = c->keep_logits ? c->logits : nullptr;
       a.amax_val = c->amax_val;
       a.amax_idx = c->amax_idx;
@@ -306,9 +319,61 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
     }
     {
       Timed t(c, K_FINISH);
-      HIP_TRY(c, launch_finish(c->d_rows, c->d_reqs + mr, n_fin, c->amax_val, c->amax_idx,
-                               g.vocab / kGroupCols, c->row_tok, c->d_out, s));
+      HIP_TRY(c, launch_finish(c->d_rows, c->d_reqs + mr, n_fin, fin_rows, c->amax_val, c->amax_idx,
+                               g.vocab / kGroupCols, c->row_tok, c->row_bad, c->fin_counters, c->d_out, s));
     }
+  }
+  return AS2D_OK;
+}
+
+// One forward pass over the rows and requests in h_rows / h_reqs (see
+// launch_pass).  Verification passes run as a captured HIP graph, one per
+// (rows, requests, keep_logits); the attention grid then covers the slot
+// capacity so that the graph stays valid as the cache grows.
+int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
+  const as2d_config& g = c->cfg;
+  hipStream_t s = c->stream;
+  const int mr = g.max_requests;
+  int fin_rows = 0;
+  for (int r = 0; r < n_fin; ++r) fin_rows += c->h_reqs[mr + r].W;
+  HIP_TRY(c, hipMemcpyAsync(c->d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(c->d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
+  int max_chunks = 1;
+  for (int r = 0; r < n_att; ++r) {
+    const int nk = c->h_reqs[r].L0 + c->h_reqs[r].W;
+    max_chunks = std::max(max_chunks, (nk + kAttnChunk - 1) / kAttnChunk);
+  }
+  if (max_chunks > c->n_chunks_cap) return fail(c, AS2D_ECAPACITY, "attention chunks %d > %d", max_chunks, c->n_chunks_cap);
+  const bool graph = with_head && c->use_graphs && !c->timing && n_fin == n_att;
+  if (graph) {
+    const auto key = std::make_tuple(M, n_att, c->keep_logits);
+    auto it = c->graphs.find(key);
+    if (it == c->graphs.end()) {
+      if (c->graphs.size() >= 64) {
+        for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
+        c->graphs.clear();
+      }
+      hipGraph_t gr = nullptr;
+      HIP_TRY(c, hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
+      int rc = launch_pass(c, M, n_att, n_fin, fin_rows, true, c->n_chunks_cap);
+      hipError_t e = hipStreamEndCapture(s, &gr);
+      if (rc) {
+        if (gr) hipGraphDestroy(gr);
+        return rc;
+      }
+      if (e != hipSuccess) return fail(c, AS2D_EHIP, "graph capture: %s", hipGetErrorString(e));
+      hipGraphExec_t ex = nullptr;
+      e = hipGraphInstantiate(&ex, gr, nullptr, nullptr, 0);
+      hipGraphDestroy(gr);
+      if (e != hipSuccess) return fail(c, AS2D_EHIP, "graph instantiate: %s", hipGetErrorString(e));
+      it = c->graphs.emplace(key, ex).first;
+    }
+    HIP_TRY(c, hipGraphLaunch(it->second, s));
+  } else {
+    int rc = launch_pass(c, M, n_att, n_fin, fin_rows, with_head, max_chunks);
+    if (rc) return rc;
+  }
+  if (with_head) {
     HIP_TRY(c, hipMemcpyAsync(c->h_out, c->d_out, sizeof(StepOut) * n_fin, hipMemcpyDeviceToHost, s));
     HIP_TRY(c, hipMemcpyAsync(c->h_tok, c->row_tok, sizeof(int) * M, hipMemcpyDeviceToHost, s));
   }
@@ -347,6 +412,7 @@ void as2d_free(as2d_ctx* c) {
   if (c->h_out) hipHostFree(c->h_out);
   if (c->h_tok) hipHostFree(c->h_tok);
   for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
+  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
   if (c->own_stream && c->stream) hipStreamDestroy(c->stream);
   delete c;
 }
@@ -370,8 +436,10 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   if (((g.n_q_heads + 2 * g.n_kv_heads) * g.head_dim) % 128 || (g.n_q_heads * g.head_dim) % 128)
     return bad("attention widths must be multiples of 128");
   if (g.dtype != AS2D_F32 && g.dtype != AS2D_BF16) return bad("dtype must be AS2D_F32 or AS2D_BF16");
-  if (g.max_requests < 1 || g.max_kv_len < 2 || g.max_k < 0 || g.max_k > 31)
-    return bad("capacity: max_requests >= 1, max_kv_len >= 2, 0 <= max_k <= 31");
+  if (g.max_requests < 1 || g.max_kv_len < 2 || g.max_kv_len > kMaxChunks * kAttnChunk || g.max_k < 0 ||
+      g.max_k > 31)
+    return bad("capacity: max_requests >= 1, 2 <= max_kv_len <= 32768, 0 <= max_k <= 31");
+  if (g.hidden > 8192) return bad("hidden must be <= 8192");
   if (!(g.rms_eps >= 0.f) || !(g.rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0 required");
   const int per_layer = g.qkv_bias ? 12 : 9;
   if (n_tensors != 1 + per_layer * g.n_layers + 2) return bad("wrong tensor count for this config");
@@ -472,7 +540,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   // KV cache: [slot][layer][kv_head][pos][d]
   c->layer_stride = (long long)nkv * g.max_kv_len * d;
   c->slot_stride = c->layer_stride * g.n_layers;
-  const size_t kv_bytes = (size_t)c->slot_stride * g.max_requests * c->es;
+  const size_t kv_bytes = (size_t)c->slot_stride * g.max_requests * sizeof(float);
   CK(dalloc(c, &c->kc, kv_bytes));
   CK(dalloc(c, &c->vc, kv_bytes));
 
@@ -482,13 +550,23 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   c->n_chunks_cap = (g.max_kv_len + kAttnChunk - 1) / kAttnChunk;
   CK(dalloc(c, &c->x, (size_t)MR * H * 4));
   CK(dalloc(c, &c->q, (size_t)MR * nq * d * 4));
-  CK(dalloc(c, &c->attn, (size_t)MR * nq * d * c->es));
-  CK(dalloc(c, &c->hbuf, (size_t)MR * F * c->es));
+  // activation planes: two bf16 planes or one float32 plane, 4 bytes per element either way
+  CK(dalloc(c, &c->xg, (size_t)MR * H * 4));
+  CK(dalloc(c, &c->attn, (size_t)MR * nq * d * 4));
+  CK(dalloc(c, &c->hbuf, (size_t)MR * F * 4));
+  if (c->bf16) {
+    c->xg_plane = (long long)MR * H;
+    c->attn_plane = (long long)MR * nq * d;
+    c->h_plane = (long long)MR * F;
+  }
   CK(dalloc(c, &c->logits, (size_t)MR * V * 4));
   CK(dalloc(c, &c->sumsq, (size_t)(H / 128) * MR * 4));
   CK(dalloc(c, &c->amax_val, (size_t)(V / 128) * MR * 4));
   CK(dalloc(c, &c->amax_idx, (size_t)(V / 128) * MR * 4));
   CK(dalloc(c, &c->row_tok, (size_t)MR * 4));
+  CK(dalloc(c, &c->row_bad, (size_t)MR * 4));
+  CK(dalloc(c, &c->fin_counters, (size_t)g.max_requests * 4));
+  HIP_TRY(c, hipMemsetAsync(c->fin_counters, 0, (size_t)g.max_requests * 4, c->stream));
   size_t part_elems = 0;
   for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
     if (p->KS > 1) part_elems = std::max(part_elems, (size_t)p->KS * MR * p->N);
@@ -522,6 +600,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   }
   memset(c->h_reqs, 0, sizeof(ReqDesc) * 2 * g.max_requests);
   c->reqs.assign(g.max_requests, ReqState());
+  c->use_graphs = env_int("AS2D_GRAPHS", 1) != 0;
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return AS2D_OK;
   }();
@@ -741,12 +820,12 @@ int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* ho
   if (layer < 0 || layer >= g.n_layers || n_tok < 0 || n_tok > g.max_kv_len || !host_k || !host_v)
     return fail(c, AS2D_EINVAL, "read_kv: bad arguments");
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  const size_t row = (size_t)g.head_dim * c->es;
+  const size_t row = (size_t)g.head_dim;
   for (int h = 0; h < g.n_kv_heads; ++h) {
-    const size_t src = ((size_t)req * c->slot_stride + (size_t)layer * c->layer_stride +
-                        (size_t)h * g.max_kv_len * g.head_dim) * c->es;
-    HIP_TRY(c, hipMemcpy((char*)host_k + h * n_tok * row, (char*)c->kc + src, n_tok * row, hipMemcpyDeviceToHost));
-    HIP_TRY(c, hipMemcpy((char*)host_v + h * n_tok * row, (char*)c->vc + src, n_tok * row, hipMemcpyDeviceToHost));
+    const size_t src = (size_t)req * c->slot_stride + (size_t)layer * c->layer_stride +
+                       (size_t)h * g.max_kv_len * g.head_dim;
+    HIP_TRY(c, hipMemcpy((float*)host_k + h * n_tok * row, c->kc + src, n_tok * row * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(c, hipMemcpy((float*)host_v + h * n_tok * row, c->vc + src, n_tok * row * 4, hipMemcpyDeviceToHost));
   }
   return AS2D_OK;
 }
@@ -755,6 +834,12 @@ int as2d_release_request(as2d_ctx* c, int32_t req) {
   int rc = check_req(c, req);
   if (rc) return rc;
   c->reqs[req] = ReqState();
+  return AS2D_OK;
+}
+
+int as2d_set_graphs(as2d_ctx* c, int32_t on) {
+  if (!c) return AS2D_EINVAL;
+  c->use_graphs = on ? 1 : 0;
   return AS2D_OK;
 }
 
@@ -789,7 +874,7 @@ int64_t as2d_step_bytes(const as2d_ctx* c, int32_t rows, int64_t kv_keys) {
   const int64_t per_layer = H * (nq + 2 * nkv) * d + nq * d * H + 3 * H * F;
   int64_t b = c->es * (g.n_layers * per_layer + V * H);  // weights, streamed once
   b += c->es * rows * H;                                 // embedding rows
-  b += c->es * g.n_layers * 2 * nkv * d * (kv_keys + rows);  // KV read + append
+  b += 4 * g.n_layers * 2 * nkv * d * (kv_keys + rows);  // float32 KV read + append
   return b;
 }
 

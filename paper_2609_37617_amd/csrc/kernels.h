@@ -1,5 +1,14 @@
 // Internal interface between the C ABI (as2d.cpp) and the gfx950 kernels
 // (kernels.hip).  Not installed; the public interface is include/as2d.h.
+//
+// Number formats.  Weights and the embedding table are stored in the model
+// dtype (bf16 or float32).  Everything else is float32 in value: the
+// residual stream, the KV cache, softmax and all accumulators.  A GEMM
+// operand that is an activation is handed over as "planes": for bf16
+// models two bf16 planes hi = bf16(a), lo = bf16(a - hi) (a = hi + lo to
+// about 2^-17 relative), multiplied into the bf16 weights by two MFMAs;
+// for float32 models a single float32 plane.  Planes are [kMaxRows][K]
+// row-major, the lo plane `plane` elements after the hi plane.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -12,7 +21,9 @@ constexpr int kTilesPerWave = 2;        // 16-column tiles per wave
 constexpr int kGroupCols = kWaves * kTilesPerWave * 16;   // 128 columns per workgroup
 constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
-constexpr int kAttnChunk = 64;          // keys per attention split
+constexpr int kAttnChunk = 32;          // keys per attention split
+constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
+constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
 
 // One processed row of a forward pass.
 struct RowDesc {
@@ -40,11 +51,13 @@ struct GemmArgs {
   const uint4* W;        // packed weight tiles
   int N, K, KT, KS, ktps;
   int M, MT;
-  // A operand
-  const void* A;         // A_PLAIN: element type [M][K]; A_NORM: float [M][K] (residual x)
-  const float* sumsq;    // A_NORM: per-row sum-of-squares partials [n_norm_groups][kMaxRows]
+  // A operand: activation planes [kMaxRows][K].  For A_NORM the planes
+  // hold x * g (residual times RMSNorm gain) and the epilogue multiplies
+  // row m by 1 / sqrt(sum(x^2) / K + eps) from the sum-of-squares partials.
+  const void* A;
+  long long a_plane;
+  const float* sumsq;    // A_NORM: [n_norm_groups][kMaxRows]
   int n_norm_groups;
-  const float* gain;     // A_NORM: RMSNorm gain [K]
   float eps;
   // split-K scratch
   float* part;           // [KS][M][N]
@@ -53,15 +66,17 @@ struct GemmArgs {
   const RowDesc* rows;
   const float* bias;     // EPI_QKV (may be null)
   float* q_out;          // EPI_QKV: [M][n_q*d]
-  void* k_cache;         // EPI_QKV: this layer's K cache, slot stride `slot_stride`
-  void* v_cache;
+  float* k_cache;        // EPI_QKV: this layer's K cache, slot stride `slot_stride`
+  float* v_cache;
   long long slot_stride; // elements between slots
   int kv_cap;            // positions per slot
   int n_q, n_kv, head_dim;
   const float* rope_cs;  // [kv_cap][head_dim/2][2] (cos, sin)
   float* x;              // EPI_RESID: residual [M][N] updated in place
   float* sumsq_out;      // EPI_RESID: [N/128][kMaxRows]
-  void* h_out;           // EPI_SWIGLU: element type [M][N/2]
+  const float* gain_next;// EPI_RESID: RMSNorm gain of the next consumer of x
+  void* out;             // EPI_RESID: planes of x * gain_next; EPI_SWIGLU: planes of h
+  long long out_plane;
   float* logits;         // EPI_ARGMAX: optional [M][N]
   float* amax_val;       // EPI_ARGMAX: [N/128][kMaxRows]
   int* amax_idx;
@@ -69,8 +84,8 @@ struct GemmArgs {
 
 struct AttnArgs {
   const float* q;        // [M][n_q*d]
-  const void* k_cache;   // this layer
-  const void* v_cache;
+  const float* k_cache;  // this layer, float32 [slot][kv_head][pos][d]
+  const float* v_cache;
   long long slot_stride;
   int kv_cap;
   const RowDesc* rows;
@@ -80,20 +95,22 @@ struct AttnArgs {
   float* pacc;           // [n_chunks_cap][kMaxRows][n_q][d]
   float* pml;            // [n_chunks_cap][kMaxRows][n_q][2]
   int n_chunks_cap;
-  void* out;             // element type [M][n_q*d]
+  void* out;             // planes [kMaxRows][n_q*d]
+  long long out_plane;
   int M;
 };
 
-// Launchers (all asynchronous on `s`).  `bf16` selects the element type:
-// true: bf16 stored as uint16 bit patterns; false: float32.
+// Launchers (all asynchronous on `s`).  `bf16` selects the model dtype.
 hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int remap_gate_up,
                        int F, hipStream_t s);
 hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed, const void* audio,
-                        int H, float* x, float* sumsq, hipStream_t s);
+                        int H, const float* gain, float* x, float* sumsq, void* xg, long long xg_plane,
+                        hipStream_t s);
 hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s);
-hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, const float* amax_val,
-                         const int* amax_idx, int n_groups, int* row_tok, StepOut* out, hipStream_t s);
-int gemm_lds_bytes(bool bf16, int MT, int chunk_kt);
+// n_rows = sum of the requests' W; counters: one per request, zero between launches.
+hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,
+                         const float* amax_val, const int* amax_idx, int n_groups, int* row_tok,
+                         int* row_bad, int* counters, StepOut* out, hipStream_t s);
 
 }  // namespace as2d

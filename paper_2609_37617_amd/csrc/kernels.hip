@@ -54,12 +54,52 @@ template <> __device__ __forceinline__ f4 mma_step<false>(uint4 a, uint4 b, f4 a
   return acc;
 }
 
+// Activation planes (see kernels.h): store value v at element i.
+template <bool BF> __device__ __forceinline__ void store_act(void* base, long long plane, size_t i, float v);
+template <> __device__ __forceinline__ void store_act<true>(void* base, long long plane, size_t i, float v) {
+  uint16_t* b = static_cast<uint16_t*>(base);
+  const uint16_t hi = f2bf(v);
+  b[i] = hi;
+  b[i + plane] = f2bf(v - bf2f(hi));
+}
+template <> __device__ __forceinline__ void store_act<false>(void* base, long long, size_t i, float v) {
+  static_cast<float*>(base)[i] = v;
+}
+
+// One k-step of one 16-row A tile: bf16 models carry (hi, lo), float32 one part.
+struct AFrag {
+  uint4 h, l;
+};
+template <bool BF> __device__ __forceinline__ f4 mma_a(const AFrag& a, uint4 b, f4 acc) {
+  if constexpr (BF) {
+    acc = mma_step<true>(a.h, b, acc);
+    acc = mma_step<true>(a.l, b, acc);
+  } else {
+    acc = mma_step<false>(a.h, b, acc);
+  }
+  return acc;
+}
+
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // Streaming (non-temporal) 16-byte load of weight tiles: read once per pass.
 __device__ __forceinline__ uint4 ldw(const uint4* p) {
   const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
+
+// Split-K partials cross workgroups (and XCDs, whose L2s are not coherent
+// with each other) inside one kernel.  They are written and read with
+// agent-scope atomic accesses, which bypass the non-coherent caching, so
+// no fence has to write back or invalidate the whole L2.
+__device__ __forceinline__ void store_partial(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_partial(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until this wave's memory operations, including the partial stores,
+// have been performed.
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Workgroup barrier ordering LDS only: outstanding global loads (the weight
 // prefetch) stay in flight across it.
@@ -139,24 +179,56 @@ hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int
 
 // ---------------------------------------------------------------------------
 // Embedding gather: residual rows x (float32) from token embeddings or audio
-// staging rows, plus per-row sum-of-squares partials over 128-column groups
-// for the first RMSNorm.
+// staging rows, the planes of x * g for the first RMSNorm (gain g), and
+// per-row sum-of-squares partials over 128-column groups.  Each thread
+// moves 8 consecutive elements per pass; every pass's loads are issued
+// before any is used.
 
 template <bool BF>
 __global__ __launch_bounds__(256) void embed_kernel(const RowDesc* __restrict__ rows,
                                                     const typename ET<BF>::T* __restrict__ embed,
                                                     const typename ET<BF>::T* __restrict__ audio,
-                                                    int H, float* __restrict__ x,
-                                                    float* __restrict__ sumsq) {
+                                                    int H, const float* __restrict__ gain,
+                                                    float* __restrict__ x, float* __restrict__ sumsq,
+                                                    void* __restrict__ xg, long long xg_plane) {
+  using T = typename ET<BF>::T;
+  constexpr int kPer = 8, kPasses = 4;   // H <= 256 * 8 * 4
   extern __shared__ float srow[];
   const int m = blockIdx.x;
   const RowDesc rd = rows[m];
-  const typename ET<BF>::T* src =
-      rd.token >= 0 ? embed + (size_t)rd.token * H : audio + (size_t)rd.src * H;
-  for (int c = threadIdx.x; c < H; c += 256) {
-    const float v = to_f(src[c]);
-    x[(size_t)m * H + c] = v;
-    srow[c] = v;
+  const T* src = rd.token >= 0 ? embed + (size_t)rd.token * H : audio + (size_t)rd.src * H;
+  float v[kPasses][kPer];
+#pragma unroll
+  for (int ps = 0; ps < kPasses; ++ps) {
+    const int c0 = (ps * 256 + threadIdx.x) * kPer;
+    if (c0 < H) {
+      if constexpr (BF) {
+        const uint4 u = *reinterpret_cast<const uint4*>(src + c0);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          v[ps][2 * t] = bf2f(w[t] & 0xffffu);
+          v[ps][2 * t + 1] = bf2f(w[t] >> 16);
+        }
+      } else {
+        const float4 a = *reinterpret_cast<const float4*>(src + c0);
+        const float4 b = *reinterpret_cast<const float4*>(src + c0 + 4);
+        v[ps][0] = a.x; v[ps][1] = a.y; v[ps][2] = a.z; v[ps][3] = a.w;
+        v[ps][4] = b.x; v[ps][5] = b.y; v[ps][6] = b.z; v[ps][7] = b.w;
+      }
+    }
+  }
+#pragma unroll
+  for (int ps = 0; ps < kPasses; ++ps) {
+    const int c0 = (ps * 256 + threadIdx.x) * kPer;
+    if (c0 < H) {
+#pragma unroll
+      for (int t = 0; t < kPer; ++t) {
+        x[(size_t)m * H + c0 + t] = v[ps][t];
+        store_act<BF>(xg, xg_plane, (size_t)m * H + c0 + t, v[ps][t] * gain[c0 + t]);
+        srow[c0 + t] = v[ps][t];
+      }
+    }
   }
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -168,14 +240,16 @@ __global__ __launch_bounds__(256) void embed_kernel(const RowDesc* __restrict__ 
 }
 
 hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed, const void* audio,
-                        int H, float* x, float* sumsq, hipStream_t s) {
+                        int H, const float* gain, float* x, float* sumsq, void* xg, long long xg_plane,
+                        hipStream_t s) {
+  if (H > 256 * 8 * 4 || H % 128) return hipErrorInvalidValue;
   const size_t lds = (size_t)H * sizeof(float);
   if (bf16)
-    embed_kernel<true><<<M, 256, lds, s>>>(rows, (const uint16_t*)embed, (const uint16_t*)audio, H,
-                                           x, sumsq);
+    embed_kernel<true><<<M, 256, lds, s>>>(rows, (const uint16_t*)embed, (const uint16_t*)audio, H, gain,
+                                           x, sumsq, xg, xg_plane);
   else
-    embed_kernel<false><<<M, 256, lds, s>>>(rows, (const float*)embed, (const float*)audio, H, x,
-                                            sumsq);
+    embed_kernel<false><<<M, 256, lds, s>>>(rows, (const float*)embed, (const float*)audio, H, gain, x,
+                                            sumsq, xg, xg_plane);
   return hipGetLastError();
 }
 
@@ -183,42 +257,40 @@ hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed
 // Weight-streaming GEMM  Y[M][N] = A[M][K] * W[N][K]^T  for small M.
 //
 // Workgroup = 4 waves over one 128-column group and one k-split; wave w
-// owns the tile pair 4*group + w.  A (all M rows of the split's K range,
-// converted to the element type, RMSNorm applied when AM == A_NORM) is
-// staged in LDS; the weight tiles stream from HBM with a U-deep register
-// prefetch, one 1 KiB fully coalesced load per tile and k-step.  With
-// KS > 1 each split writes a float32 partial and the last workgroup to
-// finish a column group (device-scope counter) sums the partials in split
-// order and runs the fused epilogue.
+// owns the tile pair 4*group + w.  Each k-step a wave loads its two 1 KiB
+// weight tiles (fully coalesced, non-temporal) and the A fragments of the
+// same k-step, U steps ahead of their use.  Up to two 16-row tiles of A
+// come straight from the L2-resident activation planes; larger M stages A
+// through LDS in chunks.  Both paths issue the same MFMA sequence per row,
+// so a row's result does not depend on M.  With KS > 1 each split writes a
+// float32 partial and the last workgroup of a column group (device-scope
+// counter) sums the partials in split order and runs the fused epilogue.
 
 constexpr int kPrefetch = 4;
 constexpr int kFStride = 132;      // floats per row of the epilogue tile
 constexpr int kFRows = 64;         // rows per epilogue pass
+constexpr int kDirectMT = 2;       // largest M-tile count loading A directly
+constexpr int kLdsBudget = 61440;  // bytes of A staging
+constexpr int kFixupBatch = 1;     // elements per thread with loads in flight in the split-K fixup
 
 __host__ __device__ inline int lds_row_stride(int chunk_kt) {
   return ((chunk_kt * 64 + 127) / 128) * 128 + 16;
 }
 
-int gemm_lds_bytes(bool, int MT, int chunk_kt) {
-  const int a = MT * 16 * lds_row_stride(chunk_kt);
-  const int f = kFRows * kFStride * 4;
-  return a > f ? a : f;
-}
-
 template <bool BF, int EPI>
-__device__ void epilogue_rows(const GemmArgs& p, const float* F, int group, int r0, int r1) {
-  using T = typename ET<BF>::T;
+__device__ void epilogue_rows(const GemmArgs& p, float* F, int group, int r0, int r1) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int N = p.N;
   if constexpr (EPI == EPI_RESID) {
-    // x += Y; then the sum of squares of the new x over this group's columns
-    float* Fw = const_cast<float*>(F);
+    // x += Y; planes of x * g for the next RMSNorm; sum of squares of x
     for (int idx = tid; idx < (r1 - r0) * 128; idx += 256) {
       const int m = r0 + (idx >> 7), c = idx & 127;
-      const size_t o = (size_t)m * N + group * 128 + c;
-      const float v = p.x[o] + Fw[(m - r0) * kFStride + c];
+      const int n = group * 128 + c;
+      const size_t o = (size_t)m * N + n;
+      const float v = p.x[o] + F[(m - r0) * kFStride + c];
       p.x[o] = v;
-      Fw[(m - r0) * kFStride + c] = v;
+      store_act<BF>(p.out, p.out_plane, o, v * p.gain_next[n]);
+      F[(m - r0) * kFStride + c] = v;
     }
     lds_sync();
     for (int m = r0 + wave; m < r1; m += 4) {
@@ -227,12 +299,11 @@ __device__ void epilogue_rows(const GemmArgs& p, const float* F, int group, int 
       if (lane == 0) p.sumsq_out[group * kMaxRows + m] = s;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    T* h = (T*)p.h_out;
     const int F2 = N / 2;
     for (int idx = tid; idx < (r1 - r0) * 64; idx += 256) {
       const int m = r0 + (idx >> 6), c = idx & 63;
       const float g = F[(m - r0) * kFStride + c], u = F[(m - r0) * kFStride + 64 + c];
-      h[(size_t)m * F2 + group * 64 + c] = from_f<BF>(g / (1.0f + expf(-g)) * u);
+      store_act<BF>(p.out, p.out_plane, (size_t)m * F2 + group * 64 + c, g / (1.0f + expf(-g)) * u);
     }
   } else if constexpr (EPI == EPI_QKV) {
     const int d = p.head_dim, half = d >> 1;
@@ -256,15 +327,11 @@ __device__ void epilogue_rows(const GemmArgs& p, const float* F, int group, int 
           p.q_out[(size_t)m * q_cols + n] = v;
         } else {
           const int kvh = (n - q_cols) / d;
-          T* kc = (T*)p.k_cache + (size_t)rd.slot * p.slot_stride +
-                  ((size_t)kvh * p.kv_cap + rd.pos) * d + dd;
-          *kc = from_f<BF>(v);
+          p.k_cache[(size_t)rd.slot * p.slot_stride + ((size_t)kvh * p.kv_cap + rd.pos) * d + dd] = v;
         }
       } else {
         const int kvh = (n - qk_cols) / d;
-        T* vc = (T*)p.v_cache + (size_t)rd.slot * p.slot_stride +
-                ((size_t)kvh * p.kv_cap + rd.pos) * d + dd;
-        *vc = from_f<BF>(v);
+        p.v_cache[(size_t)rd.slot * p.slot_stride + ((size_t)kvh * p.kv_cap + rd.pos) * d + dd] = v;
       }
     }
   } else {  // EPI_ARGMAX
@@ -293,6 +360,8 @@ template <bool BF, int MT, int AM, int EPI>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int chunk_kt) {
   using T = typename ET<BF>::T;
   constexpr int PER16 = ET<BF>::PER16;
+  constexpr int KE = 4 * PER16;           // elements per k-step
+  constexpr bool kDirect = MT <= kDirectMT;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_last;
@@ -301,17 +370,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int c
   const int group = blockIdx.x / p.KS, split = blockIdx.x - group * p.KS;
   const int kt0 = split * p.ktps;
   const int kt1 = min(p.KT, kt0 + p.ktps);
-  const int M = p.M;
-  const int stride = lds_row_stride(chunk_kt);
-
-  if constexpr (AM == A_NORM) {
-    for (int m = tid; m < M; m += 256) {
-      float ss = 0.0f;
-      for (int g = 0; g < p.n_norm_groups; ++g) ss += p.sumsq[g * kMaxRows + m];
-      s_scale[m] = 1.0f / sqrtf(ss / (float)p.K + p.eps);
-    }
-    __syncthreads();
-  }
+  const int M = p.M, K = p.K;
 
   f4 acc[MT][2];
 #pragma unroll
@@ -320,80 +379,130 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int c
     acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
   }
   const uint4* wp = p.W + (size_t)(group * kWaves + wave) * p.KT * 128 + lane;
-  const unsigned char* abase = smem + (lane & 15) * stride + (lane >> 4) * 16;
+  auto step = [&](const uint4(&bb)[2], const AFrag(&af)[MT]) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      acc[mt][0] = mma_a<BF>(af[mt], bb[0], acc[mt][0]);
+      acc[mt][1] = mma_a<BF>(af[mt], bb[1], acc[mt][1]);
+    }
+  };
 
-  for (int c0 = kt0; c0 < kt1; c0 += chunk_kt) {
-    const int c1 = min(kt1, c0 + chunk_kt);
-    const int n = c1 - c0;
-    if (c0 != kt0) lds_sync();
-    // stage A rows [0, 16 MT) x k-steps [c0, c1) as 16-byte units
-    const int units = MT * 16 * n * 4;
-    for (int u = tid; u < units; u += 256) {
-      const int m = u / (n * 4), r = u - m * (n * 4);
-      const int k = (c0 + (r >> 2)) * (4 * PER16) + (r & 3) * PER16;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (m < M) {
-        if constexpr (AM == A_PLAIN) {
-          val = *reinterpret_cast<const uint4*>((const T*)p.A + (size_t)m * p.K + k);
-        } else {
-          const float* xr = (const float*)p.A + (size_t)m * p.K + k;
-          const float sc = s_scale[m];
-          T e[PER16];
-#pragma unroll
-          for (int t = 0; t < PER16; ++t) e[t] = from_f<BF>(xr[t] * sc * p.gain[k + t]);
-          val = *reinterpret_cast<const uint4*>(e);
-        }
-      }
-      *reinterpret_cast<uint4*>(smem + m * stride + (r >> 2) * 64 + (r & 3) * 16) = val;
-    }
-    // weight prefetch for the first k-steps of this chunk (unconditional, so
-    // the load order is the same on every path into the loop below)
-    uint4 b[kPrefetch][2];
-#pragma unroll
-    for (int u = 0; u < kPrefetch; ++u) {
-      const size_t kp = (size_t)(c0 + min(u, n - 1)) * 128;
-      b[u][0] = ldw(wp + kp);
-      b[u][1] = ldw(wp + kp + 64);
-    }
-    lds_sync();
-    auto step = [&](const uint4(&bb)[2], int ks) {
+  if constexpr (kDirect) {
+    // A fragments straight from the activation planes (rows >= M read
+    // stale data that only reaches output rows that are never stored)
+    const T* abase = (const T*)p.A + (size_t)(lane & 15) * K + (lane >> 4) * PER16;
+    auto load = [&](int kt, uint4(&bb)[2], AFrag(&af)[MT]) {
+      bb[0] = ldw(wp + (size_t)kt * 128);
+      bb[1] = ldw(wp + (size_t)kt * 128 + 64);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const uint4 a = *reinterpret_cast<const uint4*>(abase + mt * 16 * stride + ks * 64);
-        acc[mt][0] = mma_step<BF>(a, bb[0], acc[mt][0]);
-        acc[mt][1] = mma_step<BF>(a, bb[1], acc[mt][1]);
+        const T* a = abase + (size_t)mt * 16 * K + (size_t)kt * KE;
+        af[mt].h = *reinterpret_cast<const uint4*>(a);
+        if constexpr (BF) af[mt].l = *reinterpret_cast<const uint4*>(a + p.a_plane);
       }
     };
-    // steady state: every refill is in range, so the loop body has no
-    // branches and the prefetch depth holds across iterations
+    const int n = kt1 - kt0;
+    uint4 b[kPrefetch][2];
+    AFrag af[kPrefetch][MT];
+#pragma unroll
+    for (int u = 0; u < kPrefetch; ++u) load(kt0 + min(u, n - 1), b[u], af[u]);
     int i = 0;
     for (; i + 2 * kPrefetch <= n; i += kPrefetch) {
 #pragma unroll
       for (int u = 0; u < kPrefetch; ++u) {
-        step(b[u], i + u);
-        const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
-        b[u][0] = ldw(wp + kn);
-        b[u][1] = ldw(wp + kn + 64);
+        step(b[u], af[u]);
+        load(kt0 + i + u + kPrefetch, b[u], af[u]);
       }
     }
-    // tail: at most 2 * kPrefetch - 1 steps left
 #pragma unroll
     for (int u = 0; u < kPrefetch; ++u) {
       if (i + u < n) {
-        step(b[u], i + u);
-        if (i + u + kPrefetch < n) {
-          const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
-          b[u][0] = ldw(wp + kn);
-          b[u][1] = ldw(wp + kn + 64);
-        }
+        step(b[u], af[u]);
+        if (i + u + kPrefetch < n) load(kt0 + i + u + kPrefetch, b[u], af[u]);
       }
     }
     i += kPrefetch;
 #pragma unroll
     for (int u = 0; u < kPrefetch; ++u)
-      if (i + u < n) step(b[u], i + u);
+      if (i + u < n) step(b[u], af[u]);
+  } else {
+    // stage the A planes of `chunk_kt` k-steps in LDS (hi region, then lo)
+    constexpr int kRegions = BF ? 2 : 1;
+    const int stride = lds_row_stride(chunk_kt);
+    const int region = MT * 16 * stride;
+    const unsigned char* lbase = smem + (lane & 15) * stride + (lane >> 4) * 16;
+    for (int c0 = kt0; c0 < kt1; c0 += chunk_kt) {
+      const int c1 = min(kt1, c0 + chunk_kt);
+      const int n = c1 - c0;
+      if (c0 != kt0) lds_sync();
+      const int units = kRegions * MT * 16 * n * 4;
+      for (int u = tid; u < units; u += 256) {
+        const int rg = u / (MT * 16 * n * 4);
+        const int r2 = u - rg * (MT * 16 * n * 4);
+        const int m = r2 / (n * 4), r = r2 - m * (n * 4);
+        const size_t e = (size_t)m * K + (size_t)(c0 + (r >> 2)) * KE + (r & 3) * PER16 + rg * p.a_plane;
+        *reinterpret_cast<uint4*>(smem + rg * region + m * stride + (r >> 2) * 64 + (r & 3) * 16) =
+            *reinterpret_cast<const uint4*>((const T*)p.A + e);
+      }
+      uint4 b[kPrefetch][2];
+#pragma unroll
+      for (int u = 0; u < kPrefetch; ++u) {
+        const size_t kp = (size_t)(c0 + min(u, n - 1)) * 128;
+        b[u][0] = ldw(wp + kp);
+        b[u][1] = ldw(wp + kp + 64);
+      }
+      lds_sync();
+      auto lds_a = [&](int ks, AFrag(&af)[MT]) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          af[mt].h = *reinterpret_cast<const uint4*>(lbase + mt * 16 * stride + ks * 64);
+          if constexpr (BF) af[mt].l = *reinterpret_cast<const uint4*>(lbase + region + mt * 16 * stride + ks * 64);
+        }
+      };
+      int i = 0;
+      for (; i + 2 * kPrefetch <= n; i += kPrefetch) {
+#pragma unroll
+        for (int u = 0; u < kPrefetch; ++u) {
+          AFrag af[MT];
+          lds_a(i + u, af);
+          step(b[u], af);
+          const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
+          b[u][0] = ldw(wp + kn);
+          b[u][1] = ldw(wp + kn + 64);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPrefetch; ++u) {
+        if (i + u < n) {
+          AFrag af[MT];
+          lds_a(i + u, af);
+          step(b[u], af);
+          if (i + u + kPrefetch < n) {
+            const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
+            b[u][0] = ldw(wp + kn);
+            b[u][1] = ldw(wp + kn + 64);
+          }
+        }
+      }
+      i += kPrefetch;
+#pragma unroll
+      for (int u = 0; u < kPrefetch; ++u) {
+        if (i + u < n) {
+          AFrag af[MT];
+          lds_a(i + u, af);
+          step(b[u], af);
+        }
+      }
+    }
   }
 
+  if constexpr (AM == A_NORM) {
+    for (int m = tid; m < M; m += 256) {
+      float ss = 0.0f;
+      for (int g = 0; g < p.n_norm_groups; ++g) ss += p.sumsq[g * kMaxRows + m];
+      s_scale[m] = 1.0f / sqrtf(ss / (float)K + p.eps);
+    }
+  }
   float* F = reinterpret_cast<float*>(smem);
   if (p.KS > 1) {
     // publish this split's partial, then let the last split of the group reduce
@@ -405,29 +514,51 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int c
         for (int i = 0; i < 4; ++i) {
           const int row = mt * 16 + (lane >> 4) * 4 + i;
           const int col = group * 128 + (wave * 2 + j) * 16 + (lane & 15);
-          if (row < M) p.part[((size_t)split * M + row) * p.N + col] = acc[mt][j][i];
+          if (row < M) store_partial(&p.part[((size_t)split * M + row) * p.N + col], acc[mt][j][i]);
         }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_last = atomicAdd(&p.counters[group], 1) == p.KS - 1;
+    wait_vmem();
+    __syncthreads();  // every wave's partial stores are performed
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(&p.counters[group], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               p.KS - 1;
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
-    if (tid == 0) p.counters[group] = 0;
+    if (tid == 0) p.counters[group] = 0;  // ready for the next launch
     for (int r0 = 0; r0 < M; r0 += kFRows) {
       const int r1 = min(M, r0 + kFRows);
-      for (int idx = tid; idx < (r1 - r0) * 128; idx += 256) {
-        const int m = r0 + (idx >> 7), c = idx & 127;
-        float s = 0.0f;
-        for (int sp = 0; sp < p.KS; ++sp) s += p.part[((size_t)sp * M + m) * p.N + group * 128 + c];
-        F[(m - r0) * kFStride + c] = s;
+      // every load of a batch of elements is issued before any is summed;
+      // each element is still summed in split order
+      const int nel = (r1 - r0) * 128;
+      for (int e0 = 0; e0 < nel; e0 += 256 * kFixupBatch) {
+        float v[kFixupBatch][kMaxSplits];
+#pragma unroll
+        for (int b = 0; b < kFixupBatch; ++b) {
+          const int idx = e0 + b * 256 + tid;
+          const int m = r0 + (idx >> 7), c = idx & 127;
+#pragma unroll
+          for (int sp = 0; sp < kMaxSplits; ++sp)
+            if (idx < nel && sp < p.KS)
+              v[b][sp] = load_partial(&p.part[((size_t)sp * M + m) * p.N + group * 128 + c]);
+        }
+#pragma unroll
+        for (int b = 0; b < kFixupBatch; ++b) {
+          const int idx = e0 + b * 256 + tid;
+          if (idx < nel) {
+            const int m = r0 + (idx >> 7), c = idx & 127;
+            float sum = 0.0f;
+#pragma unroll
+            for (int sp = 0; sp < kMaxSplits; ++sp)
+              if (sp < p.KS) sum += v[b][sp];
+            F[(m - r0) * kFStride + c] = AM == A_NORM ? sum * s_scale[m] : sum;
+          }
+        }
       }
       lds_sync();
       epilogue_rows<BF, EPI>(p, F, group, r0, r1);
       lds_sync();
     }
   } else {
-    lds_sync();  // A tiles no longer read
+    __syncthreads();  // A tiles no longer read; s_scale written
     for (int r0 = 0; r0 < M; r0 += kFRows) {
       const int r1 = min(M, r0 + kFRows);
 #pragma unroll
@@ -438,7 +569,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int c
           for (int i = 0; i < 4; ++i) {
             const int row = mt * 16 + (lane >> 4) * 4 + i;
             const int col = (wave * 2 + j) * 16 + (lane & 15);
-            if (row >= r0 && row < r1) F[(row - r0) * kFStride + col] = acc[mt][j][i];
+            if (row >= r0 && row < r1)
+              F[(row - r0) * kFStride + col] = AM == A_NORM ? acc[mt][j][i] * s_scale[row] : acc[mt][j][i];
           }
       lds_sync();
       epilogue_rows<BF, EPI>(p, F, group, r0, r1);
@@ -449,9 +581,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int c
 
 template <bool BF, int AM, int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
+  const int regions = BF ? 2 : 1;
   int chunk = a.ktps;
-  while (chunk > 1 && a.MT * 16 * lds_row_stride(chunk) > 61440) --chunk;
-  const int lds = gemm_lds_bytes(BF, a.MT, chunk);
+  while (chunk > 1 && regions * a.MT * 16 * lds_row_stride(chunk) > kLdsBudget) --chunk;
+  int lds = kFRows * kFStride * 4;
+  if (a.MT > kDirectMT) lds = max(lds, regions * a.MT * 16 * lds_row_stride(chunk));
   const dim3 grid((a.N / kGroupCols) * a.KS), block(256);
   switch (a.MT) {
 #define AS2D_MT(mt) \
@@ -477,67 +611,104 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // ---------------------------------------------------------------------------
 // Block-causal grouped-query attention, split over the key axis.
 //
-// Workgroup (chunk c, query head h, request r): keys [64c, 64c + 64) of the
-// request's cache slot are staged in LDS; each wave takes the request's rows
-// in turn and computes, for a row at position pos >= 64c, the chunk's
+// Workgroup (chunk c, query head h, request r): keys [32c, 32c + 32) of the
+// request's float32 cache slot are staged in LDS; each wave takes the
+// request's rows in turn (the next row's query is prefetched into
+// registers).  For a row at position pos >= 32c it computes the chunk's
 // softmax statistics (max m, sum l of exp(s - m)) and the unnormalised
-// output sum_j exp(s_j - m) v_j over keys j <= pos.  The merge kernel
-// combines the chunks of a row in ascending order.
+// output sum_j exp(s_j - m) v_j over keys j <= pos; lane pairs (j, j + 32)
+// each take half of the dot product of key j.  The merge kernel combines a
+// row's chunks in ascending order.
 
 template <bool BF, int D>
 __global__ __launch_bounds__(256) void attn_chunk_kernel(const AttnArgs p) {
-  using T = typename ET<BF>::T;
-  constexpr int RS = BF ? D + 2 : D + 1;  // LDS row stride (elements): odd dword stride
+  constexpr int C = kAttnChunk;
+  constexpr int RS = D + 1;                   // odd LDS row stride (floats)
+  constexpr int V4 = C * D / 4 / 256;         // float4 loads per thread per matrix
+  constexpr int QL = D / 64;                  // query elements per lane
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  T* Ks = reinterpret_cast<T*>(smem);
-  T* Vs = Ks + 64 * RS;
-  float* qs = reinterpret_cast<float*>(smem + ((2 * 64 * RS * sizeof(T) + 15) / 16) * 16);
+  float* Ks = reinterpret_cast<float*>(smem);
+  float* Vs = Ks + C * RS;
+  float* qs = Vs + C * RS;
   float* ps = qs + 4 * D;
 
   const int c = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
   const ReqDesc rq = p.reqs[r];
   const int nkeys = rq.L0 + rq.W;
-  const int key0 = c * kAttnChunk;
+  const int key0 = c * C;
   if (key0 >= nkeys) return;
-  const int nk = min(kAttnChunk, nkeys - key0);
+  const int nk = min(C, nkeys - key0);
   const int g = h * p.n_kv / p.n_q;
   const int qcols = p.n_q * D;
-  const T* kb = (const T*)p.k_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
-  const T* vb = (const T*)p.v_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
-  for (int idx = threadIdx.x; idx < nk * D; idx += 256) {
-    const int j = idx / D, dd = idx - j * D;
-    Ks[j * RS + dd] = kb[idx];
-    Vs[j * RS + dd] = vb[idx];
+  const float* kb = p.k_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
+  const float* vb = p.v_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
+  {
+    float4 kv[V4], vv[V4];
+#pragma unroll
+    for (int t = 0; t < V4; ++t) {
+      const int f = (t * 256 + threadIdx.x) * 4;   // element index in the chunk
+      if (f < nk * D) {
+        kv[t] = *reinterpret_cast<const float4*>(kb + f);
+        vv[t] = *reinterpret_cast<const float4*>(vb + f);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < V4; ++t) {
+      const int f = (t * 256 + threadIdx.x) * 4;
+      if (f < nk * D) {
+        const int j = f / D, dd = f - j * D;
+        float* kd = Ks + j * RS + dd;
+        float* vd = Vs + j * RS + dd;
+        kd[0] = kv[t].x; kd[1] = kv[t].y; kd[2] = kv[t].z; kd[3] = kv[t].w;
+        vd[0] = vv[t].x; vd[1] = vv[t].y; vd[2] = vv[t].z; vd[3] = vv[t].w;
+      }
+    }
   }
-  __syncthreads();
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j = lane & (C - 1), half = lane >> 5;
   float* qw = qs + wave * D;
-  float* pw = ps + wave * 64;
-  for (int i = wave; i < rq.W; i += 4) {
+  float* pw = ps + wave * C;
+  // first row of this wave at or after the chunk start
+  int i = wave;
+  while (i < rq.W && rq.L0 + i < key0) i += 4;
+  float qn[QL];
+  if (i < rq.W) {
+#pragma unroll
+    for (int t = 0; t < QL; ++t) qn[t] = p.q[(size_t)(rq.row_start + i) * qcols + h * D + t * 64 + lane];
+  }
+  __syncthreads();
+  for (; i < rq.W; i += 4) {
     const int pos = rq.L0 + i;
-    if (pos < key0) continue;
     const int row = rq.row_start + i;
-    for (int dd = lane; dd < D; dd += 64) qw[dd] = p.q[(size_t)row * qcols + h * D + dd];
-    __builtin_amdgcn_wave_barrier();
-    const bool valid = lane < nk && key0 + lane <= pos;
-    float s = -INFINITY;
-    if (valid) {
-      float a = 0.0f;
-      const T* kr = Ks + lane * RS;
-#pragma unroll 8
-      for (int dd = 0; dd < D; ++dd) a += qw[dd] * to_f(kr[dd]);
-      s = a * p.scale;
+#pragma unroll
+    for (int t = 0; t < QL; ++t) qw[t * 64 + lane] = qn[t];
+    if (i + 4 < rq.W) {
+#pragma unroll
+      for (int t = 0; t < QL; ++t) qn[t] = p.q[(size_t)(row + 4) * qcols + h * D + t * 64 + lane];
     }
+    __builtin_amdgcn_wave_barrier();
+    const bool valid = j < nk && key0 + j <= pos;
+    float a = 0.0f;
+    if (j < nk) {
+      const float* kr = Ks + j * RS + half * (D / 2);
+      const float* qh = qw + half * (D / 2);
+#pragma unroll 8
+      for (int dd = 0; dd < D / 2; ++dd) a += qh[dd] * kr[dd];
+    }
+    a += __shfl_xor(a, 32);  // both halves: same sum (commutative)
+    const float s = valid ? a * p.scale : -INFINITY;
     const float mx = wave_max(s);
     const float pj = valid ? expf(s - mx) : 0.0f;
-    const float l = wave_sum(pj);
-    pw[lane] = pj;
+    const float l = wave_sum(half == 0 ? pj : 0.0f);
+    if (half == 0) pw[j] = pj;
     __builtin_amdgcn_wave_barrier();
-    for (int dd = lane; dd < D; dd += 64) {
-      float a = 0.0f;
-      for (int j = 0; j < nk; ++j) a += pw[j] * to_f(Vs[j * RS + dd]);
-      p.pacc[(((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd] = a;
+#pragma unroll
+    for (int t = 0; t < QL; ++t) {
+      const int dd = t * 64 + lane;
+      float o = 0.0f;
+      for (int jj = 0; jj < nk; ++jj) o += pw[jj] * Vs[jj * RS + dd];
+      p.pacc[(((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd] = o;
     }
     if (lane == 0) {
       p.pml[(((size_t)c * kMaxRows + row) * p.n_q + h) * 2] = mx;
@@ -547,29 +718,48 @@ __global__ __launch_bounds__(256) void attn_chunk_kernel(const AttnArgs p) {
   }
 }
 
+// Merge of a row's chunks (workgroup per (head, row), thread per output
+// dimension): chunk weights exp(m_c - max m) go through LDS, then each
+// thread sums its dimension over the chunks in ascending order with the
+// loads issued in batches.
 template <bool BF, int D>
-__global__ void attn_merge_kernel(const AttnArgs p) {
-  using T = typename ET<BF>::T;
+__global__ __launch_bounds__(D) void attn_merge_kernel(const AttnArgs p) {
+  constexpr int kB = 8;
+  __shared__ float sm[kMaxChunks], sl[kMaxChunks];
   const int h = blockIdx.x, row = blockIdx.y, dd = threadIdx.x;
   const RowDesc rd = p.rows[row];
   const int nc = rd.pos / kAttnChunk + 1;
-  float mx = -INFINITY;
-  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, p.pml[(((size_t)c * kMaxRows + row) * p.n_q + h) * 2]);
-  float L = 0.0f, a = 0.0f;
-  for (int c = 0; c < nc; ++c) {
+  for (int c = dd; c < nc; c += D) {
     const size_t o = ((size_t)c * kMaxRows + row) * p.n_q + h;
-    const float w = expf(p.pml[o * 2] - mx);
-    L += p.pml[o * 2 + 1] * w;
-    a += p.pacc[o * D + dd] * w;
+    sm[c] = p.pml[o * 2];
+    sl[c] = p.pml[o * 2 + 1];
   }
-  ((T*)p.out)[(size_t)row * p.n_q * D + h * D + dd] = from_f<BF>(a / L);
+  __syncthreads();
+  float mx = -INFINITY;
+  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, sm[c]);
+  __syncthreads();
+  for (int c = dd; c < nc; c += D) sm[c] = expf(sm[c] - mx);
+  __syncthreads();
+  float L = 0.0f, a = 0.0f;
+  for (int c0 = 0; c0 < nc; c0 += kB) {
+    float v[kB];
+#pragma unroll
+    for (int b = 0; b < kB; ++b)
+      if (c0 + b < nc) v[b] = p.pacc[(((size_t)(c0 + b) * kMaxRows + row) * p.n_q + h) * D + dd];
+#pragma unroll
+    for (int b = 0; b < kB; ++b)
+      if (c0 + b < nc) {
+        L += sl[c0 + b] * sm[c0 + b];
+        a += v[b] * sm[c0 + b];
+      }
+  }
+  store_act<BF>(p.out, p.out_plane, (size_t)row * p.n_q * D + h * D + dd, a / L);
 }
 
 template <bool BF, int D>
 static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
-  using T = typename ET<BF>::T;
-  constexpr int RS = BF ? D + 2 : D + 1;
-  const size_t lds = ((2 * 64 * RS * sizeof(T) + 15) / 16) * 16 + (4 * D + 4 * 64) * sizeof(float);
+  if (max_chunks > kMaxChunks) return hipErrorInvalidValue;
+  const size_t lds = (2 * kAttnChunk * (D + 1) + 4 * D + 4 * kAttnChunk) * sizeof(float);
   attn_chunk_kernel<BF, D><<<dim3(max_chunks, a.n_q, n_reqs), 256, lds, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -586,52 +776,86 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_ch
 }
 
 // ---------------------------------------------------------------------------
-// Final arg-max over the LM head's per-group partials and greedy
-// verification (Section 4.2; Appendix C.2): accepted = first row i < W-1
-// whose greedy token differs from its candidate (W-1 if none), correction =
+// Final arg-max over the LM head's per-group partials, one workgroup per
+// verified row, then greedy verification (Section 4.2; Appendix C.2) by the
+// last row of each request to finish: accepted = first row i < W-1 whose
+// greedy token differs from its candidate (W-1 if none), correction =
 // greedy token of row `accepted`.
 
 __global__ __launch_bounds__(256) void finish_kernel(const RowDesc* __restrict__ rows,
-                                                     const ReqDesc* __restrict__ reqs,
+                                                     const ReqDesc* __restrict__ reqs, int n_reqs,
                                                      const float* __restrict__ amax_val,
                                                      const int* __restrict__ amax_idx, int n_groups,
-                                                     int* __restrict__ row_tok, StepOut* __restrict__ out) {
-  __shared__ int s_tok[32];
-  __shared__ int s_bad[32];
-  const ReqDesc rq = reqs[blockIdx.x];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int i = wave; i < rq.W; i += 4) {
-    const int row = rq.row_start + i;
-    float best = -INFINITY;
-    int bi = 0x7fffffff;
-    bool bad = false;
-    for (int g = lane; g < n_groups; g += 64) {
-      const float v = amax_val[g * kMaxRows + row];
-      const int id = amax_idx[g * kMaxRows + row];
-      if (!isfinite(v)) bad = true;
-      else if (v > best || (v == best && id < bi)) { best = v; bi = id; }
+                                                     int* __restrict__ row_tok, int* __restrict__ row_bad,
+                                                     int* __restrict__ counters, StepOut* __restrict__ out) {
+  constexpr int kPer = 8;   // groups per thread, loads in flight together
+  __shared__ float s_v[4];
+  __shared__ int s_i[4], s_b[4], s_last;
+  // which request / row this workgroup verifies
+  int r = 0, i = blockIdx.x;
+  while (r < n_reqs - 1 && i >= reqs[r].W) i -= reqs[r++].W;
+  const ReqDesc rq = reqs[r];
+  const int row = rq.row_start + i;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  float best = -INFINITY;
+  int bi = 0x7fffffff;
+  bool bad = false;
+  for (int g0 = 0; g0 < n_groups; g0 += 256 * kPer) {
+    float v[kPer];
+    int id[kPer];
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int g = g0 + t * 256 + tid;
+      if (g < n_groups) {
+        v[t] = amax_val[g * kMaxRows + row];
+        id[t] = amax_idx[g * kMaxRows + row];
+      }
     }
-    wave_argmax(best, bi);
-    const bool any_bad = (__ballot(bad) != 0) || !isfinite(best);
-    if (lane == 0) {
-      s_tok[i] = bi;
-      s_bad[i] = any_bad;
-      row_tok[row] = bi;
+#pragma unroll
+    for (int t = 0; t < kPer; ++t) {
+      const int g = g0 + t * 256 + tid;
+      if (g < n_groups) {
+        if (!isfinite(v[t])) bad = true;
+        else if (v[t] > best || (v[t] == best && id[t] < bi)) { best = v[t]; bi = id[t]; }
+      }
     }
   }
+  wave_argmax(best, bi);
+  const bool wbad = __ballot(bad) != 0;
+  if (lane == 0) { s_v[wave] = best; s_i[wave] = bi; s_b[wave] = wbad; }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int bad = 0;
-    for (int i = 0; i < rq.W; ++i) bad |= s_bad[i];
-    int a = 0;
-    while (a < rq.W - 1 && rows[rq.row_start + a].cmp == s_tok[a]) ++a;
-    out[blockIdx.x] = StepOut{a, s_tok[a], bad, 0};
+  if (tid == 0) {
+    float bv = s_v[0];
+    int bx = s_i[0], bb = s_b[0];
+    for (int w = 1; w < 4; ++w) {
+      if (s_v[w] > bv || (s_v[w] == bv && s_i[w] < bx)) { bv = s_v[w]; bx = s_i[w]; }
+      bb |= s_b[w];
+    }
+    bb |= !isfinite(bv);
+    __hip_atomic_store(&row_tok[row], bx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&row_bad[row], bb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    wait_vmem();
+    s_last = __hip_atomic_fetch_add(&counters[r], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == rq.W - 1;
+    if (s_last) {
+      counters[r] = 0;  // ready for the next launch
+      int a = 0, nan = 0;
+      for (int q = 0; q < rq.W; ++q)
+        nan |= __hip_atomic_load(&row_bad[rq.row_start + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      while (a < rq.W - 1 && rows[rq.row_start + a].cmp ==
+                                 __hip_atomic_load(&row_tok[rq.row_start + a], __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT))
+        ++a;
+      const int corr = __hip_atomic_load(&row_tok[rq.row_start + a], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      out[r] = StepOut{a, corr, nan, 0};
+    }
   }
 }
 
-hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, const float* amax_val,
-                         const int* amax_idx, int n_groups, int* row_tok, StepOut* out, hipStream_t s) {
-  finish_kernel<<<n_reqs, 256, 0, s>>>(rows, reqs, amax_val, amax_idx, n_groups, row_tok, out);
+hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,
+                         const float* amax_val, const int* amax_idx, int n_groups, int* row_tok,
+                         int* row_bad, int* counters, StepOut* out, hipStream_t s) {
+  finish_kernel<<<n_rows, 256, 0, s>>>(rows, reqs, n_reqs, amax_val, amax_idx, n_groups, row_tok, row_bad,
+                                       counters, out);
   return hipGetLastError();
 }
 

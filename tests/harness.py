@@ -117,8 +117,6 @@ def parity_round(om, gpu, req, cands, k, tol, stats, check_logits=True):
 def compare_kv(om, gpu, req, layer, n_tok, tol):
     k_g, v_g = gpu.read_kv(req, layer, n_tok)
     k_o, v_o = om.kv(layer)
-    if k_g.dtype == np.uint16:
-        k_g, v_g = gen.bf16_bits_to_f32(k_g), gen.bf16_bits_to_f32(v_g)
     ek = float(np.max(np.abs(k_g - k_o[:, :n_tok])))
     ev = float(np.max(np.abs(v_g - v_o[:, :n_tok])))
     assert ek <= tol and ev <= tol, (ek, ev)

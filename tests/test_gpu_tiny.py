@@ -50,7 +50,7 @@ def test_tiny_workload_rounds(pair):
     assert st.rounds == rq.max_rounds
     assert gpu.state(0)[0] == om.kv_len
     for l in range(shape.n_layers):
-        compare_kv(om, gpu, 0, l, om.kv_len, 1e-5 if shape.dtype == 0 else 2e-2)
+        compare_kv(om, gpu, 0, l, om.kv_len, 1e-5 if shape.dtype == 0 else 1e-3)
     print(f"{shape.name}: rounds={st.rounds} committed={st.committed} near_ties={st.near_ties} "
           f"max_logit_err={st.max_err:.3g}")
 
@@ -200,3 +200,27 @@ def test_non_finite_logits_are_reported():
         gpu.prefill(0, a_dev, instr)
     assert e.value.code == as2d.ENUMERIC
     gpu.close()
+
+
+def test_graph_replays_match_eager(pair):
+    """Verification passes replayed from a captured HIP graph give the
+    eager result bit for bit, replay after replay, with eager work and
+    synchronisations in between."""
+    shape, _, gpu = pair
+    first, L = _prefilled(gpu, shape, seed=8)
+    rng = np.random.default_rng(8)
+    cands = [int(t) for t in rng.integers(0, shape.vocab, 6)]
+    gpu.set_graphs(False)
+    ref = gpu.verify(0, cands)
+    ref_logits = gpu.logits(0)
+    gpu.rollback(0, L, first)
+    for rep in range(4):
+        gpu.set_graphs(True)
+        r = gpu.verify(0, cands)
+        assert r == ref, rep
+        assert np.array_equal(gpu.logits(0), ref_logits), rep
+        gpu.rollback(0, L, first)
+        gpu.set_graphs(False)             # eager work between replays
+        gpu.decode_one(0)
+        gpu.rollback(0, L, first)
+    gpu.set_graphs(True)
