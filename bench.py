@@ -55,26 +55,53 @@ def parse():
 
 
 def traffic_from_profiles():
-    """HBM bytes per gate/up launch from committed rocprofv3 counter
-    summaries, if present (profiles/gemm_gate_up_7b_k8_pmc.json)."""
-    p = os.path.join(PROFILES, "gemm_gate_up_7b_k8_pmc.json")
+    """HBM bytes per gate/up launch from the committed rocprofv3 counter
+    summary (profiles/gemm_gate_up_qwen7b_k8_pmc.md), if it was taken on
+    the current library sources (its `library_source_sha` line)."""
+    p = os.path.join(PROFILES, "gemm_gate_up_qwen7b_k8_pmc.md")
     if not os.path.exists(p):
         return None
+    fields = {}
+    for line in open(p):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("library_source_sha") != library_source_sha():
+        return None
     try:
-        d = json.load(open(p))
-        if d.get("kernel_source_sha") != kernel_source_sha():
-            return None
-        return d.get("traffic_bytes_per_launch")
-    except Exception:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
         return None
 
 
-def kernel_source_sha():
+def library_source_sha():
+    """Hash of the HIP library sources (a counter summary is valid only for
+    the sources it was taken on)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.h"):
-        h.update(open(os.path.join(ROOT, "paper_2609_37617_amd", "csrc", f), "rb").read())
+    d = os.path.join(ROOT, "paper_2609_37617_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        h.update(f.encode())
+        h.update(open(os.path.join(d, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+def copy_calibration(mib):
+    """One device-to-device copy of `mib` MiB through the HIP runtime (its
+    plain copy kernel reads and writes exactly that many bytes), so that
+    hardware byte counters can be scaled by what they report for it."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    n = ctypes.c_size_t(mib << 20)
+    src, dst = ctypes.c_void_p(), ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(src), n) == 0 and hip.hipMalloc(ctypes.byref(dst), n) == 0
+    assert hip.hipMemset(src, 1, n) == 0
+    assert hip.hipDeviceSynchronize() == 0
+    assert hip.hipMemcpy(dst, src, n, 3) == 0      # hipMemcpyDeviceToDevice
+    assert hip.hipDeviceSynchronize() == 0
+    hip.hipFree(src)
+    hip.hipFree(dst)
+    log(f"[bench] calibration copy: {mib} MiB read + {mib} MiB written")
 
 
 def cpu_baseline(shape, n_audio, n_instr, k, mean_committed, seed=0):
@@ -187,22 +214,14 @@ def main():
         return got, sum(len(c) + 1 for c in cands), sum(model.state(i)[0] for i in ids)
 
     if args.calib_copy_mib:
-        import torch
-        n = args.calib_copy_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copy: {args.calib_copy_mib} MiB read + {args.calib_copy_mib} MiB written")
-        del src, dst
+        copy_calibration(args.calib_copy_mib)
     for _ in range(args.warmup):
         step()
-    try:
-        import torch
-        sync = torch.cuda.synchronize if torch.cuda.is_available() else (lambda: None)
-    except Exception:
-        sync = lambda: None
+    import ctypes
+    _hip = ctypes.CDLL("libamdhip64.so")
+
+    def sync():
+        assert _hip.hipDeviceSynchronize() == 0
     sync()
     committed = rows = kvsum = 0
     t0 = time.perf_counter()
@@ -237,15 +256,16 @@ def main():
         for name, (tot, cnt) in model.timing().items():
             if cnt:
                 kernel_ms[name] = {"avg_us": tot * 1e3 / cnt, "launches": cnt, "total_ms_per_step": tot / n_t}
-        gu = kernel_ms.get("gemm_gate_up")
-        if gu:
-            gu_bytes = 2 * shape.ffn * shape.hidden * (2 if shape.dtype == wc.BF16 else 4)
-            achieved = gu_bytes / (gu["avg_us"] * 1e-6) / 1e9
-            traffic = traffic_from_profiles()
-            roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                    "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
-                    "kernel": "gemm_gate_up", "bytes_per_launch": gu_bytes,
-                    "avg_launch_us": round(gu["avg_us"], 2), "ms_per_step_with_events": round(t_evt, 3)}
+        # the dominant kernel, gate/up, timed over back-to-back launches
+        # (events around a batch, so their own overhead is amortised)
+        rows0 = reqs[0].k + 1 if len(reqs) == 1 else int(round(mean_rows))
+        gu_us = model.time_gemm(2, rows0, 4 * shape.n_layers)
+        gu_bytes = 2 * shape.ffn * shape.hidden * (2 if shape.dtype == wc.BF16 else 4)
+        achieved = gu_bytes / (gu_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic_from_profiles(),
+                "kernel": "gemm_gate_up", "rows": rows0, "bytes_per_launch": gu_bytes,
+                "avg_launch_us": round(gu_us, 2), "ms_per_step_with_events": round(t_evt, 3)}
         log("[bench] per-kernel: " + ", ".join(f"{k} {v['avg_us']:.1f}us x{v['launches'] // n_t}"
                                                for k, v in kernel_ms.items()))
 

@@ -144,10 +144,29 @@ int as2d_get_logits(as2d_ctx* ctx, int32_t req, float* host, int32_t max_rows, i
 /* Greedy token of every row of `req`'s last call: host[max_rows]. */
 int as2d_get_row_tokens(as2d_ctx* ctx, int32_t req, int32_t* host, int32_t max_rows, int32_t* n_rows);
 
-/* Verification passes are captured once per (rows, requests, keep_logits)
- * into a HIP graph and replayed (on by default); off runs every kernel
- * launch eagerly.  Results are identical either way. */
-int as2d_set_graphs(as2d_ctx* ctx, int32_t on);
+/* How verification passes run; results are bit-identical in every mode.
+ *   AS2D_EXEC_EAGER:      one kernel launch per operation (no graph);
+ *   AS2D_EXEC_GRAPH:      (default) the same launches captured once per
+ *                         (rows, requests, keep_logits) into a HIP graph;
+ *   AS2D_EXEC_PERSISTENT: one persistent kernel per pass of up to 32 rows,
+ *                         captured into a graph; larger passes use
+ *                         AS2D_EXEC_GRAPH.
+ * as2d_get_exec_info reports the mode and the persistent kernel's grid
+ * (0 when the device cannot hold it; it then falls back to graphs). */
+enum { AS2D_EXEC_EAGER = 0, AS2D_EXEC_GRAPH = 1, AS2D_EXEC_PERSISTENT = 2 };
+int as2d_set_exec_mode(as2d_ctx* ctx, int32_t mode);
+int as2d_get_exec_info(as2d_ctx* ctx, int32_t* mode, int32_t* persistent_grid);
+
+/* Timeline of the persistent step kernel (inspection only): when on, every
+ * later persistent pass records, per workgroup and phase, three
+ * wall-clock stamps (phase entered, inputs ready, phase left; 0 = not
+ * reached).  as2d_step_trace_read copies the last pass's stamps,
+ * [grid][n_phase][3] int64, into host (max entries) and reports grid and
+ * n_phase.  Phases: 0 embedding; per layer l, 1 + 6 l + {0 QKV,
+ * 1 attention chunks, 2 attention merge, 3 O, 4 gate/up, 5 down}; then the
+ * LM head and the verification. */
+int as2d_set_step_trace(as2d_ctx* ctx, int32_t on);
+int as2d_step_trace_read(as2d_ctx* ctx, int64_t* host, int64_t max, int32_t* grid, int32_t* n_phase);
 
 /* Return `req` to an earlier committed state: prefix length <= kv_len <=
  * current kv_len; root becomes the pending root.  Cache rows past kv_len
@@ -176,6 +195,13 @@ int as2d_release_request(as2d_ctx* ctx, int32_t req);
 int as2d_set_timing(as2d_ctx* ctx, int32_t on);
 int as2d_timing_read(as2d_ctx* ctx, char* names, double* total_ms, int64_t* counts, int32_t max);
 int as2d_timing_reset(as2d_ctx* ctx);
+
+/* Average duration of one GEMM kernel of kind `which` (0 QKV, 1 O,
+ * 2 gate/up, 3 down, 4 LM head) for `rows` rows, from `reps` back-to-back
+ * launches on the library's stream between two HIP events; the layer
+ * matrices are cycled so the weights stream from HBM.  Measurement only:
+ * it overwrites activation buffers and the cache rows 0..rows-1 of slot 0. */
+int as2d_time_gemm(as2d_ctx* ctx, int32_t which, int32_t rows, int32_t reps, double* avg_us);
 
 /* Algorithmic HBM bytes of one forward pass of `rows` rows whose
  * requests hold `kv_keys` attended positions in total per layer

@@ -14,14 +14,16 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libas2d.so")
 
 OK, EINVAL, ECAPACITY, ESTATE, EHIP, ENUMERIC, ENOMEM = 0, -1, -2, -3, -4, -5, -6
+EXEC_EAGER, EXEC_GRAPH, EXEC_PERSISTENT = 0, 1, 2
 F32, BF16 = 0, 1
 
 # Every symbol include/as2d.h declares.
 EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_one",
            "as2d_verify_batch", "as2d_set_keep_logits", "as2d_get_logits", "as2d_get_row_tokens",
            "as2d_rollback", "as2d_get_state", "as2d_read_kv", "as2d_release_request",
-           "as2d_set_graphs", "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_step_bytes",
-           "as2d_free", "as2d_last_error"]
+           "as2d_set_exec_mode", "as2d_get_exec_info", "as2d_set_step_trace", "as2d_step_trace_read",
+           "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_time_gemm",
+           "as2d_step_bytes", "as2d_free", "as2d_last_error"]
 
 
 class Config(ctypes.Structure):
@@ -76,10 +78,14 @@ def load_library(path: str = LIB_PATH):
     lib.as2d_get_state.argtypes = [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]
     lib.as2d_read_kv.argtypes = [_P, _I, _I, _P, _P, _I]
     lib.as2d_release_request.argtypes = [_P, _I]
-    lib.as2d_set_graphs.argtypes = [_P, _I]
+    lib.as2d_set_exec_mode.argtypes = [_P, _I]
+    lib.as2d_set_step_trace.argtypes = [_P, _I]
+    lib.as2d_step_trace_read.argtypes = [_P, _P, ctypes.c_int64, ctypes.POINTER(_I), ctypes.POINTER(_I)]
+    lib.as2d_get_exec_info.argtypes = [_P, ctypes.POINTER(_I), ctypes.POINTER(_I)]
     lib.as2d_set_timing.argtypes = [_P, _I]
     lib.as2d_timing_read.argtypes = [_P, _P, _P, _P, _I]
     lib.as2d_timing_reset.argtypes = [_P]
+    lib.as2d_time_gemm.argtypes = [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_double)]
     lib.as2d_step_bytes.argtypes = [_P, _I, ctypes.c_int64]
     lib.as2d_step_bytes.restype = ctypes.c_int64
     lib.as2d_free.argtypes = [_P]
@@ -204,8 +210,25 @@ class Model:
     def release(self, req: int):
         self._check(self.lib.as2d_release_request(self.ctx, req))
 
-    def set_graphs(self, on: bool):
-        self._check(self.lib.as2d_set_graphs(self.ctx, int(on)))
+    def set_exec_mode(self, mode: int):
+        """EXEC_EAGER, EXEC_GRAPH or EXEC_PERSISTENT (include/as2d.h)."""
+        self._check(self.lib.as2d_set_exec_mode(self.ctx, mode))
+
+    def exec_info(self):
+        mode, grid = _I(), _I()
+        self._check(self.lib.as2d_get_exec_info(self.ctx, ctypes.byref(mode), ctypes.byref(grid)))
+        return mode.value, grid.value
+
+    def set_step_trace(self, on: bool):
+        self._check(self.lib.as2d_set_step_trace(self.ctx, int(on)))
+
+    def step_trace(self) -> np.ndarray:
+        """[grid, n_phase, 3] wall-clock stamps of the last persistent pass."""
+        n = 1 << 22
+        buf = np.zeros(n, dtype=np.int64)
+        g, ph = _I(), _I()
+        self._check(self.lib.as2d_step_trace_read(self.ctx, _ptr(buf), n, ctypes.byref(g), ctypes.byref(ph)))
+        return buf[:g.value * ph.value * 3].reshape(g.value, ph.value, 3)
 
     def set_timing(self, on: bool):
         self._check(self.lib.as2d_set_timing(self.ctx, int(on)))
@@ -223,6 +246,13 @@ class Model:
             nm = names.raw[32 * i:32 * i + 32].split(b"\0")[0].decode()
             out[nm] = (ms[i], cnt[i])
         return out
+
+    def time_gemm(self, which: int, rows: int, reps: int) -> float:
+        """Average microseconds of one GEMM launch (0 QKV, 1 O, 2 gate/up,
+        3 down, 4 LM head); measurement only, clobbers activations."""
+        us = ctypes.c_double()
+        self._check(self.lib.as2d_time_gemm(self.ctx, which, rows, reps, ctypes.byref(us)))
+        return us.value
 
     def step_bytes(self, rows: int, kv_keys: int) -> int:
         return int(self.lib.as2d_step_bytes(self.ctx, rows, kv_keys))

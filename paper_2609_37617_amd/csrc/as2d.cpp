@@ -37,9 +37,11 @@ struct ReqState {
   int last_logits = 0;  // logits of the last call are in the device buffer
 };
 
-enum Kind { K_EMBED, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_LM, K_FINISH, K_COUNT };
-const char* kKindNames[K_COUNT] = {"embed", "gemm_qkv", "attention", "gemm_o",
-                                   "gemm_gate_up", "gemm_down", "gemm_lm_head", "finish"};
+enum Kind { K_EMBED, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_LM, K_FINISH, K_STEP, K_COUNT };
+const char* kKindNames[K_COUNT] = {"embed", "gemm_qkv", "attention", "gemm_o", "gemm_gate_up",
+                                   "gemm_down", "gemm_lm_head", "finish", "step_persistent"};
+
+constexpr int kStepRows = 32;  // rows of a persistent-kernel pass
 
 }  // namespace
 
@@ -82,9 +84,23 @@ struct as2d_ctx {
   std::vector<ReqState> reqs;
   int keep_logits = 0;
 
-  // captured verify passes: (rows, requests, keep_logits) -> executable graph
-  int use_graphs = 1;
-  std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
+  // execution mode of verification passes (AS2D_EXEC_*) and the captured
+  // graphs: (mode, rows, requests, keep_logits) -> executable graph
+  int exec_mode = AS2D_EXEC_GRAPH;
+  std::map<std::tuple<int, int, int, int>, hipGraphExec_t> graphs;
+
+  // persistent step kernel: per-layer activation buffers and counters
+  bool pers_ok = false;
+  int pers_grid[3] = {0, 0, 0};  // by M-tile count 1, 2
+  float *px = nullptr, *psumsq = nullptr, *pq = nullptr;
+  void *pxg = nullptr, *pattn = nullptr, *ph = nullptr;
+  int *psplit = nullptr, *pphase = nullptr, *perr = nullptr;
+  int split_stride = 0;  // counters per (layer, GEMM)
+  int n_phase = 0;
+  std::map<int, StepLayer*> step_layers;  // by M: device array of per-layer arguments
+  int h_err = 0;
+  long long* ptrace = nullptr;  // persistent-kernel timeline (as2d_set_step_trace)
+  int trace_on = 0;
 
   int timing = 0;
   double t_ms[K_COUNT] = {};
@@ -125,14 +141,19 @@ int dalloc(as2d_ctx* c, P** p, size_t bytes) {
   return AS2D_OK;
 }
 
-GemmPlan make_plan(int N, int K, int KE, int target_wgs) {
+// k-split plan of one matrix.  A tile (128-column group, k-split) is the
+// unit of work; the split count aims at about `target` tiles per matrix
+// (a few per compute unit) with at least 4 k-steps per tile and at most
+// 16 splits.  It depends only on the matrix shape, never on the rows of a
+// pass, so every row is computed alike in every pass.
+GemmPlan make_plan(int N, int K, int KE, int target) {
   GemmPlan p;
   p.N = N;
   p.K = K;
   p.KT = K / KE;
   p.groups = N / kGroupCols;
-  int ks = (int)std::lround((double)target_wgs / p.groups);
-  ks = std::max(1, std::min({ks, std::max(1, p.KT / 4), kMaxSplits}));
+  int ks = (int)std::lround((double)target / p.groups);
+  ks = std::max(1, std::min({ks, std::max(1, p.KT / 4), 16}));
   p.ktps = (p.KT + ks - 1) / ks;
   p.KS = (p.KT + p.ktps - 1) / p.ktps;
   return p;
@@ -277,6 +298,7 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
       a.A = c->attn;
       a.a_plane = c->attn_plane;
       a.x = c->x;
+      a.x_out = c->x;
       a.sumsq_out = c->sumsq;
       a.gain_next = w.g_mlp;
       a.out = c->xg;
@@ -298,6 +320,7 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
       a.A = c->hbuf;
       a.a_plane = c->h_plane;
       a.x = c->x;
+      a.x_out = c->x;
       a.sumsq_out = c->sumsq;
       a.gain_next = g_next;
       a.out = c->xg;
@@ -326,11 +349,157 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
   return AS2D_OK;
 }
 
+// Per-layer arguments of the persistent step kernel for passes of M rows
+// (device array, built once per M).
+StepLayer* step_layers_for(as2d_ctx* c, int M) {
+  auto it = c->step_layers.find(M);
+  if (it != c->step_layers.end()) return it->second;
+  const as2d_config& g = c->cfg;
+  const int H = g.hidden, F = g.ffn, d = g.head_dim, nq = g.n_q_heads, nkv = g.n_kv_heads;
+  const long long R = kStepRows;
+  const size_t xs = (size_t)R * H;                        // floats of one x / planes of one xg
+  const size_t ss = (size_t)(H / 128) * kMaxRows;         // sum-of-squares partials
+  const size_t qs = (size_t)R * nq * d;
+  auto xg = [&](int i) { return (void*)((char*)c->pxg + i * xs * 4); };
+  std::vector<StepLayer> v(g.n_layers);
+  for (int l = 0; l < g.n_layers; ++l) {
+    const LayerW& w = c->layers[l];
+    StepLayer& s = v[l];
+    float* kc = c->kc + (size_t)l * c->layer_stride;
+    float* vc = c->vc + (size_t)l * c->layer_stride;
+    int* cnt = c->psplit + (size_t)(4 * l) * c->split_stride;
+    s.qkv = base_args(c, c->p_qkv, w.qkv, M);
+    s.qkv.A = xg(2 * l);
+    s.qkv.a_plane = c->bf16 ? (long long)xs : 0;
+    s.qkv.sumsq = c->psumsq + (2 * l) * ss;
+    s.qkv.counters = cnt;
+    s.qkv.bias = w.bias;
+    s.qkv.q_out = c->pq + l * qs;
+    s.qkv.k_cache = kc;
+    s.qkv.v_cache = vc;
+    s.qkv.slot_stride = c->slot_stride;
+    s.qkv.kv_cap = g.max_kv_len;
+    s.qkv.n_q = nq;
+    s.qkv.n_kv = nkv;
+    s.qkv.head_dim = d;
+    s.qkv.rope_cs = c->rope_cs;
+
+    AttnArgs& a = s.attn;
+    a = AttnArgs{};
+    a.q = c->pq + l * qs;
+    a.k_cache = kc;
+    a.v_cache = vc;
+    a.slot_stride = c->slot_stride;
+    a.kv_cap = g.max_kv_len;
+    a.rows = c->d_rows;
+    a.reqs = c->d_reqs;
+    a.n_q = nq;
+    a.n_kv = nkv;
+    a.head_dim = d;
+    a.scale = 1.0f / std::sqrt((float)d);
+    a.pacc = c->pacc;
+    a.pml = c->pml;
+    a.n_chunks_cap = c->n_chunks_cap;
+    a.out = (char*)c->pattn + l * qs * 4;
+    a.out_plane = c->bf16 ? (long long)qs : 0;
+    a.M = M;
+
+    s.o = base_args(c, c->p_o, w.o, M);
+    s.o.A = a.out;
+    s.o.a_plane = a.out_plane;
+    s.o.counters = cnt + c->split_stride;
+    s.o.x = c->px + (2 * l) * xs;
+    s.o.x_out = c->px + (2 * l + 1) * xs;
+    s.o.sumsq_out = c->psumsq + (2 * l + 1) * ss;
+    s.o.gain_next = w.g_mlp;
+    s.o.out = xg(2 * l + 1);
+    s.o.out_plane = c->bf16 ? (long long)xs : 0;
+
+    s.gu = base_args(c, c->p_gu, w.gu, M);
+    s.gu.A = xg(2 * l + 1);
+    s.gu.a_plane = c->bf16 ? (long long)xs : 0;
+    s.gu.sumsq = c->psumsq + (2 * l + 1) * ss;
+    s.gu.counters = cnt + 2 * c->split_stride;
+    s.gu.out = (char*)c->ph + (size_t)l * R * F * 4;
+    s.gu.out_plane = c->bf16 ? R * F : 0;
+
+    s.down = base_args(c, c->p_down, w.down, M);
+    s.down.A = s.gu.out;
+    s.down.a_plane = s.gu.out_plane;
+    s.down.counters = cnt + 3 * c->split_stride;
+    s.down.x = c->px + (2 * l + 1) * xs;
+    s.down.x_out = c->px + (2 * l + 2) * xs;
+    s.down.sumsq_out = c->psumsq + (2 * l + 2) * ss;
+    s.down.gain_next = l + 1 < g.n_layers ? c->layers[l + 1].g_attn : c->g_final;
+    s.down.out = xg(2 * l + 2);
+    s.down.out_plane = c->bf16 ? (long long)xs : 0;
+  }
+  StepLayer* dv = nullptr;
+  if (hipMalloc(&dv, sizeof(StepLayer) * g.n_layers) != hipSuccess) return nullptr;
+  c->allocs.push_back(dv);
+  if (hipMemcpy(dv, v.data(), sizeof(StepLayer) * g.n_layers, hipMemcpyHostToDevice) != hipSuccess) return nullptr;
+  c->step_layers[M] = dv;
+  return dv;
+}
+
+// Launches of one verification pass through the persistent step kernel.
+int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
+  const as2d_config& g = c->cfg;
+  StepLayer* layers = step_layers_for(c, M);
+  if (!layers) return fail(c, AS2D_ENOMEM, "persistent step arguments");
+  const int L = g.n_layers, H = g.hidden;
+  const size_t xs = (size_t)kStepRows * H;
+  const size_t ss = (size_t)(H / 128) * kMaxRows;
+  StepArgs a{};
+  a.layers = layers;
+  a.n_layers = L;
+  a.lm = base_args(c, c->p_lm, c->lm, M);
+  a.lm.A = (char*)c->pxg + 2 * L * xs * 4;
+  a.lm.a_plane = c->bf16 ? (long long)xs : 0;
+  a.lm.sumsq = c->psumsq + 2 * L * ss;
+  a.lm.counters = c->psplit + (size_t)(4 * L) * c->split_stride;
+  a.lm.logits = c->keep_logits ? c->logits : nullptr;
+  a.lm.amax_val = c->amax_val;
+  a.lm.amax_idx = c->amax_idx;
+  a.M = M;
+  a.rows = c->d_rows;
+  a.embed = c->embed;
+  a.audio = c->audio;
+  a.hidden = H;
+  a.gain0 = c->layers[0].g_attn;
+  a.x0 = c->px;
+  a.sumsq0 = c->psumsq;
+  a.xg0 = c->pxg;
+  a.xg0_plane = c->bf16 ? (long long)xs : 0;
+  a.reqs = c->d_reqs;
+  a.n_reqs = n_att;
+  a.n_q = g.n_q_heads;
+  a.fin_reqs = c->d_reqs + g.max_requests;
+  a.n_fin = n_fin;
+  a.fin_rows = fin_rows;
+  a.row_tok = c->row_tok;
+  a.row_bad = c->row_bad;
+  a.out = c->d_out;
+  a.groups_qkv = c->p_qkv.groups;
+  a.groups_o = c->p_o.groups;
+  a.groups_gu = c->p_gu.groups;
+  a.groups_down = c->p_down.groups;
+  a.groups_lm = c->p_lm.groups;
+  a.phase_cnt = c->pphase;
+  a.err = c->perr;
+  a.spin_limit = env_int("AS2D_SPIN_LIMIT", 1 << 21);
+  a.trace = c->trace_on ? c->ptrace : nullptr;
+  const int MT = (M + 15) / 16;
+  Timed t(c, K_STEP);
+  HIP_TRY(c, launch_step(c->bf16, MT, g.head_dim, a, c->pers_grid[MT], c->n_phase, c->stream));
+  return AS2D_OK;
+}
+
 // One forward pass over the rows and requests in h_rows / h_reqs (see
 // launch_pass).  Verification passes run as a captured HIP graph, one per
 // (rows, requests, keep_logits); the attention grid then covers the slot
 // capacity so that the graph stays valid as the cache grows.
-int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
+int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool verify_call = false) {
   const as2d_config& g = c->cfg;
   hipStream_t s = c->stream;
   const int mr = g.max_requests;
@@ -344,9 +513,16 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
     max_chunks = std::max(max_chunks, (nk + kAttnChunk - 1) / kAttnChunk);
   }
   if (max_chunks > c->n_chunks_cap) return fail(c, AS2D_ECAPACITY, "attention chunks %d > %d", max_chunks, c->n_chunks_cap);
-  const bool graph = with_head && c->use_graphs && !c->timing && n_fin == n_att;
+  const bool verify_pass = verify_call && with_head && n_fin == n_att;
+  const bool persistent = verify_pass && c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && M <= kStepRows;
+  const bool graph = verify_pass && c->exec_mode != AS2D_EXEC_EAGER && !c->timing;
+  if (persistent && !step_layers_for(c, M)) return fail(c, AS2D_ENOMEM, "persistent step arguments");
+  auto launch = [&](bool capture) -> int {
+    if (persistent) return launch_persistent(c, M, n_att, n_fin, fin_rows);
+    return launch_pass(c, M, n_att, n_fin, fin_rows, with_head, capture ? c->n_chunks_cap : max_chunks);
+  };
   if (graph) {
-    const auto key = std::make_tuple(M, n_att, c->keep_logits);
+    const auto key = std::make_tuple((int)persistent, M, n_att, c->keep_logits);
     auto it = c->graphs.find(key);
     if (it == c->graphs.end()) {
       if (c->graphs.size() >= 64) {
@@ -355,7 +531,7 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
       }
       hipGraph_t gr = nullptr;
       HIP_TRY(c, hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
-      int rc = launch_pass(c, M, n_att, n_fin, fin_rows, true, c->n_chunks_cap);
+      int rc = launch(true);
       hipError_t e = hipStreamEndCapture(s, &gr);
       if (rc) {
         if (gr) hipGraphDestroy(gr);
@@ -370,15 +546,21 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head) {
     }
     HIP_TRY(c, hipGraphLaunch(it->second, s));
   } else {
-    int rc = launch_pass(c, M, n_att, n_fin, fin_rows, with_head, max_chunks);
+    int rc = launch(false);
     if (rc) return rc;
   }
+  if (persistent) HIP_TRY(c, hipMemcpyAsync(&c->h_err, c->perr, sizeof(int), hipMemcpyDeviceToHost, s));
   if (with_head) {
     HIP_TRY(c, hipMemcpyAsync(c->h_out, c->d_out, sizeof(StepOut) * n_fin, hipMemcpyDeviceToHost, s));
     HIP_TRY(c, hipMemcpyAsync(c->h_tok, c->row_tok, sizeof(int) * M, hipMemcpyDeviceToHost, s));
   }
   HIP_TRY(c, hipStreamSynchronize(s));
   timing_collect(c);
+  if (persistent && c->h_err) {
+    c->h_err = 0;
+    HIP_TRY(c, hipMemset(c->perr, 0, sizeof(int)));
+    return fail(c, AS2D_EHIP, "persistent step kernel: a wait timed out (workgroups not co-resident?)");
+  }
   return AS2D_OK;
 }
 
@@ -573,6 +755,36 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   CK(dalloc(c, &c->part, part_elems * 4));
   CK(dalloc(c, &c->counters, 8192 * 4));
   HIP_TRY(c, hipMemsetAsync(c->counters, 0, 8192 * 4, c->stream));
+  // persistent step kernel (verification passes of up to 32 rows)
+  if (env_int("AS2D_PERSISTENT", 1)) {
+    int dev = 0, cus = 0, occ1 = 0, occ2 = 0;
+    HIP_TRY(c, hipGetDevice(&dev));
+    HIP_TRY(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+    HIP_TRY(c, step_occupancy(c->bf16, 1, d, H, &occ1));
+    HIP_TRY(c, step_occupancy(c->bf16, 2, d, H, &occ2));
+    const int L = g.n_layers;
+    const long long R = kStepRows;
+    if (occ1 > 0 && occ2 > 0) {
+      c->pers_grid[1] = occ1 * cus;
+      c->pers_grid[2] = occ2 * cus;
+      CK(dalloc(c, &c->px, (size_t)(2 * L + 1) * R * H * 4));
+      CK(dalloc(c, &c->pxg, (size_t)(2 * L + 1) * R * H * 4));
+      CK(dalloc(c, &c->psumsq, (size_t)(2 * L + 1) * (H / 128) * kMaxRows * 4));
+      CK(dalloc(c, &c->pq, (size_t)L * R * nq * d * 4));
+      CK(dalloc(c, &c->pattn, (size_t)L * R * nq * d * 4));
+      CK(dalloc(c, &c->ph, (size_t)L * R * F * 4));
+      c->split_stride = std::max({c->p_qkv.groups, c->p_o.groups, c->p_gu.groups, c->p_down.groups,
+                                  c->p_lm.groups});
+      const size_t n_split = (size_t)(4 * L + 1) * c->split_stride;
+      CK(dalloc(c, &c->psplit, n_split * 4));
+      HIP_TRY(c, hipMemsetAsync(c->psplit, 0, n_split * 4, c->stream));
+      c->n_phase = 3 + 6 * L;
+      CK(dalloc(c, &c->pphase, (size_t)c->n_phase * 4));
+      CK(dalloc(c, &c->perr, 4));
+      HIP_TRY(c, hipMemsetAsync(c->perr, 0, 4, c->stream));
+      c->pers_ok = true;
+    }
+  }
   CK(dalloc(c, &c->pacc, (size_t)c->n_chunks_cap * MR * nq * d * 4));
   CK(dalloc(c, &c->pml, (size_t)c->n_chunks_cap * MR * nq * 2 * 4));
   CK(dalloc(c, &c->d_rows, sizeof(RowDesc) * MR));
@@ -600,7 +812,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   }
   memset(c->h_reqs, 0, sizeof(ReqDesc) * 2 * g.max_requests);
   c->reqs.assign(g.max_requests, ReqState());
-  c->use_graphs = env_int("AS2D_GRAPHS", 1) != 0;
+  c->exec_mode = env_int("AS2D_EXEC_MODE", AS2D_EXEC_GRAPH);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return AS2D_OK;
   }();
@@ -721,7 +933,7 @@ int as2d_verify_batch(as2d_ctx* c, int32_t n, const int32_t* reqs, const int32_t
     row += k + 1;
     off += k;
   }
-  int rc = run_forward(c, M, n, n, true);
+  int rc = run_forward(c, M, n, n, true, true);
   if (rc) return rc;
   for (int r = 0; r < n; ++r)
     if (c->h_out[r].nan_flag) return fail(c, AS2D_ENUMERIC, "verify: non-finite logits (request %d)", reqs[r]);
@@ -837,9 +1049,45 @@ int as2d_release_request(as2d_ctx* c, int32_t req) {
   return AS2D_OK;
 }
 
-int as2d_set_graphs(as2d_ctx* c, int32_t on) {
+int as2d_set_exec_mode(as2d_ctx* c, int32_t mode) {
   if (!c) return AS2D_EINVAL;
-  c->use_graphs = on ? 1 : 0;
+  if (mode < AS2D_EXEC_EAGER || mode > AS2D_EXEC_PERSISTENT) return fail(c, AS2D_EINVAL, "unknown exec mode %d", mode);
+  c->exec_mode = mode;
+  return AS2D_OK;
+}
+
+int as2d_get_exec_info(as2d_ctx* c, int32_t* mode, int32_t* persistent_grid) {
+  if (!c) return AS2D_EINVAL;
+  if (mode) *mode = c->exec_mode;
+  if (persistent_grid) *persistent_grid = c->pers_ok ? c->pers_grid[1] : 0;
+  return AS2D_OK;
+}
+
+int as2d_set_step_trace(as2d_ctx* c, int32_t on) {
+  if (!c) return AS2D_EINVAL;
+  if (!c->pers_ok) return fail(c, AS2D_ESTATE, "no persistent step kernel on this device");
+  if (on && !c->ptrace) {
+    const size_t n = (size_t)std::max(c->pers_grid[1], c->pers_grid[2]) * c->n_phase * 3;
+    int rc = dalloc(c, &c->ptrace, n * sizeof(long long));
+    if (rc) return rc;
+    HIP_TRY(c, hipMemset(c->ptrace, 0, n * sizeof(long long)));
+  }
+  c->trace_on = on ? 1 : 0;
+  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);  // the trace pointer is a kernel argument
+  c->graphs.clear();
+  return AS2D_OK;
+}
+
+int as2d_step_trace_read(as2d_ctx* c, int64_t* host, int64_t max, int32_t* grid, int32_t* n_phase) {
+  if (!c || !host || !grid || !n_phase) return AS2D_EINVAL;
+  if (!c->ptrace) return fail(c, AS2D_ESTATE, "step trace not enabled");
+  const int G = std::max(c->pers_grid[1], c->pers_grid[2]);
+  const int64_t n = (int64_t)G * c->n_phase * 3;
+  if (max < n) return fail(c, AS2D_EINVAL, "need %lld entries", (long long)n);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(host, c->ptrace, n * sizeof(long long), hipMemcpyDeviceToHost));
+  *grid = G;
+  *n_phase = c->n_phase;
   return AS2D_OK;
 }
 
@@ -864,6 +1112,67 @@ int as2d_timing_read(as2d_ctx* c, char* names, double* total_ms, int64_t* counts
     counts[k] = c->t_n[k];
   }
   return n;
+}
+
+int as2d_time_gemm(as2d_ctx* c, int32_t which, int32_t rows, int32_t reps, double* avg_us) {
+  if (!c || !avg_us || which < 0 || which > 4 || rows < 1 || rows > kMaxRows || reps < 1)
+    return c ? fail(c, AS2D_EINVAL, "time_gemm: bad arguments") : AS2D_EINVAL;
+  const as2d_config& g = c->cfg;
+  hipStream_t s = c->stream;
+  // rows describe positions 0..rows-1 of slot 0: only the QKV epilogue reads
+  // them (cache rows it overwrites are in bounds; their contents are garbage)
+  for (int i = 0; i < rows; ++i) c->h_rows[i] = RowDesc{0, 0, std::min(i, g.max_kv_len - 1), 0, -1, {0, 0, 0}};
+  HIP_TRY(c, hipMemcpyAsync(c->d_rows, c->h_rows, sizeof(RowDesc) * rows, hipMemcpyHostToDevice, s));
+  hipEvent_t e0 = ev_get(c, 1000), e1 = ev_get(c, 1001);
+  if (!e0 || !e1) return fail(c, AS2D_EHIP, "time_gemm: events");
+  auto launch = [&](int l) -> int {
+    const LayerW& w = c->layers[l];
+    GemmArgs a;
+    int am = A_NORM, epi = EPI_QKV;
+    switch (which) {
+      case 0:
+        a = base_args(c, c->p_qkv, w.qkv, rows);
+        a.A = c->xg; a.a_plane = c->xg_plane; a.bias = w.bias; a.q_out = c->q;
+        a.k_cache = c->kc + (size_t)l * c->layer_stride; a.v_cache = c->vc + (size_t)l * c->layer_stride;
+        a.slot_stride = c->slot_stride; a.kv_cap = g.max_kv_len; a.n_q = g.n_q_heads;
+        a.n_kv = g.n_kv_heads; a.head_dim = g.head_dim; a.rope_cs = c->rope_cs;
+        break;
+      case 1:
+        a = base_args(c, c->p_o, w.o, rows);
+        a.A = c->attn; a.a_plane = c->attn_plane; a.x = c->x; a.x_out = c->x; a.sumsq_out = c->sumsq;
+        a.gain_next = w.g_mlp; a.out = c->xg; a.out_plane = c->xg_plane;
+        am = A_PLAIN; epi = EPI_RESID;
+        break;
+      case 2:
+        a = base_args(c, c->p_gu, w.gu, rows);
+        a.A = c->xg; a.a_plane = c->xg_plane; a.out = c->hbuf; a.out_plane = c->h_plane;
+        epi = EPI_SWIGLU;
+        break;
+      case 3:
+        a = base_args(c, c->p_down, w.down, rows);
+        a.A = c->hbuf; a.a_plane = c->h_plane; a.x = c->x; a.x_out = c->x; a.sumsq_out = c->sumsq;
+        a.gain_next = w.g_attn; a.out = c->xg; a.out_plane = c->xg_plane;
+        am = A_PLAIN; epi = EPI_RESID;
+        break;
+      default:
+        a = base_args(c, c->p_lm, c->lm, rows);
+        a.A = c->xg; a.a_plane = c->xg_plane; a.amax_val = c->amax_val; a.amax_idx = c->amax_idx;
+        epi = EPI_ARGMAX;
+    }
+    HIP_TRY(c, launch_gemm(c->bf16, am, epi, a, s));
+    return AS2D_OK;
+  };
+  int rc = launch(0);  // warm-up
+  if (rc) return rc;
+  HIP_TRY(c, hipEventRecord(e0, s));
+  for (int i = 0; i < reps; ++i)
+    if ((rc = launch(which == 4 ? 0 : i % g.n_layers))) return rc;
+  HIP_TRY(c, hipEventRecord(e1, s));
+  HIP_TRY(c, hipEventSynchronize(e1));
+  float ms = 0.f;
+  HIP_TRY(c, hipEventElapsedTime(&ms, e0, e1));
+  *avg_us = ms * 1e3 / reps;
+  return AS2D_OK;
 }
 
 int64_t as2d_step_bytes(const as2d_ctx* c, int32_t rows, int64_t kv_keys) {

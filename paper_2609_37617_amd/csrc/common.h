@@ -1,0 +1,155 @@
+// Device helpers shared by the per-operation kernels (kernels.hip) and the
+// persistent step kernel (step.hip): number formats, MFMA steps, memory
+// access flavours and wave reductions.
+#pragma once
+#include <math.h>
+
+#include "kernels.h"
+
+namespace as2d {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// element formats
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;  // NaN stays NaN
+  u += 0x7fffu + ((u >> 16) & 1u);                      // round to nearest even
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+
+template <bool BF> struct ET;
+template <> struct ET<true> { typedef uint16_t T; static constexpr int PER16 = 8; };
+template <> struct ET<false> { typedef float T; static constexpr int PER16 = 4; };
+
+__device__ __forceinline__ float to_f(uint16_t v) { return bf2f(v); }
+__device__ __forceinline__ float to_f(float v) { return v; }
+
+// ---------------------------------------------------------------------------
+// Stores of values other workgroups read.  COH = true: inside one kernel,
+// possibly from another XCD (whose L2 is not coherent with the writer's):
+// agent-scope stores that write through the L2.  COH = false: read only by
+// later kernels (kernel boundaries make them visible).
+
+template <bool COH, typename V> __device__ __forceinline__ void st(V* p, V v) {
+  if constexpr (COH)
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else
+    *p = v;
+}
+template <typename V> __device__ __forceinline__ V ld_coherent(const V* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Activation planes (kernels.h): store value v at element i.
+template <bool BF, bool COH> __device__ __forceinline__ void store_act(void* base, long long plane, size_t i, float v) {
+  if constexpr (BF) {
+    uint16_t* b = static_cast<uint16_t*>(base);
+    const uint16_t hi = f2bf(v);
+    st<COH>(b + i, hi);
+    st<COH>(b + i + plane, f2bf(v - bf2f(hi)));
+  } else {
+    st<COH>(static_cast<float*>(base) + i, v);
+  }
+}
+
+// Wait until this wave's memory operations (its stores included) have been
+// performed.
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Agent-scope counter increment; returns the previous value.
+__device__ __forceinline__ int counter_add(int* c, int v) {
+  return __hip_atomic_fetch_add(c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// MFMA steps.  16 bytes of A (row m = lane%16) times 16 bytes of B (column
+// n = lane%16), accumulated into the 16x16 tile: lane holds rows
+// 4*(lane/16)+i, column lane%16.  Lane group g = lane/16 carries the
+// k-slice [g*PER16, (g+1)*PER16) of the step in both operands.
+
+template <bool BF> __device__ __forceinline__ f4 mma_step(uint4 a, uint4 b, f4 acc);
+template <> __device__ __forceinline__ f4 mma_step<true>(uint4 a, uint4 b, f4 acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+}
+template <> __device__ __forceinline__ f4 mma_step<false>(uint4 a, uint4 b, f4 acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  return acc;
+}
+
+// One k-step of one 16-row A tile: bf16 models carry (hi, lo), float32 one part.
+struct AFrag {
+  uint4 h, l;
+};
+template <bool BF> __device__ __forceinline__ f4 mma_a(const AFrag& a, uint4 b, f4 acc) {
+  if constexpr (BF) {
+    acc = mma_step<true>(a.h, b, acc);
+    acc = mma_step<true>(a.l, b, acc);
+  } else {
+    acc = mma_step<false>(a.h, b, acc);
+  }
+  return acc;
+}
+
+// Streaming (non-temporal) 16-byte load of weight tiles: read once per pass.
+__device__ __forceinline__ uint4 ldw(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// Split-K partials cross workgroups (and XCDs) inside one kernel: written
+// and read with agent-scope accesses, so no fence has to write back or
+// invalidate a whole L2.
+__device__ __forceinline__ void store_partial(float* p, float v) { st<true>(p, v); }
+__device__ __forceinline__ float load_partial(const float* p) { return ld_coherent(p); }
+
+// Workgroup barrier ordering LDS only: outstanding global loads (the weight
+// prefetch) stay in flight across it.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Fixed-pattern wave reductions; callers use lane 0's result.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+// (value, index) arg-max: larger value wins, equal values keep the lower index.
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float ov = __shfl_xor(v, o);
+    int oi = __shfl_xor(i, o);
+    if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+  }
+}
+
+// GEMM tile constants
+constexpr int kPrefetch = 4;       // k-steps of weights (and A) in flight per wave
+constexpr int kFStride = 132;      // floats per row of the epilogue tile
+constexpr int kFRows = 64;         // rows per epilogue pass
+constexpr int kDirectMT = 2;       // largest M-tile count loading A directly
+constexpr int kLdsBudget = 61440;  // bytes of A staging
+
+__host__ __device__ inline int lds_row_stride(int chunk_kt) {
+  return ((chunk_kt * 64 + 127) / 128) * 128 + 16;
+}
+
+}  // namespace as2d

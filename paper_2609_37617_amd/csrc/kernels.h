@@ -22,7 +22,7 @@ constexpr int kGroupCols = kWaves * kTilesPerWave * 16;   // 128 columns per wor
 constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
 constexpr int kAttnChunk = 32;          // keys per attention split
-constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
+constexpr int kMaxSplits = 32;          // largest k-split count of a GEMM
 constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
 
 // One processed row of a forward pass.
@@ -72,7 +72,8 @@ struct GemmArgs {
   int kv_cap;            // positions per slot
   int n_q, n_kv, head_dim;
   const float* rope_cs;  // [kv_cap][head_dim/2][2] (cos, sin)
-  float* x;              // EPI_RESID: residual [M][N] updated in place
+  const float* x;        // EPI_RESID: residual [M][N] read
+  float* x_out;          // EPI_RESID: x + Y written (may equal x)
   float* sumsq_out;      // EPI_RESID: [N/128][kMaxRows]
   const float* gain_next;// EPI_RESID: RMSNorm gain of the next consumer of x
   void* out;             // EPI_RESID: planes of x * gain_next; EPI_SWIGLU: planes of h
@@ -100,6 +101,42 @@ struct AttnArgs {
   int M;
 };
 
+// Persistent step kernel (step.hip): one verification pass of up to 32 rows.
+struct StepLayer {
+  GemmArgs qkv, o, gu, down;
+  AttnArgs attn;
+};
+
+struct StepArgs {
+  const StepLayer* layers;   // device array, one per decoder layer
+  int n_layers;
+  GemmArgs lm;
+  int M;                     // rows of the pass
+  const RowDesc* rows;
+  const void* embed;
+  const void* audio;
+  int hidden;
+  const float* gain0;        // first RMSNorm gain
+  float* x0;                 // embedding outputs (inputs of layer 0)
+  float* sumsq0;
+  void* xg0;
+  long long xg0_plane;
+  const ReqDesc* reqs;       // attention requests
+  int n_reqs;
+  int n_q;
+  const ReqDesc* fin_reqs;   // verified requests and their rows
+  int n_fin;
+  int fin_rows;
+  int* row_tok;
+  int* row_bad;
+  StepOut* out;
+  int groups_qkv, groups_o, groups_gu, groups_down, groups_lm;
+  int* phase_cnt;            // 3 + 6 * n_layers counters, cleared by the launcher
+  int* err;                  // set when a wait times out
+  int spin_limit;
+  long long* trace;          // optional [grid][3 + 6 * n_layers][3] wall-clock stamps
+};
+
 // Launchers (all asynchronous on `s`).  `bf16` selects the model dtype.
 hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int remap_gate_up,
                        int F, hipStream_t s);
@@ -107,6 +144,10 @@ hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed
                         int H, const float* gain, float* x, float* sumsq, void* xg, long long xg_plane,
                         hipStream_t s);
 hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStream_t s);
+int step_lds_bytes(int head_dim, int hidden);
+hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int* blocks_per_cu);
+hipError_t launch_step(bool bf16, int MT, int head_dim, const StepArgs& a, int grid, int n_counters,
+                       hipStream_t s);
 hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s);
 // n_rows = sum of the requests' W; counters: one per request, zero between launches.
 hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,

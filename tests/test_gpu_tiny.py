@@ -202,25 +202,40 @@ def test_non_finite_logits_are_reported():
     gpu.close()
 
 
-def test_graph_replays_match_eager(pair):
-    """Verification passes replayed from a captured HIP graph give the
-    eager result bit for bit, replay after replay, with eager work and
-    synchronisations in between."""
+@pytest.mark.parametrize("mode", ["graph", "persistent"])
+@pytest.mark.parametrize("k", [0, 6, 20])
+def test_exec_modes_match_eager(pair, mode, k):
+    """Verification passes replayed from a captured HIP graph, of per-op
+    kernels or of the persistent step kernel, give the eager result bit
+    for bit, replay after replay, with eager work and synchronisations in
+    between."""
+    from paper_2609_37617_amd import as2d
+    m = {"graph": as2d.EXEC_GRAPH, "persistent": as2d.EXEC_PERSISTENT}[mode]
     shape, _, gpu = pair
     first, L = _prefilled(gpu, shape, seed=8)
     rng = np.random.default_rng(8)
-    cands = [int(t) for t in rng.integers(0, shape.vocab, 6)]
-    gpu.set_graphs(False)
+    cands = [int(t) for t in rng.integers(0, shape.vocab, k)]
+    gpu.set_exec_mode(as2d.EXEC_EAGER)
     ref = gpu.verify(0, cands)
     ref_logits = gpu.logits(0)
+    ref_kv = gpu.read_kv(0, shape.n_layers - 1, L + k + 1)
     gpu.rollback(0, L, first)
     for rep in range(4):
-        gpu.set_graphs(True)
+        gpu.set_exec_mode(m)
         r = gpu.verify(0, cands)
         assert r == ref, rep
         assert np.array_equal(gpu.logits(0), ref_logits), rep
+        kv = gpu.read_kv(0, shape.n_layers - 1, L + k + 1)
+        assert np.array_equal(kv[0], ref_kv[0]) and np.array_equal(kv[1], ref_kv[1]), rep
         gpu.rollback(0, L, first)
-        gpu.set_graphs(False)             # eager work between replays
+        gpu.set_exec_mode(as2d.EXEC_EAGER)   # eager work between replays
         gpu.decode_one(0)
         gpu.rollback(0, L, first)
-    gpu.set_graphs(True)
+    gpu.set_exec_mode(as2d.EXEC_GRAPH)
+
+
+def test_persistent_kernel_available(pair):
+    from paper_2609_37617_amd import as2d
+    _, _, gpu = pair
+    mode, grid = gpu.exec_info()
+    assert mode == as2d.EXEC_GRAPH and grid >= 256
