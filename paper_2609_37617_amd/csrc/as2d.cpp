@@ -23,7 +23,7 @@ using namespace as2d;
 namespace {
 
 struct GemmPlan {
-  int N = 0, K = 0, KT = 0, groups = 0, KS = 1, ktps = 0;
+  int N = 0, K = 0, KT = 0, pairs = 0, KS = 1, ktps = 0, np = 1;
 };
 
 struct LayerW {
@@ -141,19 +141,22 @@ int dalloc(as2d_ctx* c, P** p, size_t bytes) {
   return AS2D_OK;
 }
 
-// k-split plan of one matrix.  A tile (128-column group, k-split) is the
-// unit of work; the split count aims at about `target` tiles per matrix
-// (a few per compute unit) with at least 4 k-steps per tile and at most
-// 16 splits.  It depends only on the matrix shape, never on the rows of a
-// pass, so every row is computed alike in every pass.
+// Work plan of one matrix.  Wide matrices (at least 1024 tile pairs) give
+// each direct-path workgroup two pairs, so one activation fragment feeds
+// twice the weights; the others one.  The k-split count then aims at about
+// `target` workgroups with at least 8 k-steps per split (two per quarter)
+// and at most kMaxSplits splits.  The plan depends only on the matrix
+// shape, never on the rows of a pass, and the pairs per workgroup do not
+// change any sum, so every row is computed alike in every pass.
 GemmPlan make_plan(int N, int K, int KE, int target) {
   GemmPlan p;
   p.N = N;
   p.K = K;
   p.KT = K / KE;
-  p.groups = N / kGroupCols;
-  int ks = (int)std::lround((double)target / p.groups);
-  ks = std::max(1, std::min({ks, std::max(1, p.KT / 4), 16}));
+  p.pairs = N / kPairCols;
+  p.np = p.pairs >= 1024 ? 2 : 1;
+  int ks = (int)std::lround((double)target / (p.pairs / p.np));
+  ks = std::max(1, std::min({ks, std::max(1, p.KT / 8), kMaxSplits}));
   p.ktps = (p.KT + ks - 1) / ks;
   p.KS = (p.KT + p.ktps - 1) / p.ktps;
   return p;
@@ -221,10 +224,11 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   a.KT = pl.KT;
   a.KS = pl.KS;
   a.ktps = pl.ktps;
+  a.np = pl.np;
   a.M = M;
   a.MT = (M + 15) / 16;
   a.sumsq = c->sumsq;
-  a.n_norm_groups = c->cfg.hidden / kGroupCols;
+  a.n_norm_pairs = c->cfg.hidden / kPairCols;
   a.a_plane = 0;
   a.eps = c->cfg.rms_eps;
   a.part = c->part;
@@ -343,7 +347,7 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
     {
       Timed t(c, K_FINISH);
       HIP_TRY(c, launch_finish(c->d_rows, c->d_reqs + mr, n_fin, fin_rows, c->amax_val, c->amax_idx,
-                               g.vocab / kGroupCols, c->row_tok, c->row_bad, c->fin_counters, c->d_out, s));
+                               g.vocab / kPairCols, c->row_tok, c->row_bad, c->fin_counters, c->d_out, s));
     }
   }
   return AS2D_OK;
@@ -358,7 +362,7 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
   const int H = g.hidden, F = g.ffn, d = g.head_dim, nq = g.n_q_heads, nkv = g.n_kv_heads;
   const long long R = kStepRows;
   const size_t xs = (size_t)R * H;                        // floats of one x / planes of one xg
-  const size_t ss = (size_t)(H / 128) * kMaxRows;         // sum-of-squares partials
+  const size_t ss = (size_t)(H / kPairCols) * kMaxRows;   // sum-of-squares partials
   const size_t qs = (size_t)R * nq * d;
   auto xg = [&](int i) { return (void*)((char*)c->pxg + i * xs * 4); };
   std::vector<StepLayer> v(g.n_layers);
@@ -449,7 +453,7 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   if (!layers) return fail(c, AS2D_ENOMEM, "persistent step arguments");
   const int L = g.n_layers, H = g.hidden;
   const size_t xs = (size_t)kStepRows * H;
-  const size_t ss = (size_t)(H / 128) * kMaxRows;
+  const size_t ss = (size_t)(H / kPairCols) * kMaxRows;
   StepArgs a{};
   a.layers = layers;
   a.n_layers = L;
@@ -480,11 +484,11 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   a.row_tok = c->row_tok;
   a.row_bad = c->row_bad;
   a.out = c->d_out;
-  a.groups_qkv = c->p_qkv.groups;
-  a.groups_o = c->p_o.groups;
-  a.groups_gu = c->p_gu.groups;
-  a.groups_down = c->p_down.groups;
-  a.groups_lm = c->p_lm.groups;
+  a.pairs_qkv = c->p_qkv.pairs;
+  a.pairs_o = c->p_o.pairs;
+  a.pairs_gu = c->p_gu.pairs;
+  a.pairs_down = c->p_down.pairs;
+  a.pairs_lm = c->p_lm.pairs;
   a.phase_cnt = c->pphase;
   a.err = c->perr;
   a.spin_limit = env_int("AS2D_SPIN_LIMIT", 1 << 21);
@@ -569,10 +573,10 @@ int upload_matrix(as2d_ctx* c, void* tmp, const void* host, size_t rows, size_t 
   return AS2D_OK;
 }
 
-int pack(as2d_ctx* c, uint4** out, const void* tmp, int N, int K, int remap, int F) {
+int pack(as2d_ctx* c, uint4** out, const void* tmp, int N, int K, int map, int arg) {
   int rc = dalloc(c, out, (size_t)N * K * c->es);
   if (rc) return rc;
-  HIP_TRY(c, launch_pack(c->bf16, tmp, *out, N, K, remap, F, c->stream));
+  HIP_TRY(c, launch_pack(c->bf16, tmp, *out, N, K, map, arg, c->stream));
   return AS2D_OK;
 }
 
@@ -654,7 +658,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   if (H % KE || (nq * d) % KE || F % KE) return bad("inner dimensions must be multiples of the k-step");
 
   // GEMM plans: k-splits depend on the matrix shape only
-  const int target = env_int("AS2D_TARGET_WGS", 512);
+  const int target = env_int("AS2D_TARGET_WGS", 256);
   c->p_qkv = make_plan(qkv_n, H, KE, target);
   c->p_o = make_plan(H, nq * d, KE, target);
   c->p_gu = make_plan(2 * F, H, KE, target);
@@ -686,7 +690,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
       HIP_TRY(c, hipMemcpyAsync(t, host[ti++], (size_t)nkv * d * H * c->es, hipMemcpyHostToDevice, c->stream));
       t += (size_t)nkv * d * H * c->es;
       HIP_TRY(c, hipMemcpyAsync(t, host[ti++], (size_t)nkv * d * H * c->es, hipMemcpyHostToDevice, c->stream));
-      CK(pack(c, &w.qkv, tmp, qkv_n, H, 0, 0));
+      CK(pack(c, &w.qkv, tmp, qkv_n, H, PACK_ROPE_PAIRS, d));
       HIP_TRY(c, hipStreamSynchronize(c->stream));
       if (g.qkv_bias) {
         CK(dalloc(c, &w.bias, qkv_n * 4));
@@ -695,22 +699,22 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
         HIP_TRY(c, hipMemcpyAsync(w.bias + (nq + nkv) * d, host[ti++], nkv * d * 4, hipMemcpyHostToDevice, c->stream));
       }
       CK(upload_matrix(c, tmp, host[ti++], H, nq * d));
-      CK(pack(c, &w.o, tmp, H, nq * d, 0, 0));
+      CK(pack(c, &w.o, tmp, H, nq * d, PACK_IDENTITY, 0));
       HIP_TRY(c, hipStreamSynchronize(c->stream));
       CK(dalloc(c, &w.g_mlp, H * 4));
       HIP_TRY(c, hipMemcpyAsync(w.g_mlp, host[ti++], H * 4, hipMemcpyHostToDevice, c->stream));
       CK(upload_matrix(c, tmp, host[ti++], F, H));
       CK(upload_matrix(c, (char*)tmp + (size_t)F * H * c->es, host[ti++], F, H));
-      CK(pack(c, &w.gu, tmp, 2 * F, H, 1, F));
+      CK(pack(c, &w.gu, tmp, 2 * F, H, PACK_GATE_UP, F));
       HIP_TRY(c, hipStreamSynchronize(c->stream));
       CK(upload_matrix(c, tmp, host[ti++], H, F));
-      CK(pack(c, &w.down, tmp, H, F, 0, 0));
+      CK(pack(c, &w.down, tmp, H, F, PACK_IDENTITY, 0));
       HIP_TRY(c, hipStreamSynchronize(c->stream));
     }
     CK(dalloc(c, &c->g_final, H * 4));
     HIP_TRY(c, hipMemcpyAsync(c->g_final, host[ti++], H * 4, hipMemcpyHostToDevice, c->stream));
     CK(upload_matrix(c, tmp, host[ti++], V, H));
-    CK(pack(c, &c->lm, tmp, V, H, 0, 0));
+    CK(pack(c, &c->lm, tmp, V, H, PACK_IDENTITY, 0));
     HIP_TRY(c, hipStreamSynchronize(c->stream));
     return AS2D_OK;
   };
@@ -742,9 +746,9 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     c->h_plane = (long long)MR * F;
   }
   CK(dalloc(c, &c->logits, (size_t)MR * V * 4));
-  CK(dalloc(c, &c->sumsq, (size_t)(H / 128) * MR * 4));
-  CK(dalloc(c, &c->amax_val, (size_t)(V / 128) * MR * 4));
-  CK(dalloc(c, &c->amax_idx, (size_t)(V / 128) * MR * 4));
+  CK(dalloc(c, &c->sumsq, (size_t)(H / kPairCols) * MR * 4));
+  CK(dalloc(c, &c->amax_val, (size_t)(V / kPairCols) * MR * 4));
+  CK(dalloc(c, &c->amax_idx, (size_t)(V / kPairCols) * MR * 4));
   CK(dalloc(c, &c->row_tok, (size_t)MR * 4));
   CK(dalloc(c, &c->row_bad, (size_t)MR * 4));
   CK(dalloc(c, &c->fin_counters, (size_t)g.max_requests * 4));
@@ -753,8 +757,11 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
     if (p->KS > 1) part_elems = std::max(part_elems, (size_t)p->KS * MR * p->N);
   CK(dalloc(c, &c->part, part_elems * 4));
-  CK(dalloc(c, &c->counters, 8192 * 4));
-  HIP_TRY(c, hipMemsetAsync(c->counters, 0, 8192 * 4, c->stream));
+  // split-K counters: one per workgroup tile (at most one per tile pair)
+  const int n_cnt = std::max({c->p_qkv.pairs, c->p_o.pairs, c->p_gu.pairs, c->p_down.pairs, c->p_lm.pairs});
+  CK(dalloc(c, &c->counters, (size_t)n_cnt * 4));
+  HIP_TRY(c, hipMemsetAsync(c->counters, 0, (size_t)n_cnt * 4, c->stream));
+  HIP_TRY(c, prepare_kernels());
   // persistent step kernel (verification passes of up to 32 rows)
   if (env_int("AS2D_PERSISTENT", 1)) {
     int dev = 0, cus = 0, occ1 = 0, occ2 = 0;
@@ -769,12 +776,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
       c->pers_grid[2] = occ2 * cus;
       CK(dalloc(c, &c->px, (size_t)(2 * L + 1) * R * H * 4));
       CK(dalloc(c, &c->pxg, (size_t)(2 * L + 1) * R * H * 4));
-      CK(dalloc(c, &c->psumsq, (size_t)(2 * L + 1) * (H / 128) * kMaxRows * 4));
+      CK(dalloc(c, &c->psumsq, (size_t)(2 * L + 1) * (H / kPairCols) * kMaxRows * 4));
       CK(dalloc(c, &c->pq, (size_t)L * R * nq * d * 4));
       CK(dalloc(c, &c->pattn, (size_t)L * R * nq * d * 4));
       CK(dalloc(c, &c->ph, (size_t)L * R * F * 4));
-      c->split_stride = std::max({c->p_qkv.groups, c->p_o.groups, c->p_gu.groups, c->p_down.groups,
-                                  c->p_lm.groups});
+      c->split_stride = std::max({c->p_qkv.pairs, c->p_o.pairs, c->p_gu.pairs, c->p_down.pairs,
+                                  c->p_lm.pairs});
       const size_t n_split = (size_t)(4 * L + 1) * c->split_stride;
       CK(dalloc(c, &c->psplit, n_split * 4));
       HIP_TRY(c, hipMemsetAsync(c->psplit, 0, n_split * 4, c->stream));

@@ -46,6 +46,18 @@ template <typename V> __device__ __forceinline__ V ld_coherent(const V* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Index of element (m, k) of an activation operand with K columns in MFMA
+// fragment order: one block of 16 rows x KE elements (one k-step of one
+// 16-row tile, 1 KiB) after another, tiles outer, k-steps inner; inside a
+// block the 16 rows are row-major, so the rows a pass uses are a prefix of
+// the block (rows past M need not be loaded).
+template <bool BF> __host__ __device__ __forceinline__ size_t frag_index(int m, int k, int K) {
+  constexpr int KE = 4 * ET<BF>::PER16;
+  return (size_t)(m >> 4) * 16 * K + (size_t)(k / KE) * 16 * KE + (size_t)(m & 15) * KE + (k % KE);
+}
+// 16-byte unit of a block that lane l feeds to the MFMA (row l % 16, k-slice l / 16).
+__device__ __forceinline__ int frag_lane_unit(int lane) { return (lane & 15) * 4 + (lane >> 4); }
+
 // Activation planes (kernels.h): store value v at element i.
 template <bool BF, bool COH> __device__ __forceinline__ void store_act(void* base, long long plane, size_t i, float v) {
   if constexpr (BF) {
@@ -120,7 +132,8 @@ __device__ __forceinline__ void lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Fixed-pattern wave reductions; callers use lane 0's result.
+// Fixed-pattern wave reductions.  Every lane ends with the same bits (a
+// butterfly adds the same two values on both partner lanes).
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -140,16 +153,26 @@ __device__ __forceinline__ void wave_argmax(float& v, int& i) {
     if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
   }
 }
+// The same over each half-wave (lanes 0-31 and 32-63 separately).
+__device__ __forceinline__ float half_sum(float v) {
+#pragma unroll
+  for (int o = 16; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ void half_argmax(float& v, int& i) {
+#pragma unroll
+  for (int o = 16; o > 0; o >>= 1) {
+    float ov = __shfl_xor(v, o);
+    int oi = __shfl_xor(i, o);
+    if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+  }
+}
 
 // GEMM tile constants
-constexpr int kPrefetch = 4;       // k-steps of weights (and A) in flight per wave
-constexpr int kFStride = 132;      // floats per row of the epilogue tile
-constexpr int kFRows = 64;         // rows per epilogue pass
-constexpr int kDirectMT = 2;       // largest M-tile count loading A directly
+constexpr int kPrefetch = 4;       // k-steps of weights in flight per wave (A staged in LDS)
+constexpr int kPrefetchDirect = 4; // k-steps of weights and A in flight per wave (A direct)
+constexpr int kFStride = 132;      // floats per row of the staged path's epilogue tile
+constexpr int kFRows = 64;         // rows per epilogue pass of the staged path
 constexpr int kLdsBudget = 61440;  // bytes of A staging
-
-__host__ __device__ inline int lds_row_stride(int chunk_kt) {
-  return ((chunk_kt * 64 + 127) / 128) * 128 + 16;
-}
 
 }  // namespace as2d

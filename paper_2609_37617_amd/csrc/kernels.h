@@ -7,23 +7,39 @@
 // operand that is an activation is handed over as "planes": for bf16
 // models two bf16 planes hi = bf16(a), lo = bf16(a - hi) (a = hi + lo to
 // about 2^-17 relative), multiplied into the bf16 weights by two MFMAs;
-// for float32 models a single float32 plane.  Planes are [kMaxRows][K]
-// row-major, the lo plane `plane` elements after the hi plane.
+// for float32 models a single float32 plane.  A plane holds [kMaxRows][K]
+// elements in MFMA fragment order (frag_index in common.h): every 16-row
+// tile and k-step is one contiguous 1 KiB block, read by one wave with one
+// load.  The lo plane starts `plane` elements after the hi plane.
+//
+// Per-pair partials (sum of squares for RMSNorm, arg-max of the LM head)
+// are row-major [row][N / 32], so the partials of one row are contiguous.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace as2d {
 
-// GEMM tiling shared by the packer and the GEMM kernels.
+// GEMM tiling shared by the packer and the GEMM kernels.  The unit of
+// output columns is a tile pair: 32 columns, two 16-column MFMA tiles.
 constexpr int kWaves = 4;               // waves per workgroup
-constexpr int kTilesPerWave = 2;        // 16-column tiles per wave
-constexpr int kGroupCols = kWaves * kTilesPerWave * 16;   // 128 columns per workgroup
+constexpr int kPairCols = 32;           // columns of a tile pair
+constexpr int kQuarters = 4;            // ordered partial sums per k-split
+constexpr int kPairsS = kWaves;         // tile pairs per workgroup, staged path
 constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
+constexpr int kDirectMT = 2;            // row tiles of the direct path (up to 32 rows)
 constexpr int kAttnChunk = 32;          // keys per attention split
-constexpr int kMaxSplits = 32;          // largest k-split count of a GEMM
+constexpr int kMaxSplits = 8;           // largest k-split count of a GEMM
 constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
+
+// Column order of a packed matrix (pack_kernel): which matrix row (output
+// column) sits at column 16 j + c of tile pair tp.
+enum PackMap {
+  PACK_IDENTITY = 0,   // n = 32 tp + 16 j + c
+  PACK_GATE_UP = 1,    // rows [gate; up] (F each): n = j F + 16 tp + c
+  PACK_ROPE_PAIRS = 2  // heads of d rows: dims i and i + d/2 share a pair
+};
 
 // One processed row of a forward pass.
 struct RowDesc {
@@ -50,18 +66,19 @@ enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_ARGMAX = 3 };
 struct GemmArgs {
   const uint4* W;        // packed weight tiles
   int N, K, KT, KS, ktps;
+  int np;                // tile pairs per workgroup on the direct path (1 or 2)
   int M, MT;
   // A operand: activation planes [kMaxRows][K].  For A_NORM the planes
   // hold x * g (residual times RMSNorm gain) and the epilogue multiplies
   // row m by 1 / sqrt(sum(x^2) / K + eps) from the sum-of-squares partials.
   const void* A;
   long long a_plane;
-  const float* sumsq;    // A_NORM: [n_norm_groups][kMaxRows]
-  int n_norm_groups;
+  const float* sumsq;    // A_NORM: per-pair partials [kMaxRows][K / 32]
+  int n_norm_pairs;
   float eps;
   // split-K scratch
   float* part;           // [KS][M][N]
-  int* counters;         // one per column group, zero between launches
+  int* counters;         // one per workgroup tile, zero between launches
   // epilogue
   const RowDesc* rows;
   const float* bias;     // EPI_QKV (may be null)
@@ -74,12 +91,12 @@ struct GemmArgs {
   const float* rope_cs;  // [kv_cap][head_dim/2][2] (cos, sin)
   const float* x;        // EPI_RESID: residual [M][N] read
   float* x_out;          // EPI_RESID: x + Y written (may equal x)
-  float* sumsq_out;      // EPI_RESID: [N/128][kMaxRows]
+  float* sumsq_out;      // EPI_RESID: per-pair partials [kMaxRows][N / 32]
   const float* gain_next;// EPI_RESID: RMSNorm gain of the next consumer of x
   void* out;             // EPI_RESID: planes of x * gain_next; EPI_SWIGLU: planes of h
   long long out_plane;
   float* logits;         // EPI_ARGMAX: optional [M][N]
-  float* amax_val;       // EPI_ARGMAX: [N/128][kMaxRows]
+  float* amax_val;       // EPI_ARGMAX: per-pair partials [kMaxRows][N / 32]
   int* amax_idx;
 };
 
@@ -130,16 +147,23 @@ struct StepArgs {
   int* row_tok;
   int* row_bad;
   StepOut* out;
-  int groups_qkv, groups_o, groups_gu, groups_down, groups_lm;
+  int pairs_qkv, pairs_o, pairs_gu, pairs_down, pairs_lm;  // tiles per phase
   int* phase_cnt;            // 3 + 6 * n_layers counters, cleared by the launcher
   int* err;                  // set when a wait times out
   int spin_limit;
   long long* trace;          // optional [grid][3 + 6 * n_layers][3] wall-clock stamps
 };
 
+// Sets the launch attributes of kernels that may use more than 64 KiB of
+// LDS; call once per process before the first launch (prepare_kernels
+// calls prepare_step_kernels).
+hipError_t prepare_kernels();
+hipError_t prepare_step_kernels();
+
 // Launchers (all asynchronous on `s`).  `bf16` selects the model dtype.
-hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int remap_gate_up,
-                       int F, hipStream_t s);
+// map: PackMap; arg: F for PACK_GATE_UP, the head dimension for PACK_ROPE_PAIRS.
+hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int map, int arg,
+                       hipStream_t s);
 hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed, const void* audio,
                         int H, const float* gain, float* x, float* sumsq, void* xg, long long xg_plane,
                         hipStream_t s);
@@ -148,10 +172,12 @@ int step_lds_bytes(int head_dim, int hidden);
 hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int* blocks_per_cu);
 hipError_t launch_step(bool bf16, int MT, int head_dim, const StepArgs& a, int grid, int n_counters,
                        hipStream_t s);
+// Attention over n_reqs requests; max_chunks bounds the 32-key chunks of
+// any request (the grid size).
 hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s);
 // n_rows = sum of the requests' W; counters: one per request, zero between launches.
 hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,
-                         const float* amax_val, const int* amax_idx, int n_groups, int* row_tok,
+                         const float* amax_val, const int* amax_idx, int n_pairs, int* row_tok,
                          int* row_bad, int* counters, StepOut* out, hipStream_t s);
 
 }  // namespace as2d

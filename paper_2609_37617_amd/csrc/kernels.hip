@@ -15,18 +15,29 @@ namespace as2d {
 
 // ---------------------------------------------------------------------------
 // Weight packing: row-major [N][K] -> 1 KiB tiles in the order one wave
-// streams them.  Tile (nt, kt) covers rows [16 nt, 16 nt + 16) and k-step kt;
-// lane l holds row 16 nt + l%16, elements [kt*KE + (l/16)*PER16, +PER16).
-// Tiles of a wave's pair (nt = 2 tp + j) are adjacent per k-step:
-//   index ((tp * KT + kt) * 2 + j) * 64 + lane.
-// remap_gate_up: virtual row v of the fused gate/up matrix ([gate; up] in
-// src, 2F rows) takes gate row 64 g + c for c < 64 and up row 64 g + c - 64
-// otherwise (g = v / 128, c = v % 128), so each 128-column group holds the
-// gate and up columns of the same 64 FFN units.
+// streams them.  Tile pair tp holds 32 output columns as two 16-column
+// tiles j; per k-step kt the pair's two tiles are adjacent:
+//   index ((tp * KT + kt) * 2 + j) * 64 + lane
+// and lane l holds matrix row n(tp, j, l % 16) at elements
+// [kt * KE + (l / 16) * PER16, + PER16) (the MFMA B operand of column l % 16).
+// The column order n(tp, j, c) is the PackMap of kernels.h: gate/up puts
+// gate unit u and up unit u in the same pair, RoPE pairs put dimensions i
+// and i + d/2 of a head in the same pair, so the fused epilogues find both
+// operands in one workgroup.
+
+__device__ __forceinline__ int packed_row(int map, int arg, int tp, int j, int c) {
+  if (map == PACK_GATE_UP) return j * arg + 16 * tp + c;
+  if (map == PACK_ROPE_PAIRS) {
+    const int d = arg, ppd = d / kPairCols;
+    const int head = tp / ppd, q = tp % ppd;
+    return head * d + j * (d / 2) + 16 * q + c;
+  }
+  return tp * kPairCols + 16 * j + c;
+}
 
 template <bool BF>
 __global__ void pack_kernel(const typename ET<BF>::T* __restrict__ src, uint4* __restrict__ dst,
-                            int N, int K, int remap, int F) {
+                            int N, int K, int map, int arg) {
   constexpr int PER16 = ET<BF>::PER16;
   constexpr int KE = 4 * PER16;
   const int KT = K / KE;
@@ -39,24 +50,22 @@ __global__ void pack_kernel(const typename ET<BF>::T* __restrict__ src, uint4* _
     const long long u = t >> 1;
     const int kt = (int)(u % KT);
     const int tp = (int)(u / KT);
-    const int nt = tp * 2 + j;
-    int row = nt * 16 + (lane & 15);
-    if (remap) {
-      const int g = row / 128, c = row % 128;
-      row = c < 64 ? 64 * g + c : F + 64 * g + (c - 64);
-    }
+    const int row = packed_row(map, arg, tp, j, lane & 15);
     const int k0 = kt * KE + (lane >> 4) * PER16;
     dst[idx] = *reinterpret_cast<const uint4*>(src + (size_t)row * K + k0);
   }
 }
 
-hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int remap, int F,
+hipError_t launch_pack(bool bf16, const void* src, uint4* dst, int N, int K, int map, int arg,
                        hipStream_t s) {
   const int threads = 256, blocks = 4096;
+  if (N % kPairCols || (map == PACK_GATE_UP && N != 2 * arg) ||
+      (map == PACK_ROPE_PAIRS && (arg % kPairCols || N % arg)))
+    return hipErrorInvalidValue;
   if (bf16)
-    pack_kernel<true><<<blocks, threads, 0, s>>>((const uint16_t*)src, dst, N, K, remap, F);
+    pack_kernel<true><<<blocks, threads, 0, s>>>((const uint16_t*)src, dst, N, K, map, arg);
   else
-    pack_kernel<false><<<blocks, threads, 0, s>>>((const float*)src, dst, N, K, remap, F);
+    pack_kernel<false><<<blocks, threads, 0, s>>>((const float*)src, dst, N, K, map, arg);
   return hipGetLastError();
 }
 
@@ -90,39 +99,64 @@ hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed
 
 // ---------------------------------------------------------------------------
 // Weight-streaming GEMM  Y[M][N] = A[M][K] * W[N][K]^T  for small M
-// (gemm_tile), one workgroup per (128-column group, k-split).
-//
-// Workgroup = 4 waves over one 128-column group and one k-split; wave w
-// owns the tile pair 4*group + w.  Each k-step a wave loads its two 1 KiB
-// weight tiles (fully coalesced, non-temporal) and the A fragments of the
-// same k-step, U steps ahead of their use.  Up to two 16-row tiles of A
-// come straight from the L2-resident activation planes; larger M stages A
-// through LDS in chunks.  Both paths issue the same MFMA sequence per row,
-// so a row's result does not depend on M.  With KS > 1 each split writes a
-// float32 partial and the last workgroup of a column group (device-scope
+// (tiles.h).  Up to 32 rows (direct path): one workgroup per (np tile
+// pairs, k-split), its four waves streaming the four quarters of the split,
+// each k-step's 1 KiB weight tiles (fully coalesced, non-temporal) and the
+// activation fragments issued three or four k-steps ahead of their use.  More rows
+// (staged path): one workgroup per (4 tile pairs, k-split), activations
+// staged through LDS.  Both paths add every element in the same order, so
+// a row's result does not depend on M.  With KS > 1 each split writes a
+// float32 partial and the last workgroup of the tile (device-scope
 // counter) sums the partials in split order and runs the fused epilogue.
 
+template <bool BF, int MT, int NP, int AM, int EPI, bool SPLIT>
+__global__ __launch_bounds__(256, MT == 1 ? (NP == 1 ? 5 : 4) : 4) void gemm_direct_kernel(const GemmArgs p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ float s_scale[kMaxRows];
+  __shared__ int s_flag;
+  const int tile = blockIdx.x / p.KS, split = blockIdx.x - tile * p.KS;
+  gemm_tile_direct<BF, MT, NP, AM, EPI, false, SPLIT>(p, p.M, tile, split, smem, s_scale, &s_flag, [] {});
+}
+
+template <bool BF, int MT, int NP, int AM, int EPI>
+static void launch_direct(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid((a.N / kPairCols / NP) * a.KS), block(256);
+  constexpr int lds = gemm_direct_lds_bytes<MT, NP>();
+  if (a.KS > 1) gemm_direct_kernel<BF, MT, NP, AM, EPI, true><<<grid, block, lds, s>>>(a);
+  else gemm_direct_kernel<BF, MT, NP, AM, EPI, false><<<grid, block, lds, s>>>(a);
+}
+
 template <bool BF, int MT, int AM, int EPI>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs p, const int chunk_kt) {
+__global__ __launch_bounds__(256) void gemm_staged_kernel(const GemmArgs p, const int chunk_kt) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;
   const int group = blockIdx.x / p.KS, split = blockIdx.x - group * p.KS;
-  gemm_tile<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, chunk_kt, [] {});
+  gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, chunk_kt);
 }
 
 template <bool BF, int AM, int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
-  const int regions = BF ? 2 : 1;
-  int chunk = a.ktps;
-  while (chunk > 1 && regions * a.MT * 16 * lds_row_stride(chunk) > kLdsBudget) --chunk;
-  int lds = kFRows * kFStride * 4;
-  if (a.MT > kDirectMT) lds = max(lds, regions * a.MT * 16 * lds_row_stride(chunk));
-  const dim3 grid((a.N / kGroupCols) * a.KS), block(256);
+  const int pairs = a.N / kPairCols;
+  if (a.MT <= kDirectMT) {
+    if (a.np != 1 && (a.np != 2 || pairs % 2)) return hipErrorInvalidValue;
+    if (a.MT == 1) {
+      if (a.np == 1) launch_direct<BF, 1, 1, AM, EPI>(a, s);
+      else launch_direct<BF, 1, 2, AM, EPI>(a, s);
+    } else {
+      if (a.np == 1) launch_direct<BF, 2, 1, AM, EPI>(a, s);
+      else launch_direct<BF, 2, 2, AM, EPI>(a, s);
+    }
+    return hipGetLastError();
+  }
+  if (pairs % kPairsS) return hipErrorInvalidValue;
+  const int chunk = staged_chunk(BF, a.MT);
+  const dim3 grid((pairs / kPairsS) * a.KS), block(256);
+  const int lds = gemm_staged_lds_bytes();
   switch (a.MT) {
 #define AS2D_MT(mt) \
-  case mt: gemm_kernel<BF, mt, AM, EPI><<<grid, block, lds, s>>>(a, chunk); break;
-    AS2D_MT(1) AS2D_MT(2) AS2D_MT(3) AS2D_MT(4) AS2D_MT(5) AS2D_MT(6) AS2D_MT(7) AS2D_MT(8) AS2D_MT(9)
+  case mt: gemm_staged_kernel<BF, mt, AM, EPI><<<grid, block, lds, s>>>(a, chunk); break;
+    AS2D_MT(3) AS2D_MT(4) AS2D_MT(5) AS2D_MT(6) AS2D_MT(7) AS2D_MT(8) AS2D_MT(9)
 #undef AS2D_MT
     default: return hipErrorInvalidValue;
   }
@@ -143,14 +177,10 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // ---------------------------------------------------------------------------
 // Block-causal grouped-query attention, split over the key axis.
 //
-// Workgroup (chunk c, query head h, request r): keys [32c, 32c + 32) of the
-// request's float32 cache slot are staged in LDS; each wave takes the
-// request's rows in turn (the next row's query is prefetched into
-// registers).  For a row at position pos >= 32c it computes the chunk's
-// softmax statistics (max m, sum l of exp(s - m)) and the unnormalised
-// output sum_j exp(s_j - m) v_j over keys j <= pos; lane pairs (j, j + 32)
-// each take half of the dot product of key j.  The merge kernel combines a
-// row's chunks in ascending order.
+// Workgroup (chunk c, query head h, request r) runs attn_chunk_tile over
+// keys [32 c, 32 c + 32) of the request's float32 cache slot; the merge
+// kernel, one workgroup per (head, row), combines a row's chunks in
+// ascending order (attn_merge_row).
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_chunk_kernel(const AttnArgs p) {
@@ -176,6 +206,9 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, h
   return hipGetLastError();
 }
 
+// Kernels whose dynamic LDS may exceed the default 64 KiB limit.
+hipError_t prepare_kernels() { return prepare_step_kernels(); }
+
 hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
   if (a.head_dim == 128) return bf16 ? attn_dispatch<true, 128>(a, n_reqs, max_chunks, s)
                                      : attn_dispatch<false, 128>(a, n_reqs, max_chunks, s);
@@ -185,14 +218,14 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_ch
 }
 
 // ---------------------------------------------------------------------------
-// Final arg-max over the LM head's per-group partials, one workgroup per
+// Final arg-max over the LM head's per-pair partials, one workgroup per
 // verified row, then greedy verification by the last row of each request
 // to finish (device-scope counter per request).
 
 __global__ __launch_bounds__(256) void finish_kernel(const RowDesc* __restrict__ rows,
                                                      const ReqDesc* __restrict__ reqs, int n_reqs,
                                                      const float* __restrict__ amax_val,
-                                                     const int* __restrict__ amax_idx, int n_groups,
+                                                     const int* __restrict__ amax_idx, int n_pairs,
                                                      int* __restrict__ row_tok, int* __restrict__ row_bad,
                                                      int* __restrict__ counters, StepOut* __restrict__ out) {
   __shared__ float s4f[4];
@@ -202,7 +235,7 @@ __global__ __launch_bounds__(256) void finish_kernel(const RowDesc* __restrict__
   while (r < n_reqs - 1 && i >= reqs[r].W) i -= reqs[r++].W;
   const ReqDesc rq = reqs[r];
   const int row = rq.row_start + i;
-  argmax_row<false>(amax_val, amax_idx, n_groups, row, &s_tok, &s_bad, s4f, s4i);
+  argmax_row<false>(amax_val, amax_idx, n_pairs, row, &s_tok, &s_bad, s4f, s4i);
   if (threadIdx.x == 0) {
     st<true>(row_tok + row, s_tok);
     st<true>(row_bad + row, s_bad);
@@ -217,9 +250,9 @@ __global__ __launch_bounds__(256) void finish_kernel(const RowDesc* __restrict__
 }
 
 hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,
-                         const float* amax_val, const int* amax_idx, int n_groups, int* row_tok,
+                         const float* amax_val, const int* amax_idx, int n_pairs, int* row_tok,
                          int* row_bad, int* counters, StepOut* out, hipStream_t s) {
-  finish_kernel<<<n_rows, 256, 0, s>>>(rows, reqs, n_reqs, amax_val, amax_idx, n_groups, row_tok, row_bad,
+  finish_kernel<<<n_rows, 256, 0, s>>>(rows, reqs, n_reqs, amax_val, amax_idx, n_pairs, row_tok, row_bad,
                                        counters, out);
   return hipGetLastError();
 }

@@ -23,9 +23,9 @@
 namespace as2d {
 
 // Phase counter layout (phase_cnt): 0 embedding; per layer l, base 1 + 6 l:
-// +0 QKV groups, +1 attention chunk tiles, +2 merged (row, head) pairs,
-// +3 O groups, +4 gate/up groups, +5 down groups; then LM head groups
-// (1 + 6 L) and verified rows (2 + 6 L).
+// +0 QKV tile pairs, +1 attention chunk tiles, +2 merged (row, head) pairs,
+// +3 O tile pairs, +4 gate/up tile pairs, +5 down tile pairs; then LM head
+// tile pairs (1 + 6 L) and verified rows (2 + 6 L).
 __device__ __forceinline__ int ph_layer(int l, int k) { return 1 + 6 * l + k; }
 
 __device__ __forceinline__ void signal_done(int* c) {
@@ -62,13 +62,13 @@ template <bool BF, int MT, int AM, int EPI>
 __device__ void gemm_phase(const GemmArgs p, int M, const int* wait_c, int wait_target, int* done_c,
                            const StepArgs& a, unsigned char* smem, float* s_scale, int* s_flag) {
   const int G = gridDim.x;
-  const int n_tiles = (p.N / kGroupCols) * p.KS;
+  const int n_tiles = (p.N / kPairCols) * p.KS;
   const int phase = (int)(done_c - a.phase_cnt);
   stamp(a, phase, 0);
   bool waited = false;
   for (int t = blockIdx.x; t < n_tiles; t += G) {
-    const int group = t / p.KS, split = t - group * p.KS;
-    const bool fin = gemm_tile<BF, MT, AM, EPI, true>(p, M, group, split, smem, s_scale, s_flag, p.ktps, [&] {
+    const int pair = t / p.KS, split = t - pair * p.KS;
+    const bool fin = gemm_tile_direct<BF, MT, 1, AM, EPI, true, true>(p, M, pair, split, smem, s_scale, s_flag, [&] {
       if (!waited) {
         wait_count(wait_c, wait_target, a.err, a.spin_limit);
         stamp(a, phase, 1);
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
   for (int l = 0; l < L; ++l) {
     const StepLayer& ly = a.layers[l];
     const int* prev = l == 0 ? &a.phase_cnt[0] : &a.phase_cnt[ph_layer(l - 1, 5)];
-    const int prev_target = l == 0 ? M : a.groups_down;
+    const int prev_target = l == 0 ? M : a.pairs_down;
     gemm_phase<BF, MT, A_NORM, EPI_QKV>(ly.qkv, M, prev, prev_target, &a.phase_cnt[ph_layer(l, 0)], a, smem,
                                          s_scale, &s_flag);
 
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
       const int nch = (rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk;
       const int h = u / nch, c = u - h * nch;
       if (!waited) {
-        wait_count(&a.phase_cnt[ph_layer(l, 0)], a.groups_qkv, a.err, a.spin_limit);
+        wait_count(&a.phase_cnt[ph_layer(l, 0)], a.pairs_qkv, a.err, a.spin_limit);
         stamp(a, ph_layer(l, 1), 1);
         waited = true;
       }
@@ -163,12 +163,12 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
 
     gemm_phase<BF, MT, A_PLAIN, EPI_RESID>(ly.o, M, &a.phase_cnt[ph_layer(l, 2)], n_merge,
                                             &a.phase_cnt[ph_layer(l, 3)], a, smem, s_scale, &s_flag);
-    gemm_phase<BF, MT, A_NORM, EPI_SWIGLU>(ly.gu, M, &a.phase_cnt[ph_layer(l, 3)], a.groups_o,
+    gemm_phase<BF, MT, A_NORM, EPI_SWIGLU>(ly.gu, M, &a.phase_cnt[ph_layer(l, 3)], a.pairs_o,
                                             &a.phase_cnt[ph_layer(l, 4)], a, smem, s_scale, &s_flag);
-    gemm_phase<BF, MT, A_PLAIN, EPI_RESID>(ly.down, M, &a.phase_cnt[ph_layer(l, 4)], a.groups_gu,
+    gemm_phase<BF, MT, A_PLAIN, EPI_RESID>(ly.down, M, &a.phase_cnt[ph_layer(l, 4)], a.pairs_gu,
                                             &a.phase_cnt[ph_layer(l, 5)], a, smem, s_scale, &s_flag);
   }
-  gemm_phase<BF, MT, A_NORM, EPI_ARGMAX>(a.lm, M, &a.phase_cnt[ph_layer(L - 1, 5)], a.groups_down,
+  gemm_phase<BF, MT, A_NORM, EPI_ARGMAX>(a.lm, M, &a.phase_cnt[ph_layer(L - 1, 5)], a.pairs_down,
                                           &a.phase_cnt[1 + 6 * L], a, smem, s_scale, &s_flag);
 
   // arg-max of each verified row on the last workgroups, then verification
@@ -177,8 +177,8 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
     int r = 0, u = i;
     while (r < a.n_fin - 1 && u >= a.fin_reqs[r].W) u -= a.fin_reqs[r++].W;
     const int row = a.fin_reqs[r].row_start + u;
-    wait_count(&a.phase_cnt[1 + 6 * L], a.groups_lm, a.err, a.spin_limit);
-    argmax_row<true>(a.lm.amax_val, a.lm.amax_idx, a.lm.N / kGroupCols, row, &s_tok, &s_bad, s4f, s4i);
+    wait_count(&a.phase_cnt[1 + 6 * L], a.pairs_lm, a.err, a.spin_limit);
+    argmax_row<true>(a.lm.amax_val, a.lm.amax_idx, a.lm.N / kPairCols, row, &s_tok, &s_bad, s4f, s4i);
     if (tid == 0) {
       st<true>(a.row_tok + row, s_tok);
       st<true>(a.row_bad + row, s_bad);
@@ -217,11 +217,24 @@ static const void* pick(bool bf16, int MT, int D) {
 }
 
 int step_lds_bytes(int head_dim, int hidden) {
-  int b = kFRows * kFStride * 4;
+  // hidden <= 8192
+  int b = gemm_direct_lds_bytes<2, 1>();
   b = max(b, head_dim == 128 ? attn_lds_bytes<128>() : attn_lds_bytes<64>());
   b = max(b, hidden * 4);                      // embedding row
   b = max(b, (256 / head_dim) * 2 * kMaxChunks * 4);  // merge scratch
   return b;
+}
+
+hipError_t prepare_step_kernels() {
+  const int lds128 = step_lds_bytes(128, 8192), lds64 = step_lds_bytes(64, 8192);
+  const void* fns[8] = {step_fn<true, 1, 128>(), step_fn<true, 2, 128>(), step_fn<false, 1, 128>(),
+                        step_fn<false, 2, 128>(), step_fn<true, 1, 64>(),  step_fn<true, 2, 64>(),
+                        step_fn<false, 1, 64>(),  step_fn<false, 2, 64>()};
+  for (int i = 0; i < 8; ++i) {
+    hipError_t e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, i < 4 ? lds128 : lds64);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int* blocks_per_cu) {

@@ -12,7 +12,7 @@ namespace as2d {
 // ---------------------------------------------------------------------------
 // Embedding gather of row m: residual x (float32) from a token embedding or
 // an audio staging row, the planes of x * g for the first RMSNorm (gain g),
-// and per-row sum-of-squares partials over 128-column groups.  256 threads;
+// and the row's sum-of-squares partials per 32-column pair.  256 threads;
 // srow: LDS scratch of H floats.
 
 template <bool BF, bool COH>
@@ -52,205 +52,437 @@ __device__ void embed_row(const RowDesc* __restrict__ rows, int m, const typenam
 #pragma unroll
       for (int t = 0; t < kPer; ++t) {
         st<COH>(x + (size_t)m * H + c0 + t, v[ps][t]);
-        store_act<BF, COH>(xg, xg_plane, (size_t)m * H + c0 + t, v[ps][t] * gain[c0 + t]);
+        store_act<BF, COH>(xg, xg_plane, frag_index<BF>(m, c0 + t, H), v[ps][t] * gain[c0 + t]);
         srow[c0 + t] = v[ps][t];
       }
     }
   }
   lds_sync();
+  // one pair per half-wave
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int g = wave; g < H / 128; g += 4) {
-    const float v0 = srow[g * 128 + lane], v1 = srow[g * 128 + 64 + lane];
-    const float s = wave_sum(v0 * v0 + v1 * v1);
-    if (lane == 0) st<COH>(sumsq + g * kMaxRows + m, s);
+  const int n_pairs = H / kPairCols;
+  for (int u0 = wave * 2; u0 < n_pairs; u0 += 8) {
+    const int g = u0 + (lane >> 5);
+    const float e = g < n_pairs ? srow[g * kPairCols + (lane & 31)] : 0.0f;
+    const float s = half_sum(e * e);
+    if ((lane & 31) == 0 && g < n_pairs) st<COH>(sumsq + (size_t)m * n_pairs + g, s);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Fused GEMM epilogues over rows [r0, r1) of one 128-column group; F holds
-// the group's finished values (float32, row stride kFStride).
+// Fused GEMM epilogues over rows [r0, r1) of `np` consecutive tile pairs
+// starting at pair `pair0`; F holds their finished values (float32, row
+// stride fs, pair pp at columns [32 pp, 32 pp + 32)).  256 threads.  Every
+// per-pair reduction runs on one half-wave in a fixed pattern, so a row's
+// results do not depend on how many pairs or rows the call covers.
 
 template <bool BF, int EPI, bool COH>
-__device__ void epilogue_rows(const GemmArgs& p, float* F, int group, int r0, int r1) {
+__device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, int np, int r0, int r1) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int N = p.N;
+  const int N = p.N, C = np * kPairCols;
+  const int n0 = pair0 * kPairCols;
+  const int units = (r1 - r0) * np;           // (row, pair) units of the reductions
   if constexpr (EPI == EPI_RESID) {
     // x_out = x + Y; planes of x_out * g for the next RMSNorm; sum of squares
-    for (int idx = tid; idx < (r1 - r0) * 128; idx += 256) {
-      const int m = r0 + (idx >> 7), c = idx & 127;
-      const int n = group * 128 + c;
+    for (int idx = tid; idx < (r1 - r0) * C; idx += 256) {
+      const int m = r0 + idx / C, c = idx % C;
+      const int n = n0 + c;
       const size_t o = (size_t)m * N + n;
-      const float v = p.x[o] + F[(m - r0) * kFStride + c];
+      const float v = p.x[o] + F[(m - r0) * fs + c];
       st<COH>(p.x_out + o, v);
-      store_act<BF, COH>(p.out, p.out_plane, o, v * p.gain_next[n]);
-      F[(m - r0) * kFStride + c] = v;
+      store_act<BF, COH>(p.out, p.out_plane, frag_index<BF>(m, n, N), v * p.gain_next[n]);
+      F[(m - r0) * fs + c] = v;
     }
     lds_sync();
-    for (int m = r0 + wave; m < r1; m += 4) {
-      const float v0 = F[(m - r0) * kFStride + lane], v1 = F[(m - r0) * kFStride + 64 + lane];
-      const float s = wave_sum(v0 * v0 + v1 * v1);
-      if (lane == 0) st<COH>(p.sumsq_out + group * kMaxRows + m, s);
+    for (int u0 = wave * 2; u0 < units; u0 += 8) {
+      const int u = u0 + (lane >> 5);
+      const bool ok = u < units;
+      const int m = ok ? r0 + u / np : r0, pp = u % np;
+      const float e = ok ? F[(m - r0) * fs + pp * kPairCols + (lane & 31)] : 0.0f;
+      const float s = half_sum(e * e);
+      if ((lane & 31) == 0 && ok) st<COH>(p.sumsq_out + (size_t)m * (N / kPairCols) + pair0 + pp, s);
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
+    // pair g: gate columns 16 g .. 16 g + 15 (tile 0), the same up columns (tile 1)
     const int F2 = N / 2;
-    for (int idx = tid; idx < (r1 - r0) * 64; idx += 256) {
-      const int m = r0 + (idx >> 6), c = idx & 63;
-      const float g = F[(m - r0) * kFStride + c], u = F[(m - r0) * kFStride + 64 + c];
-      store_act<BF, COH>(p.out, p.out_plane, (size_t)m * F2 + group * 64 + c, g / (1.0f + expf(-g)) * u);
+    for (int idx = tid; idx < (r1 - r0) * np * 16; idx += 256) {
+      const int m = r0 + idx / (np * 16), r = idx % (np * 16);
+      const int pp = r >> 4, c = r & 15;
+      const float g = F[(m - r0) * fs + pp * kPairCols + c], u = F[(m - r0) * fs + pp * kPairCols + 16 + c];
+      store_act<BF, COH>(p.out, p.out_plane, frag_index<BF>(m, (pair0 + pp) * 16 + c, F2),
+                         g / (1.0f + expf(-g)) * u);
     }
   } else if constexpr (EPI == EPI_QKV) {
-    const int d = p.head_dim, half = d >> 1;
-    const int q_cols = p.n_q * d, qk_cols = (p.n_q + p.n_kv) * d;
-    for (int idx = tid; idx < (r1 - r0) * 128; idx += 256) {
-      const int m = r0 + (idx >> 7), c = idx & 127;
-      const int n = group * 128 + c;
+    // PACK_ROPE_PAIRS: pair q of a head holds dims 16 q + c (tile 0) and
+    // d/2 + 16 q + c (tile 1), the two halves RoPE rotates together
+    const int d = p.head_dim, half = d >> 1, ppd = d / kPairCols;
+    for (int idx = tid; idx < (r1 - r0) * C; idx += 256) {
+      const int m = r0 + idx / C, c = idx % C;
+      const int pair = pair0 + c / kPairCols, j = (c >> 4) & 1, cc = c & 15;
+      const int head = pair / ppd, q = pair % ppd;
+      const int i = 16 * q + cc;                 // rotation index
+      const int dd = j * half + i;               // dimension within the head
+      const int n = head * d + dd;               // original output column
       const RowDesc rd = p.rows[m];
-      const float* Fr = F + (m - r0) * kFStride;
+      const float* Fr = F + (m - r0) * fs;
       float v = Fr[c] + (p.bias ? p.bias[n] : 0.0f);
-      const int dd = n % d;
-      if (n < qk_cols) {
-        const int i = dd % half;
-        const int pc = dd < half ? c + half : c - half;
-        const int pn = dd < half ? n + half : n - half;
-        const float partner = Fr[pc] + (p.bias ? p.bias[pn] : 0.0f);
+      if (head < p.n_q + p.n_kv) {
+        const int pn = j ? n - half : n + half;
+        const float partner = Fr[c ^ 16] + (p.bias ? p.bias[pn] : 0.0f);
         const float cs = p.rope_cs[((size_t)rd.pos * half + i) * 2];
         const float sn = p.rope_cs[((size_t)rd.pos * half + i) * 2 + 1];
-        v = dd < half ? v * cs - partner * sn : v * cs + partner * sn;
-        if (n < q_cols) {
-          st<COH>(p.q_out + (size_t)m * q_cols + n, v);
+        v = j == 0 ? v * cs - partner * sn : v * cs + partner * sn;
+        if (head < p.n_q) {
+          st<COH>(p.q_out + (size_t)m * p.n_q * d + n, v);
         } else {
-          const int kvh = (n - q_cols) / d;
+          const int kvh = head - p.n_q;
           st<COH>(p.k_cache + (size_t)rd.slot * p.slot_stride + ((size_t)kvh * p.kv_cap + rd.pos) * d + dd, v);
         }
       } else {
-        const int kvh = (n - qk_cols) / d;
+        const int kvh = head - p.n_q - p.n_kv;
         st<COH>(p.v_cache + (size_t)rd.slot * p.slot_stride + ((size_t)kvh * p.kv_cap + rd.pos) * d + dd, v);
       }
     }
-  } else {  // EPI_ARGMAX
-    for (int m = r0 + wave; m < r1; m += 4) {
-      const float v0 = F[(m - r0) * kFStride + lane], v1 = F[(m - r0) * kFStride + 64 + lane];
-      const int n0 = group * 128 + lane;
-      if (p.logits) {
-        p.logits[(size_t)m * N + n0] = v0;   // read by the host only
-        p.logits[(size_t)m * N + n0 + 64] = v1;
-      }
-      const bool bad = !(isfinite(v0) && isfinite(v1));
-      float best = v0;
-      int bi = n0;
-      if (v1 > best) { best = v1; bi = n0 + 64; }
-      wave_argmax(best, bi);
-      const bool any_bad = __ballot(bad) != 0;
-      if (lane == 0) {
-        st<COH>(p.amax_val + group * kMaxRows + m, any_bad ? __builtin_nanf("") : best);
-        st<COH>(p.amax_idx + group * kMaxRows + m, bi);
+  } else {  // EPI_ARGMAX (identity column order: column = token id)
+    for (int u0 = wave * 2; u0 < units; u0 += 8) {
+      const int u = u0 + (lane >> 5);
+      const bool ok = u < units;
+      const int m = ok ? r0 + u / np : r0, pp = u % np;
+      const int n = (pair0 + pp) * kPairCols + (lane & 31);
+      const float v = ok ? F[(m - r0) * fs + pp * kPairCols + (lane & 31)] : -INFINITY;
+      if (p.logits && ok) p.logits[(size_t)m * N + n] = v;   // read by the host only
+      const bool bad = ok && !isfinite(v);
+      float best = v;
+      int bi = n;
+      half_argmax(best, bi);
+      const unsigned long long mask = __ballot(bad);
+      const bool any_bad = ((mask >> (lane & 32)) & 0xffffffffull) != 0;
+      if ((lane & 31) == 0 && ok) {
+        st<COH>(p.amax_val + (size_t)m * (N / kPairCols) + pair0 + pp, any_bad ? __builtin_nanf("") : best);
+        st<COH>(p.amax_idx + (size_t)m * (N / kPairCols) + pair0 + pp, bi);
       }
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// One GEMM tile: 128-column group `group`, k-split `split` (see
-// kernels.hip for the scheme).  256 threads.  `wait()` is called after the
-// first weight loads are issued and before any activation is read (the
-// persistent kernel waits there for the producer of A).  Returns true when
-// this workgroup finished the group (ran its epilogue).
-//   smem: dynamic LDS (A staging for MT > kDirectMT, then the epilogue
-//   tile); s_scale: kMaxRows floats; s_flag: one int.
+// Split-K fixup, shared by both GEMM paths: the workgroup that finishes
+// tile `tile` last sums, for each of its output elements (rows < M, columns
+// [n0, n0 + C)), the KS split partials in split order, scales row m by
+// s_scale[m] (A_NORM) and writes the result to F (row stride fs, rows from
+// r0).  Loads are issued in batches across elements and splits.
 
-template <bool BF, int MT, int AM, int EPI, bool COH, class Wait>
-__device__ bool gemm_tile(const GemmArgs& p, int M, int group, int split, unsigned char* smem, float* s_scale,
-                          int* s_flag, int chunk_kt, Wait&& wait) {
-  using T = typename ET<BF>::T;
-  constexpr int PER16 = ET<BF>::PER16;
-  constexpr int KE = 4 * PER16;           // elements per k-step
-  constexpr bool kDirect = MT <= kDirectMT;
+template <int AM>
+__device__ void fixup_rows(const GemmArgs& p, int M, int n0, int C, int r0, int r1, const float* s_scale,
+                           float* F, int fs) {
+  constexpr int kEl = 2;   // elements per thread per batch (kEl x kMaxSplits loads in flight)
+  const int E = (r1 - r0) * C;
+  for (int e0 = threadIdx.x; e0 < E; e0 += 256 * kEl) {
+    float v[kEl][kMaxSplits];
+#pragma unroll
+    for (int t = 0; t < kEl; ++t) {
+      const int e = e0 + t * 256;
+      const int m = r0 + e / C, c = e % C;
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp)
+        if (e < E && sp < p.KS) v[t][sp] = load_partial(&p.part[((size_t)sp * M + m) * p.N + n0 + c]);
+    }
+#pragma unroll
+    for (int t = 0; t < kEl; ++t) {
+      const int e = e0 + t * 256;
+      if (e < E) {
+        const int m = r0 + e / C, c = e % C;
+        float sum = v[t][0];
+#pragma unroll
+        for (int sp = 1; sp < kMaxSplits; ++sp)
+          if (sp < p.KS) sum += v[t][sp];
+        F[(m - r0) * fs + c] = AM == A_NORM ? sum * s_scale[m] : sum;
+      }
+    }
+  }
+}
+
+// Quarter q of the k-range [kt0, kt0 + n): [kt0 + q n / 4, kt0 + (q + 1) n / 4).
+__device__ __forceinline__ int quarter_start(int kt0, int n, int q) { return kt0 + (q * n) / kQuarters; }
+
+// Publishes a workgroup's split partials for (rows < M, columns [n0, n0 + C))
+// given by `val(m, c)` and returns true in the workgroup that arrives last
+// at counter `cnt` (it then resets the counter for the next launch).
+template <class Val>
+__device__ bool publish_split(const GemmArgs& p, int M, int split, int n0, int C, int* cnt, int* s_flag, Val&& val) {
+  for (int e = threadIdx.x; e < M * C; e += 256) {
+    const int m = e / C, c = e % C;
+    store_partial(&p.part[((size_t)split * M + m) * p.N + n0 + c], val(m, c));
+  }
+  wait_vmem();
+  __syncthreads();  // every wave's partial stores are performed
+  if (threadIdx.x == 0) *s_flag = counter_add(cnt, 1) == p.KS - 1;
+  __syncthreads();
+  if (!*s_flag) return false;
+  if (threadIdx.x == 0) st<true>(cnt, 0);  // ready for the next launch
+  return true;
+}
+
+// Row scales 1 / sqrt(mean(x^2) + eps) of an A_NORM GEMM for rows [0, M)
+// into s_scale, from the rows' per-pair sum-of-squares partials (at most
+// 256 pairs: hidden <= 8192).  Each row is summed in a fixed pattern (lane
+// l: partials l, l + 64, ...; then a butterfly), so its value depends on
+// the row alone; wave w takes rows w, w + 4, ..., eight rows per batch with
+// all their loads in flight together.
+template <int AM>
+__device__ __forceinline__ void row_scales(const GemmArgs& p, int M, float* s_scale) {
+  if constexpr (AM == A_NORM) {
+    constexpr int kR = 8, kT = 4;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int np = p.n_norm_pairs;
+    for (int m0 = wave; m0 < M; m0 += kWaves * kR) {
+      float s[kR];
+#pragma unroll
+      for (int r = 0; r < kR; ++r) {
+        const int m = m0 + kWaves * r;
+        s[r] = 0.0f;
+#pragma unroll
+        for (int t = 0; t < kT; ++t)
+          if (m < M && lane + 64 * t < np) s[r] += p.sumsq[(size_t)m * np + lane + 64 * t];
+      }
+#pragma unroll
+      for (int r = 0; r < kR; ++r) {
+        const int m = m0 + kWaves * r;
+        const float tot = wave_sum(s[r]);
+        if (lane == 0 && m < M) s_scale[m] = 1.0f / sqrtf(tot / (float)p.K + p.eps);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// GEMM tiles.  Every output element is summed in one order whatever the
+// path, the tile shape or the number of rows: k-split s of the plan
+// (splits in order), in quarters (quarter_start, in order), each quarter
+// accumulated over its k-steps in order by MFMA from zero; then
+// ((q0 + q1) + q2) + q3 per split and the splits added in order.  A row's
+// result therefore depends on the matrix shape alone, never on the rows
+// that share the pass.
+//
+// Direct path (up to kDirectMT row tiles): a workgroup owns NP tile pairs
+// (32 NP columns) of one split; wave q streams quarter q of the split for
+// all NP pairs, with the activation fragments (one per k-step, shared by
+// the NP pairs) loaded straight from the planes, and the quarters meet in
+// LDS.  `wait()` is called after the first weight loads are issued and
+// before any activation is read (the persistent kernel waits there for the
+// producer of A).  Returns true when this workgroup finished its pairs
+// (ran their epilogue).
+//   smem: dynamic LDS of gemm_direct_lds_bytes<MT, NP>(); s_scale: kMaxRows
+//   floats; s_flag: one int.
+
+template <int MT, int NP> __host__ __device__ constexpr int gemm_direct_lds_bytes() {
+  return (kQuarters * MT * NP * 512 + 16 * MT * (NP * kPairCols + 1)) * 4;
+}
+// k-steps in flight per wave: four, fewer when a k-step holds more registers
+template <int MT, int NP> __host__ __device__ constexpr int direct_prefetch() {
+  return NP + MT >= 3 ? 3 : kPrefetchDirect;
+}
+
+// SPLIT = false: the caller guarantees KS == 1 (no fixup code, fewer registers).
+template <bool BF, int MT, int NP, int AM, int EPI, bool COH, bool SPLIT, class Wait>
+__device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, unsigned char* smem,
+                                 float* s_scale, int* s_flag, Wait&& wait) {
+  static_assert(MT <= kDirectMT, "direct path row tiles");
+  constexpr int P = direct_prefetch<MT, NP>();
+  constexpr int FS = NP * kPairCols + 1;   // row stride of the epilogue tile
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int kt0 = split * p.ktps;
-  const int kt1 = min(p.KT, kt0 + p.ktps);
-  const int K = p.K;
+  const int n_all = min(p.KT, kt0 + p.ktps) - kt0;
+  const int qa = quarter_start(kt0, n_all, wave), n = quarter_start(kt0, n_all, wave + 1) - qa;
+  const int pair0 = tile * NP;
 
-  f4 acc[MT][2];
+  f4 acc[MT][NP][2];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    acc[mt][0] = f4{0.f, 0.f, 0.f, 0.f};
-    acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
-  }
-  const uint4* wp = p.W + (size_t)(group * kWaves + wave) * p.KT * 128 + lane;
-  auto step = [&](const uint4(&bb)[2], const AFrag(&af)[MT]) {
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      acc[mt][0] = mma_a<BF>(af[mt], bb[0], acc[mt][0]);
-      acc[mt][1] = mma_a<BF>(af[mt], bb[1], acc[mt][1]);
+    for (int q = 0; q < NP; ++q) {
+      acc[mt][q][0] = f4{0.f, 0.f, 0.f, 0.f};
+      acc[mt][q][1] = f4{0.f, 0.f, 0.f, 0.f};
+    }
+  const uint4* wp = p.W + (size_t)pair0 * p.KT * 128 + lane;
+  const size_t pstride = (size_t)p.KT * 128;        // next pair's tiles
+  const uint4* ap = static_cast<const uint4*>(p.A) + frag_lane_unit(lane);
+  const long long lo = p.a_plane / ET<BF>::PER16;   // lo plane, in 16-byte units
+  auto loadW = [&](int kt, uint4(&bb)[NP][2]) {
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      bb[q][0] = ldw(wp + q * pstride + (size_t)kt * 128);
+      bb[q][1] = ldw(wp + q * pstride + (size_t)kt * 128 + 64);
     }
   };
-
-  if constexpr (kDirect) {
-    // A fragments straight from the activation planes (rows >= M read
-    // values that only reach output rows that are never stored)
-    const T* abase = (const T*)p.A + (size_t)(lane & 15) * K + (lane >> 4) * PER16;
-    auto loadW = [&](int kt, uint4(&bb)[2]) {
-      bb[0] = ldw(wp + (size_t)kt * 128);
-      bb[1] = ldw(wp + (size_t)kt * 128 + 64);
-    };
-    auto loadA = [&](int kt, AFrag(&af)[MT]) {
+  // rows >= M are not loaded: their lanes keep zeros or stale values that
+  // only reach output rows >= M, which are never stored
+  auto loadA = [&](int kt, AFrag(&af)[MT]) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const T* a = abase + (size_t)mt * 16 * K + (size_t)kt * KE;
-        af[mt].h = *reinterpret_cast<const uint4*>(a);
-        if constexpr (BF) af[mt].l = *reinterpret_cast<const uint4*>(a + p.a_plane);
+    for (int mt = 0; mt < MT; ++mt) {
+      if (mt * 16 + (lane & 15) < M) {
+        const uint4* a = ap + ((size_t)mt * p.KT + kt) * 64;
+        af[mt].h = *a;
+        if constexpr (BF) af[mt].l = a[lo];
       }
-    };
-    const int n = kt1 - kt0;
-    uint4 b[kPrefetch][2];
-    AFrag af[kPrefetch][MT];
+    }
+  };
+  auto step = [&](const uint4(&bb)[NP][2], const AFrag(&af)[MT]) {
 #pragma unroll
-    for (int u = 0; u < kPrefetch; ++u) loadW(kt0 + min(u, n - 1), b[u]);
-    wait();
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int u = 0; u < kPrefetch; ++u) loadA(kt0 + min(u, n - 1), af[u]);
-    int i = 0;
-    for (; i + 2 * kPrefetch <= n; i += kPrefetch) {
+      for (int q = 0; q < NP; ++q) {
+        acc[mt][q][0] = mma_a<BF>(af[mt], bb[q][0], acc[mt][q][0]);
+        acc[mt][q][1] = mma_a<BF>(af[mt], bb[q][1], acc[mt][q][1]);
+      }
+  };
+  // Loads retire in issue order, so every k-step's wait is exact only if
+  // the loads are always issued in the same order: (W, A) of step s + P
+  // right after step s.  The first round is written out apart from the
+  // loop because its weights are issued before `wait()` (ahead of the
+  // activations); after it the loop is entered with the loads in its own
+  // order.  Loads past the end re-read the last k-step (clamped), so no
+  // round issues a different number of loads.  A wave whose quarter is
+  // empty (splits of fewer than 4 k-steps) only joins the wait.
+  auto kk = [&](int s) { return qa + min(s, n - 1); };
+  uint4 b[P][NP][2];
+  AFrag af[P][MT];
 #pragma unroll
-      for (int u = 0; u < kPrefetch; ++u) {
+  for (int u = 0; u < P; ++u)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) af[u][mt] = AFrag{make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+  if (n > 0) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) loadW(kk(u), b[u]);
+  }
+  wait();
+  if (n > 0) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) loadA(kk(u), af[u]);
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      if (u == 0 || u < n) step(b[u], af[u]);
+      loadW(kk(u + P), b[u]);
+      loadA(kk(u + P), af[u]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    int i = P;
+    for (; i + P <= n; i += P) {
+#pragma unroll
+      for (int u = 0; u < P; ++u) {
         step(b[u], af[u]);
-        loadW(kt0 + i + u + kPrefetch, b[u]);
-        loadA(kt0 + i + u + kPrefetch, af[u]);
+        loadW(kk(i + u + P), b[u]);
+        loadA(kk(i + u + P), af[u]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 #pragma unroll
-    for (int u = 0; u < kPrefetch; ++u) {
-      if (i + u < n) {
-        step(b[u], af[u]);
-        if (i + u + kPrefetch < n) {
-          loadW(kt0 + i + u + kPrefetch, b[u]);
-          loadA(kt0 + i + u + kPrefetch, af[u]);
-        }
-      }
-    }
-    i += kPrefetch;
-#pragma unroll
-    for (int u = 0; u < kPrefetch; ++u)
+    for (int u = 0; u < P; ++u)
       if (i + u < n) step(b[u], af[u]);
+  }
+
+  // quarters meet in LDS: R[quarter][mt][pair][j][i][lane]
+  constexpr int QS = MT * NP * 512;               // floats per quarter
+  float* R = reinterpret_cast<float*>(smem);
+  float* F = R + kQuarters * QS;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int q = 0; q < NP; ++q)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          R[wave * QS + (((mt * NP + q) * 2 + j) * 4 + i) * 64 + lane] = acc[mt][q][j][i];
+  const bool split_k = SPLIT && p.KS > 1;
+  if (!split_k) row_scales<AM>(p, M, s_scale);
+  __syncthreads();
+  // element x = (((mt * NP + q) * 2 + j) * 4 + i) * 64 + l: row 16 mt + 4 (l / 16) + i,
+  // column 32 q + 16 j + l % 16
+  constexpr int kE = QS / 256;
+  float v[kE];
+#pragma unroll
+  for (int e = 0; e < kE; ++e) {
+    const int x = tid + 256 * e;
+    float s = R[x];
+#pragma unroll
+    for (int q = 1; q < kQuarters; ++q) s += R[q * QS + x];
+    v[e] = s;
+  }
+  auto row_of = [](int x) { return (x >> 6) / (8 * NP) * 16 + 4 * ((x & 63) >> 4) + ((x >> 6) & 3); };
+  auto col_of = [](int x) { return ((x >> 9) % NP) * kPairCols + ((x >> 8) & 1) * 16 + (x & 15); };
+  const int n0 = pair0 * kPairCols;
+  if (split_k) {
+    // split partials through the epilogue tile: F[row][col] first, then publish
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+      const int x = tid + 256 * e;
+      F[row_of(x) * FS + col_of(x)] = v[e];
+    }
+    __syncthreads();
+    if (!publish_split(p, M, split, n0, NP * kPairCols, &p.counters[tile], s_flag,
+                       [&](int m, int c) { return F[m * FS + c]; }))
+      return false;
+    row_scales<AM>(p, M, s_scale);
+    __syncthreads();
+    fixup_rows<AM>(p, M, n0, NP * kPairCols, 0, M, s_scale, F, FS);
   } else {
-    // stage the A planes of `chunk_kt` k-steps in LDS (hi region, then lo)
-    wait();
-    constexpr int kRegions = BF ? 2 : 1;
-    const int stride = lds_row_stride(chunk_kt);
-    const int region = MT * 16 * stride;
-    const unsigned char* lbase = smem + (lane & 15) * stride + (lane >> 4) * 16;
-    for (int c0 = kt0; c0 < kt1; c0 += chunk_kt) {
-      const int c1 = min(kt1, c0 + chunk_kt);
-      const int n = c1 - c0;
-      if (c0 != kt0) lds_sync();
-      const int units = kRegions * MT * 16 * n * 4;
-      for (int u = tid; u < units; u += 256) {
-        const int rg = u / (MT * 16 * n * 4);
-        const int r2 = u - rg * (MT * 16 * n * 4);
-        const int m = r2 / (n * 4), r = r2 - m * (n * 4);
-        const size_t e = (size_t)m * K + (size_t)(c0 + (r >> 2)) * KE + (r & 3) * PER16 + rg * p.a_plane;
-        *reinterpret_cast<uint4*>(smem + rg * region + m * stride + (r >> 2) * 64 + (r & 3) * 16) =
-            *reinterpret_cast<const uint4*>((const T*)p.A + e);
+#pragma unroll
+    for (int e = 0; e < kE; ++e) {
+      const int x = tid + 256 * e, m = row_of(x);
+      if (m < M) F[m * FS + col_of(x)] = AM == A_NORM ? v[e] * s_scale[m] : v[e];
+    }
+  }
+  lds_sync();
+  epilogue_rows<BF, EPI, COH>(p, F, FS, pair0, NP, 0, M);
+  return true;
+}
+
+// Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
+// tile pairs (one per wave) of one split; the activation fragments of
+// `chunk_kt` k-steps at a time are staged in LDS and shared by the waves,
+// each wave keeps its quarters apart in registers (running sum S).
+//   smem: dynamic LDS of gemm_staged_lds_bytes(); chunk_kt from
+//   staged_chunk().
+
+__host__ __device__ constexpr int gemm_staged_lds_bytes() {
+  return kLdsBudget > kFRows * kFStride * 4 ? kLdsBudget : kFRows * kFStride * 4;
+}
+__host__ __device__ inline int staged_chunk(bool bf16, int MT) { return kLdsBudget / ((bf16 ? 2 : 1) * MT * 1024); }
+
+template <bool BF, int MT, int AM, int EPI, bool COH>
+__device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split, unsigned char* smem,
+                                 float* s_scale, int* s_flag, int chunk_kt) {
+  constexpr int kRegions = BF ? 2 : 1;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int pair = group * kPairsS + wave;
+  const int kt0 = split * p.ktps;
+  const int n_all = min(p.KT, kt0 + p.ktps) - kt0;
+  const uint4* wp = p.W + (size_t)pair * p.KT * 128 + lane;
+  const uint4* ag = static_cast<const uint4*>(p.A);
+  const long long lo = p.a_plane / ET<BF>::PER16;
+  uint4* la = reinterpret_cast<uint4*>(smem);     // [region][mt][k-step of chunk][64]
+  const int region = MT * chunk_kt * 64;
+  const int lu = frag_lane_unit(lane);
+  f4 S[MT][2], acc[MT][2];
+  bool first_chunk = true;
+  for (int q = 0; q < kQuarters; ++q) {
+    const int qa = quarter_start(kt0, n_all, q), qb = quarter_start(kt0, n_all, q + 1);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      acc[mt][0] = f4{0.f, 0.f, 0.f, 0.f};
+      acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int c0 = qa; c0 < qb; c0 += chunk_kt) {
+      const int n = min(qb, c0 + chunk_kt) - c0;
+      if (!first_chunk) lds_sync();
+      first_chunk = false;
+      // stage: region rg, tile mt, k-step r of the chunk = one 1 KiB fragment block
+      for (int u = tid; u < kRegions * MT * n * 64; u += 256) {
+        const int l = u & 63, blk = u >> 6;
+        const int rg = blk / (MT * n), r2 = blk - rg * (MT * n);
+        const int mt = r2 / n, r = r2 - mt * n;
+        la[rg * region + (mt * chunk_kt + r) * 64 + l] = ag[rg * lo + ((size_t)mt * p.KT + c0 + r) * 64 + l];
       }
       uint4 b[kPrefetch][2];
 #pragma unroll
@@ -260,20 +492,21 @@ __device__ bool gemm_tile(const GemmArgs& p, int M, int group, int split, unsign
         b[u][1] = ldw(wp + kp + 64);
       }
       lds_sync();
-      auto lds_a = [&](int ks, AFrag(&af)[MT]) {
+      auto lds_step = [&](int ks, const uint4(&bb)[2]) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          af[mt].h = *reinterpret_cast<const uint4*>(lbase + mt * 16 * stride + ks * 64);
-          if constexpr (BF) af[mt].l = *reinterpret_cast<const uint4*>(lbase + region + mt * 16 * stride + ks * 64);
+          AFrag af;
+          af.h = la[(mt * chunk_kt + ks) * 64 + lu];
+          if constexpr (BF) af.l = la[region + (mt * chunk_kt + ks) * 64 + lu];
+          acc[mt][0] = mma_a<BF>(af, bb[0], acc[mt][0]);
+          acc[mt][1] = mma_a<BF>(af, bb[1], acc[mt][1]);
         }
       };
       int i = 0;
       for (; i + 2 * kPrefetch <= n; i += kPrefetch) {
 #pragma unroll
         for (int u = 0; u < kPrefetch; ++u) {
-          AFrag af[MT];
-          lds_a(i + u, af);
-          step(b[u], af);
+          lds_step(i + u, b[u]);
           const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
           b[u][0] = ldw(wp + kn);
           b[u][1] = ldw(wp + kn + 64);
@@ -282,9 +515,7 @@ __device__ bool gemm_tile(const GemmArgs& p, int M, int group, int split, unsign
 #pragma unroll
       for (int u = 0; u < kPrefetch; ++u) {
         if (i + u < n) {
-          AFrag af[MT];
-          lds_a(i + u, af);
-          step(b[u], af);
+          lds_step(i + u, b[u]);
           if (i + u + kPrefetch < n) {
             const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
             b[u][0] = ldw(wp + kn);
@@ -294,26 +525,19 @@ __device__ bool gemm_tile(const GemmArgs& p, int M, int group, int split, unsign
       }
       i += kPrefetch;
 #pragma unroll
-      for (int u = 0; u < kPrefetch; ++u) {
-        if (i + u < n) {
-          AFrag af[MT];
-          lds_a(i + u, af);
-          step(b[u], af);
-        }
-      }
+      for (int u = 0; u < kPrefetch; ++u)
+        if (i + u < n) lds_step(i + u, b[u]);
     }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) S[mt][j] = q == 0 ? acc[mt][j] : S[mt][j] + acc[mt][j];
   }
 
-  if constexpr (AM == A_NORM) {
-    for (int m = tid; m < M; m += 256) {
-      float ss = 0.0f;
-      for (int g = 0; g < p.n_norm_groups; ++g) ss += p.sumsq[g * kMaxRows + m];
-      s_scale[m] = 1.0f / sqrtf(ss / (float)K + p.eps);
-    }
-  }
   float* F = reinterpret_cast<float*>(smem);
-  if (p.KS > 1) {
-    // publish this split's partial, then let the last split of the group reduce
+  const int n0 = group * kPairsS * kPairCols, C = kPairsS * kPairCols;
+  // lane's value of (row m, column 32 wave + 16 j + lane % 16)
+  auto put = [&](int r0, int r1, bool scale) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -321,54 +545,46 @@ __device__ bool gemm_tile(const GemmArgs& p, int M, int group, int split, unsign
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int row = mt * 16 + (lane >> 4) * 4 + i;
-          const int col = group * 128 + (wave * 2 + j) * 16 + (lane & 15);
-          if (row < M) store_partial(&p.part[((size_t)split * M + row) * p.N + col], acc[mt][j][i]);
+          const int col = wave * kPairCols + j * 16 + (lane & 15);
+          if (row >= r0 && row < r1)
+            F[(row - r0) * kFStride + col] = AM == A_NORM && scale ? S[mt][j][i] * s_scale[row] : S[mt][j][i];
         }
+  };
+  if (p.KS > 1) {
+    // publish in row blocks through F
+    for (int r0 = 0; r0 < M; r0 += kFRows) {
+      const int r1 = min(M, r0 + kFRows);
+      lds_sync();
+      put(r0, r1, false);
+      __syncthreads();
+      for (int e = tid; e < (r1 - r0) * C; e += 256) {
+        const int m = r0 + e / C, c = e % C;
+        store_partial(&p.part[((size_t)split * M + m) * p.N + n0 + c], F[(m - r0) * kFStride + c]);
+      }
+    }
     wait_vmem();
-    __syncthreads();  // every wave's partial stores are performed
+    __syncthreads();
     if (tid == 0) *s_flag = counter_add(&p.counters[group], 1) == p.KS - 1;
     __syncthreads();
     if (!*s_flag) return false;
-    if (tid == 0) st<true>(&p.counters[group], 0);  // ready for the next launch
+    if (tid == 0) st<true>(&p.counters[group], 0);
+    row_scales<AM>(p, M, s_scale);
+    __syncthreads();
     for (int r0 = 0; r0 < M; r0 += kFRows) {
       const int r1 = min(M, r0 + kFRows);
-      // each element is summed in split order, its split loads issued together
-      for (int idx = tid; idx < (r1 - r0) * 128; idx += 256) {
-        const int m = r0 + (idx >> 7), c = idx & 127;
-        constexpr int kB = 16;
-        float sum = 0.0f;
-        for (int s0 = 0; s0 < p.KS; s0 += kB) {
-          float v[kB];
-#pragma unroll
-          for (int b = 0; b < kB; ++b)
-            if (s0 + b < p.KS) v[b] = load_partial(&p.part[((size_t)(s0 + b) * M + m) * p.N + group * 128 + c]);
-#pragma unroll
-          for (int b = 0; b < kB; ++b)
-            if (s0 + b < p.KS) sum += v[b];
-        }
-        F[(m - r0) * kFStride + c] = AM == A_NORM ? sum * s_scale[m] : sum;
-      }
+      fixup_rows<AM>(p, M, n0, C, r0, r1, s_scale, F, kFStride);
       lds_sync();
-      epilogue_rows<BF, EPI, COH>(p, F, group, r0, r1);
+      epilogue_rows<BF, EPI, COH>(p, F, kFStride, group * kPairsS, kPairsS, r0, r1);
       lds_sync();
     }
   } else {
+    row_scales<AM>(p, M, s_scale);
     __syncthreads();  // A tiles no longer read; s_scale written
     for (int r0 = 0; r0 < M; r0 += kFRows) {
       const int r1 = min(M, r0 + kFRows);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = mt * 16 + (lane >> 4) * 4 + i;
-            const int col = (wave * 2 + j) * 16 + (lane & 15);
-            if (row >= r0 && row < r1)
-              F[(row - r0) * kFStride + col] = AM == A_NORM ? acc[mt][j][i] * s_scale[row] : acc[mt][j][i];
-          }
+      put(r0, r1, true);
       lds_sync();
-      epilogue_rows<BF, EPI, COH>(p, F, group, r0, r1);
+      epilogue_rows<BF, EPI, COH>(p, F, kFStride, group * kPairsS, kPairsS, r0, r1);
       lds_sync();
     }
   }
@@ -376,8 +592,15 @@ __device__ bool gemm_tile(const GemmArgs& p, int M, int group, int split, unsign
 }
 
 // ---------------------------------------------------------------------------
-// Attention over one 32-key chunk c of request r for query head h (see
-// kernels.hip).  256 threads; smem: dynamic LDS of attn_lds_bytes(D).
+// Attention over one 32-key chunk c of request r for query head h.  The
+// chunk's keys and values (float32) are staged in LDS; each wave takes the
+// request's rows in turn (the next row's query is prefetched into
+// registers).  For a row at position pos >= 32 c, lane pairs (j, j + 32)
+// each take half of the dot product of key j (keys j <= pos), the wave
+// forms the chunk's softmax statistics (max m, sum l of exp(s - m)) and
+// each lane the unnormalised output sum_j exp(s_j - m) v_j of its
+// dimensions.  A row's chunks are combined in ascending order by
+// attn_merge_row.  256 threads; smem: attn_lds_bytes(D).
 
 template <int D> __host__ __device__ constexpr int attn_lds_bytes() {
   return (2 * kAttnChunk * (D + 1) + 4 * D + 4 * kAttnChunk) * 4;
@@ -478,19 +701,27 @@ __device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& 
 }
 
 // Merge of row `row`'s chunks for head h by D threads starting at thread t0:
-// chunk weights exp(m_c - max m) go through LDS (sm, sl: kMaxChunks floats
-// each), then each thread sums its dimension over the chunks in ascending
-// order with the loads issued in batches.  `sync` synchronises the threads
-// that share it; with valid = false the threads only join those syncs.
+// chunk weights w_c = exp(m_c - max m) go through LDS (sm, sl: kMaxChunks
+// floats each); each thread then sums its dimension over the chunks in
+// ascending order, L = sum_c l_c w_c and a = sum_c acc_c w_c, out = a / L.
+// The first kB chunks' partial sums are loaded before the statistics are
+// combined, so a row of up to kB chunks costs one round trip to memory.
+// `sync` synchronises the threads that share it; with valid = false the
+// threads only join those syncs.
 
 template <bool BF, int D, bool COH, class Sync>
 __device__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float* sm, float* sl, Sync&& sync,
                                bool valid = true) {
-  constexpr int kB = 8;
+  constexpr int kB = 32;
   const int dd = threadIdx.x - t0;
   const RowDesc rd = p.rows[row];
   const int nc = valid ? rd.pos / kAttnChunk + 1 : 0;
   auto ld = [](const float* q) { if constexpr (COH) return ld_coherent(q); else return *q; };
+  auto acc_at = [&](int c) { return p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd; };
+  float v[kB];
+#pragma unroll
+  for (int b = 0; b < kB; ++b)
+    if (b < nc) v[b] = ld(acc_at(b));
   for (int c = dd; c < nc; c += D) {
     const size_t o = ((size_t)c * kMaxRows + row) * p.n_q + h;
     sm[c] = ld(p.pml + o * 2);
@@ -504,10 +735,11 @@ __device__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float*
   sync();
   float L = 0.0f, a = 0.0f;
   for (int c0 = 0; c0 < nc; c0 += kB) {
-    float v[kB];
+    if (c0 > 0) {
 #pragma unroll
-    for (int b = 0; b < kB; ++b)
-      if (c0 + b < nc) v[b] = ld(p.pacc + (((size_t)(c0 + b) * kMaxRows + row) * p.n_q + h) * D + dd);
+      for (int b = 0; b < kB; ++b)
+        if (c0 + b < nc) v[b] = ld(acc_at(c0 + b));
+    }
 #pragma unroll
     for (int b = 0; b < kB; ++b)
       if (c0 + b < nc) {
@@ -515,42 +747,42 @@ __device__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float*
         a += v[b] * sm[c0 + b];
       }
   }
-  if (valid) store_act<BF, COH>(p.out, p.out_plane, (size_t)row * p.n_q * D + h * D + dd, a / L);
+  if (valid) store_act<BF, COH>(p.out, p.out_plane, frag_index<BF>(row, h * D + dd, p.n_q * D), a / L);
 }
 
 // ---------------------------------------------------------------------------
-// Arg-max of row `row` over the LM head's per-group partials (256 threads):
+// Arg-max of row `row` over the LM head's per-pair partials (256 threads):
 // larger value wins, equal values keep the lower token id; *bad is set for a
 // non-finite logit.  s4f / s4i: 4-entry LDS scratch.
 
 template <bool COH>
-__device__ void argmax_row(const float* amax_val, const int* amax_idx, int n_groups, int row, int* tok,
+__device__ void argmax_row(const float* amax_val, const int* amax_idx, int n_pairs, int row, int* tok,
                            int* bad, float* s4f, int* s4i) {
-  constexpr int kPer = 8;   // groups per thread, loads in flight together
+  constexpr int kPer = 8;   // pairs per thread, loads in flight together
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   float best = -INFINITY;
   int bi = 0x7fffffff;
   bool b = false;
-  for (int g0 = 0; g0 < n_groups; g0 += 256 * kPer) {
+  for (int g0 = 0; g0 < n_pairs; g0 += 256 * kPer) {
     float v[kPer];
     int id[kPer];
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
       const int g = g0 + t * 256 + tid;
-      if (g < n_groups) {
+      if (g < n_pairs) {
         if constexpr (COH) {
-          v[t] = ld_coherent(amax_val + g * kMaxRows + row);
-          id[t] = ld_coherent(amax_idx + g * kMaxRows + row);
+          v[t] = ld_coherent(amax_val + (size_t)row * n_pairs + g);
+          id[t] = ld_coherent(amax_idx + (size_t)row * n_pairs + g);
         } else {
-          v[t] = amax_val[g * kMaxRows + row];
-          id[t] = amax_idx[g * kMaxRows + row];
+          v[t] = amax_val[(size_t)row * n_pairs + g];
+          id[t] = amax_idx[(size_t)row * n_pairs + g];
         }
       }
     }
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
       const int g = g0 + t * 256 + tid;
-      if (g < n_groups) {
+      if (g < n_pairs) {
         if (!isfinite(v[t])) b = true;
         else if (v[t] > best || (v[t] == best && id[t] < bi)) { best = v[t]; bi = id[t]; }
       }
