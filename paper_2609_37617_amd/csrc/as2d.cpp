@@ -23,7 +23,7 @@ using namespace as2d;
 namespace {
 
 struct GemmPlan {
-  int N = 0, K = 0, KT = 0, pairs = 0, KS = 1, ktps = 0, np = 1;
+  int N = 0, K = 0, KT = 0, pairs = 0, KS = 1, ktps = 0, np = 1, ns = 4;
 };
 
 struct LayerW {
@@ -143,11 +143,14 @@ int dalloc(as2d_ctx* c, P** p, size_t bytes) {
 
 // Work plan of one matrix.  Wide matrices (at least 1024 tile pairs) give
 // each direct-path workgroup two pairs, so one activation fragment feeds
-// twice the weights; the others one.  The k-split count then aims at about
-// `target` workgroups with at least 8 k-steps per split (two per quarter)
-// and at most kMaxSplits splits.  The plan depends only on the matrix
-// shape, never on the rows of a pass, and the pairs per workgroup do not
-// change any sum, so every row is computed alike in every pass.
+// twice the weights; the others one pair.  Every k-split is summed in 4
+// slices (one per wave).  Each compute unit keeps only a bounded amount of
+// memory traffic in flight, so the streaming has to reach all of them: the
+// k-split count aims at about `target` workgroups per matrix, with at
+// least 8 k-steps per split and at most kMaxSplits splits.  The plan
+// depends only on the matrix shape, never on the rows of a pass, and the
+// pairs per workgroup do not change any sum, so every row is computed
+// alike in every pass.
 GemmPlan make_plan(int N, int K, int KE, int target) {
   GemmPlan p;
   p.N = N;
@@ -155,6 +158,7 @@ GemmPlan make_plan(int N, int K, int KE, int target) {
   p.KT = K / KE;
   p.pairs = N / kPairCols;
   p.np = p.pairs >= 1024 ? 2 : 1;
+  p.ns = 4;
   int ks = (int)std::lround((double)target / (p.pairs / p.np));
   ks = std::max(1, std::min({ks, std::max(1, p.KT / 8), kMaxSplits}));
   p.ktps = (p.KT + ks - 1) / ks;
@@ -225,6 +229,7 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   a.KS = pl.KS;
   a.ktps = pl.ktps;
   a.np = pl.np;
+  a.ns = pl.ns;
   a.M = M;
   a.MT = (M + 15) / 16;
   a.sumsq = c->sumsq;

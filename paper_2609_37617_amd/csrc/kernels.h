@@ -24,7 +24,7 @@ namespace as2d {
 // output columns is a tile pair: 32 columns, two 16-column MFMA tiles.
 constexpr int kWaves = 4;               // waves per workgroup
 constexpr int kPairCols = 32;           // columns of a tile pair
-constexpr int kQuarters = 4;            // ordered partial sums per k-split
+constexpr int kMaxSlices = 16;          // ordered partial sums per k-split, at most
 constexpr int kPairsS = kWaves;         // tile pairs per workgroup, staged path
 constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
@@ -67,6 +67,7 @@ struct GemmArgs {
   const uint4* W;        // packed weight tiles
   int N, K, KT, KS, ktps;
   int np;                // tile pairs per workgroup on the direct path (1 or 2)
+  int ns;                // ordered slices per k-split (4 or 16)
   int M, MT;
   // A operand: activation planes [kMaxRows][K].  For A_NORM the planes
   // hold x * g (residual times RMSNorm gain) and the epilogue multiplies

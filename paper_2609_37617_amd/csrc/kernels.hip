@@ -100,30 +100,33 @@ hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed
 // ---------------------------------------------------------------------------
 // Weight-streaming GEMM  Y[M][N] = A[M][K] * W[N][K]^T  for small M
 // (tiles.h).  Up to 32 rows (direct path): one workgroup per (np tile
-// pairs, k-split), its four waves streaming the four quarters of the split,
+// pairs, k-split), its four waves streaming the ns slices of the split,
 // each k-step's 1 KiB weight tiles (fully coalesced, non-temporal) and the
-// activation fragments issued three or four k-steps ahead of their use.  More rows
+// activation fragments issued 2 to 4 k-steps ahead of their use.  The
+// streaming must reach every compute unit (each keeps a bounded amount of
+// memory traffic in flight), so narrow matrices are split along k.  More rows
 // (staged path): one workgroup per (4 tile pairs, k-split), activations
 // staged through LDS.  Both paths add every element in the same order, so
 // a row's result does not depend on M.  With KS > 1 each split writes a
 // float32 partial and the last workgroup of the tile (device-scope
 // counter) sums the partials in split order and runs the fused epilogue.
 
-template <bool BF, int MT, int NP, int AM, int EPI, bool SPLIT>
-__global__ __launch_bounds__(256, MT == 1 ? (NP == 1 ? 5 : 4) : 4) void gemm_direct_kernel(const GemmArgs p) {
+template <bool BF, int MT, int NP, int NW, int AM, int EPI, bool SPLIT>
+__global__ __launch_bounds__(NW * 64, MT == 1 && NP == 1 ? 5 : 4) void gemm_direct_kernel(const GemmArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;
   const int tile = blockIdx.x / p.KS, split = blockIdx.x - tile * p.KS;
-  gemm_tile_direct<BF, MT, NP, AM, EPI, false, SPLIT>(p, p.M, tile, split, smem, s_scale, &s_flag, [] {});
+  gemm_tile_direct<BF, MT, NP, NW, false, AM, EPI, false, SPLIT>(p, p.M, tile, split, smem, s_scale, &s_flag,
+                                                                 [] {});
 }
 
-template <bool BF, int MT, int NP, int AM, int EPI>
+template <bool BF, int MT, int NP, int NW, int AM, int EPI>
 static void launch_direct(const GemmArgs& a, hipStream_t s) {
-  const dim3 grid((a.N / kPairCols / NP) * a.KS), block(256);
-  constexpr int lds = gemm_direct_lds_bytes<MT, NP>();
-  if (a.KS > 1) gemm_direct_kernel<BF, MT, NP, AM, EPI, true><<<grid, block, lds, s>>>(a);
-  else gemm_direct_kernel<BF, MT, NP, AM, EPI, false><<<grid, block, lds, s>>>(a);
+  const dim3 grid((a.N / kPairCols / NP) * a.KS), block(NW * 64);
+  const int lds = gemm_direct_lds_bytes<MT, NP>(a.ns);
+  if (a.KS > 1) gemm_direct_kernel<BF, MT, NP, NW, AM, EPI, true><<<grid, block, lds, s>>>(a);
+  else gemm_direct_kernel<BF, MT, NP, NW, AM, EPI, false><<<grid, block, lds, s>>>(a);
 }
 
 template <bool BF, int MT, int AM, int EPI>
@@ -139,13 +142,14 @@ template <bool BF, int AM, int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   const int pairs = a.N / kPairCols;
   if (a.MT <= kDirectMT) {
-    if (a.np != 1 && (a.np != 2 || pairs % 2)) return hipErrorInvalidValue;
+    if ((a.np != 1 && (a.np != 2 || pairs % 2)) || a.ns < kWaves || a.ns > kMaxSlices || a.ns % kWaves)
+      return hipErrorInvalidValue;
     if (a.MT == 1) {
-      if (a.np == 1) launch_direct<BF, 1, 1, AM, EPI>(a, s);
-      else launch_direct<BF, 1, 2, AM, EPI>(a, s);
+      if (a.np == 1) launch_direct<BF, 1, 1, kWaves, AM, EPI>(a, s);
+      else launch_direct<BF, 1, 2, kWaves, AM, EPI>(a, s);
     } else {
-      if (a.np == 1) launch_direct<BF, 2, 1, AM, EPI>(a, s);
-      else launch_direct<BF, 2, 2, AM, EPI>(a, s);
+      if (a.np == 1) launch_direct<BF, 2, 1, kWaves, AM, EPI>(a, s);
+      else launch_direct<BF, 2, 2, kWaves, AM, EPI>(a, s);
     }
     return hipGetLastError();
   }
@@ -199,7 +203,8 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(const AttnArgs p) {
 template <bool BF, int D>
 static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
   if (max_chunks > kMaxChunks) return hipErrorInvalidValue;
-  attn_chunk_kernel<D><<<dim3(max_chunks, a.n_q, n_reqs), 256, attn_lds_bytes<D>(), s>>>(a);
+  const dim3 grid(max_chunks, a.n_q, n_reqs);
+  attn_chunk_kernel<D><<<grid, 256, attn_lds_bytes<D>(), s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   attn_merge_kernel<BF, D><<<dim3(a.n_q, a.M), D, 0, s>>>(a);

@@ -68,7 +68,7 @@ __device__ void gemm_phase(const GemmArgs p, int M, const int* wait_c, int wait_
   bool waited = false;
   for (int t = blockIdx.x; t < n_tiles; t += G) {
     const int pair = t / p.KS, split = t - pair * p.KS;
-    const bool fin = gemm_tile_direct<BF, MT, 1, AM, EPI, true, true>(p, M, pair, split, smem, s_scale, s_flag, [&] {
+    const bool fin = gemm_tile_direct<BF, MT, 1, kWaves, false, AM, EPI, true, true>(p, M, pair, split, smem, s_scale, s_flag, [&] {
       if (!waited) {
         wait_count(wait_c, wait_target, a.err, a.spin_limit);
         stamp(a, phase, 1);
@@ -218,7 +218,7 @@ static const void* pick(bool bf16, int MT, int D) {
 
 int step_lds_bytes(int head_dim, int hidden) {
   // hidden <= 8192
-  int b = gemm_direct_lds_bytes<2, 1>();
+  int b = gemm_direct_lds_bytes<2, 1>(kMaxSlices);
   b = max(b, head_dim == 128 ? attn_lds_bytes<128>() : attn_lds_bytes<64>());
   b = max(b, hidden * 4);                      // embedding row
   b = max(b, (256 / head_dim) * 2 * kMaxChunks * 4);  // merge scratch

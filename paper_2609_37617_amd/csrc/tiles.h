@@ -72,19 +72,20 @@ __device__ void embed_row(const RowDesc* __restrict__ rows, int m, const typenam
 // ---------------------------------------------------------------------------
 // Fused GEMM epilogues over rows [r0, r1) of `np` consecutive tile pairs
 // starting at pair `pair0`; F holds their finished values (float32, row
-// stride fs, pair pp at columns [32 pp, 32 pp + 32)).  256 threads.  Every
+// stride fs, pair pp at columns [32 pp, 32 pp + 32)).  NTH threads.  Every
 // per-pair reduction runs on one half-wave in a fixed pattern, so a row's
 // results do not depend on how many pairs or rows the call covers.
 
-template <bool BF, int EPI, bool COH>
+template <bool BF, int EPI, bool COH, int NTH = 256>
 __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, int np, int r0, int r1) {
+  constexpr int kUnits = NTH / 32;              // (row, pair) units per pass: one per half-wave
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int N = p.N, C = np * kPairCols;
   const int n0 = pair0 * kPairCols;
   const int units = (r1 - r0) * np;           // (row, pair) units of the reductions
   if constexpr (EPI == EPI_RESID) {
     // x_out = x + Y; planes of x_out * g for the next RMSNorm; sum of squares
-    for (int idx = tid; idx < (r1 - r0) * C; idx += 256) {
+    for (int idx = tid; idx < (r1 - r0) * C; idx += NTH) {
       const int m = r0 + idx / C, c = idx % C;
       const int n = n0 + c;
       const size_t o = (size_t)m * N + n;
@@ -94,7 +95,7 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
       F[(m - r0) * fs + c] = v;
     }
     lds_sync();
-    for (int u0 = wave * 2; u0 < units; u0 += 8) {
+    for (int u0 = wave * 2; u0 < units; u0 += kUnits) {
       const int u = u0 + (lane >> 5);
       const bool ok = u < units;
       const int m = ok ? r0 + u / np : r0, pp = u % np;
@@ -105,7 +106,7 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
   } else if constexpr (EPI == EPI_SWIGLU) {
     // pair g: gate columns 16 g .. 16 g + 15 (tile 0), the same up columns (tile 1)
     const int F2 = N / 2;
-    for (int idx = tid; idx < (r1 - r0) * np * 16; idx += 256) {
+    for (int idx = tid; idx < (r1 - r0) * np * 16; idx += NTH) {
       const int m = r0 + idx / (np * 16), r = idx % (np * 16);
       const int pp = r >> 4, c = r & 15;
       const float g = F[(m - r0) * fs + pp * kPairCols + c], u = F[(m - r0) * fs + pp * kPairCols + 16 + c];
@@ -116,7 +117,7 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
     // PACK_ROPE_PAIRS: pair q of a head holds dims 16 q + c (tile 0) and
     // d/2 + 16 q + c (tile 1), the two halves RoPE rotates together
     const int d = p.head_dim, half = d >> 1, ppd = d / kPairCols;
-    for (int idx = tid; idx < (r1 - r0) * C; idx += 256) {
+    for (int idx = tid; idx < (r1 - r0) * C; idx += NTH) {
       const int m = r0 + idx / C, c = idx % C;
       const int pair = pair0 + c / kPairCols, j = (c >> 4) & 1, cc = c & 15;
       const int head = pair / ppd, q = pair % ppd;
@@ -144,7 +145,7 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
       }
     }
   } else {  // EPI_ARGMAX (identity column order: column = token id)
-    for (int u0 = wave * 2; u0 < units; u0 += 8) {
+    for (int u0 = wave * 2; u0 < units; u0 += kUnits) {
       const int u = u0 + (lane >> 5);
       const bool ok = u < units;
       const int m = ok ? r0 + u / np : r0, pp = u % np;
@@ -172,16 +173,16 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
 // s_scale[m] (A_NORM) and writes the result to F (row stride fs, rows from
 // r0).  Loads are issued in batches across elements and splits.
 
-template <int AM>
+template <int AM, int NTH = 256>
 __device__ void fixup_rows(const GemmArgs& p, int M, int n0, int C, int r0, int r1, const float* s_scale,
                            float* F, int fs) {
   constexpr int kEl = 2;   // elements per thread per batch (kEl x kMaxSplits loads in flight)
   const int E = (r1 - r0) * C;
-  for (int e0 = threadIdx.x; e0 < E; e0 += 256 * kEl) {
+  for (int e0 = threadIdx.x; e0 < E; e0 += NTH * kEl) {
     float v[kEl][kMaxSplits];
 #pragma unroll
     for (int t = 0; t < kEl; ++t) {
-      const int e = e0 + t * 256;
+      const int e = e0 + t * NTH;
       const int m = r0 + e / C, c = e % C;
 #pragma unroll
       for (int sp = 0; sp < kMaxSplits; ++sp)
@@ -189,7 +190,7 @@ __device__ void fixup_rows(const GemmArgs& p, int M, int n0, int C, int r0, int 
     }
 #pragma unroll
     for (int t = 0; t < kEl; ++t) {
-      const int e = e0 + t * 256;
+      const int e = e0 + t * NTH;
       if (e < E) {
         const int m = r0 + e / C, c = e % C;
         float sum = v[t][0];
@@ -202,15 +203,15 @@ __device__ void fixup_rows(const GemmArgs& p, int M, int n0, int C, int r0, int 
   }
 }
 
-// Quarter q of the k-range [kt0, kt0 + n): [kt0 + q n / 4, kt0 + (q + 1) n / 4).
-__device__ __forceinline__ int quarter_start(int kt0, int n, int q) { return kt0 + (q * n) / kQuarters; }
+// Slice q of ns of the k-range [kt0, kt0 + n): [kt0 + q n / ns, kt0 + (q + 1) n / ns).
+__device__ __forceinline__ int slice_start(int kt0, int n, int q, int ns) { return kt0 + (q * n) / ns; }
 
 // Publishes a workgroup's split partials for (rows < M, columns [n0, n0 + C))
 // given by `val(m, c)` and returns true in the workgroup that arrives last
 // at counter `cnt` (it then resets the counter for the next launch).
-template <class Val>
+template <int NTH = 256, class Val>
 __device__ bool publish_split(const GemmArgs& p, int M, int split, int n0, int C, int* cnt, int* s_flag, Val&& val) {
-  for (int e = threadIdx.x; e < M * C; e += 256) {
+  for (int e = threadIdx.x; e < M * C; e += NTH) {
     const int m = e / C, c = e % C;
     store_partial(&p.part[((size_t)split * M + m) * p.N + n0 + c], val(m, c));
   }
@@ -227,19 +228,19 @@ __device__ bool publish_split(const GemmArgs& p, int M, int split, int n0, int C
 // into s_scale, from the rows' per-pair sum-of-squares partials (at most
 // 256 pairs: hidden <= 8192).  Each row is summed in a fixed pattern (lane
 // l: partials l, l + 64, ...; then a butterfly), so its value depends on
-// the row alone; wave w takes rows w, w + 4, ..., eight rows per batch with
-// all their loads in flight together.
-template <int AM>
+// the row alone; wave w of NW takes rows w, w + NW, ..., eight rows per
+// batch with all their loads in flight together.
+template <int AM, int NW = kWaves>
 __device__ __forceinline__ void row_scales(const GemmArgs& p, int M, float* s_scale) {
   if constexpr (AM == A_NORM) {
     constexpr int kR = 8, kT = 4;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int np = p.n_norm_pairs;
-    for (int m0 = wave; m0 < M; m0 += kWaves * kR) {
+    for (int m0 = wave; m0 < M; m0 += NW * kR) {
       float s[kR];
 #pragma unroll
       for (int r = 0; r < kR; ++r) {
-        const int m = m0 + kWaves * r;
+        const int m = m0 + NW * r;
         s[r] = 0.0f;
 #pragma unroll
         for (int t = 0; t < kT; ++t)
@@ -247,7 +248,7 @@ __device__ __forceinline__ void row_scales(const GemmArgs& p, int M, float* s_sc
       }
 #pragma unroll
       for (int r = 0; r < kR; ++r) {
-        const int m = m0 + kWaves * r;
+        const int m = m0 + NW * r;
         const float tot = wave_sum(s[r]);
         if (lane == 0 && m < M) s_scale[m] = 1.0f / sqrtf(tot / (float)p.K + p.eps);
       }
@@ -258,52 +259,90 @@ __device__ __forceinline__ void row_scales(const GemmArgs& p, int M, float* s_sc
 // ---------------------------------------------------------------------------
 // GEMM tiles.  Every output element is summed in one order whatever the
 // path, the tile shape or the number of rows: k-split s of the plan
-// (splits in order), in quarters (quarter_start, in order), each quarter
-// accumulated over its k-steps in order by MFMA from zero; then
-// ((q0 + q1) + q2) + q3 per split and the splits added in order.  A row's
-// result therefore depends on the matrix shape alone, never on the rows
-// that share the pass.
+// (splits in order), in ns slices (slice_start, in order; ns from the
+// plan), each slice accumulated over its k-steps in order by MFMA from
+// zero; then (((q0 + q1) + q2) + ...) over the slices of a split and the
+// splits added in order.  A row's result therefore depends on the matrix
+// shape alone, never on the rows that share the pass or the kernel that
+// computes it.
 //
-// Direct path (up to kDirectMT row tiles): a workgroup owns NP tile pairs
-// (32 NP columns) of one split; wave q streams quarter q of the split for
-// all NP pairs, with the activation fragments (one per k-step, shared by
-// the NP pairs) loaded straight from the planes, and the quarters meet in
-// LDS.  `wait()` is called after the first weight loads are issued and
-// before any activation is read (the persistent kernel waits there for the
-// producer of A).  Returns true when this workgroup finished its pairs
-// (ran their epilogue).
-//   smem: dynamic LDS of gemm_direct_lds_bytes<MT, NP>(); s_scale: kMaxRows
-//   floats; s_flag: one int.
+// Direct path (up to kDirectMT row tiles): a workgroup of NW waves owns NP
+// tile pairs (32 NP columns) of one split; wave w streams the ns / NW
+// consecutive slices [w ns / NW, (w + 1) ns / NW) of the split for all NP
+// pairs as one contiguous run of k-steps, with the activation fragments
+// (one per k-step, shared by the NP pairs) loaded straight from the planes;
+// each slice's sums go to LDS and the slices meet there.  `wait()` is
+// called after the first weight loads are issued and before any activation
+// is read (the persistent kernel waits there for the producer of A).
+// Returns true when this workgroup finished its pairs (ran their
+// epilogue).
+//   smem: dynamic LDS of gemm_direct_lds_bytes<MT, NP>(ns); s_scale:
+//   kMaxRows floats; s_flag: one int.
 
-template <int MT, int NP> __host__ __device__ constexpr int gemm_direct_lds_bytes() {
-  return (kQuarters * MT * NP * 512 + 16 * MT * (NP * kPairCols + 1)) * 4;
+template <int MT, int NP> __host__ __device__ constexpr int gemm_direct_lds_bytes(int ns) {
+  return (ns * MT * NP * 512 + 16 * MT * (NP * kPairCols + 1)) * 4;
 }
-// k-steps in flight per wave: four, fewer when a k-step holds more registers
-template <int MT, int NP> __host__ __device__ constexpr int direct_prefetch() {
-  return NP + MT >= 3 ? 3 : kPrefetchDirect;
+// k-steps in flight per wave.  Shallow: as many as about 96 registers hold
+// (several workgroups per compute unit).  Deep: about 200 registers (one
+// workgroup per compute unit); the last round of a wave re-reads its last
+// k-step P times, so depth only pays on long runs of k-steps.
+template <int MT, int NP, bool DEEP> __host__ __device__ constexpr int direct_prefetch() {
+  return DEEP ? (MT == 1 ? 12 : 6) : (NP + MT >= 4 ? 2 : NP + MT == 3 ? 3 : kPrefetchDirect);
 }
 
 // SPLIT = false: the caller guarantees KS == 1 (no fixup code, fewer registers).
-template <bool BF, int MT, int NP, int AM, int EPI, bool COH, bool SPLIT, class Wait>
+template <bool BF, int MT, int NP, int NW, bool DEEP, int AM, int EPI, bool COH, bool SPLIT, class Wait>
 __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, unsigned char* smem,
                                  float* s_scale, int* s_flag, Wait&& wait) {
   static_assert(MT <= kDirectMT, "direct path row tiles");
-  constexpr int P = direct_prefetch<MT, NP>();
+  constexpr int P = direct_prefetch<MT, NP, DEEP>();
+  constexpr int NTH = NW * 64;
   constexpr int FS = NP * kPairCols + 1;   // row stride of the epilogue tile
+  constexpr int QS = MT * NP * 512;        // floats per slice in LDS
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int ns = p.ns, spw = ns / NW;      // slices per split, per wave
   const int kt0 = split * p.ktps;
   const int n_all = min(p.KT, kt0 + p.ktps) - kt0;
-  const int qa = quarter_start(kt0, n_all, wave), n = quarter_start(kt0, n_all, wave + 1) - qa;
+  const int s0 = wave * spw;
+  const int qa = slice_start(kt0, n_all, s0, ns), n = slice_start(kt0, n_all, s0 + spw, ns) - qa;
   const int pair0 = tile * NP;
+  float* R = reinterpret_cast<float*>(smem);   // [slice][mt][pair][j][i][lane]
+  float* F = R + ns * QS;
 
   f4 acc[MT][NP][2];
+  auto zero = [&] {
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int q = 0; q < NP; ++q) {
-      acc[mt][q][0] = f4{0.f, 0.f, 0.f, 0.f};
-      acc[mt][q][1] = f4{0.f, 0.f, 0.f, 0.f};
+      for (int q = 0; q < NP; ++q) {
+        acc[mt][q][0] = f4{0.f, 0.f, 0.f, 0.f};
+        acc[mt][q][1] = f4{0.f, 0.f, 0.f, 0.f};
+      }
+  };
+  zero();
+  // slice bookkeeping: slice `sl` of this wave ends after local k-step `next`
+  int sl = s0, next = slice_start(kt0, n_all, s0 + 1, ns) - qa;
+  auto flush = [&] {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int q = 0; q < NP; ++q)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            R[sl * QS + (((mt * NP + q) * 2 + j) * 4 + i) * 64 + lane] = acc[mt][q][j][i];
+    zero();
+  };
+  // after `done` k-steps: close every slice that has ended (empty ones included)
+  auto advance = [&](int done) {
+    while (sl < s0 + spw - 1 && next <= done) {
+      flush();
+      ++sl;
+      next = slice_start(kt0, n_all, sl + 1, ns) - qa;
     }
+  };
+
   const uint4* wp = p.W + (size_t)pair0 * p.KT * 128 + lane;
   const size_t pstride = (size_t)p.KT * 128;        // next pair's tiles
   const uint4* ap = static_cast<const uint4*>(p.A) + frag_lane_unit(lane);
@@ -327,7 +366,7 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
       }
     }
   };
-  auto step = [&](const uint4(&bb)[NP][2], const AFrag(&af)[MT]) {
+  auto step = [&](int s, const uint4(&bb)[NP][2], const AFrag(&af)[MT]) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -335,6 +374,7 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
         acc[mt][q][0] = mma_a<BF>(af[mt], bb[q][0], acc[mt][q][0]);
         acc[mt][q][1] = mma_a<BF>(af[mt], bb[q][1], acc[mt][q][1]);
       }
+    if (spw > 1) advance(s + 1);
   };
   // Loads retire in issue order, so every k-step's wait is exact only if
   // the loads are always issued in the same order: (W, A) of step s + P
@@ -342,8 +382,8 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
   // loop because its weights are issued before `wait()` (ahead of the
   // activations); after it the loop is entered with the loads in its own
   // order.  Loads past the end re-read the last k-step (clamped), so no
-  // round issues a different number of loads.  A wave whose quarter is
-  // empty (splits of fewer than 4 k-steps) only joins the wait.
+  // round issues a different number of loads.  A wave whose slices are all
+  // empty (splits of fewer k-steps than slices) only joins the wait.
   auto kk = [&](int s) { return qa + min(s, n - 1); };
   uint4 b[P][NP][2];
   AFrag af[P][MT];
@@ -356,12 +396,13 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
     for (int u = 0; u < P; ++u) loadW(kk(u), b[u]);
   }
   wait();
+  if (spw > 1) advance(0);
   if (n > 0) {
 #pragma unroll
     for (int u = 0; u < P; ++u) loadA(kk(u), af[u]);
 #pragma unroll
     for (int u = 0; u < P; ++u) {
-      if (u == 0 || u < n) step(b[u], af[u]);
+      if (u == 0 || u < n) step(u, b[u], af[u]);
       loadW(kk(u + P), b[u]);
       loadA(kk(u + P), af[u]);
       __builtin_amdgcn_sched_barrier(0);
@@ -370,7 +411,7 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
     for (; i + P <= n; i += P) {
 #pragma unroll
       for (int u = 0; u < P; ++u) {
-        step(b[u], af[u]);
+        step(i + u, b[u], af[u]);
         loadW(kk(i + u + P), b[u]);
         loadA(kk(i + u + P), af[u]);
         __builtin_amdgcn_sched_barrier(0);
@@ -378,70 +419,56 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
     }
 #pragma unroll
     for (int u = 0; u < P; ++u)
-      if (i + u < n) step(b[u], af[u]);
+      if (i + u < n) step(i + u, b[u], af[u]);
+  }
+  // the last slice, then any empty slices after it
+  for (;;) {
+    flush();
+    if (sl >= s0 + spw - 1) break;
+    ++sl;
   }
 
-  // quarters meet in LDS: R[quarter][mt][pair][j][i][lane]
-  constexpr int QS = MT * NP * 512;               // floats per quarter
-  float* R = reinterpret_cast<float*>(smem);
-  float* F = R + kQuarters * QS;
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int q = 0; q < NP; ++q)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          R[wave * QS + (((mt * NP + q) * 2 + j) * 4 + i) * 64 + lane] = acc[mt][q][j][i];
   const bool split_k = SPLIT && p.KS > 1;
-  if (!split_k) row_scales<AM>(p, M, s_scale);
+  if (!split_k) row_scales<AM, NW>(p, M, s_scale);
   __syncthreads();
   // element x = (((mt * NP + q) * 2 + j) * 4 + i) * 64 + l: row 16 mt + 4 (l / 16) + i,
   // column 32 q + 16 j + l % 16
-  constexpr int kE = QS / 256;
-  float v[kE];
-#pragma unroll
-  for (int e = 0; e < kE; ++e) {
-    const int x = tid + 256 * e;
-    float s = R[x];
-#pragma unroll
-    for (int q = 1; q < kQuarters; ++q) s += R[q * QS + x];
-    v[e] = s;
-  }
   auto row_of = [](int x) { return (x >> 6) / (8 * NP) * 16 + 4 * ((x & 63) >> 4) + ((x >> 6) & 3); };
   auto col_of = [](int x) { return ((x >> 9) % NP) * kPairCols + ((x >> 8) & 1) * 16 + (x & 15); };
+  auto slice_sum = [&](int x) {
+    float v = R[x];
+    for (int q = 1; q < ns; ++q) v += R[q * QS + x];
+    return v;
+  };
   const int n0 = pair0 * kPairCols;
   if (split_k) {
     // split partials through the epilogue tile: F[row][col] first, then publish
-#pragma unroll
-    for (int e = 0; e < kE; ++e) {
-      const int x = tid + 256 * e;
-      F[row_of(x) * FS + col_of(x)] = v[e];
-    }
+    for (int x = tid; x < QS; x += NTH) F[row_of(x) * FS + col_of(x)] = slice_sum(x);
     __syncthreads();
-    if (!publish_split(p, M, split, n0, NP * kPairCols, &p.counters[tile], s_flag,
-                       [&](int m, int c) { return F[m * FS + c]; }))
+    if (!publish_split<NTH>(p, M, split, n0, NP * kPairCols, &p.counters[tile], s_flag,
+                            [&](int m, int c) { return F[m * FS + c]; }))
       return false;
-    row_scales<AM>(p, M, s_scale);
+    row_scales<AM, NW>(p, M, s_scale);
     __syncthreads();
-    fixup_rows<AM>(p, M, n0, NP * kPairCols, 0, M, s_scale, F, FS);
+    fixup_rows<AM, NTH>(p, M, n0, NP * kPairCols, 0, M, s_scale, F, FS);
   } else {
-#pragma unroll
-    for (int e = 0; e < kE; ++e) {
-      const int x = tid + 256 * e, m = row_of(x);
-      if (m < M) F[m * FS + col_of(x)] = AM == A_NORM ? v[e] * s_scale[m] : v[e];
+    for (int x = tid; x < QS; x += NTH) {
+      const int m = row_of(x);
+      if (m < M) {
+        const float v = slice_sum(x);
+        F[m * FS + col_of(x)] = AM == A_NORM ? v * s_scale[m] : v;
+      }
     }
   }
   lds_sync();
-  epilogue_rows<BF, EPI, COH>(p, F, FS, pair0, NP, 0, M);
+  epilogue_rows<BF, EPI, COH, NTH>(p, F, FS, pair0, NP, 0, M);
   return true;
 }
 
 // Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
 // tile pairs (one per wave) of one split; the activation fragments of
 // `chunk_kt` k-steps at a time are staged in LDS and shared by the waves,
-// each wave keeps its quarters apart in registers (running sum S).
+// each wave keeps its slices apart in registers (running sum S).
 //   smem: dynamic LDS of gemm_staged_lds_bytes(); chunk_kt from
 //   staged_chunk().
 
@@ -466,8 +493,8 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   const int lu = frag_lane_unit(lane);
   f4 S[MT][2], acc[MT][2];
   bool first_chunk = true;
-  for (int q = 0; q < kQuarters; ++q) {
-    const int qa = quarter_start(kt0, n_all, q), qb = quarter_start(kt0, n_all, q + 1);
+  for (int q = 0; q < p.ns; ++q) {
+    const int qa = slice_start(kt0, n_all, q, p.ns), qb = slice_start(kt0, n_all, q + 1, p.ns);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       acc[mt][0] = f4{0.f, 0.f, 0.f, 0.f};
