@@ -203,7 +203,11 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(const AttnArgs p) {
 template <bool BF, int D>
 static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
   if (max_chunks > kMaxChunks) return hipErrorInvalidValue;
-  const dim3 grid(max_chunks, a.n_q, n_reqs);
+  // Workgroups are dealt to the 8 XCDs round-robin by linear index; with
+  // the chunk dimension a multiple of 8, every head of chunk c runs on the
+  // same XCD, so the query heads of a KV group share that chunk's keys and
+  // values in one L2 (extra chunks exit at once).
+  const dim3 grid((max_chunks + 7) / 8 * 8, a.n_q, n_reqs);
   attn_chunk_kernel<D><<<grid, 256, attn_lds_bytes<D>(), s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
