@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="(tuning only) override layer count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-width-profile", action="store_true",
+                    help="skip the per-k step times (single-request workloads with a k sweep)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a plain copy kernel "
                          "of known size, for scaling hardware byte counters)")
@@ -171,7 +173,7 @@ def main():
     if args.k is not None or args.p is not None:
         reqs = [wc.Request(r.n_audio, r.n_instr, r.reply_len, args.k if args.k is not None else r.k,
                            args.p if args.p is not None else r.p) for r in reqs]
-    max_k = max(max(r.k for r in reqs), 1)
+    max_k = max(max(r.k for r in reqs), max(wl.k_sweep, default=0) if len(reqs) == 1 else 0, 1)
     max_kv = max(r.n_audio + r.n_instr + r.reply_len for r in reqs) + max_k + 2
     max_kv = (max_kv + 63) // 64 * 64
     log(f"[bench] workload {wl.name}: {len(reqs)} request(s), shape {shape.name} L={shape.n_layers}")
@@ -199,21 +201,21 @@ def main():
 
     done = [0] * len(reqs)        # committed tokens of the current reply pass
 
-    def step():
+    def step(k_force=None):
         """One verification call over every request with reply left (one
         fused pass for several requests); returns tokens committed."""
         ids, cands = [], []
         for i, r in enumerate(reqs):
             if done[i] >= r.reply_len:
                 continue
-            k = min(r.k, r.reply_len - done[i] - 1)
+            k = min(r.k if k_force is None else k_force, r.reply_len - done[i] - 1)
             ids.append(i)
             cands.append(srcs[i].block(done[i], k))
         if not ids:
             for i in range(len(reqs)):
                 model.rollback(i, *starts[i])
                 done[i] = 0
-            return step()
+            return step(k_force)
         outs = model.verify_batch(ids, cands) if len(ids) > 1 else [model.verify(ids[0], cands[0])]
         got = 0
         for i, c, o in zip(ids, cands, outs):
@@ -278,6 +280,29 @@ def main():
         log("[bench] per-kernel: " + ", ".join(f"{k} {v['avg_us']:.1f}us x{v['launches'] // n_t}"
                                                for k, v in kernel_ms.items()))
 
+    # achievable read bandwidth of the device (plain streaming kernel, 1 GiB)
+    stream_gbps = model.stream_bandwidth(1 << 30, 10)
+    log(f"[bench] stream-read ceiling {stream_gbps:.0f} GB/s")
+    if roof is not None:
+        roof["stream_ceiling_gbps"] = round(stream_gbps, 1)
+        roof["frac_of_stream_ceiling"] = round(roof["achieved"] / stream_gbps, 4)
+
+    # width-cost profile: step time per k (the paper's R(K) curve, one request)
+    width = None
+    if not args.no_width_profile and len(reqs) == 1 and wl.k_sweep:
+        width = {}
+        for kk in wl.k_sweep:
+            for _ in range(2):
+                step(kk)
+            sync()
+            n_w = 10
+            t1 = time.perf_counter()
+            for _ in range(n_w):
+                step(kk)
+            sync()
+            width[str(kk)] = round((time.perf_counter() - t1) * 1e3 / n_w, 4)
+        log("[bench] ms per step by k: " + ", ".join(f"k={kk} {v}" for kk, v in width.items()))
+
     cpu = None
     if not args.no_cpu_baseline:
         r0 = reqs[0]
@@ -310,6 +335,8 @@ def main():
         "step_hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "stream_ceiling_gbps": round(stream_gbps, 1),
+        "ms_per_step_by_k": width,
         "kernels": {k: round(v["avg_us"], 2) for k, v in kernel_ms.items()},
     }
     print(json.dumps(out), flush=True)

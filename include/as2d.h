@@ -203,6 +203,16 @@ int as2d_timing_reset(as2d_ctx* ctx);
  * it overwrites activation buffers and the cache rows 0..rows-1 of slot 0. */
 int as2d_time_gemm(as2d_ctx* ctx, int32_t which, int32_t rows, int32_t reps, double* avg_us);
 
+/* Achievable read bandwidth of the device, the ceiling for weight-streaming
+ * kernels: a plain kernel streams `bytes` (rounded down to a multiple of
+ * 64 MiB, at least 64 MiB) of a scratch buffer with 16-byte non-temporal
+ * loads, one workgroup per compute unit and 32 KiB in flight per unit;
+ * `reps` back-to-back launches between two HIP events on the library's
+ * stream.  Writes GB/s (1e9 bytes per second) to *gbps.  Allocates and
+ * frees the scratch buffer inside the call; EINVAL for bytes < 64 MiB or
+ * reps < 1, ENOMEM if the buffer does not fit. */
+int as2d_stream_bandwidth(as2d_ctx* ctx, int64_t bytes, int32_t reps, double* gbps);
+
 /* Algorithmic HBM bytes of one forward pass of `rows` rows whose
  * requests hold `kv_keys` attended positions in total per layer
  * (weights streamed once, embedding rows, KV read and append). */

@@ -23,7 +23,7 @@ EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_o
            "as2d_rollback", "as2d_get_state", "as2d_read_kv", "as2d_release_request",
            "as2d_set_exec_mode", "as2d_get_exec_info", "as2d_set_step_trace", "as2d_step_trace_read",
            "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_time_gemm",
-           "as2d_step_bytes", "as2d_free", "as2d_last_error"]
+           "as2d_stream_bandwidth", "as2d_step_bytes", "as2d_free", "as2d_last_error"]
 
 
 class Config(ctypes.Structure):
@@ -86,6 +86,7 @@ def load_library(path: str = LIB_PATH):
     lib.as2d_timing_read.argtypes = [_P, _P, _P, _P, _I]
     lib.as2d_timing_reset.argtypes = [_P]
     lib.as2d_time_gemm.argtypes = [_P, _I, _I, _I, ctypes.POINTER(ctypes.c_double)]
+    lib.as2d_stream_bandwidth.argtypes = [_P, ctypes.c_int64, _I, ctypes.POINTER(ctypes.c_double)]
     lib.as2d_step_bytes.argtypes = [_P, _I, ctypes.c_int64]
     lib.as2d_step_bytes.restype = ctypes.c_int64
     lib.as2d_free.argtypes = [_P]
@@ -253,6 +254,12 @@ class Model:
         us = ctypes.c_double()
         self._check(self.lib.as2d_time_gemm(self.ctx, which, rows, reps, ctypes.byref(us)))
         return us.value
+
+    def stream_bandwidth(self, nbytes: int = 1 << 30, reps: int = 10) -> float:
+        """Achievable read bandwidth (GB/s) of a plain streaming kernel."""
+        gbps = ctypes.c_double()
+        self._check(self.lib.as2d_stream_bandwidth(self.ctx, nbytes, reps, ctypes.byref(gbps)))
+        return gbps.value
 
     def step_bytes(self, rows: int, kv_keys: int) -> int:
         return int(self.lib.as2d_step_bytes(self.ctx, rows, kv_keys))

@@ -151,7 +151,8 @@ int dalloc(as2d_ctx* c, P** p, size_t bytes) {
 // depends only on the matrix shape, never on the rows of a pass, and the
 // pairs per workgroup do not change any sum, so every row is computed
 // alike in every pass.
-GemmPlan make_plan(int N, int K, int KE, int target) {
+// ks_override > 0 forces the split count (tuning experiments).
+GemmPlan make_plan(int N, int K, int KE, int target, int ks_override = 0) {
   GemmPlan p;
   p.N = N;
   p.K = K;
@@ -159,7 +160,7 @@ GemmPlan make_plan(int N, int K, int KE, int target) {
   p.pairs = N / kPairCols;
   p.np = p.pairs >= 1024 ? 2 : 1;
   p.ns = 4;
-  int ks = (int)std::lround((double)target / (p.pairs / p.np));
+  int ks = ks_override > 0 ? ks_override : (int)std::lround((double)target / (p.pairs / p.np));
   ks = std::max(1, std::min({ks, std::max(1, p.KT / 8), kMaxSplits}));
   p.ktps = (p.KT + ks - 1) / ks;
   p.KS = (p.KT + p.ktps - 1) / p.ktps;
@@ -664,11 +665,11 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
 
   // GEMM plans: k-splits depend on the matrix shape only
   const int target = env_int("AS2D_TARGET_WGS", 256);
-  c->p_qkv = make_plan(qkv_n, H, KE, target);
-  c->p_o = make_plan(H, nq * d, KE, target);
-  c->p_gu = make_plan(2 * F, H, KE, target);
-  c->p_down = make_plan(H, F, KE, target);
-  c->p_lm = make_plan(V, H, KE, target);
+  c->p_qkv = make_plan(qkv_n, H, KE, target, env_int("AS2D_KS_QKV", 0));
+  c->p_o = make_plan(H, nq * d, KE, target, env_int("AS2D_KS_O", 0));
+  c->p_gu = make_plan(2 * F, H, KE, target, env_int("AS2D_KS_GU", 0));
+  c->p_down = make_plan(H, F, KE, target, env_int("AS2D_KS_DOWN", 0));
+  c->p_lm = make_plan(V, H, KE, target, env_int("AS2D_KS_LM", 0));
 
   // temporary device buffer for raw matrices before packing (largest matrix)
   size_t tmp_elems = std::max({(size_t)V * H, (size_t)qkv_n * H, (size_t)2 * F * H, (size_t)H * F});
@@ -1185,6 +1186,42 @@ int as2d_time_gemm(as2d_ctx* c, int32_t which, int32_t rows, int32_t reps, doubl
   HIP_TRY(c, hipEventElapsedTime(&ms, e0, e1));
   *avg_us = ms * 1e3 / reps;
   return AS2D_OK;
+}
+
+int as2d_stream_bandwidth(as2d_ctx* c, int64_t bytes, int32_t reps, double* gbps) {
+  constexpr int64_t kUnit = 64ll << 20;
+  if (!c || !gbps || bytes < kUnit || reps < 1)
+    return c ? fail(c, AS2D_EINVAL, "stream_bandwidth: bad arguments") : AS2D_EINVAL;
+  bytes = bytes / kUnit * kUnit;
+  hipStream_t s = c->stream;
+  int dev = 0, cus = 0;
+  HIP_TRY(c, hipGetDevice(&dev));
+  HIP_TRY(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  void* buf = nullptr;
+  unsigned* out = nullptr;
+  if (hipMalloc(&buf, (size_t)bytes) != hipSuccess) return fail(c, AS2D_ENOMEM, "stream_bandwidth: %lld bytes", (long long)bytes);
+  int rc = [&]() -> int {
+    HIP_TRY(c, hipMalloc(&out, (size_t)cus * 4 * sizeof(unsigned)));
+    HIP_TRY(c, hipMemsetAsync(buf, 0, (size_t)bytes, s));
+    // one workgroup per compute unit; the segments must be whole 8 KiB runs per wave
+    int grid = cus;
+    while (grid > 1 && (bytes / 16) % ((int64_t)grid * 4 * 512)) --grid;
+    hipEvent_t e0 = ev_get(c, 1002), e1 = ev_get(c, 1003);
+    if (!e0 || !e1) return fail(c, AS2D_EHIP, "stream_bandwidth: events");
+    HIP_TRY(c, launch_stream_read((const uint4*)buf, bytes / 16, grid, out, s));   // warm-up
+    HIP_TRY(c, hipEventRecord(e0, s));
+    for (int i = 0; i < reps; ++i) HIP_TRY(c, launch_stream_read((const uint4*)buf, bytes / 16, grid, out, s));
+    HIP_TRY(c, hipEventRecord(e1, s));
+    HIP_TRY(c, hipEventSynchronize(e1));
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, e0, e1));
+    *gbps = (double)bytes * reps / (ms * 1e-3) / 1e9;
+    return AS2D_OK;
+  }();
+  hipStreamSynchronize(s);
+  if (out) hipFree(out);
+  hipFree(buf);
+  return rc;
 }
 
 int64_t as2d_step_bytes(const as2d_ctx* c, int32_t rows, int64_t kv_keys) {

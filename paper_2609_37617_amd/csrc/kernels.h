@@ -181,4 +181,8 @@ hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, i
                          const float* amax_val, const int* amax_idx, int n_pairs, int* row_tok,
                          int* row_bad, int* counters, StepOut* out, hipStream_t s);
 
+// Streams n16 16-byte units of buf with `grid` workgroups (read-bandwidth
+// reference); n16 must split into whole 8 KiB runs per wave.
+hipError_t launch_stream_read(const uint4* buf, long long n16, int grid, unsigned* out, hipStream_t s);
+
 }  // namespace as2d

@@ -266,4 +266,39 @@ hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, i
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Read-bandwidth reference: wave w of the grid streams its contiguous
+// segment of `per_wave` 16-byte units, 8 loads (8 KiB per wave) in flight.
+
+__global__ __launch_bounds__(256) void stream_read_kernel(const uint4* __restrict__ buf, long long per_wave,
+                                                          unsigned* __restrict__ out) {
+  constexpr int D = 8;
+  const int lane = threadIdx.x & 63;
+  const long long wave = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const u32x4* p = reinterpret_cast<const u32x4*>(buf + wave * per_wave + lane);
+  const int steps = (int)(per_wave / 64);
+  u32x4 r[D];
+  unsigned acc = 0;
+#pragma unroll
+  for (int u = 0; u < D; ++u) r[u] = __builtin_nontemporal_load(p + u * 64);
+  for (int i = 0; i + D < steps; i += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      acc ^= r[u].x ^ r[u].y ^ r[u].z ^ r[u].w;
+      r[u] = __builtin_nontemporal_load(p + (long long)(i + D + u) * 64);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < D; ++u) acc ^= r[u].x ^ r[u].y ^ r[u].z ^ r[u].w;
+  if (acc == 0x9e3779b9u) out[wave] = acc;   // keeps the loads; never true for a zeroed buffer
+}
+
+hipError_t launch_stream_read(const uint4* buf, long long n16, int grid, unsigned* out, hipStream_t s) {
+  const long long waves = (long long)grid * 4;
+  const long long per_wave = n16 / waves;
+  if (grid < 1 || per_wave < 64 * 8 || per_wave % (64 * 8)) return hipErrorInvalidValue;
+  stream_read_kernel<<<grid, 256, 0, s>>>(buf, per_wave, out);
+  return hipGetLastError();
+}
+
 }  // namespace as2d
