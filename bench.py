@@ -13,6 +13,10 @@ Printed: one JSON line with committed tokens/s (`value`), ms per step, the
 step's algorithmic HBM bandwidth and its fraction of the 8 TB/s peak, the
 roofline of the dominant kernel (gate/up GEMM) from HIP events on the
 library's stream, and the float64 CPU oracle timed on a bounded sample.
+
+The K timed steps start at the beginning of the replies (so a given K
+always covers the same stream positions); `full_pass` gives the tokens per
+step of one whole pass over the replies, which a K-step window samples.
 """
 import argparse
 import json
@@ -201,6 +205,12 @@ def main():
 
     done = [0] * len(reqs)        # committed tokens of the current reply pass
 
+    def restart():
+        """Every request back to the end of its prefix (start of its reply)."""
+        for i in range(len(reqs)):
+            model.rollback(i, *starts[i])
+            done[i] = 0
+
     def step(k_force=None):
         """One verification call over every request with reply left (one
         fused pass for several requests); returns tokens committed."""
@@ -212,9 +222,7 @@ def main():
             ids.append(i)
             cands.append(srcs[i].block(done[i], k))
         if not ids:
-            for i in range(len(reqs)):
-                model.rollback(i, *starts[i])
-                done[i] = 0
+            restart()
             return step(k_force)
         outs = model.verify_batch(ids, cands) if len(ids) > 1 else [model.verify(ids[0], cands[0])]
         got = 0
@@ -228,6 +236,18 @@ def main():
         copy_calibration(args.calib_copy_mib)
     for _ in range(args.warmup):
         step()
+    # one untimed pass over every reply: the workload's tokens per step,
+    # which a window of K steps only samples (acceptance varies along the
+    # stream with the corruption draws)
+    restart()
+    pass_steps = pass_tokens = 0
+    while True:
+        pass_tokens += step()[0]
+        pass_steps += 1
+        if all(d >= r.reply_len for d, r in zip(done, reqs)):
+            break
+    # the timed window starts at the beginning of the replies
+    restart()
     import ctypes
     _hip = ctypes.CDLL("libamdhip64.so")
 
@@ -330,6 +350,8 @@ def main():
                    "k": r0.k, "p": r0.p},
         "verify_steps_per_s": round(args.steps / elapsed, 2),
         "mean_committed_per_step": round(committed / args.steps, 3),
+        "full_pass": {"steps": pass_steps, "committed": pass_tokens,
+                      "mean_committed_per_step": round(pass_tokens / pass_steps, 3)},
         "step_hbm_bytes": step_bytes,
         "step_hbm_gbps": round(gbps, 1),
         "step_hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),

@@ -56,6 +56,26 @@ def prefix(shape, n_audio, n_instr, seed=0, req=0):
             gen.instruction_tokens(shape, n_instr, seed, req))
 
 
+def oracle_prefill(om, audio, instr, chunk=2048):
+    """The oracle's prefill taken through its forward in causal row chunks:
+    row t attends to positions <= t either way, so this is the same
+    arithmetic as one forward over the whole prefix, with temporaries of
+    chunk x prefix rows instead of prefix x prefix (long prefixes)."""
+    om.reset()
+    x = np.concatenate([np.asarray(audio, dtype=np.float64).reshape(-1, om.s.hidden),
+                        om.embed_tokens(instr)], axis=0)
+    T = x.shape[0]
+    om._check_capacity(T)
+    for c0 in range(0, T, chunk):
+        c1 = min(T, c0 + chunk)
+        rows = np.array([c1 - c0 - 1]) if c1 == T else np.array([], dtype=np.int64)
+        logits = om.forward(x[c0:c1], c0, logit_rows=rows)
+    om.last_logits = logits
+    om.root = greedy(logits[0])
+    om.kv_len = om.prefix_len = T
+    return om.root, om.kv_len
+
+
 def snapshot(om):
     return (copy.deepcopy(om.k_cache), copy.deepcopy(om.v_cache), om.kv_len, om.root)
 
@@ -90,9 +110,15 @@ def parity_round(om, gpu, req, cands, k, tol, stats, check_logits=True):
     snap = snapshot(om)
     ro = om.verify(cands, k)
     rg = gpu.verify(req, cands[:k], k)
-    toks = gpu.row_tokens(req)
-    if check_logits:
-        lg = gpu.logits(req)
+    check_round(om, snap, ro, rg, gpu.row_tokens(req), gpu.logits(req) if check_logits else None,
+                cands, k, tol, stats)
+    return rg
+
+
+def check_round(om, snap, ro, rg, toks, lg, cands, k, tol, stats):
+    """The near-tie protocol for one request's verify result rg (GPU row
+    tokens toks, logits lg or None) against the oracle's ro from state snap."""
+    if lg is not None:
         assert lg.shape == ro["logits"].shape
         err = float(np.max(np.abs(lg.astype(np.float64) - ro["logits"])))
         stats.max_err = max(stats.max_err, err)
@@ -111,7 +137,6 @@ def parity_round(om, gpu, req, cands, k, tol, stats, check_logits=True):
         assert toks[:rg["accepted_len"] + 1] == ro["tokens"][:ro["accepted_len"] + 1]
     assert rg["kv_len"] == om.kv_len
     stats.committed += rg["accepted_len"] + 1
-    return rg
 
 
 def compare_kv(om, gpu, req, layer, n_tok, tol):
