@@ -24,6 +24,7 @@ namespace {
 
 struct GemmPlan {
   int N = 0, K = 0, KT = 0, pairs = 0, KS = 1, ktps = 0, np = 1, ns = 4;
+  int G = 0;  // balanced direct path: workgroups sharing the units (0: one tile per workgroup)
 };
 
 struct LayerW {
@@ -167,6 +168,45 @@ GemmPlan make_plan(int N, int K, int KE, int target, int ks_override = 0) {
   return p;
 }
 
+// Balanced plan for the direct path (gemm_range kernel): the pairs x KS
+// (pair, split) units are shared equally by G = min(compute units, units)
+// workgroups.  KS is chosen for the 256 compute units of the MI355X
+// whatever the device, so that the sums stay a function of the shape: the
+// split count with the least estimated time of the busiest workgroup,
+// i.e. units per workgroup x the longest slice of a split (in k-steps),
+// plus, with k-splits, one partial per unit and `split_cost` k-steps for
+// the fixup phase.  Every split needs kWaves k-steps (one per slice).  A
+// shape with no such split count keeps the plan `p` (G = 0).
+GemmPlan balance_plan(GemmPlan p, int cus, int split_cost, int ks_override) {
+  constexpr int kNominalCUs = 256;
+  int best_ks = 0;
+  long long best = 0;
+  for (int ks = 1; ks <= kMaxSplits; ++ks) {
+    if (ks_override > 0 && ks != ks_override) continue;
+    const int ktps = (p.KT + ks - 1) / ks;
+    const int kse = (p.KT + ktps - 1) / ktps;
+    if (kse != ks || ktps < kWaves || p.KT - (kse - 1) * ktps < kWaves) continue;
+    const long long U = (long long)p.pairs * ks;
+    const long long G = std::min<long long>(kNominalCUs, U);
+    const long long nu = (U + G - 1) / G;
+    if (nu > kMaxUnits) continue;
+    const long long cost = nu * kWaves * ((ktps + kWaves - 1) / kWaves) + (ks > 1 ? nu + split_cost : 0);
+    if (!best_ks || cost < best) {
+      best = cost;
+      best_ks = ks;
+    }
+  }
+  if (!best_ks) return p;
+  p.np = 1;
+  p.ns = kWaves;
+  p.ktps = (p.KT + best_ks - 1) / best_ks;
+  p.KS = best_ks;
+  const int U = p.pairs * p.KS;
+  p.G = std::min(cus, U);
+  if ((U + p.G - 1) / p.G > kMaxUnits) p.G = (U + kMaxUnits - 1) / kMaxUnits;
+  return p;
+}
+
 int env_int(const char* name, int def) {
   const char* v = getenv(name);
   return v && *v ? atoi(v) : def;
@@ -231,6 +271,7 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   a.ktps = pl.ktps;
   a.np = pl.np;
   a.ns = pl.ns;
+  a.G = pl.G;
   a.M = M;
   a.MT = (M + 15) / 16;
   a.sumsq = c->sumsq;
@@ -665,11 +706,32 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
 
   // GEMM plans: k-splits depend on the matrix shape only
   const int target = env_int("AS2D_TARGET_WGS", 256);
-  c->p_qkv = make_plan(qkv_n, H, KE, target, env_int("AS2D_KS_QKV", 0));
-  c->p_o = make_plan(H, nq * d, KE, target, env_int("AS2D_KS_O", 0));
-  c->p_gu = make_plan(2 * F, H, KE, target, env_int("AS2D_KS_GU", 0));
-  c->p_down = make_plan(H, F, KE, target, env_int("AS2D_KS_DOWN", 0));
-  c->p_lm = make_plan(V, H, KE, target, env_int("AS2D_KS_LM", 0));
+  const int ks_qkv = env_int("AS2D_KS_QKV", 0), ks_o = env_int("AS2D_KS_O", 0), ks_gu = env_int("AS2D_KS_GU", 0);
+  const int ks_down = env_int("AS2D_KS_DOWN", 0), ks_lm = env_int("AS2D_KS_LM", 0);
+  c->p_qkv = make_plan(qkv_n, H, KE, target, ks_qkv);
+  c->p_o = make_plan(H, nq * d, KE, target, ks_o);
+  c->p_gu = make_plan(2 * F, H, KE, target, ks_gu);
+  c->p_down = make_plan(H, F, KE, target, ks_down);
+  c->p_lm = make_plan(V, H, KE, target, ks_lm);
+  // balanced direct path, per matrix (bits: QKV 1, O 2, gate/up 4, down 8,
+  // LM head 16); the down projection measured faster with one tile per
+  // workgroup, so it is left out by default
+  const int bal = env_int("AS2D_BALANCED", 23);
+  if (bal) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                hipSuccess || cus < 1) {
+      fail(c, AS2D_EHIP, "device query");
+      as2d_free(c);
+      return AS2D_EHIP;
+    }
+    const int sc = env_int("AS2D_SPLIT_COST", 24);
+    if (bal & 1) c->p_qkv = balance_plan(c->p_qkv, cus, sc, ks_qkv);
+    if (bal & 2) c->p_o = balance_plan(c->p_o, cus, sc, ks_o);
+    if (bal & 4) c->p_gu = balance_plan(c->p_gu, cus, sc, ks_gu);
+    if (bal & 8) c->p_down = balance_plan(c->p_down, cus, sc, ks_down);
+    if (bal & 16) c->p_lm = balance_plan(c->p_lm, cus, sc, ks_lm);
+  }
 
   // temporary device buffer for raw matrices before packing (largest matrix)
   size_t tmp_elems = std::max({(size_t)V * H, (size_t)qkv_n * H, (size_t)2 * F * H, (size_t)H * F});

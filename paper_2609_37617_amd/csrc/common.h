@@ -57,6 +57,13 @@ template <bool BF> __host__ __device__ __forceinline__ size_t frag_index(int m, 
 }
 // 16-byte unit of a block that lane l feeds to the MFMA (row l % 16, k-slice l / 16).
 __device__ __forceinline__ int frag_lane_unit(int lane) { return (lane & 15) * 4 + (lane >> 4); }
+// The same for a row tile with `rows` valid rows: lanes of the rows past
+// them read row 0's unit (a line the wave loads anyway), so the load needs
+// no branch and fetches no extra line; those lanes only feed output rows
+// that are never stored.
+__device__ __forceinline__ int frag_lane_unit_clamped(int lane, int rows) {
+  return ((lane & 15) < rows ? (lane & 15) * 4 : 0) + (lane >> 4);
+}
 
 // Activation planes (kernels.h): store value v at element i.
 template <bool BF, bool COH> __device__ __forceinline__ void store_act(void* base, long long plane, size_t i, float v) {

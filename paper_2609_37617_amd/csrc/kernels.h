@@ -30,7 +30,8 @@ constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
 constexpr int kDirectMT = 2;            // row tiles of the direct path (up to 32 rows)
 constexpr int kAttnChunk = 32;          // keys per attention split
-constexpr int kMaxSplits = 8;           // largest k-split count of a GEMM
+constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
+constexpr int kMaxUnits = 24;           // (pair, split) units per workgroup, balanced direct path
 constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
 
 // Column order of a packed matrix (pack_kernel): which matrix row (output
@@ -68,6 +69,8 @@ struct GemmArgs {
   int N, K, KT, KS, ktps;
   int np;                // tile pairs per workgroup on the direct path (1 or 2)
   int ns;                // ordered slices per k-split (4 or 16)
+  int G;                 // balanced direct path: workgroups sharing the units (0: one unit
+                         // group per workgroup)
   int M, MT;
   // A operand: activation planes [kMaxRows][K].  For A_NORM the planes
   // hold x * g (residual times RMSNorm gain) and the epilogue multiplies

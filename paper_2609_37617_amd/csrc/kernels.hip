@@ -129,6 +129,55 @@ static void launch_direct(const GemmArgs& a, hipStream_t s) {
   else gemm_direct_kernel<BF, MT, NP, NW, AM, EPI, false><<<grid, block, lds, s>>>(a);
 }
 
+// Balanced direct path: one workgroup per compute unit (the dynamic LDS
+// is at least kRangeMinLds, so two never share one), each streaming an
+// equal share of the (pair, split) units.  SL > 0: the variant with the
+// activation slice in registers (KS = 1, one row tile, KT = 4 SL).
+constexpr int kRangeMinLds = 82 * 1024;
+constexpr int kRangePrefetch = 4;
+
+template <bool BF, int MT, int SL, int AM, int EPI>
+__global__ __launch_bounds__(256, 1) void gemm_range_kernel(const GemmArgs p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ float s_scale[kMaxRows];
+  __shared__ int s_flags[kMaxUnits];
+  if constexpr (SL == 0) {
+    gemm_range_direct<BF, MT, kRangePrefetch, AM, EPI>(p, p.M, smem, s_scale, s_flags);
+  } else {
+    constexpr int P = SL % kRangePrefetch == 0 ? kRangePrefetch : SL;
+    gemm_range_direct_ra<BF, P, SL, AM, EPI>(p, p.M, smem, s_scale, s_flags);
+  }
+}
+
+// slice lengths with a register-resident variant, per element type
+template <bool BF> constexpr int kRangeSL[3] = {2, 16, 28};
+template <> constexpr int kRangeSL<false>[3] = {4, 4, 4};
+
+template <bool BF, int AM, int EPI>
+static hipError_t launch_range(const GemmArgs& a, hipStream_t s) {
+  const int U = (a.N / kPairCols) * a.KS;
+  const int last = a.KT - (a.KS - 1) * a.ktps;   // k-steps of the last split
+  if (a.G < 1 || a.G > U || (U + a.G - 1) / a.G > kMaxUnits || a.ktps < kWaves || last < kWaves ||
+      a.KS > kMaxSplits || a.ns != kWaves)
+    return hipErrorInvalidValue;
+  int lds = gemm_range_lds_bytes(a.MT, (U + a.G - 1) / a.G);
+  if (lds < kRangeMinLds) lds = kRangeMinLds;
+  const int sl = a.MT == 1 && a.KS == 1 && a.KT % kWaves == 0 ? a.KT / kWaves : 0;
+  bool done = false;
+  if constexpr (AM == A_NORM && (EPI == EPI_SWIGLU || EPI == EPI_ARGMAX)) {
+    done = true;
+    if (sl == kRangeSL<BF>[0]) gemm_range_kernel<BF, 1, kRangeSL<BF>[0], AM, EPI><<<a.G, 256, lds, s>>>(a);
+    else if (sl == kRangeSL<BF>[1]) gemm_range_kernel<BF, 1, kRangeSL<BF>[1], AM, EPI><<<a.G, 256, lds, s>>>(a);
+    else if (sl == kRangeSL<BF>[2]) gemm_range_kernel<BF, 1, kRangeSL<BF>[2], AM, EPI><<<a.G, 256, lds, s>>>(a);
+    else done = false;
+  }
+  if (!done) {
+    if (a.MT == 1) gemm_range_kernel<BF, 1, 0, AM, EPI><<<a.G, 256, lds, s>>>(a);
+    else gemm_range_kernel<BF, 2, 0, AM, EPI><<<a.G, 256, lds, s>>>(a);
+  }
+  return hipGetLastError();
+}
+
 template <bool BF, int MT, int AM, int EPI>
 __global__ __launch_bounds__(256) void gemm_staged_kernel(const GemmArgs p, const int chunk_kt) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -141,6 +190,7 @@ __global__ __launch_bounds__(256) void gemm_staged_kernel(const GemmArgs p, cons
 template <bool BF, int AM, int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   const int pairs = a.N / kPairCols;
+  if (a.MT <= kDirectMT && a.G > 0) return launch_range<BF, AM, EPI>(a, s);
   if (a.MT <= kDirectMT) {
     if ((a.np != 1 && (a.np != 2 || pairs % 2)) || a.ns < kWaves || a.ns > kMaxSlices || a.ns % kWaves)
       return hipErrorInvalidValue;
@@ -216,7 +266,31 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, h
 }
 
 // Kernels whose dynamic LDS may exceed the default 64 KiB limit.
-hipError_t prepare_kernels() { return prepare_step_kernels(); }
+template <bool BF, int AM, int EPI>
+static hipError_t prepare_range() {
+  const int bytes = gemm_range_lds_bytes(kDirectMT, kMaxUnits);
+  auto allow = [bytes](const void* k) { return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, bytes); };
+  hipError_t e = allow(reinterpret_cast<const void*>(&gemm_range_kernel<BF, 1, 0, AM, EPI>));
+  if (e == hipSuccess) e = allow(reinterpret_cast<const void*>(&gemm_range_kernel<BF, 2, 0, AM, EPI>));
+  if constexpr (AM == A_NORM && (EPI == EPI_SWIGLU || EPI == EPI_ARGMAX)) {
+    if (e == hipSuccess) e = allow(reinterpret_cast<const void*>(&gemm_range_kernel<BF, 1, kRangeSL<BF>[0], AM, EPI>));
+    if (e == hipSuccess) e = allow(reinterpret_cast<const void*>(&gemm_range_kernel<BF, 1, kRangeSL<BF>[1], AM, EPI>));
+    if (e == hipSuccess) e = allow(reinterpret_cast<const void*>(&gemm_range_kernel<BF, 1, kRangeSL<BF>[2], AM, EPI>));
+  }
+  return e;
+}
+
+hipError_t prepare_kernels() {
+  hipError_t e = prepare_step_kernels();
+#define AS2D_P(bf, am, ep) \
+  if (e == hipSuccess) e = prepare_range<bf, am, ep>();
+  AS2D_P(true, A_NORM, EPI_QKV) AS2D_P(true, A_PLAIN, EPI_RESID) AS2D_P(true, A_NORM, EPI_SWIGLU)
+  AS2D_P(true, A_NORM, EPI_ARGMAX)
+  AS2D_P(false, A_NORM, EPI_QKV) AS2D_P(false, A_PLAIN, EPI_RESID) AS2D_P(false, A_NORM, EPI_SWIGLU)
+  AS2D_P(false, A_NORM, EPI_ARGMAX)
+#undef AS2D_P
+  return e;
+}
 
 hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
   if (a.head_dim == 128) return bf16 ? attn_dispatch<true, 128>(a, n_reqs, max_chunks, s)

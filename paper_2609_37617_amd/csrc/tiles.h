@@ -73,8 +73,9 @@ __device__ void embed_row(const RowDesc* __restrict__ rows, int m, const typenam
 // Fused GEMM epilogues over rows [r0, r1) of `np` consecutive tile pairs
 // starting at pair `pair0`; F holds their finished values (float32, row
 // stride fs, pair pp at columns [32 pp, 32 pp + 32)).  NTH threads.  Every
-// per-pair reduction runs on one half-wave in a fixed pattern, so a row's
-// results do not depend on how many pairs or rows the call covers.
+// per-pair sum runs on one half-wave in a fixed pattern, and the per-pair
+// arg-max is exact, so a row's results do not depend on how many pairs or
+// rows the call covers.
 
 template <bool BF, int EPI, bool COH, int NTH = 256>
 __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, int np, int r0, int r1) {
@@ -145,23 +146,28 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
       }
     }
   } else {  // EPI_ARGMAX (identity column order: column = token id)
-    for (int u0 = wave * 2; u0 < units; u0 += kUnits) {
-      const int u = u0 + (lane >> 5);
-      const bool ok = u < units;
-      const int m = ok ? r0 + u / np : r0, pp = u % np;
-      const int n = (pair0 + pp) * kPairCols + (lane & 31);
-      const float v = ok ? F[(m - r0) * fs + pp * kPairCols + (lane & 31)] : -INFINITY;
-      if (p.logits && ok) p.logits[(size_t)m * N + n] = v;   // read by the host only
-      const bool bad = ok && !isfinite(v);
-      float best = v;
-      int bi = n;
-      half_argmax(best, bi);
-      const unsigned long long mask = __ballot(bad);
-      const bool any_bad = ((mask >> (lane & 32)) & 0xffffffffull) != 0;
-      if ((lane & 31) == 0 && ok) {
-        st<COH>(p.amax_val + (size_t)m * (N / kPairCols) + pair0 + pp, any_bad ? __builtin_nanf("") : best);
-        st<COH>(p.amax_idx + (size_t)m * (N / kPairCols) + pair0 + pp, bi);
+    // one (row, pair) per thread: the largest value, the lowest column
+    // among equal values (exact, so the order of the scan is immaterial);
+    // a non-finite value makes the pair's partial NaN
+    for (int u = tid; u < units; u += NTH) {
+      const int m = r0 + u / np, pp = u % np;
+      const int n0p = (pair0 + pp) * kPairCols;
+      const float* Fr = F + (m - r0) * fs + pp * kPairCols;
+      float best = Fr[0];
+      int bi = n0p;
+      bool bad = !isfinite(best);
+      if (p.logits) p.logits[(size_t)m * N + n0p] = best;   // read by the host only
+      for (int c = 1; c < kPairCols; ++c) {
+        const float v = Fr[c];
+        if (p.logits) p.logits[(size_t)m * N + n0p + c] = v;
+        bad |= !isfinite(v);
+        if (v > best) {
+          best = v;
+          bi = n0p + c;
+        }
       }
+      st<COH>(p.amax_val + (size_t)m * (N / kPairCols) + pair0 + pp, bad ? __builtin_nanf("") : best);
+      st<COH>(p.amax_idx + (size_t)m * (N / kPairCols) + pair0 + pp, bi);
     }
   }
 }
@@ -256,6 +262,53 @@ __device__ __forceinline__ void row_scales(const GemmArgs& p, int M, float* s_sc
   }
 }
 
+// row_scales in two steps for the direct paths, with the same sums (the
+// same bits): row_scale_loads reads the sum-of-squares partials of this
+// wave's rows m = wave + NW r (r < RPW) with no branch around the loads
+// and forms each lane's partial sum; it is called right after the first
+// weight loads, so its wait is one the stream needs anyway.
+// row_scale_finish adds the lanes (same butterfly) for the rows < M and
+// writes s_scale; it runs after the stream.
+template <int AM, int RPW, int NW = kWaves>
+__device__ __forceinline__ void row_scale_loads(const GemmArgs& p, int M, float (&s)[RPW]) {
+  if constexpr (AM == A_NORM) {
+    constexpr int kT = 4;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int np = p.n_norm_pairs;
+    float v[RPW][kT];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int m = wave + NW * r, mm = m < M ? m : 0;
+#pragma unroll
+      for (int t = 0; t < kT; ++t) {
+        const int i = lane + 64 * t;
+        v[r][t] = p.sumsq[(size_t)mm * np + (i < np ? i : 0)];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      s[r] = 0.0f;
+#pragma unroll
+      for (int t = 0; t < kT; ++t)
+        if (wave + NW * r < M && lane + 64 * t < np) s[r] += v[r][t];
+    }
+  }
+}
+template <int AM, int RPW, int NW = kWaves>
+__device__ __forceinline__ void row_scale_finish(const GemmArgs& p, int M, const float (&s)[RPW], float* s_scale) {
+  if constexpr (AM == A_NORM) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) {
+      const int m = wave + NW * r;
+      if (m < M) {
+        const float tot = wave_sum(s[r]);
+        if (lane == 0) s_scale[m] = 1.0f / sqrtf(tot / (float)p.K + p.eps);
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // GEMM tiles.  Every output element is summed in one order whatever the
 // path, the tile shape or the number of rows: k-split s of the plan
@@ -345,7 +398,10 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
 
   const uint4* wp = p.W + (size_t)pair0 * p.KT * 128 + lane;
   const size_t pstride = (size_t)p.KT * 128;        // next pair's tiles
-  const uint4* ap = static_cast<const uint4*>(p.A) + frag_lane_unit(lane);
+  const uint4* ap[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+    ap[mt] = static_cast<const uint4*>(p.A) + frag_lane_unit_clamped(lane, M - mt * 16);
   const long long lo = p.a_plane / ET<BF>::PER16;   // lo plane, in 16-byte units
   auto loadW = [&](int kt, uint4(&bb)[NP][2]) {
 #pragma unroll
@@ -354,16 +410,14 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
       bb[q][1] = ldw(wp + q * pstride + (size_t)kt * 128 + 64);
     }
   };
-  // rows >= M are not loaded: their lanes keep zeros or stale values that
-  // only reach output rows >= M, which are never stored
+  // lanes of rows >= M read row 0 of their tile (frag_lane_unit_clamped):
+  // every lane loads, with no branch, so the waits stay exact
   auto loadA = [&](int kt, AFrag(&af)[MT]) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      if (mt * 16 + (lane & 15) < M) {
-        const uint4* a = ap + ((size_t)mt * p.KT + kt) * 64;
-        af[mt].h = *a;
-        if constexpr (BF) af[mt].l = a[lo];
-      }
+      const uint4* a = ap[mt] + ((size_t)mt * p.KT + kt) * 64;
+      af[mt].h = *a;
+      if constexpr (BF) af[mt].l = a[lo];
     }
   };
   auto step = [&](int s, const uint4(&bb)[NP][2], const AFrag(&af)[MT]) {
@@ -396,6 +450,9 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
     for (int u = 0; u < P; ++u) loadW(kk(u), b[u]);
   }
   wait();
+  constexpr int RPW = (MT * 16 + NW - 1) / NW;   // rows per wave of the row scales
+  float rs[RPW];
+  row_scale_loads<AM, RPW, NW>(p, M, rs);        // read while the first weights arrive
   if (spw > 1) advance(0);
   if (n > 0) {
 #pragma unroll
@@ -429,7 +486,7 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
   }
 
   const bool split_k = SPLIT && p.KS > 1;
-  if (!split_k) row_scales<AM, NW>(p, M, s_scale);
+  row_scale_finish<AM, RPW, NW>(p, M, rs, s_scale);
   __syncthreads();
   // element x = (((mt * NP + q) * 2 + j) * 4 + i) * 64 + l: row 16 mt + 4 (l / 16) + i,
   // column 32 q + 16 j + l % 16
@@ -448,8 +505,6 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
     if (!publish_split<NTH>(p, M, split, n0, NP * kPairCols, &p.counters[tile], s_flag,
                             [&](int m, int c) { return F[m * FS + c]; }))
       return false;
-    row_scales<AM, NW>(p, M, s_scale);
-    __syncthreads();
     fixup_rows<AM, NTH>(p, M, n0, NP * kPairCols, 0, M, s_scale, F, FS);
   } else {
     for (int x = tid; x < QS; x += NTH) {
@@ -463,6 +518,269 @@ __device__ bool gemm_tile_direct(const GemmArgs& p, int M, int tile, int split, 
   lds_sync();
   epilogue_rows<BF, EPI, COH, NTH>(p, F, FS, pair0, NP, 0, M);
   return true;
+}
+
+// Balanced direct path (up to kDirectMT row tiles, one tile pair per unit).
+// The units (tile pair, k-split) of a GEMM are numbered pair-major, split
+// minor; workgroup b of G takes units [b U / G, (b + 1) U / G), so every
+// workgroup streams the same share of the weights (to within one unit)
+// whatever the number of pairs, and no compute unit holds more workgroups
+// than another.  A unit is summed exactly as gemm_tile_direct sums it with
+// kWaves slices per split (wave w: slice w, k-steps in order by MFMA from
+// zero; slices added in order in LDS; splits added in order by the fixup),
+// so its results are those of the other paths bit for bit.
+//   Each wave issues its slices of all the workgroup's units as one run of
+// loads, P k-steps ahead across unit boundaries; the barrier that closes a
+// unit orders LDS only, so the run stays in flight.  Unit sums collect in
+// one LDS tile [row][32 nu + 1]; after the stream come the epilogue of the
+// workgroup's pairs (KS = 1), or its split partials and the fixup and
+// epilogue of each pair whose last split arrives here.
+//   Host-checked: every split has at least kWaves k-steps, at most
+// kMaxUnits units per workgroup, G <= U.
+//   smem: dynamic LDS of gemm_range_lds_bytes(MT, nu_max); s_flags:
+//   kMaxUnits ints.
+
+__host__ __device__ constexpr int gemm_range_lds_bytes(int MT, int nu_max) {
+  return (2 * kWaves * MT * 512 + MT * 16 * (nu_max * kPairCols + 1)) * 4;
+}
+
+// Closes unit j of the balanced path: this wave's slice sums go to LDS
+// slot j & 1, then (all slices present) the slices are added in order into
+// columns 32 j .. of F.  Every wave calls it once per unit, in unit order.
+template <int MT>
+__device__ __forceinline__ void range_close(float* R, float* F, int fs, int j, int wave, f4 (&acc)[MT][2]) {
+  constexpr int QS = MT * 512;
+  const int tid = threadIdx.x, lane = tid & 63;
+  float* Rw = R + ((j & 1) * kWaves + wave) * QS;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Rw[((mt * 2 + jj) * 4 + i) * 64 + lane] = acc[mt][jj][i];
+      acc[mt][jj] = f4{0.f, 0.f, 0.f, 0.f};
+    }
+  lds_sync();
+  const float* R0 = R + (j & 1) * kWaves * QS;
+  for (int x = tid; x < QS; x += kWaves * 64) {
+    float v = R0[x];
+#pragma unroll
+    for (int q = 1; q < kWaves; ++q) v += R0[q * QS + x];
+    // element x = ((mt * 2 + jj) * 4 + i) * 64 + l: row 16 mt + 4 (l / 16) + i, column 16 jj + l % 16
+    const int row = (x >> 9) * 16 + 4 * ((x & 63) >> 4) + ((x >> 6) & 3);
+    const int col = ((x >> 8) & 1) * 16 + (x & 15);
+    F[row * fs + j * kPairCols + col] = v;
+  }
+}
+
+// After the stream of the balanced path (s_scale already holds the row
+// scales): the epilogue of units [u0, u0 + nu) from their sums in F, or,
+// with k-splits, their partials and the fixup and epilogue of each pair
+// whose last split arrives in this workgroup.
+template <bool BF, int AM, int EPI>
+__device__ void range_finish(const GemmArgs& p, int M, float* F, int fs, int u0, int nu, const float* s_scale,
+                             int* s_flags) {
+  constexpr int NTH = kWaves * 64;
+  const int tid = threadIdx.x, KS = p.KS;
+  const int C = nu * kPairCols;
+  if (KS == 1) {
+    if constexpr (AM == A_NORM) {
+      const int wave = tid >> 6, lane = tid & 63;
+      for (int m = wave; m < M; m += kWaves)
+        for (int c = lane; c < C; c += 64) F[m * fs + c] *= s_scale[m];
+      lds_sync();
+    }
+    epilogue_rows<BF, EPI, false, NTH>(p, F, fs, u0, nu, 0, M);
+    return;
+  }
+  for (int e = tid; e < M * C; e += NTH) {
+    const int m = e / C, c = e - m * C;
+    const int u = u0 + c / kPairCols, pair = u / KS;
+    store_partial(&p.part[((size_t)(u - pair * KS) * M + m) * p.N + pair * kPairCols + (c & (kPairCols - 1))],
+                  F[m * fs + c]);
+  }
+  wait_vmem();
+  __syncthreads();  // every wave's partial stores are performed
+  if (tid < nu) {
+    const int pair = (u0 + tid) / KS;
+    const bool last = counter_add(&p.counters[pair], 1) == KS - 1;
+    if (last) st<true>(&p.counters[pair], 0);  // ready for the next launch
+    s_flags[tid] = last;
+  }
+  __syncthreads();
+  for (int j = 0; j < nu; ++j) {
+    if (!s_flags[j]) continue;
+    const int pair = (u0 + j) / KS;
+    fixup_rows<AM, NTH>(p, M, pair * kPairCols, kPairCols, 0, M, s_scale, F + j * kPairCols, fs);
+    lds_sync();
+    epilogue_rows<BF, EPI, false, NTH>(p, F + j * kPairCols, fs, pair, 1, 0, M);
+    lds_sync();
+  }
+}
+
+template <bool BF, int MT, int P, int AM, int EPI>
+__device__ void gemm_range_direct(const GemmArgs& p, int M, unsigned char* smem, float* s_scale, int* s_flags) {
+  constexpr int QS = MT * 512;                       // floats of one wave's slice
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int KS = p.KS, KT = p.KT, G = p.G;
+  const int U = (p.N / kPairCols) * KS;
+  const int u0 = (int)((long long)blockIdx.x * U / G), u1 = (int)((long long)(blockIdx.x + 1) * U / G);
+  const int nu = u1 - u0;
+  const int fs = ((U + G - 1) / G) * kPairCols + 1;
+  float* R = reinterpret_cast<float*>(smem);         // [unit & 1][wave][mt][j][i][lane]
+  float* F = R + 2 * kWaves * QS;                    // [row][fs]: unit j at columns 32 j ..
+
+  // this wave's k-steps of unit j: slice `wave` of the unit's split
+  struct Cur {
+    int j, pair, kt, end;
+  };
+  auto set_unit = [&](Cur& c, int j) {
+    const int u = u0 + j;
+    c.j = j;
+    c.pair = u / KS;
+    const int kt0 = (u - c.pair * KS) * p.ktps;
+    const int n_all = min(KT, kt0 + p.ktps) - kt0;
+    c.kt = slice_start(kt0, n_all, wave, kWaves);
+    c.end = slice_start(kt0, n_all, wave + 1, kWaves);
+  };
+  int S = 0;                                          // k-steps of this wave
+  for (int j = 0; j < nu; ++j) {
+    Cur c;
+    set_unit(c, j);
+    S += c.end - c.kt;
+  }
+
+  const uint4* ap[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+    ap[mt] = static_cast<const uint4*>(p.A) + frag_lane_unit_clamped(lane, M - mt * 16);
+  const long long lo = p.a_plane / ET<BF>::PER16;   // lo plane, in 16-byte units
+  // one k-step: the pair's two weight tiles, then the row tiles' fragments
+  // (lanes of rows >= M read row 0 of their tile: no branch, exact waits)
+  auto load = [&](const Cur& c, uint4(&bb)[2], AFrag(&af)[MT]) {
+    const uint4* w = p.W + ((size_t)c.pair * KT + c.kt) * 128 + lane;
+    bb[0] = ldw(w);
+    bb[1] = ldw(w + 64);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const uint4* a = ap[mt] + ((size_t)mt * KT + c.kt) * 64;
+      af[mt].h = *a;
+      if constexpr (BF) af[mt].l = a[lo];
+    }
+  };
+  // the load cursor steps through the units; past the last k-step it
+  // re-reads that k-step, so every round issues the same loads
+  auto advance = [&](Cur& c) {
+    if (++c.kt == c.end) {
+      if (c.j + 1 < nu) set_unit(c, c.j + 1);
+      else c.kt = c.end - 1;
+    }
+  };
+
+  f4 acc[MT][2];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt][0] = acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
+  uint4 bw[P][2];
+  AFrag af[P][MT];
+#pragma unroll
+  for (int u = 0; u < P; ++u)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) af[u][mt] = AFrag{make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+  Cur cl;
+  set_unit(cl, 0);
+  int rem = cl.end - cl.kt;                           // k-steps left in the unit being summed
+#pragma unroll
+  for (int u = 0; u < P; ++u) {
+    load(cl, bw[u], af[u]);
+    advance(cl);
+  }
+  constexpr int RPW = MT * 16 / kWaves;
+  float rs[RPW];
+  row_scale_loads<AM, RPW>(p, M, rs);                 // read while the first weights arrive
+  int cj = 0;                                         // unit being summed
+  for (int i = 0; i < S; i += P) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      if (i + u < S) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          acc[mt][0] = mma_a<BF>(af[u][mt], bw[u][0], acc[mt][0]);
+          acc[mt][1] = mma_a<BF>(af[u][mt], bw[u][1], acc[mt][1]);
+        }
+        if (--rem == 0) {
+          range_close<MT>(R, F, fs, cj, wave, acc);
+          if (++cj < nu) {
+            Cur c;
+            set_unit(c, cj);
+            rem = c.end - c.kt;
+          }
+        }
+      }
+      load(cl, bw[u], af[u]);
+      advance(cl);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  row_scale_finish<AM, RPW>(p, M, rs, s_scale);
+  lds_sync();                                         // the last unit's sums are in F
+  range_finish<BF, AM, EPI>(p, M, F, fs, u0, nu, s_scale, s_flags);
+}
+
+// The balanced path for KS = 1 and one row tile when every wave's slice
+// has SL = KT / kWaves k-steps: a wave's slice covers the same k-steps of
+// every pair, so its activation fragments are loaded once into registers
+// and only the weights stream.  Sums as in gemm_range_direct.
+template <bool BF, int P, int SL, int AM, int EPI>
+__device__ void gemm_range_direct_ra(const GemmArgs& p, int M, unsigned char* smem, float* s_scale, int* s_flags) {
+  static_assert(SL % P == 0, "slice length must be a multiple of the prefetch depth");
+  constexpr int QS = 512;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int KT = p.KT, G = p.G;
+  const int U = p.N / kPairCols;
+  const int u0 = (int)((long long)blockIdx.x * U / G), u1 = (int)((long long)(blockIdx.x + 1) * U / G);
+  const int nu = u1 - u0;
+  const int fs = ((U + G - 1) / G) * kPairCols + 1;
+  float* R = reinterpret_cast<float*>(smem);
+  float* F = R + 2 * kWaves * QS;
+  const int kt0 = wave * SL;                          // slice_start(0, KT, wave, kWaves)
+  const uint4* wb = p.W + ((size_t)u0 * KT + kt0) * 128 + lane;
+  // weights of k-step s of unit j; past the last unit, its last k-step again
+  auto loadW = [&](int j, int s, uint4(&bb)[2]) {
+    const bool past = j >= nu;
+    const uint4* w = wb + ((size_t)(past ? nu - 1 : j) * KT + (past ? SL - 1 : s)) * 128;
+    bb[0] = ldw(w);
+    bb[1] = ldw(w + 64);
+  };
+  uint4 bw[P][2];
+#pragma unroll
+  for (int u = 0; u < P; ++u) loadW(0, u, bw[u]);
+  const uint4* ap = static_cast<const uint4*>(p.A) + frag_lane_unit_clamped(lane, M) + (size_t)kt0 * 64;
+  const long long lo = p.a_plane / ET<BF>::PER16;
+  AFrag af[SL];
+#pragma unroll
+  for (int s = 0; s < SL; ++s) {
+    af[s].h = ap[(size_t)s * 64];
+    if constexpr (BF) af[s].l = ap[(size_t)s * 64 + lo];
+  }
+  float rs[16 / kWaves];
+  row_scale_loads<AM, 16 / kWaves>(p, M, rs);
+  f4 acc[1][2];
+  acc[0][0] = acc[0][1] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < nu; ++j) {
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+      acc[0][0] = mma_a<BF>(af[s], bw[s % P][0], acc[0][0]);
+      acc[0][1] = mma_a<BF>(af[s], bw[s % P][1], acc[0][1]);
+      loadW(j + (s + P) / SL, (s + P) % SL, bw[s % P]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    range_close<1>(R, F, fs, j, wave, acc);
+  }
+  row_scale_finish<AM, 16 / kWaves>(p, M, rs, s_scale);
+  lds_sync();
+  range_finish<BF, AM, EPI>(p, M, F, fs, u0, nu, s_scale, s_flags);
 }
 
 // Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
