@@ -174,10 +174,12 @@ GemmPlan make_plan(int N, int K, int KE, int target, int ks_override = 0) {
 // whatever the device, so that the sums stay a function of the shape: the
 // split count with the least estimated time of the busiest workgroup,
 // i.e. units per workgroup x the longest slice of a split (in k-steps),
-// plus, with k-splits, one partial per unit and `split_cost` k-steps for
-// the fixup phase.  Every split needs kWaves k-steps (one per slice).  A
-// shape with no such split count keeps the plan `p` (G = 0).
-GemmPlan balance_plan(GemmPlan p, int cus, int split_cost, int ks_override) {
+// plus, with k-splits, `split_cost` k-steps for the fixup phase and
+// `per_split` k-steps for each split it reads (measured on the 7B shape:
+// 16 and 5 put QKV at 3 splits, O and down at 2, gate/up and the LM head
+// at 1, the fastest of the sweep).  Every split needs kWaves k-steps (one
+// per slice).  A shape with no such split count keeps the plan `p` (G = 0).
+GemmPlan balance_plan(GemmPlan p, int cus, int split_cost, int per_split, int ks_override) {
   constexpr int kNominalCUs = 256;
   int best_ks = 0;
   long long best = 0;
@@ -190,7 +192,7 @@ GemmPlan balance_plan(GemmPlan p, int cus, int split_cost, int ks_override) {
     const long long G = std::min<long long>(kNominalCUs, U);
     const long long nu = (U + G - 1) / G;
     if (nu > kMaxUnits) continue;
-    const long long cost = nu * kWaves * ((ktps + kWaves - 1) / kWaves) + (ks > 1 ? nu + split_cost : 0);
+    const long long cost = nu * kWaves * ((ktps + kWaves - 1) / kWaves) + (ks > 1 ? split_cost + per_split * ks : 0);
     if (!best_ks || cost < best) {
       best = cost;
       best_ks = ks;
@@ -713,10 +715,8 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   c->p_gu = make_plan(2 * F, H, KE, target, ks_gu);
   c->p_down = make_plan(H, F, KE, target, ks_down);
   c->p_lm = make_plan(V, H, KE, target, ks_lm);
-  // balanced direct path, per matrix (bits: QKV 1, O 2, gate/up 4, down 8,
-  // LM head 16); the down projection measured faster with one tile per
-  // workgroup, so it is left out by default
-  const int bal = env_int("AS2D_BALANCED", 23);
+  // balanced direct path, per matrix (bits: QKV 1, O 2, gate/up 4, down 8, LM head 16)
+  const int bal = env_int("AS2D_BALANCED", 31);
   if (bal) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
@@ -725,12 +725,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
       as2d_free(c);
       return AS2D_EHIP;
     }
-    const int sc = env_int("AS2D_SPLIT_COST", 24);
-    if (bal & 1) c->p_qkv = balance_plan(c->p_qkv, cus, sc, ks_qkv);
-    if (bal & 2) c->p_o = balance_plan(c->p_o, cus, sc, ks_o);
-    if (bal & 4) c->p_gu = balance_plan(c->p_gu, cus, sc, ks_gu);
-    if (bal & 8) c->p_down = balance_plan(c->p_down, cus, sc, ks_down);
-    if (bal & 16) c->p_lm = balance_plan(c->p_lm, cus, sc, ks_lm);
+    const int sc = env_int("AS2D_SPLIT_COST", 16), ps = env_int("AS2D_SPLIT_COST_PER", 5);
+    if (bal & 1) c->p_qkv = balance_plan(c->p_qkv, cus, sc, ps, ks_qkv);
+    if (bal & 2) c->p_o = balance_plan(c->p_o, cus, sc, ps, ks_o);
+    if (bal & 4) c->p_gu = balance_plan(c->p_gu, cus, sc, ps, ks_gu);
+    if (bal & 8) c->p_down = balance_plan(c->p_down, cus, sc, ps, ks_down);
+    if (bal & 16) c->p_lm = balance_plan(c->p_lm, cus, sc, ps, ks_lm);
   }
 
   // temporary device buffer for raw matrices before packing (largest matrix)
