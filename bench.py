@@ -52,6 +52,7 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="(tuning only) override layer count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-align", action="store_true", help="skip the candidate-buffer decoding measurement")
     ap.add_argument("--no-width-profile", action="store_true",
                     help="skip the per-k step times (single-request workloads with a k sweep)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -323,6 +324,35 @@ def main():
             width[str(kk)] = round((time.perf_counter() - t1) * 1e3 / n_w, 4)
         log("[bench] ms per step by k: " + ", ".join(f"k={kk} {v}" for kk, v in width.items()))
 
+    # decoding from the candidate buffer with an edited draft (substitutions,
+    # insertions, deletions): with the bounded realignment, and with the
+    # search turned off (radius 0: every mismatch read as a substitution)
+    aligned = None
+    if not args.no_align and len(reqs) == 1:
+        r0 = reqs[0]
+        edits = (0.2, 0.05, 0.05)
+        draft = gen.edited_stream(srcs[0].ref[1:].tolist(), shape.vocab, *edits, seed=wl.seed)
+        aligned = {"draft": {"sub": edits[0], "ins": edits[1], "del": edits[2], "tokens": len(draft)},
+                   "budget": r0.k, "reply_tokens": r0.reply_len}
+        for name, radius in (("with_alignment", 8), ("without_search", 0)):
+            buf = as2d.CandidateBuffer(len(draft))
+            for i in range(0, len(draft), 8):
+                buf.publish(draft[i:i + 8], offset=i)
+            cur = as2d.ReadCursor(radius)
+            restart()
+            calls = got = 0
+            t1 = time.perf_counter()
+            while got < r0.reply_len:
+                r, _ = cur.verify_from_buffer(model, 0, buf, r0.k, r0.reply_len - got)
+                got += r["accepted_len"] + 1
+                calls += 1
+            dt = time.perf_counter() - t1
+            aligned[name] = {"calls": calls, "tokens_per_s": round(got / dt, 1),
+                             "mean_committed_per_call": round(got / calls, 3), "ms_per_call": round(dt * 1e3 / calls, 4)}
+            buf.close()
+        restart()
+        log(f"[bench] buffer decoding, edited draft: {aligned['with_alignment']} | radius 0: {aligned['without_search']}")
+
     cpu = None
     if not args.no_cpu_baseline:
         r0 = reqs[0]
@@ -359,6 +389,7 @@ def main():
         "cpu_baseline": cpu,
         "stream_ceiling_gbps": round(stream_gbps, 1),
         "ms_per_step_by_k": width,
+        "buffer_decoding": aligned,
         "kernels": {k: round(v["avg_us"], 2) for k, v in kernel_ms.items()},
     }
     print(json.dumps(out), flush=True)

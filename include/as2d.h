@@ -213,6 +213,101 @@ int as2d_time_gemm(as2d_ctx* ctx, int32_t which, int32_t rows, int32_t reps, dou
  * reps < 1, ENOMEM if the buffer does not fit. */
 int as2d_stream_bandwidth(as2d_ctx* ctx, int64_t bytes, int32_t reps, double* gbps);
 
+/*
+ * Candidate buffer (Section 4.1 "Ordered publication and buffering";
+ * Appendix C.1 "Source records and incremental publication").
+ *
+ * An ordered, append-only buffer of candidate tokens in the target
+ * vocabulary.  One producer thread publishes immutable batches of 1..8
+ * tokens, each with its provenance record; any number of threads read.
+ * A reader takes a snapshot (the published length at that moment) and may
+ * read any token below it while later batches are appended; the producer
+ * never waits for a reader.  Capacity (tokens) is fixed at creation.
+ * These calls touch no GPU state.  Errors: AS2D_EINVAL for null pointers,
+ * batch sizes outside 1..8 and reads past the published length;
+ * AS2D_ECAPACITY when a batch does not fit; AS2D_ENOMEM.
+ */
+#define AS2D_MAX_BUDGET 31   /* largest number of candidates per call (max_k <= 31) */
+
+typedef struct as2d_cbuf as2d_cbuf;
+
+typedef struct {
+  int64_t first;       /* buffer position of the batch's first token */
+  int32_t count;       /* tokens in the batch, 1..8 */
+  int32_t source_id;   /* source record (request and audio view) the batch belongs to */
+  int32_t producer_id;
+  int32_t pad;
+  int64_t offset;      /* token offset of the batch within its source sequence */
+  int64_t publish_ns;  /* publication time stamp, as given by the producer */
+  float confidence;    /* producer confidence, NaN when unavailable */
+  int32_t pad2;
+} as2d_cbuf_record;
+
+int as2d_cbuf_create(int64_t capacity, as2d_cbuf** out);
+int as2d_cbuf_free(as2d_cbuf* buf);
+/* Producer only.  *published (optional) receives the new published length. */
+int as2d_cbuf_publish(as2d_cbuf* buf, const int32_t* tokens, int32_t n, int32_t source_id, int32_t producer_id,
+                      int64_t offset, int64_t publish_ns, float confidence, int64_t* published);
+int as2d_cbuf_snapshot(const as2d_cbuf* buf, int64_t* n);
+/* Tokens [start, start + n) of the published prefix into out[n] (n = 0
+ * reads nothing, at any start >= 0). */
+int as2d_cbuf_read(const as2d_cbuf* buf, int64_t start, int32_t n, int32_t* out);
+int as2d_cbuf_n_records(const as2d_cbuf* buf, int64_t* n);
+int as2d_cbuf_get_record(const as2d_cbuf* buf, int64_t i, as2d_cbuf_record* out);
+
+/*
+ * Read cursor and candidate alignment (Section 4.1; Section 4.2 "Candidate
+ * alignment"; Appendix C.3 "Candidate alignment"; Figure 4).
+ *
+ * The cursor moves independently of publication and never changes the
+ * buffer.  A plain struct owned by the caller (one per request):
+ *   cursor: position of the next candidate to propose;
+ *   floor:  lowest position still eligible for realignment (positions below
+ *           it were accepted or retired);
+ *   radius: bound of the local search (0..64; 8 = one publication batch).
+ *
+ * as2d_cursor_propose: the ready candidates at the cursor, at most k_max of
+ * the first `snapshot` tokens (k = 0 when none is ready: a target-only
+ * step).
+ *
+ * as2d_cursor_update, after a verification call that proposed k
+ * candidates from the cursor, accepted `accepted` of them and committed
+ * the target token `token` (its correction, or the bonus token after full
+ * acceptance), with m = cursor + accepted the position that token stands
+ * for.  The target token that follows it is only known after the next
+ * call (the token is that call's root), so the rule is read as:
+ *   1. accepted > 0: floor = m;
+ *   2. if the buffer holds `token` at m (full acceptance whose bonus equals
+ *      the next candidate): cursor = floor = m + 1;
+ *   3. else the nearest match at distance d = 1..radius, forward (m + d,
+ *      below `snapshot`) before backward (m - d, not below floor):
+ *      cursor = floor = match + 1.  A forward match skips draft tokens the
+ *      target left out; a backward match recovers a token the target
+ *      inserted (the candidate it had not reached stays eligible);
+ *   4. else cursor = m + 1 (a substitution), floor unchanged.
+ * Verification decides every committed token, so the output does not
+ * depend on the rule (Appendix C.4, Proposition); the rule decides how
+ * many tokens each call commits.
+ *
+ * as2d_verify_from_buffer: one step of the decoding loop for request req:
+ * snapshot, propose at most min(budget, max_commit - 1, AS2D_MAX_BUDGET)
+ * candidates, as2d_verify, then as2d_cursor_update against a fresh
+ * snapshot.  *k_used (optional) receives the number of candidates
+ * verified.  Errors as for as2d_verify; on error the cursor is unchanged.
+ */
+typedef struct {
+  int64_t cursor, floor;
+  int32_t radius, pad;
+} as2d_read_cursor;
+
+int as2d_cursor_init(as2d_read_cursor* cur, int32_t radius);
+int as2d_cursor_propose(const as2d_cbuf* buf, const as2d_read_cursor* cur, int64_t snapshot, int32_t k_max,
+                        int32_t* cands, int32_t* k);
+int as2d_cursor_update(const as2d_cbuf* buf, as2d_read_cursor* cur, int64_t snapshot, int32_t k, int32_t accepted,
+                       int32_t token);
+int as2d_verify_from_buffer(as2d_ctx* ctx, int32_t req, const as2d_cbuf* buf, as2d_read_cursor* cur, int32_t budget,
+                            int32_t max_commit, as2d_verify_out* out, int32_t* k_used);
+
 /* Algorithmic HBM bytes of one forward pass of `rows` rows whose
  * requests hold `kv_keys` attended positions in total per layer
  * (weights streamed once, embedding rows, KV read and append). */

@@ -7,3 +7,4 @@ here, and the oracle imports nothing from the product path: the two share
 only the seeded input generators in workload/.
 """
 from .model import OracleModel, greedy, rms_norm, rope, silu, attention, verify_block
+from .align import CandidateBuffer, ReadCursor, decode_with_buffer

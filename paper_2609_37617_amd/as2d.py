@@ -23,7 +23,10 @@ EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_o
            "as2d_rollback", "as2d_get_state", "as2d_read_kv", "as2d_release_request",
            "as2d_set_exec_mode", "as2d_get_exec_info", "as2d_set_step_trace", "as2d_step_trace_read",
            "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_time_gemm",
-           "as2d_stream_bandwidth", "as2d_step_bytes", "as2d_free", "as2d_last_error"]
+           "as2d_stream_bandwidth", "as2d_step_bytes", "as2d_free", "as2d_last_error",
+           "as2d_cbuf_create", "as2d_cbuf_free", "as2d_cbuf_publish", "as2d_cbuf_snapshot",
+           "as2d_cbuf_read", "as2d_cbuf_n_records", "as2d_cbuf_get_record", "as2d_cursor_init",
+           "as2d_cursor_propose", "as2d_cursor_update", "as2d_verify_from_buffer"]
 
 
 class Config(ctypes.Structure):
@@ -43,6 +46,17 @@ class VerifyOut(ctypes.Structure):
     def as_dict(self):
         return dict(accepted_len=self.accepted_len, correction_token=self.correction_token,
                     kv_len=self.kv_len, committed=self.committed)
+
+
+class CbufRecord(ctypes.Structure):
+    _fields_ = [("first", ctypes.c_int64), ("count", ctypes.c_int32), ("source_id", ctypes.c_int32),
+                ("producer_id", ctypes.c_int32), ("pad", ctypes.c_int32), ("offset", ctypes.c_int64),
+                ("publish_ns", ctypes.c_int64), ("confidence", ctypes.c_float), ("pad2", ctypes.c_int32)]
+
+
+class ReadCursorC(ctypes.Structure):
+    _fields_ = [("cursor", ctypes.c_int64), ("floor", ctypes.c_int64), ("radius", ctypes.c_int32),
+                ("pad", ctypes.c_int32)]
 
 
 class As2dError(RuntimeError):
@@ -89,6 +103,19 @@ def load_library(path: str = LIB_PATH):
     lib.as2d_stream_bandwidth.argtypes = [_P, ctypes.c_int64, _I, ctypes.POINTER(ctypes.c_double)]
     lib.as2d_step_bytes.argtypes = [_P, _I, ctypes.c_int64]
     lib.as2d_step_bytes.restype = ctypes.c_int64
+    _L = ctypes.c_int64
+    lib.as2d_cbuf_create.argtypes = [_L, ctypes.POINTER(_P)]
+    lib.as2d_cbuf_free.argtypes = [_P]
+    lib.as2d_cbuf_publish.argtypes = [_P, _P, _I, _I, _I, _L, _L, ctypes.c_float, ctypes.POINTER(_L)]
+    lib.as2d_cbuf_snapshot.argtypes = [_P, ctypes.POINTER(_L)]
+    lib.as2d_cbuf_read.argtypes = [_P, _L, _I, _P]
+    lib.as2d_cbuf_n_records.argtypes = [_P, ctypes.POINTER(_L)]
+    lib.as2d_cbuf_get_record.argtypes = [_P, _L, ctypes.POINTER(CbufRecord)]
+    lib.as2d_cursor_init.argtypes = [ctypes.POINTER(ReadCursorC), _I]
+    lib.as2d_cursor_propose.argtypes = [_P, ctypes.POINTER(ReadCursorC), _L, _I, _P, ctypes.POINTER(_I)]
+    lib.as2d_cursor_update.argtypes = [_P, ctypes.POINTER(ReadCursorC), _L, _I, _I, _I]
+    lib.as2d_verify_from_buffer.argtypes = [_P, _I, _P, ctypes.POINTER(ReadCursorC), _I, _I,
+                                            ctypes.POINTER(VerifyOut), ctypes.POINTER(_I)]
     lib.as2d_free.argtypes = [_P]
     lib.as2d_free.restype = None
     lib.as2d_last_error.argtypes = [_P]
@@ -263,3 +290,93 @@ class Model:
 
     def step_bytes(self, rows: int, kv_keys: int) -> int:
         return int(self.lib.as2d_step_bytes(self.ctx, rows, kv_keys))
+
+
+def _rc(rc, what):
+    if rc != OK:
+        raise As2dError(rc, what)
+
+
+class CandidateBuffer:
+    """The library's candidate buffer (one producer, any readers)."""
+
+    def __init__(self, capacity: int):
+        self.lib = load_library()
+        self.h = _P()
+        _rc(self.lib.as2d_cbuf_create(capacity, ctypes.byref(self.h)), "as2d_cbuf_create")
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.as2d_cbuf_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def publish(self, tokens, source_id=0, producer_id=0, offset=-1, publish_ns=0, confidence=float("nan")) -> int:
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        n = ctypes.c_int64()
+        _rc(self.lib.as2d_cbuf_publish(self.h, _ptr(t) if t.size else None, len(t), source_id, producer_id, offset,
+                                       publish_ns, confidence, ctypes.byref(n)), "as2d_cbuf_publish")
+        return n.value
+
+    def snapshot(self) -> int:
+        n = ctypes.c_int64()
+        _rc(self.lib.as2d_cbuf_snapshot(self.h, ctypes.byref(n)), "as2d_cbuf_snapshot")
+        return n.value
+
+    def read(self, start: int, n: int) -> List[int]:
+        out = np.empty(max(n, 1), dtype=np.int32)
+        _rc(self.lib.as2d_cbuf_read(self.h, start, n, _ptr(out)), "as2d_cbuf_read")
+        return [int(v) for v in out[:n]]
+
+    def records(self) -> List[dict]:
+        n = ctypes.c_int64()
+        _rc(self.lib.as2d_cbuf_n_records(self.h, ctypes.byref(n)), "as2d_cbuf_n_records")
+        out = []
+        for i in range(n.value):
+            r = CbufRecord()
+            _rc(self.lib.as2d_cbuf_get_record(self.h, i, ctypes.byref(r)), "as2d_cbuf_get_record")
+            out.append(dict(first=r.first, count=r.count, source_id=r.source_id, producer_id=r.producer_id,
+                            offset=r.offset, publish_ns=r.publish_ns, confidence=r.confidence))
+        return out
+
+
+class ReadCursor:
+    """A read cursor over a CandidateBuffer (the library's alignment rule)."""
+
+    def __init__(self, radius: int = 8):
+        self.lib = load_library()
+        self.c = ReadCursorC()
+        _rc(self.lib.as2d_cursor_init(ctypes.byref(self.c), radius), "as2d_cursor_init")
+
+    @property
+    def cursor(self) -> int:
+        return self.c.cursor
+
+    @property
+    def floor(self) -> int:
+        return self.c.floor
+
+    def propose(self, buf: CandidateBuffer, snapshot: int, k_max: int) -> List[int]:
+        out = np.empty(max(k_max, 1), dtype=np.int32)
+        k = _I()
+        _rc(self.lib.as2d_cursor_propose(buf.h, ctypes.byref(self.c), snapshot, k_max, _ptr(out), ctypes.byref(k)),
+            "as2d_cursor_propose")
+        return [int(v) for v in out[:k.value]]
+
+    def update(self, buf: CandidateBuffer, snapshot: int, k: int, accepted: int, token: int):
+        _rc(self.lib.as2d_cursor_update(buf.h, ctypes.byref(self.c), snapshot, k, accepted, token),
+            "as2d_cursor_update")
+
+    def verify_from_buffer(self, model: "Model", req: int, buf: CandidateBuffer, budget: int, max_commit: int):
+        """One decoding step of `model`'s request `req` from the buffer;
+        returns (verify result dict, candidates verified)."""
+        out = VerifyOut()
+        k = _I()
+        model._check(self.lib.as2d_verify_from_buffer(model.ctx, req, buf.h, ctypes.byref(self.c), budget,
+                                                      max_commit, ctypes.byref(out), ctypes.byref(k)))
+        return out.as_dict(), k.value

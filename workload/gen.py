@@ -187,3 +187,28 @@ class CandidateSource:
     def block(self, n_committed: int, k: int) -> List[int]:
         """Candidates after the root y_n: positions n+1 .. n+k."""
         return [self.candidate(j) for j in range(n_committed + 1, n_committed + 1 + k)]
+
+
+def edited_stream(reference: Sequence[int], vocab: int, p_sub: float, p_ins: float, p_del: float,
+                  seed: int = 0, req: int = 0) -> List[int]:
+    """A synthetic draft of a reference token stream (the producer's text is
+    the target's text with local edits): walking the reference, each token
+    is dropped with probability p_del, else replaced by a uniform random
+    token with probability p_sub, else kept; after it, a uniform random
+    token is inserted with probability p_ins.  Draws are a fixed function
+    of (seed, req, position)."""
+    n = len(reference)
+    u = uniform_f64(stream_key(seed, "edit-u", req), 2 * n)
+    tok = uniform_int(stream_key(seed, "edit-tok", req), vocab, 2 * n)
+    out = []
+    for i, t in enumerate(reference):
+        r = u[2 * i]
+        if r < p_del:
+            pass
+        elif r < p_del + p_sub:
+            out.append(int(tok[2 * i]))
+        else:
+            out.append(int(t))
+        if u[2 * i + 1] < p_ins:
+            out.append(int(tok[2 * i + 1]))
+    return out
