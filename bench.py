@@ -324,6 +324,77 @@ def main():
             width[str(kk)] = round((time.perf_counter() - t1) * 1e3 / n_w, 4)
         log("[bench] ms per step by k: " + ", ".join(f"k={kk} {v}" for kk, v in width.items()))
 
+    # verification width profile (the paper's protocol: known-reference
+    # continuations at prefix offsets 0, 64 and 128 after prefill, 5 timed
+    # calls per width and offset) and the offline budget choice from it
+    vprof = budget_sel = None
+    if not args.no_width_profile and len(reqs) == 1:
+        from paper_2609_37617_amd import budget as bsel
+        r0 = reqs[0]
+        y = srcs[0].ref.tolist()                    # [first root, y_1, y_2, ...]
+        L0, root0 = starts[0]
+        Ks = [K for K in range(1, max_k + 2) if 128 + K <= r0.reply_len]
+        samples = {K: [] for K in Ks}
+        model.rollback(0, L0, root0)
+        for off in (0, 64, 128):
+            # commit the reference up to off + max K (rollback only shortens)
+            while model.state(0)[0] < L0 + off + Ks[-1]:
+                n = model.state(0)[2]
+                kk = min(max_k, L0 + off + Ks[-1] - model.state(0)[0])
+                assert model.verify(0, y[n + 1:n + 1 + kk])["accepted_len"] == kk
+            for K in Ks:
+                cands = y[off + 1:off + K]
+                for rep in range(6):
+                    model.rollback(0, L0 + off, y[off])
+                    t1 = time.perf_counter()
+                    r = model.verify(0, cands)
+                    dt = time.perf_counter() - t1
+                    assert r["accepted_len"] == K - 1
+                    if rep:
+                        samples[K].append(dt * 1e3)
+            model.rollback(0, L0 + off, y[off])
+            n = off
+            while model.state(0)[0] < L0 + off + Ks[-1]:      # back to off + max K for the next offset
+                n = model.state(0)[2]
+                kk = min(max_k, L0 + off + Ks[-1] - model.state(0)[0])
+                assert model.verify(0, y[n + 1:n + 1 + kk])["accepted_len"] == kk
+        vbar = {K: float(np.mean(v)) for K, v in samples.items()}
+        sd = {K: float(np.std(v, ddof=1)) for K, v in samples.items()}
+        R = bsel.cost_reduction(vbar)
+        vprof = {"K": Ks, "vbar_ms": [round(vbar[K], 4) for K in Ks], "sd_ms": [round(sd[K], 4) for K in Ks],
+                 "R_percent": [round(R[K], 2) for K in Ks],
+                 "R_err_pp": [round(100 * sd[K] / (K * vbar[1]), 2) for K in Ks], "calls_per_width": 15}
+        log("[bench] R(K) %: " + ", ".join(f"K={K} {R[K]:.1f}" for K in Ks))
+        # budget choice: development drafts replayed and priced with V(K);
+        # then the choice and its neighbours measured on a validation draft
+        target = y[1:]
+        n_tok = r0.reply_len - 1
+        edits = (0.2, 0.05, 0.05)
+        dev = [(gen.edited_stream(target, shape.vocab, *edits, seed=wl.seed + 100 + i), target, n_tok) for i in range(3)]
+        budgets = [b for b in range(0, max_k + 1) if b + 1 in vbar]
+        best, est = bsel.select_budget(vbar, dev, budgets)
+        val = gen.edited_stream(target, shape.vocab, *edits, seed=wl.seed + 200)
+        measured = {}
+        for b in sorted({best, 1, 3, 7, max(budgets)} & set(budgets)):
+            buf = as2d.CandidateBuffer(len(val))
+            for i in range(0, len(val), 8):
+                buf.publish(val[i:i + 8])
+            cur = as2d.ReadCursor(8)
+            model.rollback(0, L0, root0)
+            got = 0
+            t1 = time.perf_counter()
+            while got < r0.reply_len:
+                rr, _ = cur.verify_from_buffer(model, 0, buf, b, r0.reply_len - got)
+                got += rr["accepted_len"] + 1
+            measured[b] = round(got / (time.perf_counter() - t1), 1)
+            buf.close()
+        restart()
+        budget_sel = {"draft_edits": {"sub": edits[0], "ins": edits[1], "del": edits[2]}, "dev_traces": len(dev),
+                      "selected_budget": best,
+                      "estimated_tokens_per_s": {str(b): round(1e3 * v, 1) for b, v in est.items()},
+                      "measured_tokens_per_s_validation": {str(b): v for b, v in measured.items()}}
+        log(f"[bench] budget: selected {best}; measured on validation {measured}")
+
     # decoding from the candidate buffer with an edited draft (substitutions,
     # insertions, deletions): with the bounded realignment, and with the
     # search turned off (radius 0: every mismatch read as a substitution)
@@ -390,6 +461,8 @@ def main():
         "stream_ceiling_gbps": round(stream_gbps, 1),
         "ms_per_step_by_k": width,
         "buffer_decoding": aligned,
+        "verification_profile": vprof,
+        "budget_selection": budget_sel,
         "kernels": {k: round(v["avg_us"], 2) for k, v in kernel_ms.items()},
     }
     print(json.dumps(out), flush=True)
