@@ -53,6 +53,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--no-align", action="store_true", help="skip the candidate-buffer decoding measurement")
+    ap.add_argument("--no-decoupled", action="store_true", help="skip the concurrent-drafter measurement")
     ap.add_argument("--no-width-profile", action="store_true",
                     help="skip the per-k step times (single-request workloads with a k sweep)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -395,6 +396,86 @@ def main():
                       "measured_tokens_per_s_validation": {str(b): v for b, v in measured.items()}}
         log(f"[bench] budget: selected {best}; measured on validation {measured}")
 
+    # target-decoupled decoding with a drafter on the same GPU (3B- and 0.5B-shaped):
+    # serial comparator and concurrent run, with the stage accounting
+    decoupled = None
+    if not args.no_decoupled and len(reqs) == 1 and wl.shape.name == wc.QWEN7B.name and args.layers is None:
+        from paper_2609_37617_amd import overlap as ovl
+        r0 = reqs[0]
+        y = srcs[0].ref.tolist()
+        n_tok = r0.reply_len - 1
+        draft = gen.edited_stream(y[1:], shape.vocab, 0.2, 0.05, 0.05, seed=wl.seed + 300)
+        b = budget_sel["selected_budget"] if budget_sel else r0.k
+        decoupled = {"draft_edits": {"sub": 0.2, "ins": 0.05, "del": 0.05}, "budget": b, "tokens": n_tok}
+        for dshape in (wc.QWEN3B, wc.QWEN05B):
+            t_load = time.time()
+            d_dev = gen.make_weights(dshape, wl.seed + 1, fmt="device")
+            d_max_kv = (r0.n_audio + r0.n_instr + 2 * r0.reply_len + 63) // 64 * 64
+            drafter = as2d.Model(dshape, d_dev, max_requests=1, max_kv_len=d_max_kv, max_k=1)
+            del d_dev
+            d_first, d_L = drafter.prefill(0, gen.audio_embeddings(dshape, r0.n_audio, wl.seed + 1, 0, fmt="device"),
+                                           gen.instruction_tokens(dshape, r0.n_instr, wl.seed + 1, 0))
+            log(f"[bench] drafter {dshape.name} loaded and prefilled in {time.time() - t_load:.1f}s")
+            def warm():
+                # capture every graph the runs launch, one thread at a time
+                for kk in range(0, b + 1):
+                    restart()
+                    model.verify(0, y[1:1 + kk])
+                restart()
+                drafter.rollback(0, d_L, d_first)
+                drafter.decode_one(0)
+                drafter.rollback(0, d_L, d_first)
+
+            def one(conc):
+                restart()
+                drafter.rollback(0, d_L, d_first)
+                r = as2d.run_decoupled(model, 0, drafter, 0, draft, b, n_tok, conc)
+                assert r["committed"] == y[1:1 + n_tok]
+                acc = ovl.accounting(r["intervals"], r["total_ns"])
+                steps = [iv for iv in r["intervals"] if iv[2] == 0]
+                return acc, {"T_ms": round(acc["T"] / 1e6, 3), "D_ms": round(acc["D"] / 1e6, 3),
+                             "V_ms": round(acc["V"] / 1e6, 3), "O_ms": round(acc["O"] / 1e6, 3),
+                             "H_ms": round(acc["H"] / 1e6, 3), "rounds": acc["R"],
+                             "tokens_per_s": round(n_tok / (acc["T"] / 1e9), 1),
+                             "mean_committed_per_round": round(acc["N"] / acc["R"], 3),
+                             "verifier_ms_per_round": round(acc["V"] / acc["R"] / 1e6, 4),
+                             "producer_steps": len(steps),
+                             "producer_ms_per_step": round(sum(e - s for s, e, _, _ in steps) / max(1, len(steps)) / 1e6, 4)}
+
+            res, accs = {}, {}
+            warm()
+            accs["serial"], res["serial"] = one(False)
+            accs["concurrent"], res["concurrent"] = one(True)
+            # CU budgets: the drafter's GEMMs on `dc` workgroups, the target's on the rest
+            res["concurrent_cu_budget"] = {}
+            best = None
+            for dc in ((32, 64, 96) if dshape.name == wc.QWEN05B.name else (64,)):
+                model.set_cu_budget(256 - dc)
+                drafter.set_cu_budget(dc)
+                warm()
+                acc, row = one(True)
+                row["speedup_vs_serial"] = round(accs["serial"]["T"] / acc["T"], 4)
+                res["concurrent_cu_budget"][str(dc)] = row
+                if best is None or acc["T"] < accs[best]["T"]:
+                    best = f"budget{dc}"
+                accs[f"budget{dc}"] = acc
+                model.set_cu_budget(0)
+                drafter.set_cu_budget(0)
+            res["best_concurrent"] = best if accs[best]["T"] < accs["concurrent"]["T"] else "concurrent"
+            c = ovl.compare(accs["serial"], accs[res["best_concurrent"]])
+            res["compare"] = {"speedup": round(c["speedup"], 4), "O_a_ms": round(c["O_a"] / 1e6, 3),
+                              "added_ms": round(c["added"] / 1e6, 3), "dD_ms": round(c["dD"] / 1e6, 3),
+                              "dV_ms": round(c["dV"] / 1e6, 3), "dH_ms": round(c["dH"] / 1e6, 3),
+                              "break_even_holds": bool(c["break_even_holds"]),
+                              "bottleneck_bound": round(c["bound"], 4)}
+            decoupled[dshape.name] = res
+            drafter.close()
+            restart()
+            log(f"[bench] decoupled with {dshape.name}: serial {res['serial']['T_ms']} ms, concurrent "
+                f"{res['concurrent']['T_ms']} ms, with CU budgets " +
+                ", ".join(f"{k}: {v['T_ms']} ms ({v['speedup_vs_serial']}x)" for k, v in res["concurrent_cu_budget"].items()) +
+                f" | best {res['best_concurrent']}: {res['compare']}")
+
     # decoding from the candidate buffer with an edited draft (substitutions,
     # insertions, deletions): with the bounded realignment, and with the
     # search turned off (radius 0: every mismatch read as a substitution)
@@ -463,6 +544,7 @@ def main():
         "buffer_decoding": aligned,
         "verification_profile": vprof,
         "budget_selection": budget_sel,
+        "decoupled": decoupled,
         "kernels": {k: round(v["avg_us"], 2) for k, v in kernel_ms.items()},
     }
     print(json.dumps(out), flush=True)

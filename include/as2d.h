@@ -182,6 +182,21 @@ int as2d_get_state(as2d_ctx* ctx, int32_t req, int32_t* kv_len, int32_t* root, i
 int as2d_read_kv(as2d_ctx* ctx, int32_t req, int32_t layer, void* host_k, void* host_v, int32_t n_tok);
 
 /* Mark a slot free (its state is discarded). */
+/* Rebind the context to another stream (hip_stream = NULL: a stream of its
+ * own).  Waits for the old stream, drops cached graphs, and sizes the
+ * balanced GEMM grids (one workgroup per usable CU) and the persistent
+ * kernel's grid to the CUs the new stream may use: a stream made with
+ * hipExtStreamCreateWithCUMask confines the context to part of the device
+ * (e.g. a drafter beside the target).  Split counts, and so every result,
+ * stay as they were.  as2d_load_weights sizes them the same way for the
+ * stream it is given. */
+int as2d_set_stream(as2d_ctx* ctx, void* hip_stream);
+/* Size the balanced GEMM grids for `cus` compute units (1 .. the stream's;
+ * 0 restores all of them): each such GEMM then runs cus workgroups of one
+ * CU each, leaving the other CUs to work on other streams (a drafter beside
+ * the target).  Split counts, and so every result, are unchanged.  Drops
+ * cached graphs. */
+int as2d_set_cu_budget(as2d_ctx* ctx, int32_t cus);
 int as2d_release_request(as2d_ctx* ctx, int32_t req);
 
 /*
@@ -307,6 +322,46 @@ int as2d_cursor_update(const as2d_cbuf* buf, as2d_read_cursor* cur, int64_t snap
                        int32_t token);
 int as2d_verify_from_buffer(as2d_ctx* ctx, int32_t req, const as2d_cbuf* buf, as2d_read_cursor* cur, int32_t budget,
                             int32_t max_commit, as2d_verify_out* out, int32_t* k_used);
+
+/*
+ * Target-decoupled decoding with a producer on the same GPU (Section 4.1
+ * "Target-decoupled drafting"; the accounting of Appendix D.2, "Overlap,
+ * added work, and performance limits").
+ *
+ * The producer is a drafter model in its own context `drafter` (its own
+ * stream), request dreq, prefilled by the caller with capacity for n_draft
+ * more positions.  Producer step i is one greedy decode step of the drafter
+ * on its own output (as2d_decode_one); the token it publishes for that step
+ * is draft[i] (a caller-supplied draft of known quality driven by real
+ * drafter compute), in batches of 8 into `buf` (provenance: source 0,
+ * producer 1, offset, time since the start of the run).  The verifier
+ * (the calling thread) decodes target request treq from the buffer with
+ * as2d_verify_from_buffer and `cur` until n_commit tokens are committed;
+ * they go to committed[n_commit].
+ *   concurrent = 1: the producer runs in its own thread, never waiting for
+ *     the verifier, which never waits for it (a target-only step when no
+ *     candidate is ready); the run ends when both have stopped.
+ *   concurrent = 0: the serial comparator: before each verification the
+ *     producer generates whole batches until `budget` candidates past the
+ *     cursor are published or the draft is exhausted.
+ * Every producer step (kind 0, tokens 1) and verifier call (kind 1, tokens
+ * committed) is logged into log[log_cap] as a closed interval in ns from
+ * the start of the run (host steady clock, around the synchronous call);
+ * *n_log entries, *total_ns the whole run.  `buf` and `cur` must be fresh
+ * (nothing published, cursor 0).  A producer error stops the producer only
+ * (*producer_rc); the verifier then continues alone.  Errors: as for
+ * as2d_verify; AS2D_ECAPACITY when the log is too small.
+ */
+typedef struct {
+  int64_t start_ns, end_ns;
+  int32_t kind;    /* 0: producer step, 1: verifier call */
+  int32_t tokens;  /* tokens generated (producer) or committed (verifier) */
+} as2d_interval;
+
+int as2d_run_decoupled(as2d_ctx* target, int32_t treq, as2d_ctx* drafter, int32_t dreq, const int32_t* draft,
+                       int32_t n_draft, int32_t budget, int32_t n_commit, int32_t concurrent, as2d_cbuf* buf,
+                       as2d_read_cursor* cur, int32_t* committed, as2d_interval* log, int32_t log_cap,
+                       int32_t* n_log, int64_t* total_ns, int32_t* producer_rc);
 
 /* Algorithmic HBM bytes of one forward pass of `rows` rows whose
  * requests hold `kv_keys` attended positions in total per layer

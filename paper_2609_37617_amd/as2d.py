@@ -26,7 +26,8 @@ EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_o
            "as2d_stream_bandwidth", "as2d_step_bytes", "as2d_free", "as2d_last_error",
            "as2d_cbuf_create", "as2d_cbuf_free", "as2d_cbuf_publish", "as2d_cbuf_snapshot",
            "as2d_cbuf_read", "as2d_cbuf_n_records", "as2d_cbuf_get_record", "as2d_cursor_init",
-           "as2d_cursor_propose", "as2d_cursor_update", "as2d_verify_from_buffer"]
+           "as2d_cursor_propose", "as2d_cursor_update", "as2d_verify_from_buffer", "as2d_run_decoupled",
+           "as2d_set_stream", "as2d_set_cu_budget"]
 
 
 class Config(ctypes.Structure):
@@ -57,6 +58,11 @@ class CbufRecord(ctypes.Structure):
 class ReadCursorC(ctypes.Structure):
     _fields_ = [("cursor", ctypes.c_int64), ("floor", ctypes.c_int64), ("radius", ctypes.c_int32),
                 ("pad", ctypes.c_int32)]
+
+
+class Interval(ctypes.Structure):
+    _fields_ = [("start_ns", ctypes.c_int64), ("end_ns", ctypes.c_int64), ("kind", ctypes.c_int32),
+                ("tokens", ctypes.c_int32)]
 
 
 class As2dError(RuntimeError):
@@ -116,6 +122,10 @@ def load_library(path: str = LIB_PATH):
     lib.as2d_cursor_update.argtypes = [_P, ctypes.POINTER(ReadCursorC), _L, _I, _I, _I]
     lib.as2d_verify_from_buffer.argtypes = [_P, _I, _P, ctypes.POINTER(ReadCursorC), _I, _I,
                                             ctypes.POINTER(VerifyOut), ctypes.POINTER(_I)]
+    lib.as2d_run_decoupled.argtypes = [_P, _I, _P, _I, _P, _I, _I, _I, _I, _P, ctypes.POINTER(ReadCursorC), _P,
+                                       _P, _I, ctypes.POINTER(_I), ctypes.POINTER(_L), ctypes.POINTER(_I)]
+    lib.as2d_set_stream.argtypes = [_P, _P]
+    lib.as2d_set_cu_budget.argtypes = [_P, _I]
     lib.as2d_free.argtypes = [_P]
     lib.as2d_free.restype = None
     lib.as2d_last_error.argtypes = [_P]
@@ -288,6 +298,15 @@ class Model:
         self._check(self.lib.as2d_stream_bandwidth(self.ctx, nbytes, reps, ctypes.byref(gbps)))
         return gbps.value
 
+    def set_stream(self, stream: Optional[int]):
+        """Rebind to a HIP stream handle (None: a stream of its own)."""
+        self._check(self.lib.as2d_set_stream(self.ctx, stream))
+
+    def set_cu_budget(self, cus: int):
+        """Size the balanced GEMM grids for `cus` compute units (0: all the
+        stream's)."""
+        self._check(self.lib.as2d_set_cu_budget(self.ctx, cus))
+
     def step_bytes(self, rows: int, kv_keys: int) -> int:
         return int(self.lib.as2d_step_bytes(self.ctx, rows, kv_keys))
 
@@ -380,3 +399,28 @@ class ReadCursor:
         model._check(self.lib.as2d_verify_from_buffer(model.ctx, req, buf.h, ctypes.byref(self.c), budget,
                                                       max_commit, ctypes.byref(out), ctypes.byref(k)))
         return out.as_dict(), k.value
+
+
+def run_decoupled(target: Model, treq: int, drafter: Model, dreq: int, draft: Sequence[int], budget: int,
+                  n_commit: int, concurrent: bool, radius: int = 8, log_cap: int = 1 << 16) -> dict:
+    """as2d_run_decoupled on a fresh buffer and cursor.  Returns the
+    committed tokens, the stage intervals [(start_ns, end_ns, kind,
+    tokens)] (kind 0 producer step, 1 verifier call), the run's total ns
+    and the producer's status."""
+    lib = load_library()
+    d = np.ascontiguousarray(draft, dtype=np.int32)
+    buf = CandidateBuffer(max(len(d), 1))
+    cur = ReadCursor(radius)
+    out = np.empty(n_commit, dtype=np.int32)
+    log = (Interval * log_cap)()
+    n_log, total, prc = _I(), ctypes.c_int64(), _I()
+    rc = lib.as2d_run_decoupled(target.ctx, treq, drafter.ctx, dreq, _ptr(d) if d.size else None, len(d), budget,
+                                n_commit, int(concurrent), buf.h, ctypes.byref(cur.c), _ptr(out), log, log_cap,
+                                ctypes.byref(n_log), ctypes.byref(total), ctypes.byref(prc))
+    target._check(rc)
+    iv = [(log[i].start_ns, log[i].end_ns, log[i].kind, log[i].tokens) for i in range(n_log.value)]
+    res = dict(committed=[int(t) for t in out], intervals=iv, total_ns=total.value, producer_rc=prc.value,
+               published=buf.snapshot(), records=len(buf.records()))
+    buf.close()
+    return res
+

@@ -93,6 +93,7 @@ struct as2d_ctx {
   // persistent step kernel: per-layer activation buffers and counters
   bool pers_ok = false;
   int pers_grid[3] = {0, 0, 0};  // by M-tile count 1, 2
+  int pers_occ[3] = {0, 0, 0};   // resident step-kernel workgroups per CU, by M-tile count
   float *px = nullptr, *psumsq = nullptr, *pq = nullptr;
   void *pxg = nullptr, *pattn = nullptr, *ph = nullptr;
   int *psplit = nullptr, *pphase = nullptr, *perr = nullptr;
@@ -168,6 +169,27 @@ GemmPlan make_plan(int N, int K, int KE, int target, int ks_override = 0) {
   return p;
 }
 
+// CUs a stream may use: the population of its CU mask, or dev_cus when
+// the mask cannot be read.
+int stream_cus(hipStream_t s, int dev_cus) {
+  uint32_t mask[32] = {0};
+  const uint32_t words = (uint32_t)((dev_cus + 31) / 32);
+  if (words < 1 || words > 32 || hipExtStreamGetCUMask(s, words, mask) != hipSuccess) return dev_cus;
+  int n = 0;
+  for (uint32_t i = 0; i < words; ++i) n += __builtin_popcount(mask[i]);
+  return n > 0 && n <= dev_cus ? n : dev_cus;
+}
+
+// Workgroups of a balanced plan for `cus` compute units: one per CU, at
+// most one per unit, and at most kMaxUnits units each.  The split count is
+// not touched, so the sums do not change.
+void set_grid(GemmPlan& p, int cus) {
+  if (!p.G) return;
+  const int U = p.pairs * p.KS;
+  p.G = std::min(cus, U);
+  if ((U + p.G - 1) / p.G > kMaxUnits) p.G = (U + kMaxUnits - 1) / kMaxUnits;
+}
+
 // Balanced plan for the direct path (gemm_range kernel): the pairs x KS
 // (pair, split) units are shared equally by G = min(compute units, units)
 // workgroups.  KS is chosen for the 256 compute units of the MI355X
@@ -203,9 +225,8 @@ GemmPlan balance_plan(GemmPlan p, int cus, int split_cost, int per_split, int ks
   p.ns = kWaves;
   p.ktps = (p.KT + best_ks - 1) / best_ks;
   p.KS = best_ks;
-  const int U = p.pairs * p.KS;
-  p.G = std::min(cus, U);
-  if ((U + p.G - 1) / p.G > kMaxUnits) p.G = (U + kMaxUnits - 1) / kMaxUnits;
+  p.G = 1;
+  set_grid(p, cus);
   return p;
 }
 
@@ -725,6 +746,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
       as2d_free(c);
       return AS2D_EHIP;
     }
+    cus = stream_cus(c->stream, cus);
     const int sc = env_int("AS2D_SPLIT_COST", 16), ps = env_int("AS2D_SPLIT_COST_PER", 5);
     if (bal & 1) c->p_qkv = balance_plan(c->p_qkv, cus, sc, ps, ks_qkv);
     if (bal & 2) c->p_o = balance_plan(c->p_o, cus, sc, ps, ks_o);
@@ -840,6 +862,9 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     const int L = g.n_layers;
     const long long R = kStepRows;
     if (occ1 > 0 && occ2 > 0) {
+      cus = stream_cus(c->stream, cus);
+      c->pers_occ[1] = occ1;
+      c->pers_occ[2] = occ2;
       c->pers_grid[1] = occ1 * cus;
       c->pers_grid[2] = occ2 * cus;
       CK(dalloc(c, &c->px, (size_t)(2 * L + 1) * R * H * 4));
@@ -1114,6 +1139,45 @@ int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* ho
     HIP_TRY(c, hipMemcpy((float*)host_k + h * n_tok * row, c->kc + src, n_tok * row * 4, hipMemcpyDeviceToHost));
     HIP_TRY(c, hipMemcpy((float*)host_v + h * n_tok * row, c->vc + src, n_tok * row * 4, hipMemcpyDeviceToHost));
   }
+  return AS2D_OK;
+}
+
+int as2d_set_stream(as2d_ctx* c, void* hip_stream) {
+  if (!c) return AS2D_EINVAL;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
+  c->graphs.clear();
+  if (c->own_stream) {
+    hipStreamDestroy(c->stream);
+    c->own_stream = false;
+    c->stream = nullptr;
+  }
+  if (hip_stream) {
+    c->stream = (hipStream_t)hip_stream;
+  } else {
+    HIP_TRY(c, hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking));
+    c->own_stream = true;
+  }
+  int dev = 0, cus = 0;
+  HIP_TRY(c, hipGetDevice(&dev));
+  HIP_TRY(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  cus = stream_cus(c->stream, cus);
+  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, cus);
+  for (int mt = 1; mt <= 2; ++mt) c->pers_grid[mt] = c->pers_occ[mt] * cus;
+  return AS2D_OK;
+}
+
+int as2d_set_cu_budget(as2d_ctx* c, int32_t cus) {
+  if (!c || cus < 0) return AS2D_EINVAL;
+  int dev = 0, dev_cus = 0;
+  HIP_TRY(c, hipGetDevice(&dev));
+  HIP_TRY(c, hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev));
+  const int avail = stream_cus(c->stream, dev_cus);
+  if (cus > avail) return fail(c, AS2D_EINVAL, "cu budget %d > %d usable CUs", cus, avail);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);   // grids are kernel launch parameters
+  c->graphs.clear();
+  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, cus ? cus : avail);
   return AS2D_OK;
 }
 

@@ -2,5 +2,5 @@
 
 This package holds no arithmetic of the decoding method.
 """
-from .configs import BF16, F32, ModelShape, Request, Workload, workload, TINY, TINY_BF16, QWEN3B, QWEN7B
+from .configs import BF16, F32, ModelShape, Request, Workload, workload, TINY, TINY_BF16, QWEN3B, QWEN7B, QWEN05B
 from . import gen

@@ -61,6 +61,9 @@ TINY = ModelShape("tiny", 2, 256, 4, 2, 64, 1024, 4096, 1e4, dtype=F32, qkv_bias
 TINY_BF16 = replace(TINY, name="tiny-bf16", dtype=BF16, qkv_bias=True)
 QWEN3B = ModelShape("qwen2.5-3b-shape", 36, 2048, 16, 2, 128, 11008, 151936, 1e6)
 QWEN7B = ModelShape("qwen2-7b-shape", 28, 3584, 28, 4, 128, 18944, 152064, 1e6)
+# Drafter-sized decoder (Qwen2.5-0.5B dimensions, untied head): the producer
+# of the concurrent-drafting measurement, next to the 3B shape.
+QWEN05B = ModelShape("qwen2.5-0.5b-shape", 24, 896, 14, 2, 64, 4864, 151936, 1e6)
 
 
 @dataclass
