@@ -198,12 +198,14 @@ def main():
         instr = gen.instruction_tokens(shape, r.n_instr, wl.seed, i)
         t0 = time.time()
         first, L = model.prefill(i, audio, instr)
+        prefill_s = time.time() - t0
         y = [first] + [model.decode_one(i)["correction_token"] for _ in range(r.reply_len)]
         model.rollback(i, L, first)
         starts.append((L, first))
         srcs.append(gen.CandidateSource(y, shape.vocab, r.p, seed=wl.seed, req=i))
-        log(f"[bench] request {i}: prefix {L} rows, reference stream {r.reply_len} tokens "
-            f"({time.time() - t0:.1f}s)")
+        log(f"[bench] request {i}: prefix {L} rows prefilled in {prefill_s * 1e3:.1f} ms, reference stream "
+            f"{r.reply_len} tokens ({time.time() - t0:.1f}s)")
+        prefill_info = {"rows": L, "ms": round(prefill_s * 1e3, 2), "rows_per_s": round(L / prefill_s, 1)}
 
     done = [0] * len(reqs)        # committed tokens of the current reply pass
 
@@ -542,6 +544,7 @@ def main():
         "stream_ceiling_gbps": round(stream_gbps, 1),
         "ms_per_step_by_k": width,
         "buffer_decoding": aligned,
+        "prefill_first_request": prefill_info,
         "verification_profile": vprof,
         "budget_selection": budget_sel,
         "decoupled": decoupled,

@@ -178,14 +178,22 @@ static hipError_t launch_range(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Staged path: block b = (pair group, split, row group), the row group
+// fastest; RG row groups of MT row tiles each (RG = 1: all the pass's rows).
 template <bool BF, int MT, int AM, int EPI>
-__global__ __launch_bounds__(256) void gemm_staged_kernel(const GemmArgs p, const int chunk_kt) {
+__global__ __launch_bounds__(256) void gemm_staged_kernel(const GemmArgs p, const int chunk_kt, const int RG) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;
-  const int group = blockIdx.x / p.KS, split = blockIdx.x - group * p.KS;
-  gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, chunk_kt);
+  const int rg = blockIdx.x % RG, t = blockIdx.x / RG;
+  const int group = t / p.KS, split = t - group * p.KS;
+  gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, chunk_kt, rg * MT,
+                                          group * RG + rg);
 }
+
+// Row tiles per row group when a staged GEMM would otherwise leave compute
+// units idle.
+constexpr int kStagedGroupMT = 3;
 
 template <bool BF, int AM, int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
@@ -204,12 +212,22 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
     return hipGetLastError();
   }
   if (pairs % kPairsS) return hipErrorInvalidValue;
-  const int chunk = staged_chunk(BF, a.MT);
-  const dim3 grid((pairs / kPairsS) * a.KS), block(256);
+  const int base = (pairs / kPairsS) * a.KS;
   const int lds = gemm_staged_lds_bytes();
+  // narrow matrices: row groups of kStagedGroupMT tiles (at most 3 groups,
+  // so the counters, one per pair, cover group * RG + rg)
+  if (base < 256 && a.MT > kStagedGroupMT) {
+    const int RG = (a.MT + kStagedGroupMT - 1) / kStagedGroupMT;
+    if (RG > kPairsS) return hipErrorInvalidValue;
+    gemm_staged_kernel<BF, kStagedGroupMT, AM, EPI><<<base * RG, 256, lds, s>>>(
+        a, staged_chunk(BF, kStagedGroupMT), RG);
+    return hipGetLastError();
+  }
+  const int chunk = staged_chunk(BF, a.MT);
+  const dim3 grid(base), block(256);
   switch (a.MT) {
 #define AS2D_MT(mt) \
-  case mt: gemm_staged_kernel<BF, mt, AM, EPI><<<grid, block, lds, s>>>(a, chunk); break;
+  case mt: gemm_staged_kernel<BF, mt, AM, EPI><<<grid, block, lds, s>>>(a, chunk, 1); break;
     AS2D_MT(3) AS2D_MT(4) AS2D_MT(5) AS2D_MT(6) AS2D_MT(7) AS2D_MT(8) AS2D_MT(9)
 #undef AS2D_MT
     default: return hipErrorInvalidValue;

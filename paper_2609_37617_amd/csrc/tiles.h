@@ -784,9 +784,12 @@ __device__ void gemm_range_direct_ra(const GemmArgs& p, int M, unsigned char* sm
 }
 
 // Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
-// tile pairs (one per wave) of one split; the activation fragments of
-// `chunk_kt` k-steps at a time are staged in LDS and shared by the waves,
-// each wave keeps its slices apart in registers (running sum S).
+// tile pairs (one per wave) of one split, for row tiles [mt0, mt0 + MT);
+// the activation fragments of `chunk_kt` k-steps at a time are staged in
+// LDS and shared by the waves, each wave keeps its slices apart in
+// registers (running sum S).  Row groups (mt0 > 0) let narrow matrices use
+// more workgroups; `cnt` is the split counter of this (pairs, rows) tile
+// (default: the pair group).
 //   smem: dynamic LDS of gemm_staged_lds_bytes(); chunk_kt from
 //   staged_chunk().
 
@@ -797,7 +800,7 @@ __host__ __device__ inline int staged_chunk(bool bf16, int MT) { return kLdsBudg
 
 template <bool BF, int MT, int AM, int EPI, bool COH>
 __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split, unsigned char* smem,
-                                 float* s_scale, int* s_flag, int chunk_kt) {
+                                 float* s_scale, int* s_flag, int chunk_kt, int mt0 = 0, int cnt = -1) {
   constexpr int kRegions = BF ? 2 : 1;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int pair = group * kPairsS + wave;
@@ -827,7 +830,7 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
         const int l = u & 63, blk = u >> 6;
         const int rg = blk / (MT * n), r2 = blk - rg * (MT * n);
         const int mt = r2 / n, r = r2 - mt * n;
-        la[rg * region + (mt * chunk_kt + r) * 64 + l] = ag[rg * lo + ((size_t)mt * p.KT + c0 + r) * 64 + l];
+        la[rg * region + (mt * chunk_kt + r) * 64 + l] = ag[rg * lo + ((size_t)(mt0 + mt) * p.KT + c0 + r) * 64 + l];
       }
       uint4 b[kPrefetch][2];
 #pragma unroll
@@ -881,6 +884,8 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
 
   float* F = reinterpret_cast<float*>(smem);
   const int n0 = group * kPairsS * kPairCols, C = kPairsS * kPairCols;
+  const int R0 = mt0 * 16, R1 = min(M, (mt0 + MT) * 16);   // this workgroup's rows
+  if (cnt < 0) cnt = group;
   // lane's value of (row m, column 32 wave + 16 j + lane % 16)
   auto put = [&](int r0, int r1, bool scale) {
 #pragma unroll
@@ -889,7 +894,7 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = mt * 16 + (lane >> 4) * 4 + i;
+          const int row = (mt0 + mt) * 16 + (lane >> 4) * 4 + i;
           const int col = wave * kPairCols + j * 16 + (lane & 15);
           if (row >= r0 && row < r1)
             F[(row - r0) * kFStride + col] = AM == A_NORM && scale ? S[mt][j][i] * s_scale[row] : S[mt][j][i];
@@ -897,8 +902,8 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   };
   if (p.KS > 1) {
     // publish in row blocks through F
-    for (int r0 = 0; r0 < M; r0 += kFRows) {
-      const int r1 = min(M, r0 + kFRows);
+    for (int r0 = R0; r0 < R1; r0 += kFRows) {
+      const int r1 = min(R1, r0 + kFRows);
       lds_sync();
       put(r0, r1, false);
       __syncthreads();
@@ -909,14 +914,14 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
     }
     wait_vmem();
     __syncthreads();
-    if (tid == 0) *s_flag = counter_add(&p.counters[group], 1) == p.KS - 1;
+    if (tid == 0) *s_flag = counter_add(&p.counters[cnt], 1) == p.KS - 1;
     __syncthreads();
     if (!*s_flag) return false;
-    if (tid == 0) st<true>(&p.counters[group], 0);
+    if (tid == 0) st<true>(&p.counters[cnt], 0);
     row_scales<AM>(p, M, s_scale);
     __syncthreads();
-    for (int r0 = 0; r0 < M; r0 += kFRows) {
-      const int r1 = min(M, r0 + kFRows);
+    for (int r0 = R0; r0 < R1; r0 += kFRows) {
+      const int r1 = min(R1, r0 + kFRows);
       fixup_rows<AM>(p, M, n0, C, r0, r1, s_scale, F, kFStride);
       lds_sync();
       epilogue_rows<BF, EPI, COH>(p, F, kFStride, group * kPairsS, kPairsS, r0, r1);
@@ -925,8 +930,8 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   } else {
     row_scales<AM>(p, M, s_scale);
     __syncthreads();  // A tiles no longer read; s_scale written
-    for (int r0 = 0; r0 < M; r0 += kFRows) {
-      const int r1 = min(M, r0 + kFRows);
+    for (int r0 = R0; r0 < R1; r0 += kFRows) {
+      const int r1 = min(R1, r0 + kFRows);
       put(r0, r1, true);
       lds_sync();
       epilogue_rows<BF, EPI, COH>(p, F, kFStride, group * kPairsS, kPairsS, r0, r1);
