@@ -364,6 +364,7 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
       a.out = c->attn;
       a.out_plane = c->attn_plane;
       a.M = M;
+      a.row_groups = (M + kAttnRowGroup - 1) / kAttnRowGroup;   // a function of the graph key
       Timed t(c, K_ATTN);
       HIP_TRY(c, launch_attention(bf, a, n_att, max_chunks, s));
     }
@@ -475,6 +476,7 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     a.pml = c->pml;
     a.n_chunks_cap = c->n_chunks_cap;
     a.out = (char*)c->pattn + l * qs * 4;
+    a.row_groups = 1;
     a.out_plane = c->bf16 ? (long long)qs : 0;
     a.M = M;
 
@@ -821,7 +823,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   CK(dalloc(c, &c->vc, kv_bytes));
 
   // activations and scratch, sized for the largest pass
-  c->max_rows = std::min(kMaxRows, std::max(g.max_requests * (g.max_k + 1), 64));
+  c->max_rows = kMaxRows;   // rows per pass (prefill chunks, fused batches)
   const int MR = kMaxRows;
   c->n_chunks_cap = (g.max_kv_len + kAttnChunk - 1) / kAttnChunk;
   CK(dalloc(c, &c->x, (size_t)MR * H * 4));

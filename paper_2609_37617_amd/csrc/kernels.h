@@ -30,6 +30,7 @@ constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
 constexpr int kDirectMT = 2;            // row tiles of the direct path (up to 32 rows)
 constexpr int kAttnChunk = 32;          // keys per attention split
+constexpr int kAttnRowGroup = 16;       // rows per attention workgroup (row groups)
 constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
 constexpr int kMaxUnits = 24;           // (pair, split) units per workgroup, balanced direct path
 constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
@@ -120,6 +121,8 @@ struct AttnArgs {
   void* out;             // planes [kMaxRows][n_q*d]
   long long out_plane;
   int M;
+  int row_groups;        // attention chunk grid: z = request x row_groups + group of
+                         // kAttnRowGroup rows (at least ceil(rows of any request / kAttnRowGroup))
 };
 
 // Persistent step kernel (step.hip): one verification pass of up to 32 rows.

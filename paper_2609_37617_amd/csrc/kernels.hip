@@ -249,17 +249,21 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // ---------------------------------------------------------------------------
 // Block-causal grouped-query attention, split over the key axis.
 //
-// Workgroup (chunk c, query head h, request r) runs attn_chunk_tile over
-// keys [32 c, 32 c + 32) of the request's float32 cache slot; the merge
+// Workgroup (chunk c, query head h, request r, row group) runs
+// attn_chunk_tile over keys [32 c, 32 c + 32) of the request's float32
+// cache slot, for the group's kAttnRowGroup rows; the merge
 // kernel, one workgroup per (head, row), combines a row's chunks in
 // ascending order (attn_merge_row).
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_chunk_kernel(const AttnArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const ReqDesc rq = p.reqs[blockIdx.z];
-  if ((int)blockIdx.x * kAttnChunk >= rq.L0 + rq.W) return;
-  attn_chunk_tile<D, false>(p, blockIdx.x, blockIdx.y, rq, smem);
+  const int rg = blockIdx.z % p.row_groups;
+  const ReqDesc rq = p.reqs[blockIdx.z / p.row_groups];
+  const int r_lo = rg * kAttnRowGroup, r_hi = min(rq.W, r_lo + kAttnRowGroup);
+  // no row of the group reaches this chunk's first key
+  if (r_lo >= r_hi || (int)blockIdx.x * kAttnChunk > rq.L0 + r_hi - 1) return;
+  attn_chunk_tile<D, false>(p, blockIdx.x, blockIdx.y, rq, smem, r_lo, r_hi);
 }
 
 template <bool BF, int D>
@@ -275,7 +279,8 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, h
   // the chunk dimension a multiple of 8, every head of chunk c runs on the
   // same XCD, so the query heads of a KV group share that chunk's keys and
   // values in one L2 (extra chunks exit at once).
-  const dim3 grid((max_chunks + 7) / 8 * 8, a.n_q, n_reqs);
+  if (a.row_groups < 1) return hipErrorInvalidValue;
+  const dim3 grid((max_chunks + 7) / 8 * 8, a.n_q, n_reqs * a.row_groups);
   attn_chunk_kernel<D><<<grid, 256, attn_lds_bytes<D>(), s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -957,7 +957,8 @@ template <int D> __host__ __device__ constexpr int attn_lds_bytes() {
 }
 
 template <int D, bool COH>
-__device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem) {
+__device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem, int r_lo = 0,
+                                int r_hi = -1) {
   constexpr int C = kAttnChunk;
   constexpr int RS = D + 1;                   // odd LDS row stride (floats)
   constexpr int V4 = C * D / 4 / 256;         // float4 loads per thread per matrix
@@ -1001,21 +1002,23 @@ __device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& 
   const int j = lane & (C - 1), half = lane >> 5;
   float* qw = qs + wave * D;
   float* pw = ps + wave * C;
-  // first row of this wave at or after the chunk start
-  int i = wave;
-  while (i < rq.W && rq.L0 + i < key0) i += 4;
+  // rows [r_lo, r_hi) of the request (all by default); the first row of
+  // this wave at or after the chunk start
+  if (r_hi < 0) r_hi = rq.W;
+  int i = r_lo + wave;
+  while (i < r_hi && rq.L0 + i < key0) i += 4;
   float qn[QL];
-  if (i < rq.W) {
+  if (i < r_hi) {
 #pragma unroll
     for (int t = 0; t < QL; ++t) qn[t] = p.q[(size_t)(rq.row_start + i) * qcols + h * D + t * 64 + lane];
   }
   __syncthreads();
-  for (; i < rq.W; i += 4) {
+  for (; i < r_hi; i += 4) {
     const int pos = rq.L0 + i;
     const int row = rq.row_start + i;
 #pragma unroll
     for (int t = 0; t < QL; ++t) qw[t * 64 + lane] = qn[t];
-    if (i + 4 < rq.W) {
+    if (i + 4 < r_hi) {
 #pragma unroll
       for (int t = 0; t < QL; ++t) qn[t] = p.q[(size_t)(row + 4) * qcols + h * D + t * 64 + lane];
     }
