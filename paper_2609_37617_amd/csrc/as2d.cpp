@@ -42,7 +42,6 @@ enum Kind { K_EMBED, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_LM, K_FINISH, K_STEP, K
 const char* kKindNames[K_COUNT] = {"embed", "gemm_qkv", "attention", "gemm_o", "gemm_gate_up",
                                    "gemm_down", "gemm_lm_head", "finish", "step_persistent"};
 
-constexpr int kStepRows = 32;  // rows of a persistent-kernel pass
 
 }  // namespace
 
@@ -92,8 +91,8 @@ struct as2d_ctx {
 
   // persistent step kernel: per-layer activation buffers and counters
   bool pers_ok = false;
-  int pers_grid[3] = {0, 0, 0};  // by M-tile count 1, 2
-  int pers_occ[3] = {0, 0, 0};   // resident step-kernel workgroups per CU, by M-tile count
+  int pers_grid[3] = {0, 0, 0};  // by M-tile count 1, 2: one workgroup per usable CU
+  int pers_sl = 0;               // register-resident slice length of the gate/up plan (0: none)
   float *px = nullptr, *psumsq = nullptr, *pq = nullptr;
   void *pxg = nullptr, *pattn = nullptr, *ph = nullptr;
   int *psplit = nullptr, *pphase = nullptr, *perr = nullptr;
@@ -556,18 +555,30 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   a.row_tok = c->row_tok;
   a.row_bad = c->row_bad;
   a.out = c->d_out;
-  a.pairs_qkv = c->p_qkv.pairs;
-  a.pairs_o = c->p_o.pairs;
-  a.pairs_gu = c->p_gu.pairs;
-  a.pairs_down = c->p_down.pairs;
-  a.pairs_lm = c->p_lm.pairs;
+  // completion signals of a GEMM phase: one per workgroup of a balanced
+  // plan, else one per tile pair
+  const int grid = c->pers_grid[(M + 15) / 16];
+  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
+    if (p->G < 1 || p->G > grid)
+      return fail(c, AS2D_ESTATE, "persistent step: plan grid %d outside [1, %d]", p->G, grid);
+  {
+    GemmArgs probe[5] = {base_args(c, c->p_qkv, nullptr, M), base_args(c, c->p_o, nullptr, M),
+                         base_args(c, c->p_gu, nullptr, M), base_args(c, c->p_down, nullptr, M), a.lm};
+    for (const GemmArgs& p : probe)
+      if (!range_plan_ok(p)) return fail(c, AS2D_ESTATE, "persistent step: plan outside the balanced path");
+  }
+  a.done_qkv = c->p_qkv.G;
+  a.done_o = c->p_o.G;
+  a.done_gu = c->p_gu.G;
+  a.done_down = c->p_down.G;
+  a.done_lm = c->p_lm.G;
   a.phase_cnt = c->pphase;
   a.err = c->perr;
   a.spin_limit = env_int("AS2D_SPIN_LIMIT", 1 << 21);
   a.trace = c->trace_on ? c->ptrace : nullptr;
   const int MT = (M + 15) / 16;
   Timed t(c, K_STEP);
-  HIP_TRY(c, launch_step(c->bf16, MT, g.head_dim, a, c->pers_grid[MT], c->n_phase, c->stream));
+  HIP_TRY(c, launch_step(c->bf16, MT, g.head_dim, c->pers_sl, a, grid, c->n_phase, c->stream));
   return AS2D_OK;
 }
 
@@ -854,21 +865,23 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   CK(dalloc(c, &c->counters, (size_t)n_cnt * 4));
   HIP_TRY(c, hipMemsetAsync(c->counters, 0, (size_t)n_cnt * 4, c->stream));
   HIP_TRY(c, prepare_kernels());
-  // persistent step kernel (verification passes of up to 32 rows)
-  if (env_int("AS2D_PERSISTENT", 1)) {
+  // persistent step kernel (verification passes of up to 32 rows; every
+  // GEMM on a balanced plan)
+  bool all_balanced = true;
+  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) all_balanced &= p->G > 0;
+  if (all_balanced && env_int("AS2D_PERSISTENT", 1)) {
     int dev = 0, cus = 0, occ1 = 0, occ2 = 0;
     HIP_TRY(c, hipGetDevice(&dev));
     HIP_TRY(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-    HIP_TRY(c, step_occupancy(c->bf16, 1, d, H, &occ1));
-    HIP_TRY(c, step_occupancy(c->bf16, 2, d, H, &occ2));
+    c->pers_sl = step_ra_slice(c->bf16, c->p_gu.KS, c->p_gu.KT);
+    HIP_TRY(c, step_occupancy(c->bf16, 1, d, H, c->pers_sl, &occ1));
+    HIP_TRY(c, step_occupancy(c->bf16, 2, d, H, 0, &occ2));
     const int L = g.n_layers;
     const long long R = kStepRows;
     if (occ1 > 0 && occ2 > 0) {
       cus = stream_cus(c->stream, cus);
-      c->pers_occ[1] = occ1;
-      c->pers_occ[2] = occ2;
-      c->pers_grid[1] = occ1 * cus;
-      c->pers_grid[2] = occ2 * cus;
+      c->pers_grid[1] = cus;
+      c->pers_grid[2] = cus;
       CK(dalloc(c, &c->px, (size_t)(2 * L + 1) * R * H * 4));
       CK(dalloc(c, &c->pxg, (size_t)(2 * L + 1) * R * H * 4));
       CK(dalloc(c, &c->psumsq, (size_t)(2 * L + 1) * (H / kPairCols) * kMaxRows * 4));
@@ -1165,7 +1178,8 @@ int as2d_set_stream(as2d_ctx* c, void* hip_stream) {
   HIP_TRY(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
   cus = stream_cus(c->stream, cus);
   for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, cus);
-  for (int mt = 1; mt <= 2; ++mt) c->pers_grid[mt] = c->pers_occ[mt] * cus;
+  if (c->pers_ok)
+    for (int mt = 1; mt <= 2; ++mt) c->pers_grid[mt] = cus;
   return AS2D_OK;
 }
 

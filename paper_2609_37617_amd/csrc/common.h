@@ -31,6 +31,27 @@ __device__ __forceinline__ float to_f(uint16_t v) { return bf2f(v); }
 __device__ __forceinline__ float to_f(float v) { return v; }
 
 // ---------------------------------------------------------------------------
+// Global-memory views of device pointers.  A pointer the compiler cannot
+// trace to a kernel argument (one read from a device-side argument array)
+// is generic, and generic (flat) accesses are counted on both the vector
+// memory and the LDS counters, so every LDS wait would also wait for the
+// weight prefetch.  Accesses through these views are global instructions.
+template <class T> using gmem_t = __attribute__((address_space(1))) T;
+template <class T> __device__ __forceinline__ gmem_t<T>* gmem(T* p) { return (gmem_t<T>*)p; }
+template <class T> __device__ __forceinline__ const gmem_t<T>* gmem(const T* p) { return (const gmem_t<T>*)p; }
+
+// Plain 16-byte load (activation fragments).
+__device__ __forceinline__ uint4 ldg(const uint4* p) {
+  const u32x4 v = *gmem(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float4 ldg(const float4* p) {
+  const f4 v = *gmem(reinterpret_cast<const f4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+template <class V> __device__ __forceinline__ V ldg(const V* p) { return *gmem(p); }
+
+// ---------------------------------------------------------------------------
 // Stores of values other workgroups read.  COH = true: inside one kernel,
 // possibly from another XCD (whose L2 is not coherent with the writer's):
 // agent-scope stores that write through the L2.  COH = false: read only by
@@ -38,12 +59,12 @@ __device__ __forceinline__ float to_f(float v) { return v; }
 
 template <bool COH, typename V> __device__ __forceinline__ void st(V* p, V v) {
   if constexpr (COH)
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(gmem(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   else
-    *p = v;
+    *gmem(p) = v;
 }
 template <typename V> __device__ __forceinline__ V ld_coherent(const V* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load(gmem(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Index of element (m, k) of an activation operand with K columns in MFMA
@@ -79,11 +100,26 @@ template <bool BF, bool COH> __device__ __forceinline__ void store_act(void* bas
 
 // Wait until this wave's memory operations (its stores included) have been
 // performed.
+// Reads a struct that no thread writes while the kernel runs (per-layer
+// arguments, request descriptors) through the constant address space: the
+// fields arrive by scalar loads in scalar registers, so no later wait on
+// the vector memory counter (which covers the weight prefetch) is needed
+// for them.
+template <class T> __device__ __forceinline__ T load_invariant(const T* p) {
+  static_assert(sizeof(T) % 4 == 0 && alignof(T) >= 4, "copied as 32-bit words");
+  T out;
+  const __attribute__((address_space(4))) uint32_t* src = (const __attribute__((address_space(4))) uint32_t*)p;
+  uint32_t* dst = reinterpret_cast<uint32_t*>(&out);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) dst[i] = src[i];
+  return out;
+}
+
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Agent-scope counter increment; returns the previous value.
 __device__ __forceinline__ int counter_add(int* c, int v) {
-  return __hip_atomic_fetch_add(c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_fetch_add(gmem(c), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------------------
@@ -121,7 +157,7 @@ template <bool BF> __device__ __forceinline__ f4 mma_a(const AFrag& a, uint4 b, 
 
 // Streaming (non-temporal) 16-byte load of weight tiles: read once per pass.
 __device__ __forceinline__ uint4 ldw(const uint4* p) {
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  const u32x4 v = __builtin_nontemporal_load(gmem(reinterpret_cast<const u32x4*>(p)));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 

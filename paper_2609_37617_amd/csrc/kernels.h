@@ -29,6 +29,7 @@ constexpr int kPairsS = kWaves;         // tile pairs per workgroup, staged path
 constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
 constexpr int kDirectMT = 2;            // row tiles of the direct path (up to 32 rows)
+constexpr int kStepRows = kDirectMT * 16;  // rows of a persistent-kernel pass
 constexpr int kAttnChunk = 32;          // keys per attention split
 constexpr int kAttnRowGroup = 16;       // rows per attention workgroup (row groups)
 constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
@@ -154,7 +155,7 @@ struct StepArgs {
   int* row_tok;
   int* row_bad;
   StepOut* out;
-  int pairs_qkv, pairs_o, pairs_gu, pairs_down, pairs_lm;  // tiles per phase
+  int done_qkv, done_o, done_gu, done_down, done_lm;  // completion signals per GEMM phase
   int* phase_cnt;            // 3 + 6 * n_layers counters, cleared by the launcher
   int* err;                  // set when a wait times out
   int spin_limit;
@@ -165,6 +166,10 @@ struct StepArgs {
 // LDS; call once per process before the first launch (prepare_kernels
 // calls prepare_step_kernels).
 hipError_t prepare_kernels();
+// The host-side conditions of the balanced path (gemm_range_direct):
+// 1 <= G <= units, at most kMaxUnits units per workgroup, every split at
+// least kWaves k-steps, KS <= kMaxSplits, kWaves slices, MT <= kDirectMT.
+bool range_plan_ok(const GemmArgs& a);
 hipError_t prepare_step_kernels();
 
 // Launchers (all asynchronous on `s`).  `bf16` selects the model dtype.
@@ -175,9 +180,12 @@ hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed
                         int H, const float* gain, float* x, float* sumsq, void* xg, long long xg_plane,
                         hipStream_t s);
 hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStream_t s);
-int step_lds_bytes(int head_dim, int hidden);
-hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int* blocks_per_cu);
-hipError_t launch_step(bool bf16, int MT, int head_dim, const StepArgs& a, int grid, int n_counters,
+int step_lds_bytes(int MT, int head_dim, int hidden);
+// Slice length of the register-resident balanced variant for a gate/up
+// plan (KS, KT) with one row tile, or 0: the persistent kernel to launch.
+int step_ra_slice(bool bf16, int KS, int KT);
+hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int sl, int* blocks_per_cu);
+hipError_t launch_step(bool bf16, int MT, int head_dim, int sl, const StepArgs& a, int grid, int n_counters,
                        hipStream_t s);
 // Attention over n_reqs requests; max_chunks bounds the 32-key chunks of
 // any request (the grid size).

@@ -133,8 +133,6 @@ static void launch_direct(const GemmArgs& a, hipStream_t s) {
 // is at least kRangeMinLds, so two never share one), each streaming an
 // equal share of the (pair, split) units.  SL > 0: the variant with the
 // activation slice in registers (KS = 1, one row tile, KT = 4 SL).
-constexpr int kRangeMinLds = 82 * 1024;
-constexpr int kRangePrefetch = 4;
 
 template <bool BF, int MT, int SL, int AM, int EPI>
 __global__ __launch_bounds__(256, 1) void gemm_range_kernel(const GemmArgs p) {
@@ -142,36 +140,33 @@ __global__ __launch_bounds__(256, 1) void gemm_range_kernel(const GemmArgs p) {
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flags[kMaxUnits];
   if constexpr (SL == 0) {
-    gemm_range_direct<BF, MT, kRangePrefetch, AM, EPI>(p, p.M, smem, s_scale, s_flags);
+    gemm_range_direct<BF, MT, kRangePrefetch, AM, EPI, false>(p, p.M, smem, s_scale, s_flags, [] {});
   } else {
     constexpr int P = SL % kRangePrefetch == 0 ? kRangePrefetch : SL;
-    gemm_range_direct_ra<BF, P, SL, AM, EPI>(p, p.M, smem, s_scale, s_flags);
+    gemm_range_direct_ra<BF, P, SL, AM, EPI, false>(p, p.M, smem, s_scale, s_flags, [] {});
   }
 }
 
-// slice lengths with a register-resident variant, per element type
-template <bool BF> constexpr int kRangeSL[3] = {2, 16, 28};
-template <> constexpr int kRangeSL<false>[3] = {4, 4, 4};
+bool range_plan_ok(const GemmArgs& a) {
+  const int U = (a.N / kPairCols) * a.KS;
+  const int last = a.KT - (a.KS - 1) * a.ktps;   // k-steps of the last split
+  return a.G >= 1 && a.G <= U && (U + a.G - 1) / a.G <= kMaxUnits && a.ktps >= kWaves && last >= kWaves &&
+         a.KS <= kMaxSplits && a.ns == kWaves && a.MT >= 1 && a.MT <= kDirectMT;
+}
 
 template <bool BF, int AM, int EPI>
 static hipError_t launch_range(const GemmArgs& a, hipStream_t s) {
+  if (!range_plan_ok(a)) return hipErrorInvalidValue;
   const int U = (a.N / kPairCols) * a.KS;
-  const int last = a.KT - (a.KS - 1) * a.ktps;   // k-steps of the last split
-  if (a.G < 1 || a.G > U || (U + a.G - 1) / a.G > kMaxUnits || a.ktps < kWaves || last < kWaves ||
-      a.KS > kMaxSplits || a.ns != kWaves)
-    return hipErrorInvalidValue;
   int lds = gemm_range_lds_bytes(a.MT, (U + a.G - 1) / a.G);
   if (lds < kRangeMinLds) lds = kRangeMinLds;
-  const int sl = a.MT == 1 && a.KS == 1 && a.KT % kWaves == 0 ? a.KT / kWaves : 0;
-  bool done = false;
+  const int sl = range_ra_slice<BF>(AM, EPI, a.MT, a.KS, a.KT);
   if constexpr (AM == A_NORM && (EPI == EPI_SWIGLU || EPI == EPI_ARGMAX)) {
-    done = true;
     if (sl == kRangeSL<BF>[0]) gemm_range_kernel<BF, 1, kRangeSL<BF>[0], AM, EPI><<<a.G, 256, lds, s>>>(a);
     else if (sl == kRangeSL<BF>[1]) gemm_range_kernel<BF, 1, kRangeSL<BF>[1], AM, EPI><<<a.G, 256, lds, s>>>(a);
     else if (sl == kRangeSL<BF>[2]) gemm_range_kernel<BF, 1, kRangeSL<BF>[2], AM, EPI><<<a.G, 256, lds, s>>>(a);
-    else done = false;
   }
-  if (!done) {
+  if (!sl) {
     if (a.MT == 1) gemm_range_kernel<BF, 1, 0, AM, EPI><<<a.G, 256, lds, s>>>(a);
     else gemm_range_kernel<BF, 2, 0, AM, EPI><<<a.G, 256, lds, s>>>(a);
   }
@@ -256,14 +251,14 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // ascending order (attn_merge_row).
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_chunk_kernel(const AttnArgs p) {
+__global__ __launch_bounds__(256, 4) void attn_chunk_kernel(const AttnArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int rg = blockIdx.z % p.row_groups;
   const ReqDesc rq = p.reqs[blockIdx.z / p.row_groups];
   const int r_lo = rg * kAttnRowGroup, r_hi = min(rq.W, r_lo + kAttnRowGroup);
   // no row of the group reaches this chunk's first key
   if (r_lo >= r_hi || (int)blockIdx.x * kAttnChunk > rq.L0 + r_hi - 1) return;
-  attn_chunk_tile<D, false>(p, blockIdx.x, blockIdx.y, rq, smem, r_lo, r_hi);
+  attn_chunk_tile<D, false, kAttnRowGroup / 4>(p, blockIdx.x, blockIdx.y, rq, smem, r_lo, r_hi);
 }
 
 template <bool BF, int D>

@@ -2,9 +2,9 @@
 // (embedding, every decoder layer, LM head and greedy verification) for up
 // to 32 rows.
 //
-// All workgroups are resident at once (grid = occupancy x CUs).  The pass
-// is a sequence of phases; a phase's tiles are dealt round-robin to the
-// workgroups, which walk the phases in order.  A tile that consumes the
+// All workgroups are resident at once (one per compute unit).  The pass
+// is a sequence of phases; a phase's work is split over the workgroups,
+// which walk the phases in order.  A tile that consumes the
 // previous phase's output first issues its weight loads (weights do not
 // depend on activations), then waits until the producing phase's
 // completion counter reaches its target, so weight streaming continues
@@ -22,10 +22,10 @@
 
 namespace as2d {
 
-// Phase counter layout (phase_cnt): 0 embedding; per layer l, base 1 + 6 l:
-// +0 QKV tile pairs, +1 attention chunk tiles, +2 merged (row, head) pairs,
-// +3 O tile pairs, +4 gate/up tile pairs, +5 down tile pairs; then LM head
-// tile pairs (1 + 6 L) and verified rows (2 + 6 L).
+// Phase counter layout (phase_cnt): 0 embedded rows; per layer l, base
+// 1 + 6 l: +0 QKV, +1 attention chunk tiles, +2 merged (row, head) pairs,
+// +3 O, +4 gate/up, +5 down; then the LM head (1 + 6 L) and verified rows
+// (2 + 6 L).  A GEMM phase counts the signals of its G workgroups.
 __device__ __forceinline__ int ph_layer(int l, int k) { return 1 + 6 * l + k; }
 
 __device__ __forceinline__ void signal_done(int* c) {
@@ -36,11 +36,12 @@ __device__ __forceinline__ void signal_done(int* c) {
 // Waits until *c >= target.  Bounded: after spin_limit polls the error
 // flag is raised; once it is raised (by any workgroup) every wait returns
 // at once, so all waves reach the end of the kernel.
-__device__ __noinline__ void wait_count(const int* c, int target, int* err, int spin_limit) {
+__device__ __forceinline__ void wait_count(const int* c, int target, int* err, int spin_limit) {
   if (threadIdx.x == 0) {
     int n = 0;
-    while (ld_coherent(c) < target) {
-      if (ld_coherent(err)) break;
+    for (;;) {
+      const int v = ld_coherent(c), e = ld_coherent(err);   // one round trip per poll
+      if (v >= target || e) break;
       __builtin_amdgcn_s_sleep(1);
       if (++n > spin_limit) {
         st<true>(err, 1);
@@ -58,33 +59,48 @@ __device__ __forceinline__ void stamp(const StepArgs& a, int phase, int which) {
     a.trace[((size_t)blockIdx.x * (3 + 6 * a.n_layers) + phase) * 3 + which] = wall_clock64();
 }
 
-template <bool BF, int MT, int AM, int EPI>
-__device__ void gemm_phase(const GemmArgs p, int M, const int* wait_c, int wait_target, int* done_c,
-                           const StepArgs& a, unsigned char* smem, float* s_scale, int* s_flag) {
-  const int G = gridDim.x;
-  const int n_tiles = (p.N / kPairCols) * p.KS;
+// One GEMM phase of a balanced plan: workgroup b < G streams its share of
+// the (pair, split) units (the same units and sums as the balanced
+// kernel), issuing its first weight loads before the wait for the
+// producer, and signals once its partials, fixups and epilogues are
+// stored, so the phase is done at G signals.
+template <bool BF, int MT, int SL, int AM, int EPI>
+__device__ __forceinline__ void gemm_phase(const GemmArgs& p, int M, const int* wait_c, int wait_target, int* done_c,
+                           const StepArgs& a, unsigned char* smem, float* s_scale, int* s_flags) {
   const int phase = (int)(done_c - a.phase_cnt);
   stamp(a, phase, 0);
   bool waited = false;
-  for (int t = blockIdx.x; t < n_tiles; t += G) {
-    const int pair = t / p.KS, split = t - pair * p.KS;
-    const bool fin = gemm_tile_direct<BF, MT, 1, kWaves, false, AM, EPI, true, true>(p, M, pair, split, smem, s_scale, s_flag, [&] {
-      if (!waited) {
-        wait_count(wait_c, wait_target, a.err, a.spin_limit);
-        stamp(a, phase, 1);
-        waited = true;
+  auto wait = [&] {
+    if (!waited) {
+      wait_count(wait_c, wait_target, a.err, a.spin_limit);
+      stamp(a, phase, 1);
+      waited = true;
+    }
+  };
+  if ((int)blockIdx.x < p.G) {
+    bool ra = false;
+    if constexpr (SL > 0 && MT == 1 && AM == A_NORM && (EPI == EPI_SWIGLU || EPI == EPI_ARGMAX)) {
+      if (range_ra_slice<BF>(AM, EPI, MT, p.KS, p.KT) == SL) {
+        constexpr int P = SL % kRangePrefetch == 0 ? kRangePrefetch : SL;
+        gemm_range_direct_ra<BF, P, SL, AM, EPI, true>(p, M, smem, s_scale, s_flags, wait);
+        ra = true;
       }
-    });
-    if (fin) signal_done(done_c);
+    }
+    if (!ra) gemm_range_direct<BF, MT, kRangePrefetch, AM, EPI, true>(p, M, smem, s_scale, s_flags, wait);
+    wait_vmem();
+    signal_done(done_c);
   }
   stamp(a, phase, 2);
 }
 
-template <bool BF, int MT, int D>
-__global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
+// SL: slice length of the register-resident balanced variant for the
+// gate/up and LM-head phases (0: none).  One workgroup per compute unit.
+template <bool BF, int MT, int D, int SL>
+__global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
-  __shared__ int s_flag, s_tok, s_bad;
+  __shared__ int s_flags[kMaxUnits];
+  __shared__ int s_tok, s_bad;
   __shared__ float s4f[4];
   __shared__ int s4i[4];
   const int G = gridDim.x, tid = threadIdx.x;
@@ -101,45 +117,63 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
   stamp(a, 0, 2);
   // attention tiles of this pass: n_q heads x chunks of each request
   int n_chunk_tiles = 0;
-  for (int r = 0; r < a.n_reqs; ++r)
-    n_chunk_tiles += a.n_q * ((a.reqs[r].L0 + a.reqs[r].W + kAttnChunk - 1) / kAttnChunk);
+  for (int r = 0; r < a.n_reqs; ++r) {
+    const ReqDesc rq = load_invariant(a.reqs + r);
+    n_chunk_tiles += a.n_q * ((rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk);
+  }
   constexpr int kMergeGroups = 256 / D;  // (row, head) merges per workgroup pass
 
   for (int l = 0; l < L; ++l) {
-    const StepLayer& ly = a.layers[l];
+    const StepLayer* ly = a.layers + l;
     const int* prev = l == 0 ? &a.phase_cnt[0] : &a.phase_cnt[ph_layer(l - 1, 5)];
-    const int prev_target = l == 0 ? M : a.pairs_down;
-    gemm_phase<BF, MT, A_NORM, EPI_QKV>(ly.qkv, M, prev, prev_target, &a.phase_cnt[ph_layer(l, 0)], a, smem,
-                                         s_scale, &s_flag);
+    const int prev_target = l == 0 ? M : a.done_down;
+    gemm_phase<BF, MT, SL, A_NORM, EPI_QKV>(load_invariant(&ly->qkv), M, prev, prev_target, &a.phase_cnt[ph_layer(l, 0)], a, smem,
+                                             s_scale, s_flags);
 
-    // attention chunks
+    // attention chunks; the next tile's keys and values are requested
+    // while the current tile's rows run
     stamp(a, ph_layer(l, 1), 0);
-    bool waited = false;
-    for (int t = blockIdx.x; t < n_chunk_tiles; t += G) {
-      int r = 0, u = t;
-      for (;; ++r) {
-        const int n = a.n_q * ((a.reqs[r].L0 + a.reqs[r].W + kAttnChunk - 1) / kAttnChunk);
-        if (u < n || r == a.n_reqs - 1) break;
-        u -= n;
+    if ((int)blockIdx.x < n_chunk_tiles) {
+      wait_count(&a.phase_cnt[ph_layer(l, 0)], a.done_qkv, a.err, a.spin_limit);
+      stamp(a, ph_layer(l, 1), 1);
+      const AttnArgs at = load_invariant(&ly->attn);
+      // tile t: request, head and chunk
+      auto tile_of = [&](int t, ReqDesc& rq, int& h, int& c) {
+        int r = 0, u = t;
+        for (;; ++r) {
+          rq = load_invariant(a.reqs + r);
+          const int n = a.n_q * ((rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk);
+          if (u < n || r == a.n_reqs - 1) break;
+          u -= n;
+        }
+        const int nch = (rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk;
+        h = u / nch;
+        c = u - h * nch;
+      };
+      ReqDesc rq, rq2;
+      int h, c, h2 = 0, c2 = 0;
+      tile_of(blockIdx.x, rq, h, c);
+      AttnKV<D> cur, nxt;
+      attn_load_kv<D>(at, c, h, rq, cur);
+      for (int t = blockIdx.x; t < n_chunk_tiles; t += G) {
+        const bool more = t + G < n_chunk_tiles;
+        if (more) tile_of(t + G, rq2, h2, c2);
+        attn_tile_kv<D, true, kStepRows / 4>(at, c, h, rq, smem, cur, [&] {
+          if (more) attn_load_kv<D>(at, c2, h2, rq2, nxt);
+        });
+        signal_done(&a.phase_cnt[ph_layer(l, 1)]);
+        cur = nxt;
+        rq = rq2;
+        h = h2;
+        c = c2;
       }
-      const ReqDesc rq = a.reqs[r];
-      const int nch = (rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk;
-      const int h = u / nch, c = u - h * nch;
-      if (!waited) {
-        wait_count(&a.phase_cnt[ph_layer(l, 0)], a.pairs_qkv, a.err, a.spin_limit);
-        stamp(a, ph_layer(l, 1), 1);
-        waited = true;
-      }
-      const AttnArgs at = ly.attn;
-      attn_chunk_tile<D, true>(at, c, h, rq, smem);
-      signal_done(&a.phase_cnt[ph_layer(l, 1)]);
     }
     stamp(a, ph_layer(l, 1), 2);
 
     // merge of every (row, head): kMergeGroups per workgroup pass
     const int n_merge = M * a.n_q;
     stamp(a, ph_layer(l, 2), 0);
-    waited = false;
+    bool waited = false;
     for (int t0 = blockIdx.x * kMergeGroups; t0 < n_merge; t0 += G * kMergeGroups) {
       if (!waited) {
         wait_count(&a.phase_cnt[ph_layer(l, 1)], n_chunk_tiles, a.err, a.spin_limit);
@@ -149,7 +183,7 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
       const int grp = tid / D;
       const int t = t0 + grp;
       float* sm = reinterpret_cast<float*>(smem) + grp * 2 * kMaxChunks;
-      const AttnArgs at = ly.attn;
+      const AttnArgs at = load_invariant(&ly->attn);
       if (t < n_merge)
         attn_merge_row<BF, D, true>(at, t / a.n_q, t % a.n_q, grp * D, sm, sm + kMaxChunks,
                                     [] { __syncthreads(); }, true);
@@ -161,23 +195,23 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
     }
     stamp(a, ph_layer(l, 2), 2);
 
-    gemm_phase<BF, MT, A_PLAIN, EPI_RESID>(ly.o, M, &a.phase_cnt[ph_layer(l, 2)], n_merge,
-                                            &a.phase_cnt[ph_layer(l, 3)], a, smem, s_scale, &s_flag);
-    gemm_phase<BF, MT, A_NORM, EPI_SWIGLU>(ly.gu, M, &a.phase_cnt[ph_layer(l, 3)], a.pairs_o,
-                                            &a.phase_cnt[ph_layer(l, 4)], a, smem, s_scale, &s_flag);
-    gemm_phase<BF, MT, A_PLAIN, EPI_RESID>(ly.down, M, &a.phase_cnt[ph_layer(l, 4)], a.pairs_gu,
-                                            &a.phase_cnt[ph_layer(l, 5)], a, smem, s_scale, &s_flag);
+    gemm_phase<BF, MT, SL, A_PLAIN, EPI_RESID>(load_invariant(&ly->o), M, &a.phase_cnt[ph_layer(l, 2)], n_merge,
+                                                &a.phase_cnt[ph_layer(l, 3)], a, smem, s_scale, s_flags);
+    gemm_phase<BF, MT, SL, A_NORM, EPI_SWIGLU>(load_invariant(&ly->gu), M, &a.phase_cnt[ph_layer(l, 3)], a.done_o,
+                                                &a.phase_cnt[ph_layer(l, 4)], a, smem, s_scale, s_flags);
+    gemm_phase<BF, MT, SL, A_PLAIN, EPI_RESID>(load_invariant(&ly->down), M, &a.phase_cnt[ph_layer(l, 4)], a.done_gu,
+                                                &a.phase_cnt[ph_layer(l, 5)], a, smem, s_scale, s_flags);
   }
-  gemm_phase<BF, MT, A_NORM, EPI_ARGMAX>(a.lm, M, &a.phase_cnt[ph_layer(L - 1, 5)], a.pairs_down,
-                                          &a.phase_cnt[1 + 6 * L], a, smem, s_scale, &s_flag);
+  gemm_phase<BF, MT, SL, A_NORM, EPI_ARGMAX>(a.lm, M, &a.phase_cnt[ph_layer(L - 1, 5)], a.done_down,
+                                              &a.phase_cnt[1 + 6 * L], a, smem, s_scale, s_flags);
 
   // arg-max of each verified row on the last workgroups, then verification
   // by the last row to finish
   for (int i = G - 1 - blockIdx.x; i < a.fin_rows; i += G) {
     int r = 0, u = i;
-    while (r < a.n_fin - 1 && u >= a.fin_reqs[r].W) u -= a.fin_reqs[r++].W;
-    const int row = a.fin_reqs[r].row_start + u;
-    wait_count(&a.phase_cnt[1 + 6 * L], a.pairs_lm, a.err, a.spin_limit);
+    while (r < a.n_fin - 1 && u >= load_invariant(a.fin_reqs + r).W) u -= load_invariant(a.fin_reqs + r++).W;
+    const int row = load_invariant(a.fin_reqs + r).row_start + u;
+    wait_count(&a.phase_cnt[1 + 6 * L], a.done_lm, a.err, a.spin_limit);
     argmax_row<true>(a.lm.amax_val, a.lm.amax_idx, a.lm.N / kPairCols, row, &s_tok, &s_bad, s4f, s4i);
     if (tid == 0) {
       st<true>(a.row_tok + row, s_tok);
@@ -185,7 +219,7 @@ __global__ __launch_bounds__(256, 2) void step_kernel(const StepArgs a) {
       wait_vmem();
       if (counter_add(&a.phase_cnt[2 + 6 * L], 1) == a.fin_rows - 1) {
         for (int q = 0; q < a.n_fin; ++q) {
-          const ReqDesc rq = a.fin_reqs[q];
+          const ReqDesc rq = load_invariant(a.fin_reqs + q);
           int bad = 0;
           for (int w = 0; w < rq.W; ++w) bad |= ld_coherent(a.row_bad + rq.row_start + w);
           a.out[q] = verify_request(a.rows, rq, [&](int rr) { return ld_coherent(a.row_tok + rr); }, bad);
@@ -202,62 +236,68 @@ __global__ void clear_kernel(int* p, int n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
-template <bool BF, int MT, int D>
+template <bool BF, int MT, int D, int SL>
 static const void* step_fn() {
-  return reinterpret_cast<const void*>(&step_kernel<BF, MT, D>);
+  return reinterpret_cast<const void*>(&step_kernel<BF, MT, D, SL>);
 }
 
-static const void* pick(bool bf16, int MT, int D) {
-  if (D == 128) {
-    if (bf16) return MT == 1 ? step_fn<true, 1, 128>() : step_fn<true, 2, 128>();
-    return MT == 1 ? step_fn<false, 1, 128>() : step_fn<false, 2, 128>();
-  }
-  if (bf16) return MT == 1 ? step_fn<true, 1, 64>() : step_fn<true, 2, 64>();
-  return MT == 1 ? step_fn<false, 1, 64>() : step_fn<false, 2, 64>();
+// The instantiated kernels: (bf16, MT, head_dim, SL) for SL = 0 and the
+// register-resident slice lengths (one row tile only).
+template <bool BF, int D>
+static const void* pick_sl(int MT, int SL) {
+  if (MT == 2) return step_fn<BF, 2, D, 0>();
+  if (SL == kRangeSL<BF>[0]) return step_fn<BF, 1, D, kRangeSL<BF>[0]>();
+  if (SL == kRangeSL<BF>[1]) return step_fn<BF, 1, D, kRangeSL<BF>[1]>();
+  if (SL == kRangeSL<BF>[2]) return step_fn<BF, 1, D, kRangeSL<BF>[2]>();
+  return step_fn<BF, 1, D, 0>();
 }
 
-int step_lds_bytes(int head_dim, int hidden) {
+static const void* pick(bool bf16, int MT, int D, int SL) {
+  if (D == 128) return bf16 ? pick_sl<true, 128>(MT, SL) : pick_sl<false, 128>(MT, SL);
+  return bf16 ? pick_sl<true, 64>(MT, SL) : pick_sl<false, 64>(MT, SL);
+}
+
+int step_ra_slice(bool bf16, int KS, int KT) {
+  return bf16 ? range_ra_slice<true>(A_NORM, EPI_SWIGLU, 1, KS, KT)
+              : range_ra_slice<false>(A_NORM, EPI_SWIGLU, 1, KS, KT);
+}
+
+int step_lds_bytes(int MT, int head_dim, int hidden) {
   // hidden <= 8192
-  int b = gemm_direct_lds_bytes<2, 1>(kMaxSlices);
+  int b = kRangeMinLds;                                 // one workgroup per compute unit
+  b = max(b, gemm_range_lds_bytes(MT, kMaxUnits));
   b = max(b, head_dim == 128 ? attn_lds_bytes<128>() : attn_lds_bytes<64>());
-  b = max(b, hidden * 4);                      // embedding row
-  b = max(b, (256 / head_dim) * 2 * kMaxChunks * 4);  // merge scratch
+  b = max(b, hidden * 4);                               // embedding row
+  b = max(b, (256 / head_dim) * 2 * kMaxChunks * 4);    // merge scratch
   return b;
 }
 
 hipError_t prepare_step_kernels() {
-  const int lds128 = step_lds_bytes(128, 8192), lds64 = step_lds_bytes(64, 8192);
-  const void* fns[8] = {step_fn<true, 1, 128>(), step_fn<true, 2, 128>(), step_fn<false, 1, 128>(),
-                        step_fn<false, 2, 128>(), step_fn<true, 1, 64>(),  step_fn<true, 2, 64>(),
-                        step_fn<false, 1, 64>(),  step_fn<false, 2, 64>()};
-  for (int i = 0; i < 8; ++i) {
-    hipError_t e = hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, i < 4 ? lds128 : lds64);
-    if (e != hipSuccess) return e;
-  }
+  for (int bf = 0; bf < 2; ++bf)
+    for (int d = 64; d <= 128; d += 64)
+      for (int mt = 1; mt <= 2; ++mt)
+        for (int i = -1; i < 3; ++i) {
+          const int sl = i < 0 ? 0 : (bf ? kRangeSL<true>[i] : kRangeSL<false>[i]);
+          hipError_t e = hipFuncSetAttribute(pick(bf, mt, d, sl), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             step_lds_bytes(mt, d, 8192));
+          if (e != hipSuccess) return e;
+        }
   return hipSuccess;
 }
 
-hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int* blocks_per_cu) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, pick(bf16, MT, head_dim), 256,
-                                                      step_lds_bytes(head_dim, hidden));
+hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int sl, int* blocks_per_cu) {
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, pick(bf16, MT, head_dim, sl), 256,
+                                                      step_lds_bytes(MT, head_dim, hidden));
 }
 
-hipError_t launch_step(bool bf16, int MT, int head_dim, const StepArgs& a, int grid, int n_counters,
+hipError_t launch_step(bool bf16, int MT, int head_dim, int sl, const StepArgs& a, int grid, int n_counters,
                        hipStream_t s) {
   clear_kernel<<<8, 256, 0, s>>>(a.phase_cnt, n_counters);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t lds = step_lds_bytes(head_dim, a.hidden);
-#define AS2D_S(bf, mt, d) step_kernel<bf, mt, d><<<grid, 256, lds, s>>>(a)
-  if (head_dim == 128) {
-    if (bf16) { if (MT == 1) AS2D_S(true, 1, 128); else AS2D_S(true, 2, 128); }
-    else { if (MT == 1) AS2D_S(false, 1, 128); else AS2D_S(false, 2, 128); }
-  } else {
-    if (bf16) { if (MT == 1) AS2D_S(true, 1, 64); else AS2D_S(true, 2, 64); }
-    else { if (MT == 1) AS2D_S(false, 1, 64); else AS2D_S(false, 2, 64); }
-  }
-#undef AS2D_S
-  return hipGetLastError();
+  const void* fn = pick(bf16, MT, head_dim, sl);
+  void* args[] = {const_cast<StepArgs*>(&a)};
+  return hipLaunchKernel(fn, dim3(grid), dim3(256), args, step_lds_bytes(MT, head_dim, a.hidden), s);
 }
 
 }  // namespace as2d

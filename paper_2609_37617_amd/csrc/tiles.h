@@ -16,13 +16,13 @@ namespace as2d {
 // srow: LDS scratch of H floats.
 
 template <bool BF, bool COH>
-__device__ void embed_row(const RowDesc* __restrict__ rows, int m, const typename ET<BF>::T* __restrict__ embed,
+__device__ __forceinline__ void embed_row(const RowDesc* __restrict__ rows, int m, const typename ET<BF>::T* __restrict__ embed,
                           const typename ET<BF>::T* __restrict__ audio, int H, const float* __restrict__ gain,
                           float* __restrict__ x, float* __restrict__ sumsq, void* __restrict__ xg,
                           long long xg_plane, float* srow) {
   using T = typename ET<BF>::T;
   constexpr int kPer = 8, kPasses = 4;   // H <= 256 * 8 * 4
-  const RowDesc rd = rows[m];
+  const RowDesc rd = load_invariant(rows + m);
   const T* src = rd.token >= 0 ? embed + (size_t)rd.token * H : audio + (size_t)rd.src * H;
   float v[kPasses][kPer];
 #pragma unroll
@@ -78,7 +78,7 @@ __device__ void embed_row(const RowDesc* __restrict__ rows, int m, const typenam
 // rows the call covers.
 
 template <bool BF, int EPI, bool COH, int NTH = 256>
-__device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, int np, int r0, int r1) {
+__device__ __forceinline__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, int np, int r0, int r1) {
   constexpr int kUnits = NTH / 32;              // (row, pair) units per pass: one per half-wave
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int N = p.N, C = np * kPairCols;
@@ -90,9 +90,9 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
       const int m = r0 + idx / C, c = idx % C;
       const int n = n0 + c;
       const size_t o = (size_t)m * N + n;
-      const float v = p.x[o] + F[(m - r0) * fs + c];
+      const float v = ldg(p.x + o) + F[(m - r0) * fs + c];
       st<COH>(p.x_out + o, v);
-      store_act<BF, COH>(p.out, p.out_plane, frag_index<BF>(m, n, N), v * p.gain_next[n]);
+      store_act<BF, COH>(p.out, p.out_plane, frag_index<BF>(m, n, N), v * ldg(p.gain_next + n));
       F[(m - r0) * fs + c] = v;
     }
     lds_sync();
@@ -125,14 +125,14 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
       const int i = 16 * q + cc;                 // rotation index
       const int dd = j * half + i;               // dimension within the head
       const int n = head * d + dd;               // original output column
-      const RowDesc rd = p.rows[m];
+      const RowDesc rd = load_invariant(p.rows + m);
       const float* Fr = F + (m - r0) * fs;
-      float v = Fr[c] + (p.bias ? p.bias[n] : 0.0f);
+      float v = Fr[c] + (p.bias ? ldg(p.bias + n) : 0.0f);
       if (head < p.n_q + p.n_kv) {
         const int pn = j ? n - half : n + half;
-        const float partner = Fr[c ^ 16] + (p.bias ? p.bias[pn] : 0.0f);
-        const float cs = p.rope_cs[((size_t)rd.pos * half + i) * 2];
-        const float sn = p.rope_cs[((size_t)rd.pos * half + i) * 2 + 1];
+        const float partner = Fr[c ^ 16] + (p.bias ? ldg(p.bias + pn) : 0.0f);
+        const float cs = ldg(p.rope_cs + ((size_t)rd.pos * half + i) * 2);
+        const float sn = ldg(p.rope_cs + ((size_t)rd.pos * half + i) * 2 + 1);
         v = j == 0 ? v * cs - partner * sn : v * cs + partner * sn;
         if (head < p.n_q) {
           st<COH>(p.q_out + (size_t)m * p.n_q * d + n, v);
@@ -180,7 +180,7 @@ __device__ void epilogue_rows(const GemmArgs& p, float* F, int fs, int pair0, in
 // r0).  Loads are issued in batches across elements and splits.
 
 template <int AM, int NTH = 256>
-__device__ void fixup_rows(const GemmArgs& p, int M, int n0, int C, int r0, int r1, const float* s_scale,
+__device__ __forceinline__ void fixup_rows(const GemmArgs& p, int M, int n0, int C, int r0, int r1, const float* s_scale,
                            float* F, int fs) {
   constexpr int kEl = 2;   // elements per thread per batch (kEl x kMaxSplits loads in flight)
   const int E = (r1 - r0) * C;
@@ -216,7 +216,7 @@ __device__ __forceinline__ int slice_start(int kt0, int n, int q, int ns) { retu
 // given by `val(m, c)` and returns true in the workgroup that arrives last
 // at counter `cnt` (it then resets the counter for the next launch).
 template <int NTH = 256, class Val>
-__device__ bool publish_split(const GemmArgs& p, int M, int split, int n0, int C, int* cnt, int* s_flag, Val&& val) {
+__device__ __forceinline__ bool publish_split(const GemmArgs& p, int M, int split, int n0, int C, int* cnt, int* s_flag, Val&& val) {
   for (int e = threadIdx.x; e < M * C; e += NTH) {
     const int m = e / C, c = e % C;
     store_partial(&p.part[((size_t)split * M + m) * p.N + n0 + c], val(m, c));
@@ -282,7 +282,7 @@ __device__ __forceinline__ void row_scale_loads(const GemmArgs& p, int M, float 
 #pragma unroll
       for (int t = 0; t < kT; ++t) {
         const int i = lane + 64 * t;
-        v[r][t] = p.sumsq[(size_t)mm * np + (i < np ? i : 0)];
+        v[r][t] = ldg(p.sumsq + (size_t)mm * np + (i < np ? i : 0));
       }
     }
 #pragma unroll
@@ -544,6 +544,25 @@ __host__ __device__ constexpr int gemm_range_lds_bytes(int MT, int nu_max) {
   return (2 * kWaves * MT * 512 + MT * 16 * (nu_max * kPairCols + 1)) * 4;
 }
 
+// Launch constants of the balanced path: dynamic LDS of at least
+// kRangeMinLds keeps one workgroup per compute unit; kRangePrefetch
+// k-steps in flight per wave; slice lengths (KT / kWaves) that have the
+// register-resident variant, per element type.
+constexpr int kRangeMinLds = 82 * 1024;
+constexpr int kRangePrefetch = 4;
+template <bool BF> inline constexpr int kRangeSL[3] = {2, 16, 28};
+template <> inline constexpr int kRangeSL<false>[3] = {4, 4, 4};
+
+// The balanced path takes the register-resident variant for KS = 1, one
+// row tile and a slice length from kRangeSL, for the gate/up and LM-head
+// products (normalised A): its slice length, else 0.
+template <bool BF>
+__host__ __device__ inline int range_ra_slice(int AM, int EPI, int MT, int KS, int KT) {
+  if (AM != A_NORM || (EPI != EPI_SWIGLU && EPI != EPI_ARGMAX) || MT != 1 || KS != 1 || KT % kWaves) return 0;
+  const int sl = KT / kWaves;
+  return sl == kRangeSL<BF>[0] || sl == kRangeSL<BF>[1] || sl == kRangeSL<BF>[2] ? sl : 0;
+}
+
 // Closes unit j of the balanced path: this wave's slice sums go to LDS
 // slot j & 1, then (all slices present) the slices are added in order into
 // columns 32 j .. of F.  Every wave calls it once per unit, in unit order.
@@ -577,8 +596,8 @@ __device__ __forceinline__ void range_close(float* R, float* F, int fs, int j, i
 // scales): the epilogue of units [u0, u0 + nu) from their sums in F, or,
 // with k-splits, their partials and the fixup and epilogue of each pair
 // whose last split arrives in this workgroup.
-template <bool BF, int AM, int EPI>
-__device__ void range_finish(const GemmArgs& p, int M, float* F, int fs, int u0, int nu, const float* s_scale,
+template <bool BF, int AM, int EPI, bool COH>
+__device__ __forceinline__ void range_finish(const GemmArgs& p, int M, float* F, int fs, int u0, int nu, const float* s_scale,
                              int* s_flags) {
   constexpr int NTH = kWaves * 64;
   const int tid = threadIdx.x, KS = p.KS;
@@ -590,7 +609,7 @@ __device__ void range_finish(const GemmArgs& p, int M, float* F, int fs, int u0,
         for (int c = lane; c < C; c += 64) F[m * fs + c] *= s_scale[m];
       lds_sync();
     }
-    epilogue_rows<BF, EPI, false, NTH>(p, F, fs, u0, nu, 0, M);
+    epilogue_rows<BF, EPI, COH, NTH>(p, F, fs, u0, nu, 0, M);
     return;
   }
   for (int e = tid; e < M * C; e += NTH) {
@@ -613,13 +632,14 @@ __device__ void range_finish(const GemmArgs& p, int M, float* F, int fs, int u0,
     const int pair = (u0 + j) / KS;
     fixup_rows<AM, NTH>(p, M, pair * kPairCols, kPairCols, 0, M, s_scale, F + j * kPairCols, fs);
     lds_sync();
-    epilogue_rows<BF, EPI, false, NTH>(p, F + j * kPairCols, fs, pair, 1, 0, M);
+    epilogue_rows<BF, EPI, COH, NTH>(p, F + j * kPairCols, fs, pair, 1, 0, M);
     lds_sync();
   }
 }
 
-template <bool BF, int MT, int P, int AM, int EPI>
-__device__ void gemm_range_direct(const GemmArgs& p, int M, unsigned char* smem, float* s_scale, int* s_flags) {
+template <bool BF, int MT, int P, int AM, int EPI, bool COH, class Wait>
+__device__ __forceinline__ void gemm_range_direct(const GemmArgs& p, int M, unsigned char* smem, float* s_scale, int* s_flags,
+                                  Wait&& wait) {
   constexpr int QS = MT * 512;                       // floats of one wave's slice
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -658,16 +678,22 @@ __device__ void gemm_range_direct(const GemmArgs& p, int M, unsigned char* smem,
   const long long lo = p.a_plane / ET<BF>::PER16;   // lo plane, in 16-byte units
   // one k-step: the pair's two weight tiles, then the row tiles' fragments
   // (lanes of rows >= M read row 0 of their tile: no branch, exact waits)
-  auto load = [&](const Cur& c, uint4(&bb)[2], AFrag(&af)[MT]) {
+  auto loadW = [&](const Cur& c, uint4(&bb)[2]) {
     const uint4* w = p.W + ((size_t)c.pair * KT + c.kt) * 128 + lane;
     bb[0] = ldw(w);
     bb[1] = ldw(w + 64);
+  };
+  auto loadA = [&](const Cur& c, AFrag(&af)[MT]) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const uint4* a = ap[mt] + ((size_t)mt * KT + c.kt) * 64;
-      af[mt].h = *a;
-      if constexpr (BF) af[mt].l = a[lo];
+      af[mt].h = ldg(a);
+      if constexpr (BF) af[mt].l = ldg(a + lo);
     }
+  };
+  auto load = [&](const Cur& c, uint4(&bb)[2], AFrag(&af)[MT]) {
+    loadW(c, bb);
+    loadA(c, af);
   };
   // the load cursor steps through the units; past the last k-step it
   // re-reads that k-step, so every round issues the same loads
@@ -690,10 +716,21 @@ __device__ void gemm_range_direct(const GemmArgs& p, int M, unsigned char* smem,
   Cur cl;
   set_unit(cl, 0);
   int rem = cl.end - cl.kt;                           // k-steps left in the unit being summed
+  // the first round: weights first, then (after `wait()`, which the
+  // persistent kernel uses to wait for the producer of A) the activations
+  {
+    Cur ca = cl;
 #pragma unroll
-  for (int u = 0; u < P; ++u) {
-    load(cl, bw[u], af[u]);
-    advance(cl);
+    for (int u = 0; u < P; ++u) {
+      loadW(cl, bw[u]);
+      advance(cl);
+    }
+    wait();
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      loadA(ca, af[u]);
+      advance(ca);
+    }
   }
   constexpr int RPW = MT * 16 / kWaves;
   float rs[RPW];
@@ -724,15 +761,16 @@ __device__ void gemm_range_direct(const GemmArgs& p, int M, unsigned char* smem,
   }
   row_scale_finish<AM, RPW>(p, M, rs, s_scale);
   lds_sync();                                         // the last unit's sums are in F
-  range_finish<BF, AM, EPI>(p, M, F, fs, u0, nu, s_scale, s_flags);
+  range_finish<BF, AM, EPI, COH>(p, M, F, fs, u0, nu, s_scale, s_flags);
 }
 
 // The balanced path for KS = 1 and one row tile when every wave's slice
 // has SL = KT / kWaves k-steps: a wave's slice covers the same k-steps of
 // every pair, so its activation fragments are loaded once into registers
 // and only the weights stream.  Sums as in gemm_range_direct.
-template <bool BF, int P, int SL, int AM, int EPI>
-__device__ void gemm_range_direct_ra(const GemmArgs& p, int M, unsigned char* smem, float* s_scale, int* s_flags) {
+template <bool BF, int P, int SL, int AM, int EPI, bool COH, class Wait>
+__device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, unsigned char* smem, float* s_scale, int* s_flags,
+                                     Wait&& wait) {
   static_assert(SL % P == 0, "slice length must be a multiple of the prefetch depth");
   constexpr int QS = 512;
   const int lane = threadIdx.x & 63;
@@ -756,13 +794,14 @@ __device__ void gemm_range_direct_ra(const GemmArgs& p, int M, unsigned char* sm
   uint4 bw[P][2];
 #pragma unroll
   for (int u = 0; u < P; ++u) loadW(0, u, bw[u]);
+  wait();   // the persistent kernel waits here for the producer of A
   const uint4* ap = static_cast<const uint4*>(p.A) + frag_lane_unit_clamped(lane, M) + (size_t)kt0 * 64;
   const long long lo = p.a_plane / ET<BF>::PER16;
   AFrag af[SL];
 #pragma unroll
   for (int s = 0; s < SL; ++s) {
-    af[s].h = ap[(size_t)s * 64];
-    if constexpr (BF) af[s].l = ap[(size_t)s * 64 + lo];
+    af[s].h = ldg(ap + (size_t)s * 64);
+    if constexpr (BF) af[s].l = ldg(ap + (size_t)s * 64 + lo);
   }
   float rs[16 / kWaves];
   row_scale_loads<AM, 16 / kWaves>(p, M, rs);
@@ -780,7 +819,7 @@ __device__ void gemm_range_direct_ra(const GemmArgs& p, int M, unsigned char* sm
   }
   row_scale_finish<AM, 16 / kWaves>(p, M, rs, s_scale);
   lds_sync();
-  range_finish<BF, AM, EPI>(p, M, F, fs, u0, nu, s_scale, s_flags);
+  range_finish<BF, AM, EPI, COH>(p, M, F, fs, u0, nu, s_scale, s_flags);
 }
 
 // Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
@@ -950,52 +989,69 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
 // forms the chunk's softmax statistics (max m, sum l of exp(s - m)) and
 // each lane the unnormalised output sum_j exp(s_j - m) v_j of its
 // dimensions.  A row's chunks are combined in ascending order by
-// attn_merge_row.  256 threads; smem: attn_lds_bytes(D).
+// attn_merge_row.  Both sums run in ascending order as single fused
+// multiply-adds; their operands are read from LDS first, so a row costs a
+// few LDS round trips rather than one per key.  256 threads; smem:
+// attn_lds_bytes(D).
 
 template <int D> __host__ __device__ constexpr int attn_lds_bytes() {
   return (2 * kAttnChunk * (D + 1) + 4 * D + 4 * kAttnChunk) * 4;
 }
 
-template <int D, bool COH>
-__device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem, int r_lo = 0,
-                                int r_hi = -1) {
+// The chunk's keys and values in registers: thread x holds float4 number
+// t * 256 + x of each (row-major [key][D]); elements past the request's
+// keys hold unused values.
+template <int D> struct AttnKV {
+  static constexpr int V4 = kAttnChunk * D / 4 / 256;
+  float4 k[V4], v[V4];
+};
+
+template <int D>
+__device__ __forceinline__ void attn_load_kv(const AttnArgs& p, int c, int h, const ReqDesc& rq, AttnKV<D>& r) {
+  constexpr int C = kAttnChunk;
+  const int key0 = c * C;
+  const int nk = min(C, rq.L0 + rq.W - key0);
+  const int g = h * p.n_kv / p.n_q;
+  const float* kb = p.k_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
+  const float* vb = p.v_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
+  // elements past the request's keys read the last key's instead (in the
+  // slot; unused): no branch around the loads, so the waits stay exact
+#pragma unroll
+  for (int t = 0; t < AttnKV<D>::V4; ++t) {
+    const int f = min((t * 256 + (int)threadIdx.x) * 4, nk * D - 4);   // element index in the chunk
+    r.k[t] = ldg(reinterpret_cast<const float4*>(kb + f));
+    r.v[t] = ldg(reinterpret_cast<const float4*>(vb + f));
+  }
+}
+
+// The tile from keys and values already in registers; `pre` runs once the
+// registers are in LDS and the first query is requested (the persistent
+// kernel loads the next tile's keys and values there).
+// Rows [r_lo, r_hi) of the request (all by default), r_hi - r_lo <= 4 RPW
+// (checked by the callers' hosts).
+template <int D, bool COH, int RPW, class Pre>
+__device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem,
+                                             const AttnKV<D>& r, Pre&& pre, int r_lo = 0, int r_hi = -1) {
   constexpr int C = kAttnChunk;
   constexpr int RS = D + 1;                   // odd LDS row stride (floats)
-  constexpr int V4 = C * D / 4 / 256;         // float4 loads per thread per matrix
   constexpr int QL = D / 64;                  // query elements per lane
+  constexpr int DH = D / 2;                   // dot-product elements per lane
   float* Ks = reinterpret_cast<float*>(smem);
   float* Vs = Ks + C * RS;
   float* qs = Vs + C * RS;
   float* ps = qs + 4 * D;
 
-  const int nkeys = rq.L0 + rq.W;
   const int key0 = c * C;
-  const int nk = min(C, nkeys - key0);
-  const int g = h * p.n_kv / p.n_q;
+  const int nk = min(C, rq.L0 + rq.W - key0);
   const int qcols = p.n_q * D;
-  const float* kb = p.k_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
-  const float* vb = p.v_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
-  {
-    float4 kv[V4], vv[V4];
 #pragma unroll
-    for (int t = 0; t < V4; ++t) {
-      const int f = (t * 256 + threadIdx.x) * 4;   // element index in the chunk
-      if (f < nk * D) {
-        kv[t] = *reinterpret_cast<const float4*>(kb + f);
-        vv[t] = *reinterpret_cast<const float4*>(vb + f);
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < V4; ++t) {
-      const int f = (t * 256 + threadIdx.x) * 4;
-      if (f < nk * D) {
-        const int j = f / D, dd = f - j * D;
-        float* kd = Ks + j * RS + dd;
-        float* vd = Vs + j * RS + dd;
-        kd[0] = kv[t].x; kd[1] = kv[t].y; kd[2] = kv[t].z; kd[3] = kv[t].w;
-        vd[0] = vv[t].x; vd[1] = vv[t].y; vd[2] = vv[t].z; vd[3] = vv[t].w;
-      }
-    }
+  for (int t = 0; t < AttnKV<D>::V4; ++t) {   // rows >= nk: unused values
+    const int f = (t * 256 + threadIdx.x) * 4;
+    const int j = f / D, dd = f - j * D;
+    float* kd = Ks + j * RS + dd;
+    float* vd = Vs + j * RS + dd;
+    kd[0] = r.k[t].x; kd[1] = r.k[t].y; kd[2] = r.k[t].z; kd[3] = r.k[t].w;
+    vd[0] = r.v[t].x; vd[1] = r.v[t].y; vd[2] = r.v[t].z; vd[3] = r.v[t].w;
   }
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -1007,29 +1063,47 @@ __device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& 
   if (r_hi < 0) r_hi = rq.W;
   int i = r_lo + wave;
   while (i < r_hi && rq.L0 + i < key0) i += 4;
-  float qn[QL];
-  if (i < r_hi) {
+  // the queries of all this wave's rows (at most RPW) are loaded first, so
+  // no load follows a store and the row loop never waits for its stores;
+  // row min(ii, r_hi - 1) keeps the loads free of branches (rows past the
+  // end are loaded, never used)
+  auto qrow = [&](int ii) { return p.q + (size_t)(rq.row_start + min(ii, r_hi - 1)) * qcols + h * D + lane; };
+  float qa[RPW][QL];
 #pragma unroll
-    for (int t = 0; t < QL; ++t) qn[t] = p.q[(size_t)(rq.row_start + i) * qcols + h * D + t * 64 + lane];
-  }
+  for (int k = 0; k < RPW; ++k)
+#pragma unroll
+    for (int t = 0; t < QL; ++t) qa[k][t] = ldg(qrow(i + 4 * k) + t * 64);
+  pre();
   __syncthreads();
-  for (; i < r_hi; i += 4) {
-    const int pos = rq.L0 + i;
-    const int row = rq.row_start + i;
 #pragma unroll
-    for (int t = 0; t < QL; ++t) qw[t * 64 + lane] = qn[t];
-    if (i + 4 < r_hi) {
+  for (int k = 0; k < RPW; ++k) {
+    if (i + 4 * k >= r_hi) break;
+    const int pos = rq.L0 + i + 4 * k;
+    const int row = rq.row_start + i + 4 * k;
 #pragma unroll
-      for (int t = 0; t < QL; ++t) qn[t] = p.q[(size_t)(row + 4) * qcols + h * D + t * 64 + lane];
-    }
+    for (int t = 0; t < QL; ++t) qw[t * 64 + lane] = qa[k][t];
     __builtin_amdgcn_wave_barrier();
     const bool valid = j < nk && key0 + j <= pos;
     float a = 0.0f;
     if (j < nk) {
-      const float* kr = Ks + j * RS + half * (D / 2);
-      const float* qh = qw + half * (D / 2);
-#pragma unroll 8
-      for (int dd = 0; dd < D / 2; ++dd) a += qh[dd] * kr[dd];
+      // in blocks of 32 elements: each block's operands are read, then
+      // its multiply-adds run in order
+      constexpr int B = 32;
+#pragma unroll
+      for (int b0 = 0; b0 < DH; b0 += B) {
+        const float* kr = Ks + j * RS + half * DH + b0;
+        const float4* qh = reinterpret_cast<const float4*>(qw + half * DH + b0);
+        float kk[B], qq[B];
+#pragma unroll
+        for (int d4 = 0; d4 < B / 4; ++d4) {
+          const float4 q4 = qh[d4];
+          qq[4 * d4] = q4.x; qq[4 * d4 + 1] = q4.y; qq[4 * d4 + 2] = q4.z; qq[4 * d4 + 3] = q4.w;
+        }
+#pragma unroll
+        for (int dd = 0; dd < B; ++dd) kk[dd] = kr[dd];
+#pragma unroll
+        for (int dd = 0; dd < B; ++dd) a = __builtin_fmaf(qq[dd], kk[dd], a);
+      }
     }
     a += __shfl_xor(a, 32);  // both halves: same sum (commutative)
     const float s = valid ? a * p.scale : -INFINITY;
@@ -1038,19 +1112,36 @@ __device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& 
     const float l = wave_sum(half == 0 ? pj : 0.0f);
     if (half == 0) pw[j] = pj;
     __builtin_amdgcn_wave_barrier();
+    float pv[C];
+#pragma unroll
+    for (int j4 = 0; j4 < C / 4; ++j4) {
+      const float4 p4 = reinterpret_cast<const float4*>(pw)[j4];
+      pv[4 * j4] = p4.x; pv[4 * j4 + 1] = p4.y; pv[4 * j4 + 2] = p4.z; pv[4 * j4 + 3] = p4.w;
+    }
 #pragma unroll
     for (int t = 0; t < QL; ++t) {
       const int dd = t * 64 + lane;
+      float vv[C];
+#pragma unroll
+      for (int jj = 0; jj < C; ++jj) vv[jj] = Vs[jj * RS + dd];   // rows >= nk: read, never used
       float o = 0.0f;
-      for (int jj = 0; jj < nk; ++jj) o += pw[jj] * Vs[jj * RS + dd];
+#pragma unroll
+      for (int jj = 0; jj < C; ++jj) o = jj < nk ? __builtin_fmaf(pv[jj], vv[jj], o) : o;
       st<COH>(p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd, o);
     }
-    if (lane == 0) {
-      st<COH>(p.pml + (((size_t)c * kMaxRows + row) * p.n_q + h) * 2, mx);
-      st<COH>(p.pml + (((size_t)c * kMaxRows + row) * p.n_q + h) * 2 + 1, l);
-    }
+    // (m, l): every lane stores, even lanes m and odd lanes l, one store
+    // with no branch around it
+    st<COH>(p.pml + (((size_t)c * kMaxRows + row) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l : mx);
     __builtin_amdgcn_wave_barrier();
   }
+}
+
+template <int D, bool COH, int RPW>
+__device__ __forceinline__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem,
+                                                int r_lo = 0, int r_hi = -1) {
+  AttnKV<D> r;
+  attn_load_kv<D>(p, c, h, rq, r);
+  attn_tile_kv<D, COH, RPW>(p, c, h, rq, smem, r, [] {}, r_lo, r_hi);
 }
 
 // Merge of row `row`'s chunks for head h by D threads starting at thread t0:
@@ -1063,18 +1154,20 @@ __device__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& 
 // threads only join those syncs.
 
 template <bool BF, int D, bool COH, class Sync>
-__device__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float* sm, float* sl, Sync&& sync,
+__device__ __forceinline__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float* sm, float* sl, Sync&& sync,
                                bool valid = true) {
   constexpr int kB = 32;
   const int dd = threadIdx.x - t0;
-  const RowDesc rd = p.rows[row];
+  const RowDesc rd = load_invariant(p.rows + row);
   const int nc = valid ? rd.pos / kAttnChunk + 1 : 0;
-  auto ld = [](const float* q) { if constexpr (COH) return ld_coherent(q); else return *q; };
+  auto ld = [](const float* q) { if constexpr (COH) return ld_coherent(q); else return ldg(q); };
   auto acc_at = [&](int c) { return p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd; };
+  // loads past the row's chunks read its last chunk (unused): no branch
+  // around them, so the waits stay exact
+  const int cl = max(nc, 1) - 1;
   float v[kB];
 #pragma unroll
-  for (int b = 0; b < kB; ++b)
-    if (b < nc) v[b] = ld(acc_at(b));
+  for (int b = 0; b < kB; ++b) v[b] = ld(acc_at(min(b, cl)));
   for (int c = dd; c < nc; c += D) {
     const size_t o = ((size_t)c * kMaxRows + row) * p.n_q + h;
     sm[c] = ld(p.pml + o * 2);
@@ -1090,8 +1183,7 @@ __device__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float*
   for (int c0 = 0; c0 < nc; c0 += kB) {
     if (c0 > 0) {
 #pragma unroll
-      for (int b = 0; b < kB; ++b)
-        if (c0 + b < nc) v[b] = ld(acc_at(c0 + b));
+      for (int b = 0; b < kB; ++b) v[b] = ld(acc_at(min(c0 + b, cl)));
     }
 #pragma unroll
     for (int b = 0; b < kB; ++b)
@@ -1109,7 +1201,7 @@ __device__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float*
 // non-finite logit.  s4f / s4i: 4-entry LDS scratch.
 
 template <bool COH>
-__device__ void argmax_row(const float* amax_val, const int* amax_idx, int n_pairs, int row, int* tok,
+__device__ __forceinline__ void argmax_row(const float* amax_val, const int* amax_idx, int n_pairs, int row, int* tok,
                            int* bad, float* s4f, int* s4i) {
   constexpr int kPer = 8;   // pairs per thread, loads in flight together
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -1164,7 +1256,7 @@ __device__ void argmax_row(const float* amax_val, const int* amax_idx, int n_pai
 // token differs from its candidate (W-1 if none); the correction is the
 // greedy token of row `accepted`.
 template <class TokAt>
-__device__ StepOut verify_request(const RowDesc* rows, const ReqDesc& rq, TokAt&& tok_at, int bad) {
+__device__ __forceinline__ StepOut verify_request(const RowDesc* rows, const ReqDesc& rq, TokAt&& tok_at, int bad) {
   int a = 0;
   while (a < rq.W - 1 && rows[rq.row_start + a].cmp == tok_at(rq.row_start + a)) ++a;
   return StepOut{a, tok_at(rq.row_start + a), bad, 0};
