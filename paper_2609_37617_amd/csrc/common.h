@@ -175,17 +175,43 @@ __device__ __forceinline__ void lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Fixed-pattern wave reductions.  Every lane ends with the same bits (a
-// butterfly adds the same two values on both partner lanes).
+// Fixed-pattern wave reductions on cross-lane data movement that does not
+// go through LDS: DPP (pairs and quads, then mirrors of 8 and 16 lanes),
+// a swizzle across the 16-lane rows of each half and, for the whole wave,
+// the two halves read into scalar registers.  Each step adds the same two
+// values on both partner lanes, so every lane (of the half, or of the
+// wave) ends with the same bits.
+template <int CTRL> __device__ __forceinline__ float dpp_get(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // lane i of 8 <- lane 7 - i
+constexpr int kDppMirror = 0x140;      // lane i of 16 <- lane 15 - i
+__device__ __forceinline__ float swizzle_xor16(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+template <class Op> __device__ __forceinline__ float half_reduce(float v, Op op) {
+  v = op(v, dpp_get<kDppXor1>(v));
+  v = op(v, dpp_get<kDppXor2>(v));
+  v = op(v, dpp_get<kDppHalfMirror>(v));
+  v = op(v, dpp_get<kDppMirror>(v));
+  return op(v, swizzle_xor16(v));
+}
+__device__ __forceinline__ float lane_value(float v, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+// Sum / max over each half-wave (lanes 0-31 and 32-63 separately).
+__device__ __forceinline__ float half_sum(float v) {
+  return half_reduce(v, [](float a, float b) { return a + b; });
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v = half_sum(v);
+  return lane_value(v, 0) + lane_value(v, 32);
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = half_reduce(v, [](float a, float b) { return fmaxf(a, b); });
+  return fmaxf(lane_value(v, 0), lane_value(v, 32));
 }
 // (value, index) arg-max: larger value wins, equal values keep the lower index.
 __device__ __forceinline__ void wave_argmax(float& v, int& i) {
@@ -197,11 +223,6 @@ __device__ __forceinline__ void wave_argmax(float& v, int& i) {
   }
 }
 // The same over each half-wave (lanes 0-31 and 32-63 separately).
-__device__ __forceinline__ float half_sum(float v) {
-#pragma unroll
-  for (int o = 16; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
 __device__ __forceinline__ void half_argmax(float& v, int& i) {
 #pragma unroll
   for (int o = 16; o > 0; o >>= 1) {

@@ -130,43 +130,50 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
     gemm_phase<BF, MT, SL, A_NORM, EPI_QKV>(load_invariant(&ly->qkv), M, prev, prev_target, &a.phase_cnt[ph_layer(l, 0)], a, smem,
                                              s_scale, s_flags);
 
-    // attention chunks; the next tile's keys and values are requested
-    // while the current tile's rows run
+    // attention chunks
     stamp(a, ph_layer(l, 1), 0);
+    // tile t: request, head and chunk
+    auto tile_of = [&](int t, ReqDesc& rq, int& h, int& c) {
+      int r = 0, u = t;
+      for (;; ++r) {
+        rq = load_invariant(a.reqs + r);
+        const int n = a.n_q * ((rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk);
+        if (u < n || r == a.n_reqs - 1) break;
+        u -= n;
+      }
+      const int nch = (rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk;
+      h = u / nch;
+      c = u - h * nch;
+    };
     if ((int)blockIdx.x < n_chunk_tiles) {
+      // one tile per workgroup; the next tile's keys and values are
+      // requested while the current tile's rows run
       wait_count(&a.phase_cnt[ph_layer(l, 0)], a.done_qkv, a.err, a.spin_limit);
       stamp(a, ph_layer(l, 1), 1);
       const AttnArgs at = load_invariant(&ly->attn);
-      // tile t: request, head and chunk
-      auto tile_of = [&](int t, ReqDesc& rq, int& h, int& c) {
-        int r = 0, u = t;
-        for (;; ++r) {
-          rq = load_invariant(a.reqs + r);
-          const int n = a.n_q * ((rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk);
-          if (u < n || r == a.n_reqs - 1) break;
-          u -= n;
-        }
-        const int nch = (rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk;
-        h = u / nch;
-        c = u - h * nch;
-      };
       ReqDesc rq, rq2;
       int h, c, h2 = 0, c2 = 0;
       tile_of(blockIdx.x, rq, h, c);
       AttnKV<D> cur, nxt;
       attn_load_kv<D>(at, c, h, rq, cur);
+      int mine = 0;
       for (int t = blockIdx.x; t < n_chunk_tiles; t += G) {
         const bool more = t + G < n_chunk_tiles;
         if (more) tile_of(t + G, rq2, h2, c2);
         attn_tile_kv<D, true, kStepRows / 4>(at, c, h, rq, smem, cur, [&] {
           if (more) attn_load_kv<D>(at, c2, h2, rq2, nxt);
         });
-        signal_done(&a.phase_cnt[ph_layer(l, 1)]);
+        lds_sync();   // the next tile overwrites the chunk in LDS
+        ++mine;
         cur = nxt;
         rq = rq2;
         h = h2;
         c = c2;
       }
+      // one signal for all this workgroup's tiles, once their stores are done
+      wait_vmem();
+      __syncthreads();
+      if (tid == 0) counter_add(&a.phase_cnt[ph_layer(l, 1)], mine);
     }
     stamp(a, ph_layer(l, 1), 2);
 

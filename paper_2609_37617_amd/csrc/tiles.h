@@ -1024,6 +1024,69 @@ __device__ __forceinline__ void attn_load_kv(const AttnArgs& p, int c, int h, co
   }
 }
 
+// One row of a chunk tile, by one wave: the query is in qw (LDS, D
+// floats), the chunk's keys and values in Ks / Vs (row stride D + 1), pw is
+// C floats of LDS scratch; stores the row's partial output and (m, l).
+template <int D, bool COH>
+__device__ __forceinline__ void attn_row(const AttnArgs& p, int c, int h, int key0, int nk, int pos, int row,
+                                         const float* Ks, const float* Vs, const float* qw, float* pw) {
+  constexpr int C = kAttnChunk;
+  constexpr int RS = D + 1;
+  constexpr int QL = D / 64;
+  constexpr int DH = D / 2;
+  const int lane = threadIdx.x & 63;
+  const int j = lane & (C - 1), half = lane >> 5;
+  const bool valid = j < nk && key0 + j <= pos;
+  float a = 0.0f;
+  if (j < nk) {
+    // in blocks of 32 elements: each block's operands are read, then
+    // its multiply-adds run in order
+    constexpr int B = 32;
+#pragma unroll
+    for (int b0 = 0; b0 < DH; b0 += B) {
+      const float* kr = Ks + j * RS + half * DH + b0;
+      const float4* qh = reinterpret_cast<const float4*>(qw + half * DH + b0);
+      float kk[B], qq[B];
+#pragma unroll
+      for (int d4 = 0; d4 < B / 4; ++d4) {
+        const float4 q4 = qh[d4];
+        qq[4 * d4] = q4.x; qq[4 * d4 + 1] = q4.y; qq[4 * d4 + 2] = q4.z; qq[4 * d4 + 3] = q4.w;
+      }
+#pragma unroll
+      for (int dd = 0; dd < B; ++dd) kk[dd] = kr[dd];
+#pragma unroll
+      for (int dd = 0; dd < B; ++dd) a = __builtin_fmaf(qq[dd], kk[dd], a);
+    }
+  }
+  a += __shfl_xor(a, 32);  // both halves: same sum (commutative)
+  const float s = valid ? a * p.scale : -INFINITY;
+  const float mx = wave_max(s);
+  const float pj = valid ? expf(s - mx) : 0.0f;
+  const float l = wave_sum(half == 0 ? pj : 0.0f);
+  if (half == 0) pw[j] = pj;
+  __builtin_amdgcn_wave_barrier();
+  float pv[C];
+#pragma unroll
+  for (int j4 = 0; j4 < C / 4; ++j4) {
+    const float4 p4 = reinterpret_cast<const float4*>(pw)[j4];
+    pv[4 * j4] = p4.x; pv[4 * j4 + 1] = p4.y; pv[4 * j4 + 2] = p4.z; pv[4 * j4 + 3] = p4.w;
+  }
+#pragma unroll
+  for (int t = 0; t < QL; ++t) {
+    const int dd = t * 64 + lane;
+    float vv[C];
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) vv[jj] = Vs[jj * RS + dd];   // rows >= nk: read, never used
+    float o = 0.0f;
+#pragma unroll
+    for (int jj = 0; jj < C; ++jj) o = jj < nk ? __builtin_fmaf(pv[jj], vv[jj], o) : o;
+    st<COH>(p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd, o);
+  }
+  // (m, l): every lane stores, even lanes m and odd lanes l, one store
+  // with no branch around it
+  st<COH>(p.pml + (((size_t)c * kMaxRows + row) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l : mx);
+}
+
 // The tile from keys and values already in registers; `pre` runs once the
 // registers are in LDS and the first query is requested (the persistent
 // kernel loads the next tile's keys and values there).
@@ -1035,7 +1098,6 @@ __device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, co
   constexpr int C = kAttnChunk;
   constexpr int RS = D + 1;                   // odd LDS row stride (floats)
   constexpr int QL = D / 64;                  // query elements per lane
-  constexpr int DH = D / 2;                   // dot-product elements per lane
   float* Ks = reinterpret_cast<float*>(smem);
   float* Vs = Ks + C * RS;
   float* qs = Vs + C * RS;
@@ -1055,7 +1117,6 @@ __device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, co
   }
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int j = lane & (C - 1), half = lane >> 5;
   float* qw = qs + wave * D;
   float* pw = ps + wave * C;
   // rows [r_lo, r_hi) of the request (all by default); the first row of
@@ -1083,55 +1144,7 @@ __device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, co
 #pragma unroll
     for (int t = 0; t < QL; ++t) qw[t * 64 + lane] = qa[k][t];
     __builtin_amdgcn_wave_barrier();
-    const bool valid = j < nk && key0 + j <= pos;
-    float a = 0.0f;
-    if (j < nk) {
-      // in blocks of 32 elements: each block's operands are read, then
-      // its multiply-adds run in order
-      constexpr int B = 32;
-#pragma unroll
-      for (int b0 = 0; b0 < DH; b0 += B) {
-        const float* kr = Ks + j * RS + half * DH + b0;
-        const float4* qh = reinterpret_cast<const float4*>(qw + half * DH + b0);
-        float kk[B], qq[B];
-#pragma unroll
-        for (int d4 = 0; d4 < B / 4; ++d4) {
-          const float4 q4 = qh[d4];
-          qq[4 * d4] = q4.x; qq[4 * d4 + 1] = q4.y; qq[4 * d4 + 2] = q4.z; qq[4 * d4 + 3] = q4.w;
-        }
-#pragma unroll
-        for (int dd = 0; dd < B; ++dd) kk[dd] = kr[dd];
-#pragma unroll
-        for (int dd = 0; dd < B; ++dd) a = __builtin_fmaf(qq[dd], kk[dd], a);
-      }
-    }
-    a += __shfl_xor(a, 32);  // both halves: same sum (commutative)
-    const float s = valid ? a * p.scale : -INFINITY;
-    const float mx = wave_max(s);
-    const float pj = valid ? expf(s - mx) : 0.0f;
-    const float l = wave_sum(half == 0 ? pj : 0.0f);
-    if (half == 0) pw[j] = pj;
-    __builtin_amdgcn_wave_barrier();
-    float pv[C];
-#pragma unroll
-    for (int j4 = 0; j4 < C / 4; ++j4) {
-      const float4 p4 = reinterpret_cast<const float4*>(pw)[j4];
-      pv[4 * j4] = p4.x; pv[4 * j4 + 1] = p4.y; pv[4 * j4 + 2] = p4.z; pv[4 * j4 + 3] = p4.w;
-    }
-#pragma unroll
-    for (int t = 0; t < QL; ++t) {
-      const int dd = t * 64 + lane;
-      float vv[C];
-#pragma unroll
-      for (int jj = 0; jj < C; ++jj) vv[jj] = Vs[jj * RS + dd];   // rows >= nk: read, never used
-      float o = 0.0f;
-#pragma unroll
-      for (int jj = 0; jj < C; ++jj) o = jj < nk ? __builtin_fmaf(pv[jj], vv[jj], o) : o;
-      st<COH>(p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd, o);
-    }
-    // (m, l): every lane stores, even lanes m and odd lanes l, one store
-    // with no branch around it
-    st<COH>(p.pml + (((size_t)c * kMaxRows + row) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l : mx);
+    attn_row<D, COH>(p, c, h, key0, nk, pos, row, Ks, Vs, qw, pw);
     __builtin_amdgcn_wave_barrier();
   }
 }
