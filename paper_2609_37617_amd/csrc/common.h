@@ -233,10 +233,9 @@ __device__ __forceinline__ void half_argmax(float& v, int& i) {
 }
 
 // GEMM tile constants
-constexpr int kPrefetch = 4;       // k-steps of weights in flight per wave (A staged in LDS)
 constexpr int kPrefetchDirect = 4; // k-steps of weights and A in flight per wave (A direct)
 constexpr int kFStride = 132;      // floats per row of the staged path's epilogue tile
 constexpr int kFRows = 64;         // rows per epilogue pass of the staged path
-constexpr int kLdsBudget = 61440;  // bytes of A staging
+constexpr int kStagedLds = 147456; // bytes of A staging (two buffers), staged path
 
 }  // namespace as2d

@@ -175,15 +175,16 @@ static hipError_t launch_range(const GemmArgs& a, hipStream_t s) {
 
 // Staged path: block b = (pair group, split, row group), the row group
 // fastest; RG row groups of MT row tiles each (RG = 1: all the pass's rows).
+// Three row tiles (the row groups of narrow matrices) fit two workgroups
+// per compute unit; more rows need the whole register file.
 template <bool BF, int MT, int AM, int EPI>
-__global__ __launch_bounds__(256) void gemm_staged_kernel(const GemmArgs p, const int chunk_kt, const int RG) {
+__global__ __launch_bounds__(256, MT == 3 ? 2 : 1) void gemm_staged_kernel(const GemmArgs p, const int RG) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;
   const int rg = blockIdx.x % RG, t = blockIdx.x / RG;
   const int group = t / p.KS, split = t - group * p.KS;
-  gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, chunk_kt, rg * MT,
-                                          group * RG + rg);
+  gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, rg * MT, group * RG + rg);
 }
 
 // Row tiles per row group when a staged GEMM would otherwise leave compute
@@ -208,21 +209,19 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   }
   if (pairs % kPairsS) return hipErrorInvalidValue;
   const int base = (pairs / kPairsS) * a.KS;
-  const int lds = gemm_staged_lds_bytes();
   // narrow matrices: row groups of kStagedGroupMT tiles (at most 3 groups,
   // so the counters, one per pair, cover group * RG + rg)
   if (base < 256 && a.MT > kStagedGroupMT) {
     const int RG = (a.MT + kStagedGroupMT - 1) / kStagedGroupMT;
     if (RG > kPairsS) return hipErrorInvalidValue;
-    gemm_staged_kernel<BF, kStagedGroupMT, AM, EPI><<<base * RG, 256, lds, s>>>(
-        a, staged_chunk(BF, kStagedGroupMT), RG);
+    gemm_staged_kernel<BF, kStagedGroupMT, AM, EPI>
+        <<<base * RG, 256, gemm_staged_lds_bytes<BF, kStagedGroupMT>(), s>>>(a, RG);
     return hipGetLastError();
   }
-  const int chunk = staged_chunk(BF, a.MT);
   const dim3 grid(base), block(256);
   switch (a.MT) {
 #define AS2D_MT(mt) \
-  case mt: gemm_staged_kernel<BF, mt, AM, EPI><<<grid, block, lds, s>>>(a, chunk, 1); break;
+  case mt: gemm_staged_kernel<BF, mt, AM, EPI><<<grid, block, gemm_staged_lds_bytes<BF, mt>(), s>>>(a, 1); break;
     AS2D_MT(3) AS2D_MT(4) AS2D_MT(5) AS2D_MT(6) AS2D_MT(7) AS2D_MT(8) AS2D_MT(9)
 #undef AS2D_MT
     default: return hipErrorInvalidValue;
@@ -298,10 +297,24 @@ static hipError_t prepare_range() {
   return e;
 }
 
+template <bool BF, int AM, int EPI>
+static hipError_t prepare_staged() {
+  hipError_t e = hipSuccess;
+  auto allow = [&](const void* k, int bytes) {
+    if (e == hipSuccess) e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  };
+#define AS2D_S(mt) \
+  allow(reinterpret_cast<const void*>(&gemm_staged_kernel<BF, mt, AM, EPI>), gemm_staged_lds_bytes<BF, mt>());
+  AS2D_S(3) AS2D_S(4) AS2D_S(5) AS2D_S(6) AS2D_S(7) AS2D_S(8) AS2D_S(9)
+#undef AS2D_S
+  return e;
+}
+
 hipError_t prepare_kernels() {
   hipError_t e = prepare_step_kernels();
 #define AS2D_P(bf, am, ep) \
-  if (e == hipSuccess) e = prepare_range<bf, am, ep>();
+  if (e == hipSuccess) e = prepare_range<bf, am, ep>(); \
+  if (e == hipSuccess) e = prepare_staged<bf, am, ep>();
   AS2D_P(true, A_NORM, EPI_QKV) AS2D_P(true, A_PLAIN, EPI_RESID) AS2D_P(true, A_NORM, EPI_SWIGLU)
   AS2D_P(true, A_NORM, EPI_ARGMAX)
   AS2D_P(false, A_NORM, EPI_QKV) AS2D_P(false, A_PLAIN, EPI_RESID) AS2D_P(false, A_NORM, EPI_SWIGLU)

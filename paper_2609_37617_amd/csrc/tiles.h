@@ -824,23 +824,33 @@ __device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, u
 
 // Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
 // tile pairs (one per wave) of one split, for row tiles [mt0, mt0 + MT);
-// the activation fragments of `chunk_kt` k-steps at a time are staged in
-// LDS and shared by the waves, each wave keeps its slices apart in
-// registers (running sum S).  Row groups (mt0 > 0) let narrow matrices use
+// each wave keeps its slices apart in registers (running sum S).  The
+// split's slices are cut into chunks of at most CK k-steps; a chunk's
+// activation fragments are staged in LDS and shared by the waves, its
+// weights held in registers.  Two LDS buffers: the next chunk's weights
+// and activation fragments are requested before the current chunk is
+// summed and written to the other buffer after it, so memory latency
+// overlaps the MFMA work.  Row groups (mt0 > 0) let narrow matrices use
 // more workgroups; `cnt` is the split counter of this (pairs, rows) tile
 // (default: the pair group).
-//   smem: dynamic LDS of gemm_staged_lds_bytes(); chunk_kt from
-//   staged_chunk().
+//   smem: dynamic LDS of gemm_staged_lds_bytes<BF, MT>().
 
-__host__ __device__ constexpr int gemm_staged_lds_bytes() {
-  return kLdsBudget > kFRows * kFStride * 4 ? kLdsBudget : kFRows * kFStride * 4;
+template <bool BF, int MT> __host__ __device__ constexpr int staged_ck() {
+  constexpr int per = 2 * (BF ? 2 : 1) * MT * 1024;   // both buffers, one k-step
+  return kStagedLds / per > 4 ? 4 : kStagedLds / per;
 }
-__host__ __device__ inline int staged_chunk(bool bf16, int MT) { return kLdsBudget / ((bf16 ? 2 : 1) * MT * 1024); }
+template <bool BF, int MT> __host__ __device__ constexpr int gemm_staged_lds_bytes() {
+  constexpr int a = 2 * (BF ? 2 : 1) * MT * staged_ck<BF, MT>() * 1024, f = kFRows * kFStride * 4;
+  return a > f ? a : f;
+}
 
 template <bool BF, int MT, int AM, int EPI, bool COH>
 __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split, unsigned char* smem,
-                                 float* s_scale, int* s_flag, int chunk_kt, int mt0 = 0, int cnt = -1) {
+                                 float* s_scale, int* s_flag, int mt0 = 0, int cnt = -1) {
   constexpr int kRegions = BF ? 2 : 1;
+  constexpr int CK = staged_ck<BF, MT>();
+  constexpr int BUF = kRegions * MT * CK * 64;     // 16-byte elements per buffer
+  constexpr int NV = (BUF + 255) / 256;            // of which each thread stages at most NV
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int pair = group * kPairsS + wave;
   const int kt0 = split * p.ktps;
@@ -848,78 +858,119 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   const uint4* wp = p.W + (size_t)pair * p.KT * 128 + lane;
   const uint4* ag = static_cast<const uint4*>(p.A);
   const long long lo = p.a_plane / ET<BF>::PER16;
-  uint4* la = reinterpret_cast<uint4*>(smem);     // [region][mt][k-step of chunk][64]
-  const int region = MT * chunk_kt * 64;
-  const int lu = frag_lane_unit(lane);
-  f4 S[MT][2], acc[MT][2];
-  bool first_chunk = true;
-  for (int q = 0; q < p.ns; ++q) {
-    const int qa = slice_start(kt0, n_all, q, p.ns), qb = slice_start(kt0, n_all, q + 1, p.ns);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      acc[mt][0] = f4{0.f, 0.f, 0.f, 0.f};
-      acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
+  uint4* la = reinterpret_cast<uint4*>(smem);     // [buffer][region][mt][k-step of chunk][lane]
+
+  // chunk (slice q, first k-step c0, n k-steps); q == ns: past the end
+  struct Chunk {
+    int q, c0, n;
+  };
+  auto first_of = [&](int q) {
+    Chunk c;
+    c.q = q;
+    c.c0 = slice_start(kt0, n_all, q, p.ns);
+    c.n = min(slice_start(kt0, n_all, q + 1, p.ns) - c.c0, CK);
+    return c;
+  };
+  auto next_of = [&](const Chunk& c) {
+    const int qb = slice_start(kt0, n_all, c.q + 1, p.ns);
+    if (c.c0 + c.n < qb) {
+      Chunk d = c;
+      d.c0 += c.n;
+      d.n = min(qb - d.c0, CK);
+      return d;
     }
-    for (int c0 = qa; c0 < qb; c0 += chunk_kt) {
-      const int n = min(qb, c0 + chunk_kt) - c0;
-      if (!first_chunk) lds_sync();
-      first_chunk = false;
-      // stage: region rg, tile mt, k-step r of the chunk = one 1 KiB fragment block
-      for (int u = tid; u < kRegions * MT * n * 64; u += 256) {
-        const int l = u & 63, blk = u >> 6;
-        const int rg = blk / (MT * n), r2 = blk - rg * (MT * n);
-        const int mt = r2 / n, r = r2 - mt * n;
-        la[rg * region + (mt * chunk_kt + r) * 64 + l] = ag[rg * lo + ((size_t)(mt0 + mt) * p.KT + c0 + r) * 64 + l];
-      }
-      uint4 b[kPrefetch][2];
+    return first_of(c.q + 1);
+  };
+  // element u of chunk d's staging: block (region, tile, k-step) u / 64,
+  // position u % 64 of the block in LDS, which holds the 16-byte unit lane
+  // u % 64 feeds to the MFMA (frag_lane_unit): the waves then read their
+  // fragments as 64 consecutive units, free of bank conflicts (read in
+  // fragment order, lanes 64 bytes apart, four of eight lanes met in one
+  // bank); returns its source and sets its place in a buffer
+  auto elem = [&](const Chunk& d, int u, int& dst) {
+    const int pos = u & 63, b = u >> 6;
+    const int rg = b / (MT * d.n), r2 = b - rg * (MT * d.n);
+    const int mt = r2 / d.n, r = r2 - mt * d.n;
+    dst = ((rg * MT + mt) * CK + r) * 64 + pos;
+    return ag + rg * lo + ((size_t)(mt0 + mt) * p.KT + d.c0 + r) * 64 + frag_lane_unit(pos);
+  };
+  // requests chunk d: CK k-steps of weights (past the chunk its last
+  // again, clamped to the matrix: unused) and this thread's NV staging
+  // elements (u = tid + 256 i; past the chunk's last element that one
+  // again: no branch around the loads, so they all stay in flight)
+  auto request = [&](const Chunk& d, uint4(&wb)[CK][2], uint4(&av)[NV], int(&ad)[NV]) {
 #pragma unroll
-      for (int u = 0; u < kPrefetch; ++u) {
-        const size_t kp = (size_t)(c0 + min(u, n - 1)) * 128;
-        b[u][0] = ldw(wp + kp);
-        b[u][1] = ldw(wp + kp + 64);
+    for (int r = 0; r < CK; ++r) {
+      const size_t kp = (size_t)min(d.c0 + min(r, max(d.n, 1) - 1), p.KT - 1) * 128;
+      wb[r][0] = ldw(wp + kp);
+      wb[r][1] = ldw(wp + kp + 64);
+    }
+    const int total = max(kRegions * MT * d.n * 64, 1);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) av[i] = ldg(elem(d, min((int)tid + 256 * i, total - 1), ad[i]));
+  };
+  auto stage = [&](const Chunk& d, uint4* buf, const uint4(&av)[NV], const int(&ad)[NV]) {
+    const int total = kRegions * MT * d.n * 64;
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if ((int)tid + 256 * i < total) buf[ad[i]] = av[i];
+  };
+
+  f4 S[MT][2], acc[MT][2];
+  uint4 w0[CK][2], w1[CK][2], av[NV];
+  int ad[NV];
+  // one chunk: request the next one (weights into wn, fragments into
+  // registers), sum this one from LDS buffer bi with weights wc, stage the
+  // next one into the other buffer; false after the last chunk
+  auto step = [&](Chunk& cur, int bi, const uint4(&wc)[CK][2], uint4(&wn)[CK][2]) {
+    const Chunk nxt = next_of(cur);
+    const bool more = nxt.q < p.ns;
+    // after the last chunk, the current one again (unused): the same loads
+    // on every path keep the compiler's waits exact
+    request(more ? nxt : cur, wn, av, ad);
+    if (cur.c0 == slice_start(kt0, n_all, cur.q, p.ns)) {   // a slice begins
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        acc[mt][0] = f4{0.f, 0.f, 0.f, 0.f};
+        acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
       }
-      lds_sync();
-      auto lds_step = [&](int ks, const uint4(&bb)[2]) {
+    }
+    const uint4* lb = la + bi * BUF;
+#pragma unroll
+    for (int ks = 0; ks < CK; ++ks) {
+      if (ks < cur.n) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           AFrag af;
-          af.h = la[(mt * chunk_kt + ks) * 64 + lu];
-          if constexpr (BF) af.l = la[region + (mt * chunk_kt + ks) * 64 + lu];
-          acc[mt][0] = mma_a<BF>(af, bb[0], acc[mt][0]);
-          acc[mt][1] = mma_a<BF>(af, bb[1], acc[mt][1]);
-        }
-      };
-      int i = 0;
-      for (; i + 2 * kPrefetch <= n; i += kPrefetch) {
-#pragma unroll
-        for (int u = 0; u < kPrefetch; ++u) {
-          lds_step(i + u, b[u]);
-          const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
-          b[u][0] = ldw(wp + kn);
-          b[u][1] = ldw(wp + kn + 64);
+          af.h = lb[(mt * CK + ks) * 64 + lane];
+          if constexpr (BF) af.l = lb[MT * CK * 64 + (mt * CK + ks) * 64 + lane];
+          acc[mt][0] = mma_a<BF>(af, wc[ks][0], acc[mt][0]);
+          acc[mt][1] = mma_a<BF>(af, wc[ks][1], acc[mt][1]);
         }
       }
-#pragma unroll
-      for (int u = 0; u < kPrefetch; ++u) {
-        if (i + u < n) {
-          lds_step(i + u, b[u]);
-          if (i + u + kPrefetch < n) {
-            const size_t kn = (size_t)(c0 + i + u + kPrefetch) * 128;
-            b[u][0] = ldw(wp + kn);
-            b[u][1] = ldw(wp + kn + 64);
-          }
-        }
-      }
-      i += kPrefetch;
-#pragma unroll
-      for (int u = 0; u < kPrefetch; ++u)
-        if (i + u < n) lds_step(i + u, b[u]);
     }
+    if (cur.c0 + cur.n == slice_start(kt0, n_all, cur.q + 1, p.ns)) {   // the slice ends
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) S[mt][j] = q == 0 ? acc[mt][j] : S[mt][j] + acc[mt][j];
+        for (int j = 0; j < 2; ++j) S[mt][j] = cur.q == 0 ? acc[mt][j] : S[mt][j] + acc[mt][j];
+    }
+    if (!more) return false;
+    // the other buffer was last read in the previous chunk, before the
+    // barrier that ended it
+    stage(nxt, la + (bi ^ 1) * BUF, av, ad);
+    lds_sync();
+    cur = nxt;
+    return true;
+  };
+  Chunk cur = first_of(0);
+  request(cur, w0, av, ad);
+  stage(cur, la, av, ad);
+  lds_sync();
+  // chunks alternate between buffers 0 and 1 and weight sets w0 and w1
+  while (step(cur, 0, w0, w1) && step(cur, 1, w1, w0)) {
   }
+  lds_sync();   // the A buffers are no longer read (F reuses the LDS)
 
   float* F = reinterpret_cast<float*>(smem);
   const int n0 = group * kPairsS * kPairCols, C = kPairsS * kPairCols;
