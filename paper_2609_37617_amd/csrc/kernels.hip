@@ -209,9 +209,11 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   }
   if (pairs % kPairsS) return hipErrorInvalidValue;
   const int base = (pairs / kPairsS) * a.KS;
-  // narrow matrices: row groups of kStagedGroupMT tiles (at most 3 groups,
-  // so the counters, one per pair, cover group * RG + rg)
-  if (base < 256 && a.MT > kStagedGroupMT) {
+  // matrices with fewer than two workgroups per compute unit: row groups of
+  // kStagedGroupMT tiles, so that the grid fills the chip in even rounds
+  // (at most 3 groups, so the counters, one per pair, cover group * RG + rg;
+  // each group reads the weights again, from L2 or the MALL)
+  if (base < 512 && a.MT > kStagedGroupMT) {
     const int RG = (a.MT + kStagedGroupMT - 1) / kStagedGroupMT;
     if (RG > kPairsS) return hipErrorInvalidValue;
     gemm_staged_kernel<BF, kStagedGroupMT, AM, EPI>
