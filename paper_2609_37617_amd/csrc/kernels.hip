@@ -175,10 +175,10 @@ static hipError_t launch_range(const GemmArgs& a, hipStream_t s) {
 
 // Staged path: block b = (pair group, split, row group), the row group
 // fastest; RG row groups of MT row tiles each (RG = 1: all the pass's rows).
-// Three row tiles (the row groups of narrow matrices) fit two workgroups
-// per compute unit; more rows need the whole register file.
+// Three row tiles (the row groups) fit four workgroups per compute unit;
+// more rows need the whole register file.
 template <bool BF, int MT, int AM, int EPI>
-__global__ __launch_bounds__(256, MT == 3 ? 2 : 1) void gemm_staged_kernel(const GemmArgs p, const int RG) {
+__global__ __launch_bounds__(256, MT == 3 ? 4 : 1) void gemm_staged_kernel(const GemmArgs p, const int RG) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;

@@ -837,7 +837,8 @@ __device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, u
 
 template <bool BF, int MT> __host__ __device__ constexpr int staged_ck() {
   constexpr int per = 2 * (BF ? 2 : 1) * MT * 1024;   // both buffers, one k-step
-  return kStagedLds / per > 4 ? 4 : kStagedLds / per;
+  constexpr int cap = MT == 3 ? 2 : 4;                 // three row tiles: small enough for 4 workgroups per CU
+  return kStagedLds / per > cap ? cap : kStagedLds / per;
 }
 template <bool BF, int MT> __host__ __device__ constexpr int gemm_staged_lds_bytes() {
   constexpr int a = 2 * (BF ? 2 : 1) * MT * staged_ck<BF, MT>() * 1024, f = kFRows * kFStride * 4;
