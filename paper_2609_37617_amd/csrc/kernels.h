@@ -31,7 +31,7 @@ constexpr int kMaxRows = kMaxMTiles * 16;
 constexpr int kDirectMT = 2;            // row tiles of the direct path (up to 32 rows)
 constexpr int kStepRows = kDirectMT * 16;  // rows of a persistent-kernel pass
 constexpr int kAttnChunk = 32;          // keys per attention split
-constexpr int kAttnRowGroup = 16;       // rows per attention workgroup (row groups)
+constexpr int kAttnRowGroup = 32;       // rows per attention workgroup (row groups)
 constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
 constexpr int kMaxUnits = 24;           // (pair, split) units per workgroup, balanced direct path
 constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
