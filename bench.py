@@ -275,6 +275,25 @@ def main():
     log(f"[bench] {args.steps} steps in {elapsed:.3f}s: {ms:.3f} ms/step, {committed / elapsed:.1f} tok/s, "
         f"{gbps:.0f} GB/s ({gbps / PEAK_HBM_GBPS:.1%} of peak)")
 
+    # the same window through the persistent step kernel (one launch per
+    # pass; opt-in, reported beside the headline, which is the graph mode)
+    exec_modes = {"graph_ms_per_step": round(ms, 4)}
+    if model.exec_info()[1] > 0:
+        restart()
+        model.set_exec_mode(as2d.EXEC_PERSISTENT)
+        for _ in range(2):
+            step()
+        restart()
+        sync()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        sync()
+        exec_modes["persistent_ms_per_step"] = round((time.perf_counter() - t1) * 1e3 / args.steps, 4)
+        model.set_exec_mode(as2d.EXEC_GRAPH)
+        restart()
+        log(f"[bench] persistent step kernel: {exec_modes['persistent_ms_per_step']:.3f} ms/step")
+
     roof = None
     kernel_ms = {}
     if not args.no_kernel_timing:
@@ -542,6 +561,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "stream_ceiling_gbps": round(stream_gbps, 1),
+        "exec_modes": exec_modes,
         "ms_per_step_by_k": width,
         "buffer_decoding": aligned,
         "prefill_first_request": prefill_info,
