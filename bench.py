@@ -166,7 +166,7 @@ def cpu_baseline(shape, n_audio, n_instr, k, mean_committed, seed=0, min_seconds
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on exactly one GPU: this build has no multi-GPU path "
+        print(f"bench.py runs on exactly one GPU: the library has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
     from paper_2609_37617_amd import as2d
