@@ -4,11 +4,13 @@
 //
 // All workgroups are resident at once (one per compute unit).  The pass
 // is a sequence of phases; a phase's work is split over the workgroups,
-// which walk the phases in order.  A tile that consumes the
-// previous phase's output first issues its weight loads (weights do not
+// which walk the phases in order.  A GEMM phase runs the balanced units of
+// its plan: a workgroup first issues its weight loads (weights do not
 // depend on activations), then waits until the producing phase's
 // completion counter reaches its target, so weight streaming continues
 // across phase boundaries instead of stopping at a kernel boundary.
+// Attention tiles are dealt round-robin, the next tile's keys and values
+// loaded while the current one runs.
 //
 // Cross-workgroup data is written with write-through (agent-scope) stores
 // and every activation buffer is written once per launch (per-layer

@@ -1035,8 +1035,8 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
 // ---------------------------------------------------------------------------
 // Attention over one 32-key chunk c of request r for query head h.  The
 // chunk's keys and values (float32) are staged in LDS; each wave takes the
-// request's rows in turn (the next row's query is prefetched into
-// registers).  For a row at position pos >= 32 c, lane pairs (j, j + 32)
+// request's rows in turn (all its rows' queries are loaded into registers
+// first).  For a row at position pos >= 32 c, lane pairs (j, j + 32)
 // each take half of the dot product of key j (keys j <= pos), the wave
 // forms the chunk's softmax statistics (max m, sum l of exp(s - m)) and
 // each lane the unnormalised output sum_j exp(s_j - m) v_j of its
