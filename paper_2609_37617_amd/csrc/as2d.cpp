@@ -97,6 +97,7 @@ struct as2d_ctx {
   void *pxg = nullptr, *pattn = nullptr, *ph = nullptr;
   int *psplit = nullptr, *pphase = nullptr, *perr = nullptr;
   int split_stride = 0;  // counters per (layer, GEMM)
+  int rg_grid = 448;     // staged GEMMs: least grid for row groups of 2-3 tiles
   int n_phase = 0;
   std::map<int, StepLayer*> step_layers;  // by M: device array of per-layer arguments
   int h_err = 0;
@@ -296,6 +297,7 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   a.G = pl.G;
   a.M = M;
   a.MT = (M + 15) / 16;
+  a.rg_grid = c->rg_grid;
   a.sumsq = c->sumsq;
   a.n_norm_pairs = c->cfg.hidden / kPairCols;
   a.a_plane = 0;
@@ -744,6 +746,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   const int target = env_int("AS2D_TARGET_WGS", 256);
   const int ks_qkv = env_int("AS2D_KS_QKV", 0), ks_o = env_int("AS2D_KS_O", 0), ks_gu = env_int("AS2D_KS_GU", 0);
   const int ks_down = env_int("AS2D_KS_DOWN", 0), ks_lm = env_int("AS2D_KS_LM", 0);
+  c->rg_grid = env_int("AS2D_RG_GRID", 448);
   c->p_qkv = make_plan(qkv_n, H, KE, target, ks_qkv);
   c->p_o = make_plan(H, nq * d, KE, target, ks_o);
   c->p_gu = make_plan(2 * F, H, KE, target, ks_gu);
@@ -860,8 +863,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
     if (p->KS > 1) part_elems = std::max(part_elems, (size_t)p->KS * MR * p->N);
   CK(dalloc(c, &c->part, part_elems * 4));
-  // split-K counters: one per workgroup tile (at most one per tile pair)
-  const int n_cnt = std::max({c->p_qkv.pairs, c->p_o.pairs, c->p_gu.pairs, c->p_down.pairs, c->p_lm.pairs});
+  // split-K counters: one per workgroup tile (at most one per tile pair on
+  // the direct path; on the staged path one per (group of kPairsS pairs,
+  // row group), at most kMaxMTiles row groups)
+  int n_cnt = 0;
+  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
+    n_cnt = std::max({n_cnt, p->pairs, (p->pairs / kPairsS) * kMaxMTiles});
   CK(dalloc(c, &c->counters, (size_t)n_cnt * 4));
   HIP_TRY(c, hipMemsetAsync(c->counters, 0, (size_t)n_cnt * 4, c->stream));
   HIP_TRY(c, prepare_kernels());

@@ -74,6 +74,8 @@ struct GemmArgs {
   int G;                 // balanced direct path: workgroups sharing the units (0: one unit
                          // group per workgroup)
   int M, MT;
+  int rg_grid;           // staged path with row groups: row groups of 3, 2 tiles are
+                         // used only if their grid reaches rg_grid workgroups (else 1 tile)
   // A operand: activation planes [kMaxRows][K].  For A_NORM the planes
   // hold x * g (residual times RMSNorm gain) and the epilogue multiplies
   // row m by 1 / sqrt(sum(x^2) / K + eps) from the sum-of-squares partials.

@@ -173,23 +173,35 @@ static hipError_t launch_range(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Staged path: block b = (pair group, split, row group), the row group
+// Most row tiles per row group when a staged GEMM would otherwise leave
+// compute units idle.
+constexpr int kStagedGroupMT = 3;
+
+// Workgroups are dealt to the 8 XCDs round-robin by linear index.  The
+// index v of the work a block takes: XCD j's blocks take one contiguous
+// range of v (the first n % 8 XCDs one more each), in dispatch order.
+__device__ __forceinline__ int xcd_contiguous(int b, int n) {
+  const int per = n >> 3, rem = n & 7, j = b & 7, slot = b >> 3;
+  return j < rem ? j * (per + 1) + slot : rem * (per + 1) + (j - rem) * per + slot;
+}
+
+// Staged path: work item v = (pair group, split, row group), the row group
 // fastest; RG row groups of MT row tiles each (RG = 1: all the pass's rows).
-// Three row tiles (the row groups) fit four workgroups per compute unit;
+// With row groups, the RG blocks of one (pair group, split) run on one XCD
+// at about the same time (xcd_contiguous), so its weight tiles come from
+// memory once and from that XCD's L2 for the other row groups.
+// Row groups (up to three row tiles) fit four workgroups per compute unit;
 // more rows need the whole register file.
 template <bool BF, int MT, int AM, int EPI>
-__global__ __launch_bounds__(256, MT == 3 ? 4 : 1) void gemm_staged_kernel(const GemmArgs p, const int RG) {
+__global__ __launch_bounds__(256, MT <= kStagedGroupMT ? 4 : 1) void gemm_staged_kernel(const GemmArgs p, const int RG) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;
-  const int rg = blockIdx.x % RG, t = blockIdx.x / RG;
+  const int v = RG > 1 ? xcd_contiguous(blockIdx.x, gridDim.x) : (int)blockIdx.x;
+  const int rg = v % RG, t = v / RG;
   const int group = t / p.KS, split = t - group * p.KS;
   gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, rg * MT, group * RG + rg);
 }
-
-// Row tiles per row group when a staged GEMM would otherwise leave compute
-// units idle.
-constexpr int kStagedGroupMT = 3;
 
 template <bool BF, int AM, int EPI>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
@@ -210,14 +222,19 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   if (pairs % kPairsS) return hipErrorInvalidValue;
   const int base = (pairs / kPairsS) * a.KS;
   // matrices with fewer than two workgroups per compute unit: row groups of
-  // kStagedGroupMT tiles, so that the grid fills the chip in even rounds
-  // (at most 3 groups, so the counters, one per pair, cover group * RG + rg;
-  // each group reads the weights again, from L2 or the MALL)
+  // g <= kStagedGroupMT tiles, the largest g whose grid reaches rg_grid
+  // workgroups (else one tile), so that each compute unit keeps several
+  // workgroups' loads in flight.  Each group reads the weights again (from
+  // its XCD's L2: xcd_contiguous).  The counters (group * RG + rg) cover
+  // (pairs / kPairsS) * kMaxMTiles tiles.
   if (base < 512 && a.MT > kStagedGroupMT) {
-    const int RG = (a.MT + kStagedGroupMT - 1) / kStagedGroupMT;
-    if (RG > kPairsS) return hipErrorInvalidValue;
-    gemm_staged_kernel<BF, kStagedGroupMT, AM, EPI>
-        <<<base * RG, 256, gemm_staged_lds_bytes<BF, kStagedGroupMT>(), s>>>(a, RG);
+    int g = kStagedGroupMT;
+    while (g > 1 && base * ((a.MT + g - 1) / g) < a.rg_grid) --g;
+    const int RG = (a.MT + g - 1) / g;
+    if (RG > kMaxMTiles) return hipErrorInvalidValue;
+    if (g == 3) gemm_staged_kernel<BF, 3, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 3>(), s>>>(a, RG);
+    else if (g == 2) gemm_staged_kernel<BF, 2, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 2>(), s>>>(a, RG);
+    else gemm_staged_kernel<BF, 1, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 1>(), s>>>(a, RG);
     return hipGetLastError();
   }
   const dim3 grid(base), block(256);
@@ -307,7 +324,7 @@ static hipError_t prepare_staged() {
   };
 #define AS2D_S(mt) \
   allow(reinterpret_cast<const void*>(&gemm_staged_kernel<BF, mt, AM, EPI>), gemm_staged_lds_bytes<BF, mt>());
-  AS2D_S(3) AS2D_S(4) AS2D_S(5) AS2D_S(6) AS2D_S(7) AS2D_S(8) AS2D_S(9)
+  AS2D_S(1) AS2D_S(2) AS2D_S(3) AS2D_S(4) AS2D_S(5) AS2D_S(6) AS2D_S(7) AS2D_S(8) AS2D_S(9)
 #undef AS2D_S
   return e;
 }

@@ -837,7 +837,7 @@ __device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, u
 
 template <bool BF, int MT> __host__ __device__ constexpr int staged_ck() {
   constexpr int per = 2 * (BF ? 2 : 1) * MT * 1024;   // both buffers, one k-step
-  constexpr int cap = MT == 3 ? 2 : 4;                 // three row tiles: small enough for 4 workgroups per CU
+  constexpr int cap = MT == 2 || MT == 3 ? 2 : 4;     // row groups of 2-3 tiles: few enough registers for 4 workgroups per CU
   return kStagedLds / per > cap ? cap : kStagedLds / per;
 }
 template <bool BF, int MT> __host__ __device__ constexpr int gemm_staged_lds_bytes() {
@@ -887,13 +887,16 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   // u % 64 feeds to the MFMA (frag_lane_unit): the waves then read their
   // fragments as 64 consecutive units, free of bank conflicts (read in
   // fragment order, lanes 64 bytes apart, four of eight lanes met in one
-  // bank); returns its source and sets its place in a buffer
+  // bank); returns its source and sets its place in a buffer.  A tile past
+  // the pass's last one (the last row group of a pass may reach beyond
+  // kMaxMTiles) loads the last one instead: its rows are never stored.
+  const int mt_last = (M - 1) >> 4;
   auto elem = [&](const Chunk& d, int u, int& dst) {
     const int pos = u & 63, b = u >> 6;
     const int rg = b / (MT * d.n), r2 = b - rg * (MT * d.n);
     const int mt = r2 / d.n, r = r2 - mt * d.n;
     dst = ((rg * MT + mt) * CK + r) * 64 + pos;
-    return ag + rg * lo + ((size_t)(mt0 + mt) * p.KT + d.c0 + r) * 64 + frag_lane_unit(pos);
+    return ag + rg * lo + ((size_t)min(mt0 + mt, mt_last) * p.KT + d.c0 + r) * 64 + frag_lane_unit(pos);
   };
   // requests chunk d: CK k-steps of weights (past the chunk its last
   // again, clamped to the matrix: unused) and this thread's NV staging
