@@ -200,7 +200,8 @@ __global__ __launch_bounds__(256, MT <= kStagedGroupMT ? 4 : 1) void gemm_staged
   const int v = RG > 1 ? xcd_contiguous(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const int rg = v % RG, t = v / RG;
   const int group = t / p.KS, split = t - group * p.KS;
-  gemm_tile_staged<BF, MT, AM, EPI, false>(p, p.M, group, split, smem, s_scale, &s_flag, rg * MT, group * RG + rg);
+  gemm_tile_staged<BF, MT, AM, EPI, false, (MT <= kStagedGroupMT)>(p, p.M, group, split, smem, s_scale, &s_flag,
+                                                                   rg * MT, group * RG + rg);
 }
 
 template <bool BF, int AM, int EPI>

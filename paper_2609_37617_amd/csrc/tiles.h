@@ -833,6 +833,8 @@ __device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, u
 // overlaps the MFMA work.  Row groups (mt0 > 0) let narrow matrices use
 // more workgroups; `cnt` is the split counter of this (pairs, rows) tile
 // (default: the pair group).
+// WC: weight tiles by ordinary cached loads (the other row groups of the
+// pass read them again from L2), else by streaming loads.
 //   smem: dynamic LDS of gemm_staged_lds_bytes<BF, MT>().
 
 template <bool BF, int MT> __host__ __device__ constexpr int staged_ck() {
@@ -845,7 +847,7 @@ template <bool BF, int MT> __host__ __device__ constexpr int gemm_staged_lds_byt
   return a > f ? a : f;
 }
 
-template <bool BF, int MT, int AM, int EPI, bool COH>
+template <bool BF, int MT, int AM, int EPI, bool COH, bool WC = false>
 __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split, unsigned char* smem,
                                  float* s_scale, int* s_flag, int mt0 = 0, int cnt = -1) {
   constexpr int kRegions = BF ? 2 : 1;
@@ -906,8 +908,13 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
 #pragma unroll
     for (int r = 0; r < CK; ++r) {
       const size_t kp = (size_t)min(d.c0 + min(r, max(d.n, 1) - 1), p.KT - 1) * 128;
-      wb[r][0] = ldw(wp + kp);
-      wb[r][1] = ldw(wp + kp + 64);
+      if constexpr (WC) {
+        wb[r][0] = ldg(wp + kp);
+        wb[r][1] = ldg(wp + kp + 64);
+      } else {
+        wb[r][0] = ldw(wp + kp);
+        wb[r][1] = ldw(wp + kp + 64);
+      }
     }
     const int total = max(kRegions * MT * d.n * 64, 1);
 #pragma unroll
