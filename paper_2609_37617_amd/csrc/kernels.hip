@@ -265,11 +265,12 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 //
 // Workgroup (chunk c, query head h, request r, row group) runs
 // attn_chunk_tile over keys [32 c, 32 c + 32) of the request's float32
-// cache slot, for the group's kAttnRowGroup rows; the merge
-// kernel, one workgroup per (head, row), combines a row's chunks in
-// ascending order (attn_merge_row).
+// cache slot, for the group's kAttnRowGroup rows, in batches of RB rows
+// per wave (kAttnBatch when a pass has more than one row group, else one);
+// the merge kernel, one workgroup per (head, row), combines a row's chunks
+// in ascending order (attn_merge_row).
 
-template <int D>
+template <int D, int RB>
 __global__ __launch_bounds__(256, 4) void attn_chunk_kernel(const AttnArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int rg = blockIdx.z % p.row_groups;
@@ -277,7 +278,7 @@ __global__ __launch_bounds__(256, 4) void attn_chunk_kernel(const AttnArgs p) {
   const int r_lo = rg * kAttnRowGroup, r_hi = min(rq.W, r_lo + kAttnRowGroup);
   // no row of the group reaches this chunk's first key
   if (r_lo >= r_hi || (int)blockIdx.x * kAttnChunk > rq.L0 + r_hi - 1) return;
-  attn_chunk_tile<D, false, kAttnRowGroup / 4>(p, blockIdx.x, blockIdx.y, rq, smem, r_lo, r_hi);
+  attn_chunk_tile<D, false, kAttnRowGroup / 4, RB>(p, blockIdx.x, blockIdx.y, rq, smem, r_lo, r_hi);
 }
 
 template <bool BF, int D>
@@ -295,7 +296,8 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, h
   // values in one L2 (extra chunks exit at once).
   if (a.row_groups < 1) return hipErrorInvalidValue;
   const dim3 grid((max_chunks + 7) / 8 * 8, a.n_q, n_reqs * a.row_groups);
-  attn_chunk_kernel<D><<<grid, 256, attn_lds_bytes<D>(), s>>>(a);
+  if (a.row_groups > 1) attn_chunk_kernel<D, kAttnBatch><<<grid, 256, attn_lds_bytes<D, kAttnBatch>(), s>>>(a);
+  else attn_chunk_kernel<D, 1><<<grid, 256, attn_lds_bytes<D>(), s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   attn_merge_kernel<BF, D><<<dim3(a.n_q, a.M), D, 0, s>>>(a);

@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
       for (int t = blockIdx.x; t < n_chunk_tiles; t += G) {
         const bool more = t + G < n_chunk_tiles;
         if (more) tile_of(t + G, rq2, h2, c2);
-        attn_tile_kv<D, true, kStepRows / 4>(at, c, h, rq, smem, cur, [&] {
+        attn_tile_kv<D, true, kStepRows / 4, 1>(at, c, h, rq, smem, cur, [&] {
           if (more) attn_load_kv<D>(at, c2, h2, rq2, nxt);
         });
         lds_sync();   // the next tile overwrites the chunk in LDS

@@ -1045,19 +1045,22 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
 // ---------------------------------------------------------------------------
 // Attention over one 32-key chunk c of request r for query head h.  The
 // chunk's keys and values (float32) are staged in LDS; each wave takes the
-// request's rows in turn (all its rows' queries are loaded into registers
-// first).  For a row at position pos >= 32 c, lane pairs (j, j + 32)
-// each take half of the dot product of key j (keys j <= pos), the wave
-// forms the chunk's softmax statistics (max m, sum l of exp(s - m)) and
-// each lane the unnormalised output sum_j exp(s_j - m) v_j of its
-// dimensions.  A row's chunks are combined in ascending order by
-// attn_merge_row.  Both sums run in ascending order as single fused
-// multiply-adds; their operands are read from LDS first, so a row costs a
-// few LDS round trips rather than one per key.  256 threads; smem:
-// attn_lds_bytes(D).
+// request's rows in turn, kAttnBatch rows at a time (all its rows' queries
+// are loaded into registers first).  For a row at position pos >= 32 c,
+// lane pairs (j, j + 32) each take half of the dot product of key j (keys
+// j <= pos), the wave forms the chunk's softmax statistics (max m, sum l
+// of exp(s - m)) and each lane the unnormalised output
+// sum_j exp(s_j - m) v_j of its dimensions.  A row's chunks are combined
+// in ascending order by attn_merge_row.  Both sums run in ascending order
+// as single fused multiply-adds; their operands are read from LDS first,
+// each key and value element once for a batch of RB rows (RB > 1 for tiles
+// of many rows: a batch costs less than its rows one by one, but more than
+// one row).  256 threads; smem: attn_lds_bytes<D, RB>().
 
-template <int D> __host__ __device__ constexpr int attn_lds_bytes() {
-  return (2 * kAttnChunk * (D + 1) + 4 * D + 4 * kAttnChunk) * 4;
+constexpr int kAttnBatch = 2;   // rows a wave takes together in tiles of many rows
+
+template <int D, int RB = 1> __host__ __device__ constexpr int attn_lds_bytes() {
+  return (2 * kAttnChunk * (D + 1) + 4 * RB * (D + kAttnChunk)) * 4;
 }
 
 // The chunk's keys and values in registers: thread x holds float4 number
@@ -1086,67 +1089,96 @@ __device__ __forceinline__ void attn_load_kv(const AttnArgs& p, int c, int h, co
   }
 }
 
-// One row of a chunk tile, by one wave: the query is in qw (LDS, D
-// floats), the chunk's keys and values in Ks / Vs (row stride D + 1), pw is
-// C floats of LDS scratch; stores the row's partial output and (m, l).
-template <int D, bool COH>
-__device__ __forceinline__ void attn_row(const AttnArgs& p, int c, int h, int key0, int nk, int pos, int row,
-                                         const float* Ks, const float* Vs, const float* qw, float* pw) {
+// Up to RB rows of a chunk tile, by one wave: the queries are in qw (LDS,
+// RB x D floats), the chunk's keys and values in Ks / Vs (row stride
+// D + 1), pw is RB x C floats of LDS scratch; stores each of the first nb
+// rows' partial output and (m, l).  Every row's sums take the same
+// operands in the same order whatever the batch.
+template <int D, bool COH, int RB>
+__device__ __forceinline__ void attn_rows(const AttnArgs& p, int c, int h, int key0, int nk, const int (&pos)[RB],
+                                          const int (&row)[RB], int nb, const float* Ks, const float* Vs,
+                                          const float* qw, float* pw) {
   constexpr int C = kAttnChunk;
   constexpr int RS = D + 1;
   constexpr int QL = D / 64;
   constexpr int DH = D / 2;
   const int lane = threadIdx.x & 63;
   const int j = lane & (C - 1), half = lane >> 5;
-  const bool valid = j < nk && key0 + j <= pos;
-  float a = 0.0f;
+  float a[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) a[r] = 0.0f;
   if (j < nk) {
-    // in blocks of 32 elements: each block's operands are read, then
-    // its multiply-adds run in order
-    constexpr int B = 32;
+    // in blocks of B elements: each block's keys are read once, then for
+    // each row its query elements and its multiply-adds in order (one row:
+    // blocks of 32, fewer LDS round trips; batches: 16, fewer registers)
+    constexpr int B = RB == 1 ? 32 : 16;
 #pragma unroll
     for (int b0 = 0; b0 < DH; b0 += B) {
       const float* kr = Ks + j * RS + half * DH + b0;
-      const float4* qh = reinterpret_cast<const float4*>(qw + half * DH + b0);
-      float kk[B], qq[B];
-#pragma unroll
-      for (int d4 = 0; d4 < B / 4; ++d4) {
-        const float4 q4 = qh[d4];
-        qq[4 * d4] = q4.x; qq[4 * d4 + 1] = q4.y; qq[4 * d4 + 2] = q4.z; qq[4 * d4 + 3] = q4.w;
-      }
+      float kk[B];
 #pragma unroll
       for (int dd = 0; dd < B; ++dd) kk[dd] = kr[dd];
 #pragma unroll
-      for (int dd = 0; dd < B; ++dd) a = __builtin_fmaf(qq[dd], kk[dd], a);
+      for (int r = 0; r < RB; ++r) {
+        const float4* qh = reinterpret_cast<const float4*>(qw + r * D + half * DH + b0);
+        float qq[B];
+#pragma unroll
+        for (int d4 = 0; d4 < B / 4; ++d4) {
+          const float4 q4 = qh[d4];
+          qq[4 * d4] = q4.x; qq[4 * d4 + 1] = q4.y; qq[4 * d4 + 2] = q4.z; qq[4 * d4 + 3] = q4.w;
+        }
+#pragma unroll
+        for (int dd = 0; dd < B; ++dd) a[r] = __builtin_fmaf(qq[dd], kk[dd], a[r]);
+      }
     }
   }
-  a += __shfl_xor(a, 32);  // both halves: same sum (commutative)
-  const float s = valid ? a * p.scale : -INFINITY;
-  const float mx = wave_max(s);
-  const float pj = valid ? expf(s - mx) : 0.0f;
-  const float l = wave_sum(half == 0 ? pj : 0.0f);
-  if (half == 0) pw[j] = pj;
-  __builtin_amdgcn_wave_barrier();
-  float pv[C];
+  float mx[RB], l[RB];
 #pragma unroll
-  for (int j4 = 0; j4 < C / 4; ++j4) {
-    const float4 p4 = reinterpret_cast<const float4*>(pw)[j4];
-    pv[4 * j4] = p4.x; pv[4 * j4 + 1] = p4.y; pv[4 * j4 + 2] = p4.z; pv[4 * j4 + 3] = p4.w;
+  for (int r = 0; r < RB; ++r) {
+    const float ar = a[r] + __shfl_xor(a[r], 32);  // both halves: same sum (commutative)
+    const bool valid = j < nk && key0 + j <= pos[r];
+    const float s = valid ? ar * p.scale : -INFINITY;
+    mx[r] = wave_max(s);
+    const float pj = valid ? expf(s - mx[r]) : 0.0f;
+    l[r] = wave_sum(half == 0 ? pj : 0.0f);
+    if (half == 0) pw[r * C + j] = pj;
   }
+  __builtin_amdgcn_wave_barrier();
 #pragma unroll
   for (int t = 0; t < QL; ++t) {
     const int dd = t * 64 + lane;
-    float vv[C];
+    float o[RB];
 #pragma unroll
-    for (int jj = 0; jj < C; ++jj) vv[jj] = Vs[jj * RS + dd];   // rows >= nk: read, never used
-    float o = 0.0f;
+    for (int r = 0; r < RB; ++r) o[r] = 0.0f;
+    // keys in blocks of KB: each block's values are read once, then for
+    // each row its weights and its multiply-adds in key order
+    constexpr int KB = RB == 1 ? C : 16;
 #pragma unroll
-    for (int jj = 0; jj < C; ++jj) o = jj < nk ? __builtin_fmaf(pv[jj], vv[jj], o) : o;
-    st<COH>(p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd, o);
+    for (int j0 = 0; j0 < C; j0 += KB) {
+      float vv[KB];
+#pragma unroll
+      for (int jj = 0; jj < KB; ++jj) vv[jj] = Vs[(j0 + jj) * RS + dd];   // rows >= nk: read, never used
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        float pv[KB];
+#pragma unroll
+        for (int j4 = 0; j4 < KB / 4; ++j4) {
+          const float4 p4 = reinterpret_cast<const float4*>(pw + r * C + j0)[j4];
+          pv[4 * j4] = p4.x; pv[4 * j4 + 1] = p4.y; pv[4 * j4 + 2] = p4.z; pv[4 * j4 + 3] = p4.w;
+        }
+#pragma unroll
+        for (int jj = 0; jj < KB; ++jj) o[r] = j0 + jj < nk ? __builtin_fmaf(pv[jj], vv[jj], o[r]) : o[r];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+      if (r < nb) st<COH>(p.pacc + (((size_t)c * kMaxRows + row[r]) * p.n_q + h) * D + dd, o[r]);
   }
   // (m, l): every lane stores, even lanes m and odd lanes l, one store
   // with no branch around it
-  st<COH>(p.pml + (((size_t)c * kMaxRows + row) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l : mx);
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+    if (r < nb) st<COH>(p.pml + (((size_t)c * kMaxRows + row[r]) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l[r] : mx[r]);
 }
 
 // The tile from keys and values already in registers; `pre` runs once the
@@ -1154,16 +1186,17 @@ __device__ __forceinline__ void attn_row(const AttnArgs& p, int c, int h, int ke
 // kernel loads the next tile's keys and values there).
 // Rows [r_lo, r_hi) of the request (all by default), r_hi - r_lo <= 4 RPW
 // (checked by the callers' hosts).
-template <int D, bool COH, int RPW, class Pre>
+template <int D, bool COH, int RPW, int RB, class Pre>
 __device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem,
                                              const AttnKV<D>& r, Pre&& pre, int r_lo = 0, int r_hi = -1) {
   constexpr int C = kAttnChunk;
+  static_assert(RPW % RB == 0, "rows per wave in whole batches");
   constexpr int RS = D + 1;                   // odd LDS row stride (floats)
   constexpr int QL = D / 64;                  // query elements per lane
   float* Ks = reinterpret_cast<float*>(smem);
   float* Vs = Ks + C * RS;
   float* qs = Vs + C * RS;
-  float* ps = qs + 4 * D;
+  float* ps = qs + 4 * RB * D;
 
   const int key0 = c * C;
   const int nk = min(C, rq.L0 + rq.W - key0);
@@ -1179,8 +1212,8 @@ __device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, co
   }
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float* qw = qs + wave * D;
-  float* pw = ps + wave * C;
+  float* qw = qs + wave * RB * D;
+  float* pw = ps + wave * RB * C;
   // rows [r_lo, r_hi) of the request (all by default); the first row of
   // this wave at or after the chunk start
   if (r_hi < 0) r_hi = rq.W;
@@ -1199,24 +1232,29 @@ __device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, co
   pre();
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < RPW; ++k) {
-    if (i + 4 * k >= r_hi) break;
-    const int pos = rq.L0 + i + 4 * k;
-    const int row = rq.row_start + i + 4 * k;
+  for (int k0 = 0; k0 < RPW; k0 += RB) {
+    if (i + 4 * k0 >= r_hi) break;
+    const int nb = min(RB, (r_hi - 1 - (i + 4 * k0)) / 4 + 1);   // rows of this batch
+    int pos[RB], row[RB];
 #pragma unroll
-    for (int t = 0; t < QL; ++t) qw[t * 64 + lane] = qa[k][t];
+    for (int b = 0; b < RB; ++b) {
+      pos[b] = rq.L0 + i + 4 * (k0 + b);
+      row[b] = rq.row_start + i + 4 * (k0 + b);
+#pragma unroll
+      for (int t = 0; t < QL; ++t) qw[b * D + t * 64 + lane] = qa[k0 + b][t];
+    }
     __builtin_amdgcn_wave_barrier();
-    attn_row<D, COH>(p, c, h, key0, nk, pos, row, Ks, Vs, qw, pw);
+    attn_rows<D, COH, RB>(p, c, h, key0, nk, pos, row, nb, Ks, Vs, qw, pw);
     __builtin_amdgcn_wave_barrier();
   }
 }
 
-template <int D, bool COH, int RPW>
+template <int D, bool COH, int RPW, int RB>
 __device__ __forceinline__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem,
                                                 int r_lo = 0, int r_hi = -1) {
   AttnKV<D> r;
   attn_load_kv<D>(p, c, h, rq, r);
-  attn_tile_kv<D, COH, RPW>(p, c, h, rq, smem, r, [] {}, r_lo, r_hi);
+  attn_tile_kv<D, COH, RPW, RB>(p, c, h, rq, smem, r, [] {}, r_lo, r_hi);
 }
 
 // Merge of row `row`'s chunks for head h by D threads starting at thread t0:
