@@ -192,16 +192,17 @@ __device__ __forceinline__ int xcd_contiguous(int b, int n) {
 // memory once and from that XCD's L2 for the other row groups.
 // Row groups (up to three row tiles) fit four workgroups per compute unit;
 // more rows need the whole register file.
-template <bool BF, int MT, int AM, int EPI>
-__global__ __launch_bounds__(256, MT <= kStagedGroupMT ? 4 : 1) void gemm_staged_kernel(const GemmArgs p, const int RG) {
+template <bool BF, int MT, int AM, int EPI, int NPW = 1>
+__global__ __launch_bounds__(256, NPW > 1 ? 2 : MT <= kStagedGroupMT ? 4 : 1) void gemm_staged_kernel(const GemmArgs p,
+                                                                                                    const int RG) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flag;
   const int v = RG > 1 ? xcd_contiguous(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const int rg = v % RG, t = v / RG;
   const int group = t / p.KS, split = t - group * p.KS;
-  gemm_tile_staged<BF, MT, AM, EPI, false, (MT <= kStagedGroupMT)>(p, p.M, group, split, smem, s_scale, &s_flag,
-                                                                   rg * MT, group * RG + rg);
+  gemm_tile_staged<BF, MT, AM, EPI, false, (MT <= kStagedGroupMT), NPW>(p, p.M, group, split, smem, s_scale, &s_flag,
+                                                                        rg * MT, group * RG + rg);
 }
 
 template <bool BF, int AM, int EPI>
@@ -233,7 +234,12 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
     while (g > 1 && base * ((a.MT + g - 1) / g) < a.rg_grid) --g;
     const int RG = (a.MT + g - 1) / g;
     if (RG > kMaxMTiles) return hipErrorInvalidValue;
-    if (g == 3) gemm_staged_kernel<BF, 3, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 3>(), s>>>(a, RG);
+    if (g == 3 && pairs % (2 * kPairsS) == 0) {
+      // two pairs per wave: each staged activation fragment feeds twice the
+      // weights, half the workgroups
+      gemm_staged_kernel<BF, 3, AM, EPI, 2>
+          <<<base / 2 * RG, 256, gemm_staged_lds_bytes<BF, 3, 2>(), s>>>(a, RG);
+    } else if (g == 3) gemm_staged_kernel<BF, 3, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 3>(), s>>>(a, RG);
     else if (g == 2) gemm_staged_kernel<BF, 2, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 2>(), s>>>(a, RG);
     else gemm_staged_kernel<BF, 1, AM, EPI><<<base * RG, 256, gemm_staged_lds_bytes<BF, 1>(), s>>>(a, RG);
     return hipGetLastError();

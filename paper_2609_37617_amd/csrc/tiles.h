@@ -822,8 +822,8 @@ __device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, u
   range_finish<BF, AM, EPI, COH>(p, M, F, fs, u0, nu, s_scale, s_flags);
 }
 
-// Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS
-// tile pairs (one per wave) of one split, for row tiles [mt0, mt0 + MT);
+// Staged path (more than kDirectMT row tiles): a workgroup owns kPairsS NPW
+// tile pairs (NPW per wave) of one split, for row tiles [mt0, mt0 + MT);
 // each wave keeps its slices apart in registers (running sum S).  The
 // split's slices are cut into chunks of at most CK k-steps; a chunk's
 // activation fragments are staged in LDS and shared by the waves, its
@@ -835,30 +835,36 @@ __device__ __forceinline__ void gemm_range_direct_ra(const GemmArgs& p, int M, u
 // (default: the pair group).
 // WC: weight tiles by ordinary cached loads (the other row groups of the
 // pass read them again from L2), else by streaming loads.
-//   smem: dynamic LDS of gemm_staged_lds_bytes<BF, MT>().
+//   smem: dynamic LDS of gemm_staged_lds_bytes<BF, MT, NPW>().
 
 template <bool BF, int MT> __host__ __device__ constexpr int staged_ck() {
   constexpr int per = 2 * (BF ? 2 : 1) * MT * 1024;   // both buffers, one k-step
   constexpr int cap = MT == 2 || MT == 3 ? 2 : 4;     // row groups of 2-3 tiles: few enough registers for 4 workgroups per CU
   return kStagedLds / per > cap ? cap : kStagedLds / per;
 }
-template <bool BF, int MT> __host__ __device__ constexpr int gemm_staged_lds_bytes() {
-  constexpr int a = 2 * (BF ? 2 : 1) * MT * staged_ck<BF, MT>() * 1024, f = kFRows * kFStride * 4;
+// Epilogue tile of the staged path with NPW pairs per wave: row stride
+// (floats) and rows per pass (at most the workgroup's rows).
+template <int NPW> __host__ __device__ constexpr int staged_fstride() { return kPairsS * NPW * kPairCols + 4; }
+template <int MT> __host__ __device__ constexpr int staged_frows() { return MT * 16 < kFRows ? MT * 16 : kFRows; }
+template <bool BF, int MT, int NPW = 1> __host__ __device__ constexpr int gemm_staged_lds_bytes() {
+  constexpr int a = 2 * (BF ? 2 : 1) * MT * staged_ck<BF, MT>() * 1024;
+  constexpr int f = staged_frows<MT>() * staged_fstride<NPW>() * 4;
   return a > f ? a : f;
 }
 
-template <bool BF, int MT, int AM, int EPI, bool COH, bool WC = false>
+template <bool BF, int MT, int AM, int EPI, bool COH, bool WC = false, int NPW = 1>
 __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split, unsigned char* smem,
                                  float* s_scale, int* s_flag, int mt0 = 0, int cnt = -1) {
   constexpr int kRegions = BF ? 2 : 1;
+  constexpr int PG = kPairsS * NPW;                // pairs of the workgroup, NPW per wave
   constexpr int CK = staged_ck<BF, MT>();
   constexpr int BUF = kRegions * MT * CK * 64;     // 16-byte elements per buffer
   constexpr int NV = (BUF + 255) / 256;            // of which each thread stages at most NV
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int pair = group * kPairsS + wave;
   const int kt0 = split * p.ktps;
   const int n_all = min(p.KT, kt0 + p.ktps) - kt0;
-  const uint4* wp = p.W + (size_t)pair * p.KT * 128 + lane;
+  const size_t pstride = (size_t)p.KT * 128;                                   // 16-byte units per pair
+  const uint4* wp = p.W + (size_t)(group * PG + wave * NPW) * pstride + lane;   // this wave's first pair
   const uint4* ag = static_cast<const uint4*>(p.A);
   const long long lo = p.a_plane / ET<BF>::PER16;
   uint4* la = reinterpret_cast<uint4*>(smem);     // [buffer][region][mt][k-step of chunk][lane]
@@ -904,16 +910,19 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   // again, clamped to the matrix: unused) and this thread's NV staging
   // elements (u = tid + 256 i; past the chunk's last element that one
   // again: no branch around the loads, so they all stay in flight)
-  auto request = [&](const Chunk& d, uint4(&wb)[CK][2], uint4(&av)[NV], int(&ad)[NV]) {
+  auto request = [&](const Chunk& d, uint4(&wb)[CK][NPW][2], uint4(&av)[NV], int(&ad)[NV]) {
 #pragma unroll
     for (int r = 0; r < CK; ++r) {
       const size_t kp = (size_t)min(d.c0 + min(r, max(d.n, 1) - 1), p.KT - 1) * 128;
-      if constexpr (WC) {
-        wb[r][0] = ldg(wp + kp);
-        wb[r][1] = ldg(wp + kp + 64);
-      } else {
-        wb[r][0] = ldw(wp + kp);
-        wb[r][1] = ldw(wp + kp + 64);
+#pragma unroll
+      for (int q = 0; q < NPW; ++q) {
+        if constexpr (WC) {
+          wb[r][q][0] = ldg(wp + q * pstride + kp);
+          wb[r][q][1] = ldg(wp + q * pstride + kp + 64);
+        } else {
+          wb[r][q][0] = ldw(wp + q * pstride + kp);
+          wb[r][q][1] = ldw(wp + q * pstride + kp + 64);
+        }
       }
     }
     const int total = max(kRegions * MT * d.n * 64, 1);
@@ -927,13 +936,13 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
       if ((int)tid + 256 * i < total) buf[ad[i]] = av[i];
   };
 
-  f4 S[MT][2], acc[MT][2];
-  uint4 w0[CK][2], w1[CK][2], av[NV];
+  f4 S[MT][NPW][2], acc[MT][NPW][2];
+  uint4 w0[CK][NPW][2], w1[CK][NPW][2], av[NV];
   int ad[NV];
   // one chunk: request the next one (weights into wn, fragments into
   // registers), sum this one from LDS buffer bi with weights wc, stage the
   // next one into the other buffer; false after the last chunk
-  auto step = [&](Chunk& cur, int bi, const uint4(&wc)[CK][2], uint4(&wn)[CK][2]) {
+  auto step = [&](Chunk& cur, int bi, const uint4(&wc)[CK][NPW][2], uint4(&wn)[CK][NPW][2]) {
     const Chunk nxt = next_of(cur);
     const bool more = nxt.q < p.ns;
     // after the last chunk, the current one again (unused): the same loads
@@ -941,10 +950,12 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
     request(more ? nxt : cur, wn, av, ad);
     if (cur.c0 == slice_start(kt0, n_all, cur.q, p.ns)) {   // a slice begins
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        acc[mt][0] = f4{0.f, 0.f, 0.f, 0.f};
-        acc[mt][1] = f4{0.f, 0.f, 0.f, 0.f};
-      }
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int q = 0; q < NPW; ++q) {
+          acc[mt][q][0] = f4{0.f, 0.f, 0.f, 0.f};
+          acc[mt][q][1] = f4{0.f, 0.f, 0.f, 0.f};
+        }
     }
     const uint4* lb = la + bi * BUF;
 #pragma unroll
@@ -955,8 +966,11 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
           AFrag af;
           af.h = lb[(mt * CK + ks) * 64 + lane];
           if constexpr (BF) af.l = lb[MT * CK * 64 + (mt * CK + ks) * 64 + lane];
-          acc[mt][0] = mma_a<BF>(af, wc[ks][0], acc[mt][0]);
-          acc[mt][1] = mma_a<BF>(af, wc[ks][1], acc[mt][1]);
+#pragma unroll
+          for (int q = 0; q < NPW; ++q) {
+            acc[mt][q][0] = mma_a<BF>(af, wc[ks][q][0], acc[mt][q][0]);
+            acc[mt][q][1] = mma_a<BF>(af, wc[ks][q][1], acc[mt][q][1]);
+          }
         }
       }
     }
@@ -964,7 +978,9 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) S[mt][j] = cur.q == 0 ? acc[mt][j] : S[mt][j] + acc[mt][j];
+        for (int q = 0; q < NPW; ++q)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) S[mt][q][j] = cur.q == 0 ? acc[mt][q][j] : S[mt][q][j] + acc[mt][q][j];
     }
     if (!more) return false;
     // the other buffer was last read in the previous chunk, before the
@@ -984,33 +1000,36 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
   lds_sync();   // the A buffers are no longer read (F reuses the LDS)
 
   float* F = reinterpret_cast<float*>(smem);
-  const int n0 = group * kPairsS * kPairCols, C = kPairsS * kPairCols;
+  constexpr int FS = staged_fstride<NPW>(), FR = staged_frows<MT>();
+  const int n0 = group * PG * kPairCols, C = PG * kPairCols;
   const int R0 = mt0 * 16, R1 = min(M, (mt0 + MT) * 16);   // this workgroup's rows
   if (cnt < 0) cnt = group;
-  // lane's value of (row m, column 32 wave + 16 j + lane % 16)
+  // lane's value of (row m, column 32 (NPW wave + q) + 16 j + lane % 16)
   auto put = [&](int r0, int r1, bool scale) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int q = 0; q < NPW; ++q)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = (mt0 + mt) * 16 + (lane >> 4) * 4 + i;
-          const int col = wave * kPairCols + j * 16 + (lane & 15);
-          if (row >= r0 && row < r1)
-            F[(row - r0) * kFStride + col] = AM == A_NORM && scale ? S[mt][j][i] * s_scale[row] : S[mt][j][i];
-        }
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = (mt0 + mt) * 16 + (lane >> 4) * 4 + i;
+            const int col = (wave * NPW + q) * kPairCols + j * 16 + (lane & 15);
+            if (row >= r0 && row < r1)
+              F[(row - r0) * FS + col] = AM == A_NORM && scale ? S[mt][q][j][i] * s_scale[row] : S[mt][q][j][i];
+          }
   };
   if (p.KS > 1) {
     // publish in row blocks through F
-    for (int r0 = R0; r0 < R1; r0 += kFRows) {
-      const int r1 = min(R1, r0 + kFRows);
+    for (int r0 = R0; r0 < R1; r0 += FR) {
+      const int r1 = min(R1, r0 + FR);
       lds_sync();
       put(r0, r1, false);
       __syncthreads();
       for (int e = tid; e < (r1 - r0) * C; e += 256) {
         const int m = r0 + e / C, c = e % C;
-        store_partial(&p.part[((size_t)split * M + m) * p.N + n0 + c], F[(m - r0) * kFStride + c]);
+        store_partial(&p.part[((size_t)split * M + m) * p.N + n0 + c], F[(m - r0) * FS + c]);
       }
     }
     wait_vmem();
@@ -1021,21 +1040,21 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
     if (tid == 0) st<true>(&p.counters[cnt], 0);
     row_scales<AM>(p, M, s_scale);
     __syncthreads();
-    for (int r0 = R0; r0 < R1; r0 += kFRows) {
-      const int r1 = min(R1, r0 + kFRows);
-      fixup_rows<AM>(p, M, n0, C, r0, r1, s_scale, F, kFStride);
+    for (int r0 = R0; r0 < R1; r0 += FR) {
+      const int r1 = min(R1, r0 + FR);
+      fixup_rows<AM>(p, M, n0, C, r0, r1, s_scale, F, FS);
       lds_sync();
-      epilogue_rows<BF, EPI, COH>(p, F, kFStride, group * kPairsS, kPairsS, r0, r1);
+      epilogue_rows<BF, EPI, COH>(p, F, FS, group * PG, PG, r0, r1);
       lds_sync();
     }
   } else {
     row_scales<AM>(p, M, s_scale);
     __syncthreads();  // A tiles no longer read; s_scale written
-    for (int r0 = R0; r0 < R1; r0 += kFRows) {
-      const int r1 = min(R1, r0 + kFRows);
+    for (int r0 = R0; r0 < R1; r0 += FR) {
+      const int r1 = min(R1, r0 + FR);
       put(r0, r1, true);
       lds_sync();
-      epilogue_rows<BF, EPI, COH>(p, F, kFStride, group * kPairsS, kPairsS, r0, r1);
+      epilogue_rows<BF, EPI, COH>(p, F, FS, group * PG, PG, r0, r1);
       lds_sync();
     }
   }
