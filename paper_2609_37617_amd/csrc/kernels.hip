@@ -105,9 +105,9 @@ hipError_t launch_embed(bool bf16, const RowDesc* rows, int M, const void* embed
 // activation fragments issued 2 to 4 k-steps ahead of their use.  The
 // streaming must reach every compute unit (each keeps a bounded amount of
 // memory traffic in flight), so narrow matrices are split along k.  More rows
-// (staged path): one workgroup per (4 tile pairs, k-split), activations
-// staged through LDS.  Both paths add every element in the same order, so
-// a row's result does not depend on M.  With KS > 1 each split writes a
+// (staged path): one workgroup per (4 or 8 tile pairs, k-split, row group),
+// activations staged through LDS.  Both paths add every element in the same
+// order, so a row's result does not depend on M.  With KS > 1 each split writes a
 // float32 partial and the last workgroup of the tile (device-scope
 // counter) sums the partials in split order and runs the fused epilogue.
 
@@ -190,8 +190,9 @@ __device__ __forceinline__ int xcd_contiguous(int b, int n) {
 // With row groups, the RG blocks of one (pair group, split) run on one XCD
 // at about the same time (xcd_contiguous), so its weight tiles come from
 // memory once and from that XCD's L2 for the other row groups.
-// Row groups (up to three row tiles) fit four workgroups per compute unit;
-// more rows need the whole register file.
+// Row groups (up to three row tiles) fit four workgroups per compute unit,
+// or two with two pairs per wave (NPW = 2: a pair group of 8 pairs); more
+// rows need the whole register file.
 template <bool BF, int MT, int AM, int EPI, int NPW = 1>
 __global__ __launch_bounds__(256, NPW > 1 ? 2 : MT <= kStagedGroupMT ? 4 : 1) void gemm_staged_kernel(const GemmArgs p,
                                                                                                     const int RG) {
