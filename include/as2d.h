@@ -12,7 +12,9 @@
  *
  * Conventions for every call:
  *   - Return value: AS2D_OK (0) or a negative AS2D_E* code.  Outputs are
- *     written only on success; as2d_last_error() then holds a message.
+ *     written only on success; on failure as2d_last_error(ctx) holds a
+ *     message (for a failed as2d_load_weights, which leaves no context,
+ *     as2d_last_error(NULL) on the same thread).
  *   - Host pointers are owned by the caller and only read (or written, for
  *     outputs) during the call; the library copies what it keeps.
  *   - All device memory (packed weights, KV cache slots, scratch) is owned
@@ -125,7 +127,13 @@ int as2d_decode_one(as2d_ctx* ctx, int32_t req, as2d_verify_out* out);
  * reqs[i], ks[i] as in as2d_verify; cands_flat holds the requests'
  * candidates back to back (sum of ks entries).  Each request's rows attend
  * only to its own cache slot.  outs[i] receives request i's result.
- * sum(ks[i] + 1) <= max_requests * (max_k + 1).
+ * sum(ks[i] + 1) <= 144.
+ * Non-finite logits are a per-request outcome: a request with a
+ * non-finite logit in any of its rows keeps its state and gets
+ * accepted_len = correction_token = -1, the other requests are committed
+ * as usual, their outs written, and the call returns AS2D_ENUMERIC
+ * (as2d_verify and as2d_decode_one, one request each, then write
+ * *out the same way).
  */
 int as2d_verify_batch(as2d_ctx* ctx, int32_t n, const int32_t* reqs, const int32_t* cands_flat,
                       const int32_t* ks, as2d_verify_out* outs);
@@ -143,6 +151,13 @@ int as2d_get_logits(as2d_ctx* ctx, int32_t req, float* host, int32_t max_rows, i
 
 /* Greedy token of every row of `req`'s last call: host[max_rows]. */
 int as2d_get_row_tokens(as2d_ctx* ctx, int32_t req, int32_t* host, int32_t max_rows, int32_t* n_rows);
+
+/* Top-2 logit margin of every row of `req`'s last call: host[max_rows]
+ * receives the largest logit minus the second-largest (0 when two token
+ * ids tie for the maximum), computed on the device beside the arg-max, so
+ * a caller can flag near-tied decisions (Appendix F.6 records near-tied
+ * top-1 differences across backends) without fetching logits. */
+int as2d_get_row_margins(as2d_ctx* ctx, int32_t req, float* host, int32_t max_rows, int32_t* n_rows);
 
 /* How verification passes run; results are bit-identical in every mode.
  *   AS2D_EXEC_EAGER:      one kernel launch per operation (no graph);
@@ -181,22 +196,20 @@ int as2d_get_state(as2d_ctx* ctx, int32_t req, int32_t* kv_len, int32_t* root, i
  * float32 for every model dtype. */
 int as2d_read_kv(as2d_ctx* ctx, int32_t req, int32_t layer, void* host_k, void* host_v, int32_t n_tok);
 
-/* Mark a slot free (its state is discarded). */
 /* Rebind the context to another stream (hip_stream = NULL: a stream of its
- * own).  Waits for the old stream, drops cached graphs, and sizes the
- * balanced GEMM grids (one workgroup per usable CU) and the persistent
- * kernel's grid to the CUs the new stream may use: a stream made with
- * hipExtStreamCreateWithCUMask confines the context to part of the device
- * (e.g. a drafter beside the target).  Split counts, and so every result,
- * stay as they were.  as2d_load_weights sizes them the same way for the
- * stream it is given. */
+ * own).  Waits for the old stream and drops cached graphs.  A stream
+ * confined to part of the device by a CU mask is refused (AS2D_EINVAL);
+ * as2d_load_weights refuses one the same way.  Results do not depend on
+ * the stream. */
 int as2d_set_stream(as2d_ctx* ctx, void* hip_stream);
-/* Size the balanced GEMM grids for `cus` compute units (1 .. the stream's;
- * 0 restores all of them): each such GEMM then runs cus workgroups of one
- * CU each, leaving the other CUs to work on other streams (a drafter beside
- * the target).  Split counts, and so every result, are unchanged.  Drops
- * cached graphs. */
+/* Size the balanced GEMM grids (and the persistent kernel's) for `cus`
+ * compute units (1 .. the device's; 0 restores all of them): each such
+ * GEMM then runs cus workgroups of one CU each, leaving the other CUs to
+ * work on other streams (a drafter beside the target).  Split counts, and
+ * so every result, are unchanged.  Waits for the stream and drops cached
+ * graphs and per-pass argument arrays. */
 int as2d_set_cu_budget(as2d_ctx* ctx, int32_t cus);
+/* Mark a slot free (its state is discarded). */
 int as2d_release_request(as2d_ctx* ctx, int32_t req);
 
 /*
@@ -347,7 +360,11 @@ int as2d_verify_from_buffer(as2d_ctx* ctx, int32_t req, const as2d_cbuf* buf, as
  * Every producer step (kind 0, tokens 1) and verifier call (kind 1, tokens
  * committed) is logged into log[log_cap] as a closed interval in ns from
  * the start of the run (host steady clock, around the synchronous call);
- * *n_log entries, *total_ns the whole run.  `buf` and `cur` must be fresh
+ * *n_log entries, *total_ns the whole run.  Before the producer thread
+ * starts, the call captures (under each context's execution mode) every
+ * verification graph the two threads will launch: the target's passes of
+ * 1..budget + 1 rows and the drafter's one-row step, so no graph is captured
+ * while the other thread runs.  `buf` and `cur` must be fresh
  * (nothing published, cursor 0).  A producer error stops the producer only
  * (*producer_rc); the verifier then continues alone.  Errors: as for
  * as2d_verify; AS2D_ECAPACITY when the log is too small.

@@ -20,6 +20,7 @@ F32, BF16 = 0, 1
 # Every symbol include/as2d.h declares.
 EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_one",
            "as2d_verify_batch", "as2d_set_keep_logits", "as2d_get_logits", "as2d_get_row_tokens",
+           "as2d_get_row_margins",
            "as2d_rollback", "as2d_get_state", "as2d_read_kv", "as2d_release_request",
            "as2d_set_exec_mode", "as2d_get_exec_info", "as2d_set_step_trace", "as2d_step_trace_read",
            "as2d_set_timing", "as2d_timing_read", "as2d_timing_reset", "as2d_time_gemm",
@@ -94,6 +95,7 @@ def load_library(path: str = LIB_PATH):
     lib.as2d_set_keep_logits.argtypes = [_P, _I]
     lib.as2d_get_logits.argtypes = [_P, _I, _P, _I, ctypes.POINTER(_I)]
     lib.as2d_get_row_tokens.argtypes = [_P, _I, _P, _I, ctypes.POINTER(_I)]
+    lib.as2d_get_row_margins.argtypes = [_P, _I, _P, _I, ctypes.POINTER(_I)]
     lib.as2d_rollback.argtypes = [_P, _I, _I, _I]
     lib.as2d_get_state.argtypes = [_P, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)]
     lib.as2d_read_kv.argtypes = [_P, _I, _I, _P, _P, _I]
@@ -160,7 +162,7 @@ class Model:
         rc = self.lib.as2d_load_weights(ctypes.byref(cfg), arr, len(self._keep), stream, ctypes.byref(ctx))
         self._keep = None
         if rc != OK:
-            raise As2dError(rc, "as2d_load_weights failed (see argument checks in include/as2d.h)")
+            raise As2dError(rc, self.lib.as2d_last_error(None).decode())
         self.ctx = ctx
 
     def close(self):
@@ -214,6 +216,19 @@ class Model:
         self._check(self.lib.as2d_verify_batch(self.ctx, n, _ptr(r), _ptr(flat), _ptr(ks), outs))
         return [o.as_dict() for o in outs]
 
+    def verify_batch_status(self, reqs: Sequence[int], cands: Sequence[Sequence[int]]):
+        """as2d_verify_batch returning (status, per-request results) without
+        raising: with AS2D_ENUMERIC the requests whose logits are finite are
+        committed and the others report accepted_len -1."""
+        n = len(reqs)
+        r = np.ascontiguousarray(reqs, dtype=np.int32)
+        ks = np.array([len(c) for c in cands], dtype=np.int32)
+        flat = np.ascontiguousarray(np.concatenate([np.asarray(c, dtype=np.int32) for c in cands])
+                                    if ks.sum() else np.zeros(1, np.int32), dtype=np.int32)
+        outs = (VerifyOut * n)()
+        rc = self.lib.as2d_verify_batch(self.ctx, n, _ptr(r), _ptr(flat), _ptr(ks), outs)
+        return rc, [o.as_dict() for o in outs]
+
     def set_keep_logits(self, on: bool):
         self._check(self.lib.as2d_set_keep_logits(self.ctx, int(on)))
 
@@ -228,6 +243,13 @@ class Model:
         n = _I()
         self._check(self.lib.as2d_get_row_tokens(self.ctx, req, _ptr(buf), max_rows, ctypes.byref(n)))
         return [int(t) for t in buf[:n.value]]
+
+    def row_margins(self, req: int, max_rows: int = 32) -> np.ndarray:
+        """Top-2 logit margin of every row of the last call (device-side)."""
+        buf = np.empty(max_rows, dtype=np.float32)
+        n = _I()
+        self._check(self.lib.as2d_get_row_margins(self.ctx, req, _ptr(buf), max_rows, ctypes.byref(n)))
+        return buf[:n.value].copy()
 
     def rollback(self, req: int, kv_len: int, root: int):
         self._check(self.lib.as2d_rollback(self.ctx, req, kv_len, root))

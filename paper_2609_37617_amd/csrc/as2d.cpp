@@ -16,6 +16,7 @@
 #include <tuple>
 #include <vector>
 
+#include "internal.h"
 #include "kernels.h"
 
 using namespace as2d;
@@ -36,6 +37,24 @@ struct ReqState {
   int active = 0, kv_len = 0, prefix_len = 0, root = -1;
   int last_row_start = 0, last_rows = 0;
   int last_logits = 0;  // logits of the last call are in the device buffer
+};
+
+// Device memory one forward pass works in besides the weights and the KV
+// cache: activations, split-K and attention partials, arg-max partials,
+// counters and the pass's descriptors and results.  A context holds one
+// set sized for its largest pass; the launcher takes the set as an
+// argument.
+struct PassBufs {
+  float *x = nullptr, *q = nullptr, *logits = nullptr, *sumsq = nullptr;
+  float *amax_val = nullptr, *amax_val2 = nullptr, *row_margin = nullptr;
+  float *part = nullptr, *pacc = nullptr, *pml = nullptr;
+  int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr, *row_bad = nullptr, *fin_counters = nullptr;
+  void *xg = nullptr, *attn = nullptr, *hbuf = nullptr;  // activation planes
+  long long xg_plane = 0, attn_plane = 0, h_plane = 0;    // offset of the lo plane (bf16), elements
+  int part_rows = 0;                                      // row stride of the attention partials
+  RowDesc* d_rows = nullptr;
+  ReqDesc* d_reqs = nullptr;  // [2 * max_requests]: attention requests, then finish requests
+  StepOut* d_out = nullptr;
 };
 
 enum Kind { K_EMBED, K_QKV, K_ATTN, K_O, K_GU, K_DOWN, K_LM, K_FINISH, K_STEP, K_COUNT };
@@ -63,23 +82,18 @@ struct as2d_ctx {
   float *kc = nullptr, *vc = nullptr;  // float32 KV cache
   long long slot_stride = 0, layer_stride = 0;
 
-  float *x = nullptr, *q = nullptr, *logits = nullptr, *sumsq = nullptr, *amax_val = nullptr;
-  float *part = nullptr, *pacc = nullptr, *pml = nullptr, *rope_cs = nullptr;
-  int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr, *row_bad = nullptr;
-  int* fin_counters = nullptr;
-  void *xg = nullptr, *attn = nullptr, *hbuf = nullptr, *audio = nullptr;  // activation planes
-  long long xg_plane = 0, attn_plane = 0, h_plane = 0;
+  PassBufs b;                 // the context's pass buffers
+  float* rope_cs = nullptr;   // rotary table [max_kv_len][head_dim / 2][2]
+  void* audio = nullptr;      // audio rows of the prefill being run
   size_t audio_cap = 0;
   int n_chunks_cap = 0;
   int max_rows = 0;
 
-  RowDesc* d_rows = nullptr;
-  ReqDesc* d_reqs = nullptr;  // [2 * max_requests]: attention requests, then finish requests
-  StepOut* d_out = nullptr;
   RowDesc* h_rows = nullptr;
   ReqDesc* h_reqs = nullptr;
   StepOut* h_out = nullptr;
   int* h_tok = nullptr;
+  float* h_margin = nullptr;
 
   std::vector<ReqState> reqs;
   int keep_logits = 0;
@@ -100,6 +114,7 @@ struct as2d_ctx {
   int rg_grid = 448;     // staged GEMMs: least grid for row groups of 2-3 tiles
   int n_phase = 0;
   std::map<int, StepLayer*> step_layers;  // by M: device array of per-layer arguments
+  int cu_budget = 0;                      // as2d_set_cu_budget (0: all compute units)
   int h_err = 0;
   long long* ptrace = nullptr;  // persistent-kernel timeline (as2d_set_step_trace)
   int trace_on = 0;
@@ -112,6 +127,10 @@ struct as2d_ctx {
 };
 
 namespace {
+
+// Message of the last as2d_load_weights failure on this thread (there is
+// no context to hold it): as2d_last_error(NULL) returns it.
+thread_local std::string t_load_err;
 
 int fail(as2d_ctx* c, int code, const char* fmt, ...) {
   if (c) {
@@ -169,15 +188,24 @@ GemmPlan make_plan(int N, int K, int KE, int target, int ks_override = 0) {
   return p;
 }
 
-// CUs a stream may use: the population of its CU mask, or dev_cus when
-// the mask cannot be read.
-int stream_cus(hipStream_t s, int dev_cus) {
+// Whether a stream is confined to part of the device by a CU mask
+// (hipExtStreamCreateWithCUMask).  Such streams are refused: the first
+// concurrent run on masked streams ended in a host segmentation fault whose
+// cause has not been found, so the library never runs on one.  A stream
+// whose mask cannot be read is taken as unrestricted.
+const char* const kRestrictedStream =
+    "streams restricted by a CU mask are not supported (use as2d_set_cu_budget to share the device)";
+bool stream_restricted(hipStream_t s) {
+  int dev = 0, dev_cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || dev_cus < 1)
+    return false;
   uint32_t mask[32] = {0};
   const uint32_t words = (uint32_t)((dev_cus + 31) / 32);
-  if (words < 1 || words > 32 || hipExtStreamGetCUMask(s, words, mask) != hipSuccess) return dev_cus;
+  if (words > 32 || hipExtStreamGetCUMask(s, words, mask) != hipSuccess) return false;
   int n = 0;
   for (uint32_t i = 0; i < words; ++i) n += __builtin_popcount(mask[i]);
-  return n > 0 && n <= dev_cus ? n : dev_cus;
+  return n > 0 && n < dev_cus;
 }
 
 // Workgroups of a balanced plan for `cus` compute units: one per CU, at
@@ -284,7 +312,8 @@ int check_req(as2d_ctx* c, int req) {
   return AS2D_OK;
 }
 
-GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
+GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M, const PassBufs* bp = nullptr) {
+  const PassBufs& B = bp ? *bp : c->b;
   GemmArgs a{};
   a.W = W;
   a.N = pl.N;
@@ -298,13 +327,13 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
   a.M = M;
   a.MT = (M + 15) / 16;
   a.rg_grid = c->rg_grid;
-  a.sumsq = c->sumsq;
+  a.sumsq = B.sumsq;
   a.n_norm_pairs = c->cfg.hidden / kPairCols;
   a.a_plane = 0;
   a.eps = c->cfg.rms_eps;
-  a.part = c->part;
-  a.counters = c->counters;
-  a.rows = c->d_rows;
+  a.part = B.part;
+  a.counters = B.counters;
+  a.rows = B.d_rows;
   return a;
 }
 
@@ -313,15 +342,16 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M) {
 // finish requests (d_reqs[max_requests..)) covering fin_rows rows;
 // with_head = run the LM head and verification.  max_chunks bounds the
 // attention key chunks (chunks past a request's keys exit at once).
-int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool with_head, int max_chunks) {
+int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int fin_rows, bool with_head,
+                int max_chunks) {
   const as2d_config& g = c->cfg;
   hipStream_t s = c->stream;
   const bool bf = c->bf16;
   const int mr = g.max_requests;
   {
     Timed t(c, K_EMBED);
-    HIP_TRY(c, launch_embed(bf, c->d_rows, M, c->embed, c->audio, g.hidden, c->layers[0].g_attn, c->x,
-                            c->sumsq, c->xg, c->xg_plane, s));
+    HIP_TRY(c, launch_embed(bf, B.d_rows, M, c->embed, c->audio, g.hidden, c->layers[0].g_attn, B.x,
+                            B.sumsq, B.xg, B.xg_plane, s));
   }
   const int d = g.head_dim;
   for (int l = 0; l < g.n_layers; ++l) {
@@ -330,11 +360,11 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
     float* vc = c->vc + (size_t)l * c->layer_stride;
     const float* g_next = l + 1 < g.n_layers ? c->layers[l + 1].g_attn : c->g_final;
     {
-      GemmArgs a = base_args(c, c->p_qkv, w.qkv, M);
-      a.A = c->xg;
-      a.a_plane = c->xg_plane;
+      GemmArgs a = base_args(c, c->p_qkv, w.qkv, M, &B);
+      a.A = B.xg;
+      a.a_plane = B.xg_plane;
       a.bias = w.bias;
-      a.q_out = c->q;
+      a.q_out = B.q;
       a.k_cache = kc;
       a.v_cache = vc;
       a.slot_stride = c->slot_stride;
@@ -348,78 +378,80 @@ int launch_pass(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool wit
     }
     {
       AttnArgs a{};
-      a.q = c->q;
+      a.q = B.q;
       a.k_cache = kc;
       a.v_cache = vc;
       a.slot_stride = c->slot_stride;
       a.kv_cap = g.max_kv_len;
-      a.rows = c->d_rows;
-      a.reqs = c->d_reqs;
+      a.rows = B.d_rows;
+      a.reqs = B.d_reqs;
       a.n_q = g.n_q_heads;
       a.n_kv = g.n_kv_heads;
       a.head_dim = d;
       a.scale = 1.0f / std::sqrt((float)d);
-      a.pacc = c->pacc;
-      a.pml = c->pml;
-      a.n_chunks_cap = c->n_chunks_cap;
-      a.out = c->attn;
-      a.out_plane = c->attn_plane;
+      a.pacc = B.pacc;
+      a.pml = B.pml;
+      a.part_rows = B.part_rows;
+      a.out = B.attn;
+      a.out_plane = B.attn_plane;
       a.M = M;
       a.row_groups = (M + kAttnRowGroup - 1) / kAttnRowGroup;   // a function of the graph key
       Timed t(c, K_ATTN);
       HIP_TRY(c, launch_attention(bf, a, n_att, max_chunks, s));
     }
     {
-      GemmArgs a = base_args(c, c->p_o, w.o, M);
-      a.A = c->attn;
-      a.a_plane = c->attn_plane;
-      a.x = c->x;
-      a.x_out = c->x;
-      a.sumsq_out = c->sumsq;
+      GemmArgs a = base_args(c, c->p_o, w.o, M, &B);
+      a.A = B.attn;
+      a.a_plane = B.attn_plane;
+      a.x = B.x;
+      a.x_out = B.x;
+      a.sumsq_out = B.sumsq;
       a.gain_next = w.g_mlp;
-      a.out = c->xg;
-      a.out_plane = c->xg_plane;
+      a.out = B.xg;
+      a.out_plane = B.xg_plane;
       Timed t(c, K_O);
       HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_RESID, a, s));
     }
     {
-      GemmArgs a = base_args(c, c->p_gu, w.gu, M);
-      a.A = c->xg;
-      a.a_plane = c->xg_plane;
-      a.out = c->hbuf;
-      a.out_plane = c->h_plane;
+      GemmArgs a = base_args(c, c->p_gu, w.gu, M, &B);
+      a.A = B.xg;
+      a.a_plane = B.xg_plane;
+      a.out = B.hbuf;
+      a.out_plane = B.h_plane;
       Timed t(c, K_GU);
       HIP_TRY(c, launch_gemm(bf, A_NORM, EPI_SWIGLU, a, s));
     }
     {
-      GemmArgs a = base_args(c, c->p_down, w.down, M);
-      a.A = c->hbuf;
-      a.a_plane = c->h_plane;
-      a.x = c->x;
-      a.x_out = c->x;
-      a.sumsq_out = c->sumsq;
+      GemmArgs a = base_args(c, c->p_down, w.down, M, &B);
+      a.A = B.hbuf;
+      a.a_plane = B.h_plane;
+      a.x = B.x;
+      a.x_out = B.x;
+      a.sumsq_out = B.sumsq;
       a.gain_next = g_next;
-      a.out = c->xg;
-      a.out_plane = c->xg_plane;
+      a.out = B.xg;
+      a.out_plane = B.xg_plane;
       Timed t(c, K_DOWN);
-      HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_RESID, a, s));
+      HIP_TRY(c, launch_gemm(bf, A_PLAIN, EPI_DOWN, a, s));
     }
   }
   if (with_head) {
     {
-      GemmArgs a = base_args(c, c->p_lm, c->lm, M);
-      a.A = c->xg;
-      a.a_plane = c->xg_plane;
-      a.logits = c->keep_logits ? c->logits : nullptr;
-      a.amax_val = c->amax_val;
-      a.amax_idx = c->amax_idx;
+      GemmArgs a = base_args(c, c->p_lm, c->lm, M, &B);
+      a.A = B.xg;
+      a.a_plane = B.xg_plane;
+      a.logits = c->keep_logits ? B.logits : nullptr;
+      a.amax_val = B.amax_val;
+      a.amax_val2 = B.amax_val2;
+      a.amax_idx = B.amax_idx;
       Timed t(c, K_LM);
       HIP_TRY(c, launch_gemm(bf, A_NORM, EPI_ARGMAX, a, s));
     }
     {
       Timed t(c, K_FINISH);
-      HIP_TRY(c, launch_finish(c->d_rows, c->d_reqs + mr, n_fin, fin_rows, c->amax_val, c->amax_idx,
-                               g.vocab / kPairCols, c->row_tok, c->row_bad, c->fin_counters, c->d_out, s));
+      HIP_TRY(c, launch_finish(B.d_rows, B.d_reqs + mr, n_fin, fin_rows, B.amax_val, B.amax_val2, B.amax_idx,
+                               g.vocab / kPairCols, B.row_tok, B.row_bad, B.row_margin, B.fin_counters,
+                               B.d_out, s));
     }
   }
   return AS2D_OK;
@@ -467,15 +499,15 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     a.v_cache = vc;
     a.slot_stride = c->slot_stride;
     a.kv_cap = g.max_kv_len;
-    a.rows = c->d_rows;
-    a.reqs = c->d_reqs;
+    a.rows = c->b.d_rows;
+    a.reqs = c->b.d_reqs;
     a.n_q = nq;
     a.n_kv = nkv;
     a.head_dim = d;
     a.scale = 1.0f / std::sqrt((float)d);
-    a.pacc = c->pacc;
-    a.pml = c->pml;
-    a.n_chunks_cap = c->n_chunks_cap;
+    a.pacc = c->b.pacc;
+    a.pml = c->b.pml;
+    a.part_rows = c->b.part_rows;
     a.out = (char*)c->pattn + l * qs * 4;
     a.row_groups = 1;
     a.out_plane = c->bf16 ? (long long)qs : 0;
@@ -535,11 +567,12 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   a.lm.a_plane = c->bf16 ? (long long)xs : 0;
   a.lm.sumsq = c->psumsq + 2 * L * ss;
   a.lm.counters = c->psplit + (size_t)(4 * L) * c->split_stride;
-  a.lm.logits = c->keep_logits ? c->logits : nullptr;
-  a.lm.amax_val = c->amax_val;
-  a.lm.amax_idx = c->amax_idx;
+  a.lm.logits = c->keep_logits ? c->b.logits : nullptr;
+  a.lm.amax_val = c->b.amax_val;
+  a.lm.amax_val2 = c->b.amax_val2;
+  a.lm.amax_idx = c->b.amax_idx;
   a.M = M;
-  a.rows = c->d_rows;
+  a.rows = c->b.d_rows;
   a.embed = c->embed;
   a.audio = c->audio;
   a.hidden = H;
@@ -548,15 +581,16 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   a.sumsq0 = c->psumsq;
   a.xg0 = c->pxg;
   a.xg0_plane = c->bf16 ? (long long)xs : 0;
-  a.reqs = c->d_reqs;
+  a.reqs = c->b.d_reqs;
   a.n_reqs = n_att;
   a.n_q = g.n_q_heads;
-  a.fin_reqs = c->d_reqs + g.max_requests;
+  a.fin_reqs = c->b.d_reqs + g.max_requests;
   a.n_fin = n_fin;
   a.fin_rows = fin_rows;
-  a.row_tok = c->row_tok;
-  a.row_bad = c->row_bad;
-  a.out = c->d_out;
+  a.row_tok = c->b.row_tok;
+  a.row_bad = c->b.row_bad;
+  a.row_margin = c->b.row_margin;
+  a.out = c->b.d_out;
   // completion signals of a GEMM phase: one per workgroup of a balanced
   // plan, else one per tile pair
   const int grid = c->pers_grid[(M + 15) / 16];
@@ -584,6 +618,39 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   return AS2D_OK;
 }
 
+// The executable graph of a verification pass of M rows over n_att
+// requests (fin_rows rows verified), captured on first use.  Kernel
+// arguments hold only pointers and sizes (the row and request descriptors
+// are read from device memory when the graph runs) and the attention grid
+// covers the slot capacity, so one graph serves every pass of that shape.
+int graph_for(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool persistent, hipGraphExec_t* out) {
+  const auto key = std::make_tuple((int)persistent, M, n_att, c->keep_logits);
+  auto it = c->graphs.find(key);
+  if (it == c->graphs.end()) {
+    if (c->graphs.size() >= 64) {
+      for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
+      c->graphs.clear();
+    }
+    hipGraph_t gr = nullptr;
+    HIP_TRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
+    int rc = persistent ? launch_persistent(c, M, n_att, n_fin, fin_rows)
+                        : launch_pass(c, c->b, M, n_att, n_fin, fin_rows, true, c->n_chunks_cap);
+    hipError_t e = hipStreamEndCapture(c->stream, &gr);
+    if (rc) {
+      if (gr) hipGraphDestroy(gr);
+      return rc;
+    }
+    if (e != hipSuccess) return fail(c, AS2D_EHIP, "graph capture: %s", hipGetErrorString(e));
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, gr, nullptr, nullptr, 0);
+    hipGraphDestroy(gr);
+    if (e != hipSuccess) return fail(c, AS2D_EHIP, "graph instantiate: %s", hipGetErrorString(e));
+    it = c->graphs.emplace(key, ex).first;
+  }
+  *out = it->second;
+  return AS2D_OK;
+}
+
 // One forward pass over the rows and requests in h_rows / h_reqs (see
 // launch_pass).  Verification passes run as a captured HIP graph, one per
 // (rows, requests, keep_logits); the attention grid then covers the slot
@@ -594,8 +661,8 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool v
   const int mr = g.max_requests;
   int fin_rows = 0;
   for (int r = 0; r < n_fin; ++r) fin_rows += c->h_reqs[mr + r].W;
-  HIP_TRY(c, hipMemcpyAsync(c->d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
-  HIP_TRY(c, hipMemcpyAsync(c->d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(c->b.d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(c->b.d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
   int max_chunks = 1;
   for (int r = 0; r < n_att; ++r) {
     const int nk = c->h_reqs[r].L0 + c->h_reqs[r].W;
@@ -606,42 +673,21 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool v
   const bool persistent = verify_pass && c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && M <= kStepRows;
   const bool graph = verify_pass && c->exec_mode != AS2D_EXEC_EAGER && !c->timing;
   if (persistent && !step_layers_for(c, M)) return fail(c, AS2D_ENOMEM, "persistent step arguments");
-  auto launch = [&](bool capture) -> int {
-    if (persistent) return launch_persistent(c, M, n_att, n_fin, fin_rows);
-    return launch_pass(c, M, n_att, n_fin, fin_rows, with_head, capture ? c->n_chunks_cap : max_chunks);
-  };
   if (graph) {
-    const auto key = std::make_tuple((int)persistent, M, n_att, c->keep_logits);
-    auto it = c->graphs.find(key);
-    if (it == c->graphs.end()) {
-      if (c->graphs.size() >= 64) {
-        for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
-        c->graphs.clear();
-      }
-      hipGraph_t gr = nullptr;
-      HIP_TRY(c, hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
-      int rc = launch(true);
-      hipError_t e = hipStreamEndCapture(s, &gr);
-      if (rc) {
-        if (gr) hipGraphDestroy(gr);
-        return rc;
-      }
-      if (e != hipSuccess) return fail(c, AS2D_EHIP, "graph capture: %s", hipGetErrorString(e));
-      hipGraphExec_t ex = nullptr;
-      e = hipGraphInstantiate(&ex, gr, nullptr, nullptr, 0);
-      hipGraphDestroy(gr);
-      if (e != hipSuccess) return fail(c, AS2D_EHIP, "graph instantiate: %s", hipGetErrorString(e));
-      it = c->graphs.emplace(key, ex).first;
-    }
-    HIP_TRY(c, hipGraphLaunch(it->second, s));
+    hipGraphExec_t ex = nullptr;
+    int rc = graph_for(c, M, n_att, n_fin, fin_rows, persistent, &ex);
+    if (rc) return rc;
+    HIP_TRY(c, hipGraphLaunch(ex, s));
   } else {
-    int rc = launch(false);
+    int rc = persistent ? launch_persistent(c, M, n_att, n_fin, fin_rows)
+                        : launch_pass(c, c->b, M, n_att, n_fin, fin_rows, with_head, max_chunks);
     if (rc) return rc;
   }
   if (persistent) HIP_TRY(c, hipMemcpyAsync(&c->h_err, c->perr, sizeof(int), hipMemcpyDeviceToHost, s));
   if (with_head) {
-    HIP_TRY(c, hipMemcpyAsync(c->h_out, c->d_out, sizeof(StepOut) * n_fin, hipMemcpyDeviceToHost, s));
-    HIP_TRY(c, hipMemcpyAsync(c->h_tok, c->row_tok, sizeof(int) * M, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipMemcpyAsync(c->h_out, c->b.d_out, sizeof(StepOut) * n_fin, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipMemcpyAsync(c->h_tok, c->b.row_tok, sizeof(int) * M, hipMemcpyDeviceToHost, s));
+    HIP_TRY(c, hipMemcpyAsync(c->h_margin, c->b.row_margin, sizeof(float) * M, hipMemcpyDeviceToHost, s));
   }
   HIP_TRY(c, hipStreamSynchronize(s));
   timing_collect(c);
@@ -652,6 +698,24 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool v
   }
   return AS2D_OK;
 }
+
+}  // namespace
+
+int as2d_prepare_graphs(as2d_ctx* c, int32_t max_rows) {
+  if (!c || max_rows < 1) return AS2D_EINVAL;
+  if (c->exec_mode == AS2D_EXEC_EAGER || c->timing) return AS2D_OK;   // no graphs in these modes
+  max_rows = std::min(max_rows, c->cfg.max_k + 1);
+  for (int M = 1; M <= max_rows; ++M) {
+    const bool persistent = c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && M <= kStepRows;
+    if (persistent && !step_layers_for(c, M)) return fail(c, AS2D_ENOMEM, "persistent step arguments");
+    hipGraphExec_t ex = nullptr;
+    const int rc = graph_for(c, M, 1, 1, M, persistent, &ex);
+    if (rc) return rc;
+  }
+  return AS2D_OK;
+}
+
+namespace {
 
 int upload_matrix(as2d_ctx* c, void* tmp, const void* host, size_t rows, size_t cols) {
   HIP_TRY(c, hipMemcpyAsync(tmp, host, rows * cols * c->es, hipMemcpyHostToDevice, c->stream));
@@ -665,6 +729,135 @@ int pack(as2d_ctx* c, uint4** out, const void* tmp, int N, int K, int map, int a
   return AS2D_OK;
 }
 
+// Forget everything captured from the current launch parameters: the
+// verification graphs (grids are kernel launch parameters) and the
+// persistent kernel's per-layer argument arrays (they hold each plan's
+// grid).  Called after a grid change, with the stream idle.
+void drop_launch_state(as2d_ctx* c) {
+  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
+  c->graphs.clear();
+  for (auto& kv : c->step_layers) {
+    auto it = std::find(c->allocs.begin(), c->allocs.end(), (void*)kv.second);
+    if (it != c->allocs.end()) c->allocs.erase(it);
+    hipFree(kv.second);
+  }
+  c->step_layers.clear();
+}
+
+// Balanced GEMM grids and the persistent kernel's grid for `cus` compute
+// units (0: the whole device).  Split counts, and so every result, do not
+// depend on it.
+int set_grids(as2d_ctx* c, int cus) {
+  int dev = 0, dev_cus = 0;
+  HIP_TRY(c, hipGetDevice(&dev));
+  HIP_TRY(c, hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev));
+  const int n = cus > 0 ? std::min(cus, dev_cus) : dev_cus;
+  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, n);
+  if (c->pers_ok)
+    for (int mt = 1; mt <= 2; ++mt) c->pers_grid[mt] = n;
+  return AS2D_OK;
+}
+
+// Checks the arguments of a verification call of n requests (at most
+// max_rows rows in all) and writes its row and request descriptors into
+// h_rows / h_reqs; *M receives the row count.
+int assemble_verify(as2d_ctx* c, int n, const int32_t* reqs, const int32_t* cands, const int32_t* ks,
+                    const as2d_verify_out* outs, int max_rows, int* M_out) {
+  if (!c) return AS2D_EINVAL;
+  const as2d_config& g = c->cfg;
+  if (n < 1 || n > g.max_requests || !reqs || !ks || !outs) return fail(c, AS2D_EINVAL, "verify: bad arguments");
+  int M = 0, off = 0;
+  const int mr = g.max_requests;
+  for (int r = 0; r < n; ++r) {
+    int rc = check_req(c, reqs[r]);
+    if (rc) return rc;
+    for (int q = 0; q < r; ++q)
+      if (reqs[q] == reqs[r]) return fail(c, AS2D_EINVAL, "verify: request %d listed twice", reqs[r]);
+    const ReqState& st = c->reqs[reqs[r]];
+    if (!st.active) return fail(c, AS2D_ESTATE, "verify: request %d has not been prefilled", reqs[r]);
+    const int k = ks[r];
+    if (k < 0 || k > g.max_k) return fail(c, AS2D_EINVAL, "verify: k=%d outside [0, %d]", k, g.max_k);
+    if (k && !cands) return fail(c, AS2D_EINVAL, "verify: null candidates");
+    for (int i = 0; i < k; ++i)
+      if (cands[off + i] < 0 || cands[off + i] >= g.vocab)
+        return fail(c, AS2D_EINVAL, "verify: candidate id %d out of range", cands[off + i]);
+    if (st.kv_len + k + 1 > g.max_kv_len)
+      return fail(c, AS2D_ECAPACITY, "verify: request %d needs %d positions > %d", reqs[r], st.kv_len + k + 1, g.max_kv_len);
+    M += k + 1;
+    off += k;
+  }
+  if (M > max_rows) return fail(c, AS2D_EINVAL, "verify: %d rows exceed %d", M, max_rows);
+  int row = 0;
+  off = 0;
+  for (int r = 0; r < n; ++r) {
+    const ReqState& st = c->reqs[reqs[r]];
+    const int k = ks[r];
+    for (int i = 0; i <= k; ++i) {
+      RowDesc rd{};
+      rd.token = i == 0 ? st.root : cands[off + i - 1];
+      rd.src = 0;
+      rd.pos = st.kv_len + i;
+      rd.slot = reqs[r];
+      rd.cmp = i < k ? cands[off + i] : -1;
+      c->h_rows[row + i] = rd;
+    }
+    c->h_reqs[r] = ReqDesc{row, k + 1, st.kv_len, reqs[r]};
+    c->h_reqs[mr + r] = c->h_reqs[r];
+    row += k + 1;
+    off += k;
+  }
+  *M_out = M;
+  return AS2D_OK;
+}
+
+// Commits the outcome in h_out of the verification call assembled by
+// assemble_verify: accepted rows stay in the cache, the correction becomes
+// the root; a request with non-finite logits keeps its state.
+int commit_verify(as2d_ctx* c, int n, const int32_t* reqs, const int32_t* ks, as2d_verify_out* outs) {
+  const as2d_config& g = c->cfg;
+  int n_bad = 0, first_bad = -1;
+  for (int r = 0; r < n; ++r) {
+    ReqState& st = c->reqs[reqs[r]];
+    const StepOut& o = c->h_out[r];
+    st.last_row_start = c->h_reqs[r].row_start;
+    st.last_rows = ks[r] + 1;
+    st.last_logits = c->keep_logits;
+    if (o.nan_flag) {
+      // no token can be chosen: this request keeps its state
+      if (!n_bad++) first_bad = reqs[r];
+      outs[r].accepted_len = -1;
+      outs[r].correction_token = -1;
+      outs[r].kv_len = st.kv_len;
+      outs[r].committed = st.kv_len - st.prefix_len;
+      continue;
+    }
+    st.kv_len += o.accepted + 1;
+    st.root = o.correction;
+    outs[r].accepted_len = o.accepted;
+    outs[r].correction_token = o.correction;
+    outs[r].kv_len = st.kv_len;
+    outs[r].committed = st.kv_len - st.prefix_len;
+  }
+  // other requests' last-call rows are no longer in the device buffers
+  for (int q = 0; q < g.max_requests; ++q) {
+    bool in = false;
+    for (int r = 0; r < n; ++r) in |= reqs[r] == q;
+    if (!in) c->reqs[q].last_logits = 0, c->reqs[q].last_rows = 0;
+  }
+  if (n_bad) return fail(c, AS2D_ENUMERIC, "verify: non-finite logits in %d request(s) (first: %d)", n_bad, first_bad);
+  return AS2D_OK;
+}
+
+// Split-K counters a pass may use: one per workgroup tile (at most one per
+// tile pair on the direct path; on the staged path one per (group of
+// kPairsS pairs, row group), at most kMaxMTiles row groups).
+int split_counter_count(const as2d_ctx* c) {
+  int n = 0;
+  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
+    n = std::max({n, p->pairs, (p->pairs / kPairsS) * kMaxMTiles});
+  return n;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -672,7 +865,10 @@ int pack(as2d_ctx* c, uint4** out, const void* tmp, int N, int K, int map, int a
 
 extern "C" {
 
-const char* as2d_last_error(const as2d_ctx* c) { return c ? c->err.c_str() : "null context"; }
+const char* as2d_last_error(const as2d_ctx* c) {
+  if (c) return c->err.c_str();
+  return t_load_err.empty() ? "null context" : t_load_err.c_str();
+}
 
 void as2d_free(as2d_ctx* c) {
   if (!c) return;
@@ -682,6 +878,7 @@ void as2d_free(as2d_ctx* c) {
   if (c->h_reqs) hipHostFree(c->h_reqs);
   if (c->h_out) hipHostFree(c->h_out);
   if (c->h_tok) hipHostFree(c->h_tok);
+  if (c->h_margin) hipHostFree(c->h_margin);
   for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
   for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
   if (c->own_stream && c->stream) hipStreamDestroy(c->stream);
@@ -693,11 +890,18 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   if (!cfg || !host || !out) return AS2D_EINVAL;
   *out = nullptr;
   const as2d_config g = *cfg;
+  t_load_err.clear();
   auto c = new as2d_ctx();
-  auto bad = [&](const char* msg) {
+  // every failure below frees the context; its message stays readable
+  // through as2d_last_error(NULL)
+  auto give_up = [&](int code) {
+    t_load_err = c->err.empty() ? "as2d_load_weights failed" : c->err;
     as2d_free(c);
-    (void)msg;
-    return AS2D_EINVAL;
+    return code;
+  };
+  auto bad = [&](const char* msg) {
+    c->err = std::string("as2d_load_weights: ") + msg;
+    return give_up(AS2D_EINVAL);
   };
   if (g.n_layers < 1 || g.hidden % 128 || g.ffn % 64 || g.vocab % 128 || g.vocab <= 0)
     return bad("shape: need n_layers >= 1, hidden % 128 == 0, ffn % 64 == 0, vocab % 128 == 0");
@@ -735,11 +939,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     c->stream = (hipStream_t)hip_stream;
   } else {
     if (hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking) != hipSuccess) {
-      as2d_free(c);
-      return AS2D_EHIP;
+      c->err = "as2d_load_weights: hipStreamCreateWithFlags failed";
+      return give_up(AS2D_EHIP);
     }
     c->own_stream = true;
   }
+  if (stream_restricted(c->stream)) return bad(kRestrictedStream);
   if (H % KE || (nq * d) % KE || F % KE) return bad("inner dimensions must be multiples of the k-step");
 
   // GEMM plans: k-splits depend on the matrix shape only
@@ -758,11 +963,9 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
                                                 hipSuccess || cus < 1) {
-      fail(c, AS2D_EHIP, "device query");
-      as2d_free(c);
-      return AS2D_EHIP;
+      fail(c, AS2D_EHIP, "as2d_load_weights: device query");
+      return give_up(AS2D_EHIP);
     }
-    cus = stream_cus(c->stream, cus);
     const int sc = env_int("AS2D_SPLIT_COST", 16), ps = env_int("AS2D_SPLIT_COST_PER", 5);
     if (bal & 1) c->p_qkv = balance_plan(c->p_qkv, cus, sc, ps, ks_qkv);
     if (bal & 2) c->p_o = balance_plan(c->p_o, cus, sc, ps, ks_o);
@@ -775,9 +978,8 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   size_t tmp_elems = std::max({(size_t)V * H, (size_t)qkv_n * H, (size_t)2 * F * H, (size_t)H * F});
   void* tmp = nullptr;
   if (hipMalloc(&tmp, tmp_elems * c->es) != hipSuccess) {
-    fail(c, AS2D_ENOMEM, "staging buffer");
-    as2d_free(c);
-    return AS2D_ENOMEM;
+    fail(c, AS2D_ENOMEM, "as2d_load_weights: staging buffer");
+    return give_up(AS2D_ENOMEM);
   }
   auto run = [&]() -> int {
     int ti = 0;
@@ -840,37 +1042,34 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   c->max_rows = kMaxRows;   // rows per pass (prefill chunks, fused batches)
   const int MR = kMaxRows;
   c->n_chunks_cap = (g.max_kv_len + kAttnChunk - 1) / kAttnChunk;
-  CK(dalloc(c, &c->x, (size_t)MR * H * 4));
-  CK(dalloc(c, &c->q, (size_t)MR * nq * d * 4));
+  CK(dalloc(c, &c->b.x, (size_t)MR * H * 4));
+  CK(dalloc(c, &c->b.q, (size_t)MR * nq * d * 4));
   // activation planes: two bf16 planes or one float32 plane, 4 bytes per element either way
-  CK(dalloc(c, &c->xg, (size_t)MR * H * 4));
-  CK(dalloc(c, &c->attn, (size_t)MR * nq * d * 4));
-  CK(dalloc(c, &c->hbuf, (size_t)MR * F * 4));
+  CK(dalloc(c, &c->b.xg, (size_t)MR * H * 4));
+  CK(dalloc(c, &c->b.attn, (size_t)MR * nq * d * 4));
+  CK(dalloc(c, &c->b.hbuf, (size_t)MR * F * 4));
   if (c->bf16) {
-    c->xg_plane = (long long)MR * H;
-    c->attn_plane = (long long)MR * nq * d;
-    c->h_plane = (long long)MR * F;
+    c->b.xg_plane = (long long)MR * H;
+    c->b.attn_plane = (long long)MR * nq * d;
+    c->b.h_plane = (long long)MR * F;
   }
-  CK(dalloc(c, &c->logits, (size_t)MR * V * 4));
-  CK(dalloc(c, &c->sumsq, (size_t)(H / kPairCols) * MR * 4));
-  CK(dalloc(c, &c->amax_val, (size_t)(V / kPairCols) * MR * 4));
-  CK(dalloc(c, &c->amax_idx, (size_t)(V / kPairCols) * MR * 4));
-  CK(dalloc(c, &c->row_tok, (size_t)MR * 4));
-  CK(dalloc(c, &c->row_bad, (size_t)MR * 4));
-  CK(dalloc(c, &c->fin_counters, (size_t)g.max_requests * 4));
-  HIP_TRY(c, hipMemsetAsync(c->fin_counters, 0, (size_t)g.max_requests * 4, c->stream));
+  CK(dalloc(c, &c->b.logits, (size_t)MR * V * 4));
+  CK(dalloc(c, &c->b.sumsq, (size_t)(H / kPairCols) * MR * 4));
+  CK(dalloc(c, &c->b.amax_val, (size_t)(V / kPairCols) * MR * 4));
+  CK(dalloc(c, &c->b.amax_val2, (size_t)(V / kPairCols) * MR * 4));
+  CK(dalloc(c, &c->b.row_margin, (size_t)MR * 4));
+  CK(dalloc(c, &c->b.amax_idx, (size_t)(V / kPairCols) * MR * 4));
+  CK(dalloc(c, &c->b.row_tok, (size_t)MR * 4));
+  CK(dalloc(c, &c->b.row_bad, (size_t)MR * 4));
+  CK(dalloc(c, &c->b.fin_counters, (size_t)g.max_requests * 4));
+  HIP_TRY(c, hipMemsetAsync(c->b.fin_counters, 0, (size_t)g.max_requests * 4, c->stream));
   size_t part_elems = 0;
   for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
     if (p->KS > 1) part_elems = std::max(part_elems, (size_t)p->KS * MR * p->N);
-  CK(dalloc(c, &c->part, part_elems * 4));
-  // split-K counters: one per workgroup tile (at most one per tile pair on
-  // the direct path; on the staged path one per (group of kPairsS pairs,
-  // row group), at most kMaxMTiles row groups)
-  int n_cnt = 0;
-  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
-    n_cnt = std::max({n_cnt, p->pairs, (p->pairs / kPairsS) * kMaxMTiles});
-  CK(dalloc(c, &c->counters, (size_t)n_cnt * 4));
-  HIP_TRY(c, hipMemsetAsync(c->counters, 0, (size_t)n_cnt * 4, c->stream));
+  CK(dalloc(c, &c->b.part, part_elems * 4));
+  const int n_cnt = split_counter_count(c);
+  CK(dalloc(c, &c->b.counters, (size_t)n_cnt * 4));
+  HIP_TRY(c, hipMemsetAsync(c->b.counters, 0, (size_t)n_cnt * 4, c->stream));
   HIP_TRY(c, prepare_kernels());
   // persistent step kernel (verification passes of up to 32 rows; every
   // GEMM on a balanced plan)
@@ -886,7 +1085,6 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     const int L = g.n_layers;
     const long long R = kStepRows;
     if (occ1 > 0 && occ2 > 0) {
-      cus = stream_cus(c->stream, cus);
       c->pers_grid[1] = cus;
       c->pers_grid[2] = cus;
       CK(dalloc(c, &c->px, (size_t)(2 * L + 1) * R * H * 4));
@@ -907,11 +1105,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
       c->pers_ok = true;
     }
   }
-  CK(dalloc(c, &c->pacc, (size_t)c->n_chunks_cap * MR * nq * d * 4));
-  CK(dalloc(c, &c->pml, (size_t)c->n_chunks_cap * MR * nq * 2 * 4));
-  CK(dalloc(c, &c->d_rows, sizeof(RowDesc) * MR));
-  CK(dalloc(c, &c->d_reqs, sizeof(ReqDesc) * 2 * g.max_requests));
-  CK(dalloc(c, &c->d_out, sizeof(StepOut) * g.max_requests));
+  c->b.part_rows = MR;
+  CK(dalloc(c, &c->b.pacc, (size_t)c->n_chunks_cap * MR * nq * d * 4));
+  CK(dalloc(c, &c->b.pml, (size_t)c->n_chunks_cap * MR * nq * 2 * 4));
+  CK(dalloc(c, &c->b.d_rows, sizeof(RowDesc) * MR));
+  CK(dalloc(c, &c->b.d_reqs, sizeof(ReqDesc) * 2 * g.max_requests));
+  CK(dalloc(c, &c->b.d_out, sizeof(StepOut) * g.max_requests));
 
   // rotary table, evaluated in double precision: [pos][i] -> (cos, sin)
   {
@@ -929,7 +1128,8 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   if (hipHostMalloc((void**)&c->h_rows, sizeof(RowDesc) * MR, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->h_reqs, sizeof(ReqDesc) * 2 * g.max_requests, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->h_out, sizeof(StepOut) * g.max_requests, 0) != hipSuccess ||
-      hipHostMalloc((void**)&c->h_tok, sizeof(int) * MR, 0) != hipSuccess) {
+      hipHostMalloc((void**)&c->h_tok, sizeof(int) * MR, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_margin, sizeof(float) * MR, 0) != hipSuccess) {
     return fail(c, AS2D_ENOMEM, "pinned host buffers");
   }
   memset(c->h_reqs, 0, sizeof(ReqDesc) * 2 * g.max_requests);
@@ -938,10 +1138,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return AS2D_OK;
   }();
-  if (rc) {
-    as2d_free(c);
-    return rc;
-  }
+  if (rc) return give_up(rc);
   *out = c;
   return AS2D_OK;
 #undef CK
@@ -1005,6 +1202,9 @@ int as2d_prefill_kv(as2d_ctx* c, int32_t req, const void* audio, int32_t n_audio
   }
   st.active = 1;
   st.kv_len = st.prefix_len = total;
+  // the prefill's passes overwrote the shared logits and row-token buffers
+  for (int q = 0; q < g.max_requests; ++q)
+    if (q != req) c->reqs[q].last_logits = 0, c->reqs[q].last_rows = 0;
   *first_token = st.root;
   *kv_len = total;
   return AS2D_OK;
@@ -1012,73 +1212,11 @@ int as2d_prefill_kv(as2d_ctx* c, int32_t req, const void* audio, int32_t n_audio
 
 int as2d_verify_batch(as2d_ctx* c, int32_t n, const int32_t* reqs, const int32_t* cands,
                       const int32_t* ks, as2d_verify_out* outs) {
-  if (!c) return AS2D_EINVAL;
-  const as2d_config& g = c->cfg;
-  if (n < 1 || n > g.max_requests || !reqs || !ks || !outs) return fail(c, AS2D_EINVAL, "verify: bad arguments");
-  int M = 0, off = 0;
-  const int mr = g.max_requests;
-  for (int r = 0; r < n; ++r) {
-    int rc = check_req(c, reqs[r]);
-    if (rc) return rc;
-    for (int q = 0; q < r; ++q)
-      if (reqs[q] == reqs[r]) return fail(c, AS2D_EINVAL, "verify: request %d listed twice", reqs[r]);
-    const ReqState& st = c->reqs[reqs[r]];
-    if (!st.active) return fail(c, AS2D_ESTATE, "verify: request %d has not been prefilled", reqs[r]);
-    const int k = ks[r];
-    if (k < 0 || k > g.max_k) return fail(c, AS2D_EINVAL, "verify: k=%d outside [0, %d]", k, g.max_k);
-    if (k && !cands) return fail(c, AS2D_EINVAL, "verify: null candidates");
-    for (int i = 0; i < k; ++i)
-      if (cands[off + i] < 0 || cands[off + i] >= g.vocab)
-        return fail(c, AS2D_EINVAL, "verify: candidate id %d out of range", cands[off + i]);
-    if (st.kv_len + k + 1 > g.max_kv_len)
-      return fail(c, AS2D_ECAPACITY, "verify: request %d needs %d positions > %d", reqs[r], st.kv_len + k + 1, g.max_kv_len);
-    M += k + 1;
-    off += k;
-  }
-  if (M > kMaxRows) return fail(c, AS2D_EINVAL, "verify: %d rows exceed %d", M, kMaxRows);
-  int row = 0;
-  off = 0;
-  for (int r = 0; r < n; ++r) {
-    const ReqState& st = c->reqs[reqs[r]];
-    const int k = ks[r];
-    for (int i = 0; i <= k; ++i) {
-      RowDesc rd{};
-      rd.token = i == 0 ? st.root : cands[off + i - 1];
-      rd.src = 0;
-      rd.pos = st.kv_len + i;
-      rd.slot = reqs[r];
-      rd.cmp = i < k ? cands[off + i] : -1;
-      c->h_rows[row + i] = rd;
-    }
-    c->h_reqs[r] = ReqDesc{row, k + 1, st.kv_len, reqs[r]};
-    c->h_reqs[mr + r] = c->h_reqs[r];
-    row += k + 1;
-    off += k;
-  }
-  int rc = run_forward(c, M, n, n, true, true);
+  int M = 0;
+  int rc = assemble_verify(c, n, reqs, cands, ks, outs, kMaxRows, &M);
   if (rc) return rc;
-  for (int r = 0; r < n; ++r)
-    if (c->h_out[r].nan_flag) return fail(c, AS2D_ENUMERIC, "verify: non-finite logits (request %d)", reqs[r]);
-  for (int r = 0; r < n; ++r) {
-    ReqState& st = c->reqs[reqs[r]];
-    const StepOut& o = c->h_out[r];
-    st.kv_len += o.accepted + 1;
-    st.root = o.correction;
-    st.last_row_start = c->h_reqs[r].row_start;
-    st.last_rows = ks[r] + 1;
-    st.last_logits = c->keep_logits;
-    outs[r].accepted_len = o.accepted;
-    outs[r].correction_token = o.correction;
-    outs[r].kv_len = st.kv_len;
-    outs[r].committed = st.kv_len - st.prefix_len;
-  }
-  // other requests' last-call rows are no longer in the device buffers
-  for (int q = 0; q < g.max_requests; ++q) {
-    bool in = false;
-    for (int r = 0; r < n; ++r) in |= reqs[r] == q;
-    if (!in) c->reqs[q].last_logits = 0, c->reqs[q].last_rows = 0;
-  }
-  return AS2D_OK;
+  if ((rc = run_forward(c, M, n, n, true, true))) return rc;
+  return commit_verify(c, n, reqs, ks, outs);
 }
 
 int as2d_verify(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k, as2d_verify_out* out) {
@@ -1103,7 +1241,7 @@ int as2d_get_logits(as2d_ctx* c, int32_t req, float* host, int32_t max_rows, int
   if (!host || !n_rows) return fail(c, AS2D_EINVAL, "get_logits: null pointer");
   if (!st.last_logits || !st.last_rows) return fail(c, AS2D_ESTATE, "get_logits: no logits kept for request %d", req);
   if (max_rows < st.last_rows) return fail(c, AS2D_EINVAL, "get_logits: need %d rows", st.last_rows);
-  HIP_TRY(c, hipMemcpy(host, c->logits + (size_t)st.last_row_start * c->cfg.vocab,
+  HIP_TRY(c, hipMemcpy(host, c->b.logits + (size_t)st.last_row_start * c->cfg.vocab,
                        (size_t)st.last_rows * c->cfg.vocab * 4, hipMemcpyDeviceToHost));
   *n_rows = st.last_rows;
   return AS2D_OK;
@@ -1117,6 +1255,18 @@ int as2d_get_row_tokens(as2d_ctx* c, int32_t req, int32_t* host, int32_t max_row
   if (!st.last_rows) return fail(c, AS2D_ESTATE, "get_row_tokens: no rows for request %d", req);
   if (max_rows < st.last_rows) return fail(c, AS2D_EINVAL, "get_row_tokens: need %d rows", st.last_rows);
   memcpy(host, c->h_tok + st.last_row_start, sizeof(int) * st.last_rows);
+  *n_rows = st.last_rows;
+  return AS2D_OK;
+}
+
+int as2d_get_row_margins(as2d_ctx* c, int32_t req, float* host, int32_t max_rows, int32_t* n_rows) {
+  int rc = check_req(c, req);
+  if (rc) return rc;
+  const ReqState& st = c->reqs[req];
+  if (!host || !n_rows) return fail(c, AS2D_EINVAL, "get_row_margins: null pointer");
+  if (!st.last_rows) return fail(c, AS2D_ESTATE, "get_row_margins: no rows for request %d", req);
+  if (max_rows < st.last_rows) return fail(c, AS2D_EINVAL, "get_row_margins: need %d rows", st.last_rows);
+  memcpy(host, c->h_margin + st.last_row_start, sizeof(float) * st.last_rows);
   *n_rows = st.last_rows;
   return AS2D_OK;
 }
@@ -1166,9 +1316,9 @@ int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* ho
 
 int as2d_set_stream(as2d_ctx* c, void* hip_stream) {
   if (!c) return AS2D_EINVAL;
+  if (hip_stream && stream_restricted((hipStream_t)hip_stream)) return fail(c, AS2D_EINVAL, "set_stream: %s", kRestrictedStream);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
-  c->graphs.clear();
+  drop_launch_state(c);
   if (c->own_stream) {
     hipStreamDestroy(c->stream);
     c->own_stream = false;
@@ -1180,14 +1330,7 @@ int as2d_set_stream(as2d_ctx* c, void* hip_stream) {
     HIP_TRY(c, hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking));
     c->own_stream = true;
   }
-  int dev = 0, cus = 0;
-  HIP_TRY(c, hipGetDevice(&dev));
-  HIP_TRY(c, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-  cus = stream_cus(c->stream, cus);
-  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, cus);
-  if (c->pers_ok)
-    for (int mt = 1; mt <= 2; ++mt) c->pers_grid[mt] = cus;
-  return AS2D_OK;
+  return set_grids(c, c->cu_budget);
 }
 
 int as2d_set_cu_budget(as2d_ctx* c, int32_t cus) {
@@ -1195,13 +1338,11 @@ int as2d_set_cu_budget(as2d_ctx* c, int32_t cus) {
   int dev = 0, dev_cus = 0;
   HIP_TRY(c, hipGetDevice(&dev));
   HIP_TRY(c, hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev));
-  const int avail = stream_cus(c->stream, dev_cus);
-  if (cus > avail) return fail(c, AS2D_EINVAL, "cu budget %d > %d usable CUs", cus, avail);
+  if (cus > dev_cus) return fail(c, AS2D_EINVAL, "cu budget %d > %d compute units", cus, dev_cus);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);   // grids are kernel launch parameters
-  c->graphs.clear();
-  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, cus ? cus : avail);
-  return AS2D_OK;
+  drop_launch_state(c);
+  c->cu_budget = cus;
+  return set_grids(c, cus);
 }
 
 int as2d_release_request(as2d_ctx* c, int32_t req) {
@@ -1284,7 +1425,7 @@ int as2d_time_gemm(as2d_ctx* c, int32_t which, int32_t rows, int32_t reps, doubl
   // rows describe positions 0..rows-1 of slot 0: only the QKV epilogue reads
   // them (cache rows it overwrites are in bounds; their contents are garbage)
   for (int i = 0; i < rows; ++i) c->h_rows[i] = RowDesc{0, 0, std::min(i, g.max_kv_len - 1), 0, -1, {0, 0, 0}};
-  HIP_TRY(c, hipMemcpyAsync(c->d_rows, c->h_rows, sizeof(RowDesc) * rows, hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(c->b.d_rows, c->h_rows, sizeof(RowDesc) * rows, hipMemcpyHostToDevice, s));
   hipEvent_t e0 = ev_get(c, 1000), e1 = ev_get(c, 1001);
   if (!e0 || !e1) return fail(c, AS2D_EHIP, "time_gemm: events");
   auto launch = [&](int l) -> int {
@@ -1294,31 +1435,32 @@ int as2d_time_gemm(as2d_ctx* c, int32_t which, int32_t rows, int32_t reps, doubl
     switch (which) {
       case 0:
         a = base_args(c, c->p_qkv, w.qkv, rows);
-        a.A = c->xg; a.a_plane = c->xg_plane; a.bias = w.bias; a.q_out = c->q;
+        a.A = c->b.xg; a.a_plane = c->b.xg_plane; a.bias = w.bias; a.q_out = c->b.q;
         a.k_cache = c->kc + (size_t)l * c->layer_stride; a.v_cache = c->vc + (size_t)l * c->layer_stride;
         a.slot_stride = c->slot_stride; a.kv_cap = g.max_kv_len; a.n_q = g.n_q_heads;
         a.n_kv = g.n_kv_heads; a.head_dim = g.head_dim; a.rope_cs = c->rope_cs;
         break;
       case 1:
         a = base_args(c, c->p_o, w.o, rows);
-        a.A = c->attn; a.a_plane = c->attn_plane; a.x = c->x; a.x_out = c->x; a.sumsq_out = c->sumsq;
-        a.gain_next = w.g_mlp; a.out = c->xg; a.out_plane = c->xg_plane;
+        a.A = c->b.attn; a.a_plane = c->b.attn_plane; a.x = c->b.x; a.x_out = c->b.x; a.sumsq_out = c->b.sumsq;
+        a.gain_next = w.g_mlp; a.out = c->b.xg; a.out_plane = c->b.xg_plane;
         am = A_PLAIN; epi = EPI_RESID;
         break;
       case 2:
         a = base_args(c, c->p_gu, w.gu, rows);
-        a.A = c->xg; a.a_plane = c->xg_plane; a.out = c->hbuf; a.out_plane = c->h_plane;
+        a.A = c->b.xg; a.a_plane = c->b.xg_plane; a.out = c->b.hbuf; a.out_plane = c->b.h_plane;
         epi = EPI_SWIGLU;
         break;
       case 3:
         a = base_args(c, c->p_down, w.down, rows);
-        a.A = c->hbuf; a.a_plane = c->h_plane; a.x = c->x; a.x_out = c->x; a.sumsq_out = c->sumsq;
-        a.gain_next = w.g_attn; a.out = c->xg; a.out_plane = c->xg_plane;
-        am = A_PLAIN; epi = EPI_RESID;
+        a.A = c->b.hbuf; a.a_plane = c->b.h_plane; a.x = c->b.x; a.x_out = c->b.x; a.sumsq_out = c->b.sumsq;
+        a.gain_next = w.g_attn; a.out = c->b.xg; a.out_plane = c->b.xg_plane;
+        am = A_PLAIN; epi = EPI_DOWN;
         break;
       default:
         a = base_args(c, c->p_lm, c->lm, rows);
-        a.A = c->xg; a.a_plane = c->xg_plane; a.amax_val = c->amax_val; a.amax_idx = c->amax_idx;
+        a.A = c->b.xg; a.a_plane = c->b.xg_plane; a.amax_val = c->b.amax_val; a.amax_val2 = c->b.amax_val2;
+        a.amax_idx = c->b.amax_idx;
         epi = EPI_ARGMAX;
     }
     HIP_TRY(c, launch_gemm(c->bf16, am, epi, a, s));

@@ -18,6 +18,9 @@
 // until `budget` candidates past the cursor are published (or the draft is
 // exhausted), so the two never overlap.
 //
+// Graphs are captured for both contexts before the producer thread starts,
+// so no two threads ever capture at the same time.
+//
 // Every producer step and verifier call is logged as a closed interval
 // (host steady clock, ns from the start of the run); the run ends when
 // both sides have stopped (the producer's drain included).
@@ -29,6 +32,7 @@
 #include <vector>
 
 #include "../../include/as2d.h"
+#include "internal.h"
 
 namespace {
 
@@ -94,6 +98,12 @@ extern "C" int as2d_run_decoupled(as2d_ctx* target, int32_t treq, as2d_ctx* draf
   int64_t pub = 0;
   as2d_cbuf_snapshot(buf, &pub);
   if (pub != 0 || cur->cursor != 0) return AS2D_EINVAL;   // a fresh buffer and cursor
+  // every graph either thread will launch is captured here, one context
+  // at a time, before the producer thread starts: the target's passes of
+  // 1..budget + 1 rows and the drafter's one-row decode step
+  int prc = as2d_prepare_graphs(target, budget + 1);
+  if (prc == AS2D_OK) prc = as2d_prepare_graphs(drafter, 1);
+  if (prc != AS2D_OK) return prc;
   Log lg{log, log_cap};
   Producer prod{drafter, dreq, draft, n_draft, buf};
   std::atomic<bool> stop{false};

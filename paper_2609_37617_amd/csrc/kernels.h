@@ -64,7 +64,9 @@ struct StepOut {
 };
 
 enum AMode { A_PLAIN = 0, A_NORM = 1 };
-enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_ARGMAX = 3 };
+// EPI_DOWN is EPI_RESID under its own id: the O and down projections then
+// run as distinct kernel instantiations, so profiles attribute them apart.
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_ARGMAX = 3, EPI_DOWN = 4 };
 
 struct GemmArgs {
   const uint4* W;        // packed weight tiles
@@ -104,8 +106,9 @@ struct GemmArgs {
   void* out;             // EPI_RESID: planes of x * gain_next; EPI_SWIGLU: planes of h
   long long out_plane;
   float* logits;         // EPI_ARGMAX: optional [M][N]
-  float* amax_val;       // EPI_ARGMAX: per-pair partials [kMaxRows][N / 32]
-  int* amax_idx;
+  float* amax_val;       // EPI_ARGMAX: per-pair partials [kMaxRows][N / 32]: largest value,
+  float* amax_val2;      //   second-largest value,
+  int* amax_idx;         //   lowest column holding the largest value
 };
 
 struct AttnArgs {
@@ -118,9 +121,9 @@ struct AttnArgs {
   const ReqDesc* reqs;
   int n_q, n_kv, head_dim;
   float scale;
-  float* pacc;           // [n_chunks_cap][kMaxRows][n_q][d]
-  float* pml;            // [n_chunks_cap][kMaxRows][n_q][2]
-  int n_chunks_cap;
+  float* pacc;           // [chunk][part_rows][n_q][d]
+  float* pml;            // [chunk][part_rows][n_q][2]
+  int part_rows;         // row stride of the partials (at least the pass's rows)
   void* out;             // planes [kMaxRows][n_q*d]
   long long out_plane;
   int M;
@@ -156,6 +159,7 @@ struct StepArgs {
   int fin_rows;
   int* row_tok;
   int* row_bad;
+  float* row_margin;
   StepOut* out;
   int done_qkv, done_o, done_gu, done_down, done_lm;  // completion signals per GEMM phase
   int* phase_cnt;            // 3 + 6 * n_layers counters, cleared by the launcher
@@ -193,9 +197,14 @@ hipError_t launch_step(bool bf16, int MT, int head_dim, int sl, const StepArgs& 
 // any request (the grid size).
 hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s);
 // n_rows = sum of the requests' W; counters: one per request, zero between launches.
+// Writes each verified row's greedy token, non-finite flag and top-2 margin.
 hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,
-                         const float* amax_val, const int* amax_idx, int n_pairs, int* row_tok,
-                         int* row_bad, int* counters, StepOut* out, hipStream_t s);
+                         const float* amax_val, const float* amax_val2, const int* amax_idx, int n_pairs,
+                         int* row_tok, int* row_bad, float* row_margin, int* counters, StepOut* out,
+                         hipStream_t s);
+
+// Zeroes n ints (a kernel, not a memset, so that it may be captured).
+hipError_t launch_fill_zero(int* p, int n, hipStream_t s);
 
 // Streams n16 16-byte units of buf with `grid` workgroups (read-bandwidth
 // reference); n16 must split into whole 8 KiB runs per wave.

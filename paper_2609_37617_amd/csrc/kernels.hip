@@ -260,9 +260,9 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 #define AS2D_G(bf, am, ep) \
   if (bf16 == bf && amode == am && epi == ep) return gemm_dispatch<bf, am, ep>(a, s);
   AS2D_G(true, A_NORM, EPI_QKV) AS2D_G(true, A_PLAIN, EPI_RESID) AS2D_G(true, A_NORM, EPI_SWIGLU)
-  AS2D_G(true, A_NORM, EPI_ARGMAX)
+  AS2D_G(true, A_NORM, EPI_ARGMAX) AS2D_G(true, A_PLAIN, EPI_DOWN)
   AS2D_G(false, A_NORM, EPI_QKV) AS2D_G(false, A_PLAIN, EPI_RESID) AS2D_G(false, A_NORM, EPI_SWIGLU)
-  AS2D_G(false, A_NORM, EPI_ARGMAX)
+  AS2D_G(false, A_NORM, EPI_ARGMAX) AS2D_G(false, A_PLAIN, EPI_DOWN)
 #undef AS2D_G
   return hipErrorInvalidValue;
 }
@@ -345,9 +345,9 @@ hipError_t prepare_kernels() {
   if (e == hipSuccess) e = prepare_range<bf, am, ep>(); \
   if (e == hipSuccess) e = prepare_staged<bf, am, ep>();
   AS2D_P(true, A_NORM, EPI_QKV) AS2D_P(true, A_PLAIN, EPI_RESID) AS2D_P(true, A_NORM, EPI_SWIGLU)
-  AS2D_P(true, A_NORM, EPI_ARGMAX)
+  AS2D_P(true, A_NORM, EPI_ARGMAX) AS2D_P(true, A_PLAIN, EPI_DOWN)
   AS2D_P(false, A_NORM, EPI_QKV) AS2D_P(false, A_PLAIN, EPI_RESID) AS2D_P(false, A_NORM, EPI_SWIGLU)
-  AS2D_P(false, A_NORM, EPI_ARGMAX)
+  AS2D_P(false, A_NORM, EPI_ARGMAX) AS2D_P(false, A_PLAIN, EPI_DOWN)
 #undef AS2D_P
   return e;
 }
@@ -368,20 +368,24 @@ hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_ch
 __global__ __launch_bounds__(256) void finish_kernel(const RowDesc* __restrict__ rows,
                                                      const ReqDesc* __restrict__ reqs, int n_reqs,
                                                      const float* __restrict__ amax_val,
+                                                     const float* __restrict__ amax_val2,
                                                      const int* __restrict__ amax_idx, int n_pairs,
                                                      int* __restrict__ row_tok, int* __restrict__ row_bad,
+                                                     float* __restrict__ row_margin,
                                                      int* __restrict__ counters, StepOut* __restrict__ out) {
-  __shared__ float s4f[4];
+  __shared__ float s4f[4], s4s[4];
   __shared__ int s4i[4];
   __shared__ int s_tok, s_bad;
+  __shared__ float s_margin;
   int r = 0, i = blockIdx.x;
   while (r < n_reqs - 1 && i >= reqs[r].W) i -= reqs[r++].W;
   const ReqDesc rq = reqs[r];
   const int row = rq.row_start + i;
-  argmax_row<false>(amax_val, amax_idx, n_pairs, row, &s_tok, &s_bad, s4f, s4i);
+  argmax_row<false>(amax_val, amax_val2, amax_idx, n_pairs, row, &s_tok, &s_bad, &s_margin, s4f, s4s, s4i);
   if (threadIdx.x == 0) {
     st<true>(row_tok + row, s_tok);
     st<true>(row_bad + row, s_bad);
+    row_margin[row] = s_margin;   // read by the host after the pass
     wait_vmem();
     if (counter_add(&counters[r], 1) == rq.W - 1) {
       counters[r] = 0;  // ready for the next launch
@@ -393,10 +397,24 @@ __global__ __launch_bounds__(256) void finish_kernel(const RowDesc* __restrict__
 }
 
 hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,
-                         const float* amax_val, const int* amax_idx, int n_pairs, int* row_tok,
-                         int* row_bad, int* counters, StepOut* out, hipStream_t s) {
-  finish_kernel<<<n_rows, 256, 0, s>>>(rows, reqs, n_reqs, amax_val, amax_idx, n_pairs, row_tok, row_bad,
-                                       counters, out);
+                         const float* amax_val, const float* amax_val2, const int* amax_idx, int n_pairs,
+                         int* row_tok, int* row_bad, float* row_margin, int* counters, StepOut* out,
+                         hipStream_t s) {
+  finish_kernel<<<n_rows, 256, 0, s>>>(rows, reqs, n_reqs, amax_val, amax_val2, amax_idx, n_pairs, row_tok,
+                                       row_bad, row_margin, counters, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Zero fill.
+
+__global__ void fill_zero_kernel(int* __restrict__ p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
+hipError_t launch_fill_zero(int* p, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  fill_zero_kernel<<<min((n + 255) / 256, 1024), 256, 0, s>>>(p, n);
   return hipGetLastError();
 }
 

@@ -103,7 +103,8 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
   __shared__ float s_scale[kMaxRows];
   __shared__ int s_flags[kMaxUnits];
   __shared__ int s_tok, s_bad;
-  __shared__ float s4f[4];
+  __shared__ float s_margin;
+  __shared__ float s4f[4], s4s[4];
   __shared__ int s4i[4];
   const int G = gridDim.x, tid = threadIdx.x;
   const int M = a.M, L = a.n_layers;
@@ -208,7 +209,7 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
                                                 &a.phase_cnt[ph_layer(l, 3)], a, smem, s_scale, s_flags);
     gemm_phase<BF, MT, SL, A_NORM, EPI_SWIGLU>(load_invariant(&ly->gu), M, &a.phase_cnt[ph_layer(l, 3)], a.done_o,
                                                 &a.phase_cnt[ph_layer(l, 4)], a, smem, s_scale, s_flags);
-    gemm_phase<BF, MT, SL, A_PLAIN, EPI_RESID>(load_invariant(&ly->down), M, &a.phase_cnt[ph_layer(l, 4)], a.done_gu,
+    gemm_phase<BF, MT, SL, A_PLAIN, EPI_DOWN>(load_invariant(&ly->down), M, &a.phase_cnt[ph_layer(l, 4)], a.done_gu,
                                                 &a.phase_cnt[ph_layer(l, 5)], a, smem, s_scale, s_flags);
   }
   gemm_phase<BF, MT, SL, A_NORM, EPI_ARGMAX>(a.lm, M, &a.phase_cnt[ph_layer(L - 1, 5)], a.done_down,
@@ -221,10 +222,12 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
     while (r < a.n_fin - 1 && u >= load_invariant(a.fin_reqs + r).W) u -= load_invariant(a.fin_reqs + r++).W;
     const int row = load_invariant(a.fin_reqs + r).row_start + u;
     wait_count(&a.phase_cnt[1 + 6 * L], a.done_lm, a.err, a.spin_limit);
-    argmax_row<true>(a.lm.amax_val, a.lm.amax_idx, a.lm.N / kPairCols, row, &s_tok, &s_bad, s4f, s4i);
+    argmax_row<true>(a.lm.amax_val, a.lm.amax_val2, a.lm.amax_idx, a.lm.N / kPairCols, row, &s_tok, &s_bad,
+                     &s_margin, s4f, s4s, s4i);
     if (tid == 0) {
       st<true>(a.row_tok + row, s_tok);
       st<true>(a.row_bad + row, s_bad);
+      a.row_margin[row] = s_margin;   // read by the host after the pass
       wait_vmem();
       if (counter_add(&a.phase_cnt[2 + 6 * L], 1) == a.fin_rows - 1) {
         for (int q = 0; q < a.n_fin; ++q) {

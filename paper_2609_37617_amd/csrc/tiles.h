@@ -84,7 +84,7 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& p, float* F, int f
   const int N = p.N, C = np * kPairCols;
   const int n0 = pair0 * kPairCols;
   const int units = (r1 - r0) * np;           // (row, pair) units of the reductions
-  if constexpr (EPI == EPI_RESID) {
+  if constexpr (EPI == EPI_RESID || EPI == EPI_DOWN) {
     // x_out = x + Y; planes of x_out * g for the next RMSNorm; sum of squares
     for (int idx = tid; idx < (r1 - r0) * C; idx += NTH) {
       const int m = r0 + idx / C, c = idx % C;
@@ -147,13 +147,14 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& p, float* F, int f
     }
   } else {  // EPI_ARGMAX (identity column order: column = token id)
     // one (row, pair) per thread: the largest value, the lowest column
-    // among equal values (exact, so the order of the scan is immaterial);
-    // a non-finite value makes the pair's partial NaN
+    // among equal values and the second-largest value (equal to the
+    // largest when two columns tie); exact, so the order of the scan is
+    // immaterial.  A non-finite value makes the pair's partial NaN.
     for (int u = tid; u < units; u += NTH) {
       const int m = r0 + u / np, pp = u % np;
       const int n0p = (pair0 + pp) * kPairCols;
       const float* Fr = F + (m - r0) * fs + pp * kPairCols;
-      float best = Fr[0];
+      float best = Fr[0], second = -INFINITY;
       int bi = n0p;
       bool bad = !isfinite(best);
       if (p.logits) p.logits[(size_t)m * N + n0p] = best;   // read by the host only
@@ -162,12 +163,17 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& p, float* F, int f
         if (p.logits) p.logits[(size_t)m * N + n0p + c] = v;
         bad |= !isfinite(v);
         if (v > best) {
+          second = best;
           best = v;
           bi = n0p + c;
+        } else {
+          second = fmaxf(second, v);
         }
       }
-      st<COH>(p.amax_val + (size_t)m * (N / kPairCols) + pair0 + pp, bad ? __builtin_nanf("") : best);
-      st<COH>(p.amax_idx + (size_t)m * (N / kPairCols) + pair0 + pp, bi);
+      const size_t o = (size_t)m * (N / kPairCols) + pair0 + pp;
+      st<COH>(p.amax_val + o, bad ? __builtin_nanf("") : best);
+      st<COH>(p.amax_val2 + o, second);
+      st<COH>(p.amax_idx + o, bi);
     }
   }
 }
@@ -1191,13 +1197,13 @@ __device__ __forceinline__ void attn_rows(const AttnArgs& p, int c, int h, int k
     }
 #pragma unroll
     for (int r = 0; r < RB; ++r)
-      if (r < nb) st<COH>(p.pacc + (((size_t)c * kMaxRows + row[r]) * p.n_q + h) * D + dd, o[r]);
+      if (r < nb) st<COH>(p.pacc + (((size_t)c * p.part_rows + row[r]) * p.n_q + h) * D + dd, o[r]);
   }
   // (m, l): every lane stores, even lanes m and odd lanes l, one store
   // with no branch around it
 #pragma unroll
   for (int r = 0; r < RB; ++r)
-    if (r < nb) st<COH>(p.pml + (((size_t)c * kMaxRows + row[r]) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l[r] : mx[r]);
+    if (r < nb) st<COH>(p.pml + (((size_t)c * p.part_rows + row[r]) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l[r] : mx[r]);
 }
 
 // The tile from keys and values already in registers; `pre` runs once the
@@ -1293,7 +1299,7 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, int row, int h
   const RowDesc rd = load_invariant(p.rows + row);
   const int nc = valid ? rd.pos / kAttnChunk + 1 : 0;
   auto ld = [](const float* q) { if constexpr (COH) return ld_coherent(q); else return ldg(q); };
-  auto acc_at = [&](int c) { return p.pacc + (((size_t)c * kMaxRows + row) * p.n_q + h) * D + dd; };
+  auto acc_at = [&](int c) { return p.pacc + (((size_t)c * p.part_rows + row) * p.n_q + h) * D + dd; };
   // loads past the row's chunks read its last chunk (unused): no branch
   // around them, so the waits stay exact
   const int cl = max(nc, 1) - 1;
@@ -1301,7 +1307,7 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, int row, int h
 #pragma unroll
   for (int b = 0; b < kB; ++b) v[b] = ld(acc_at(min(b, cl)));
   for (int c = dd; c < nc; c += D) {
-    const size_t o = ((size_t)c * kMaxRows + row) * p.n_q + h;
+    const size_t o = ((size_t)c * p.part_rows + row) * p.n_q + h;
     sm[c] = ld(p.pml + o * 2);
     sl[c] = ld(p.pml + o * 2 + 1);
   }
@@ -1330,30 +1336,44 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, int row, int h
 // ---------------------------------------------------------------------------
 // Arg-max of row `row` over the LM head's per-pair partials (256 threads):
 // larger value wins, equal values keep the lower token id; *bad is set for a
-// non-finite logit.  s4f / s4i: 4-entry LDS scratch.
+// non-finite logit and *margin receives the gap between the largest and
+// the second-largest logit of the row (0 when two token ids tie).  The
+// (value, id, second) partials merge as: the winner's value and id, and
+// the larger of the loser's value and the winner's second; the winner is
+// decided by the total order (value descending, id ascending), so the
+// result does not depend on the order of the merges.  s4f, s4s / s4i:
+// 4-entry LDS scratch.
+
+__device__ __forceinline__ void top2_merge(float& v, int& i, float& v2, float ov, int oi, float ov2) {
+  if (ov > v || (ov == v && oi < i)) {
+    v2 = fmaxf(v, ov2);
+    v = ov;
+    i = oi;
+  } else {
+    v2 = fmaxf(v2, ov);
+  }
+}
 
 template <bool COH>
-__device__ __forceinline__ void argmax_row(const float* amax_val, const int* amax_idx, int n_pairs, int row, int* tok,
-                           int* bad, float* s4f, int* s4i) {
+__device__ __forceinline__ void argmax_row(const float* amax_val, const float* amax_val2, const int* amax_idx,
+                                           int n_pairs, int row, int* tok, int* bad, float* margin, float* s4f,
+                                           float* s4s, int* s4i) {
   constexpr int kPer = 8;   // pairs per thread, loads in flight together
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  float best = -INFINITY;
+  float best = -INFINITY, second = -INFINITY;
   int bi = 0x7fffffff;
   bool b = false;
+  auto ld = [](const auto* q) { if constexpr (COH) return ld_coherent(q); else return *q; };
   for (int g0 = 0; g0 < n_pairs; g0 += 256 * kPer) {
-    float v[kPer];
+    float v[kPer], v2[kPer];
     int id[kPer];
 #pragma unroll
     for (int t = 0; t < kPer; ++t) {
       const int g = g0 + t * 256 + tid;
       if (g < n_pairs) {
-        if constexpr (COH) {
-          v[t] = ld_coherent(amax_val + (size_t)row * n_pairs + g);
-          id[t] = ld_coherent(amax_idx + (size_t)row * n_pairs + g);
-        } else {
-          v[t] = amax_val[(size_t)row * n_pairs + g];
-          id[t] = amax_idx[(size_t)row * n_pairs + g];
-        }
+        v[t] = ld(amax_val + (size_t)row * n_pairs + g);
+        v2[t] = ld(amax_val2 + (size_t)row * n_pairs + g);
+        id[t] = ld(amax_idx + (size_t)row * n_pairs + g);
       }
     }
 #pragma unroll
@@ -1361,24 +1381,29 @@ __device__ __forceinline__ void argmax_row(const float* amax_val, const int* ama
       const int g = g0 + t * 256 + tid;
       if (g < n_pairs) {
         if (!isfinite(v[t])) b = true;
-        else if (v[t] > best || (v[t] == best && id[t] < bi)) { best = v[t]; bi = id[t]; }
+        else top2_merge(best, bi, second, v[t], id[t], v2[t]);
       }
     }
   }
-  wave_argmax(best, bi);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(best, o), ov2 = __shfl_xor(second, o);
+    const int oi = __shfl_xor(bi, o);
+    top2_merge(best, bi, second, ov, oi, ov2);
+  }
   const bool wb = __ballot(b) != 0;
-  if (lane == 0) { s4f[wave] = best; s4i[wave] = bi | (wb ? 0x80000000 : 0); }
+  if (lane == 0) { s4f[wave] = best; s4s[wave] = second; s4i[wave] = bi | (wb ? 0x80000000 : 0); }
   __syncthreads();
   if (tid == 0) {
-    float bv = s4f[0];
+    float bv = s4f[0], bv2 = s4s[0];
     int bx = s4i[0] & 0x7fffffff, bb = s4i[0] < 0;
     for (int w = 1; w < 4; ++w) {
-      const int iw = s4i[w] & 0x7fffffff;
-      if (s4f[w] > bv || (s4f[w] == bv && iw < bx)) { bv = s4f[w]; bx = iw; }
+      top2_merge(bv, bx, bv2, s4f[w], s4i[w] & 0x7fffffff, s4s[w]);
       bb |= s4i[w] < 0;
     }
     *tok = bx;
     *bad = bb | !isfinite(bv);
+    *margin = bv - bv2;
   }
   __syncthreads();
 }
