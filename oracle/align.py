@@ -114,18 +114,20 @@ class ReadCursor:
         self.c = m + 1
 
 
-def decode_with_buffer(model, publish_schedule, budget, reply_len, radius=RADIUS):
+def decode_with_buffer(model, publish_schedule, budget, reply_len, radius=RADIUS, cursor=None):
     """Greedy decoding of `reply_len` tokens after a prefilled model state,
     proposing candidates from a CandidateBuffer through a ReadCursor.
 
     model: an OracleModel (or anything with .root and .verify(cands, k)).
     publish_schedule(step, buffer): called before each verification call;
     publishes whatever batches are ready at that step.
+    cursor: the ReadCursor to use (default: a fresh one of `radius`), so a
+    schedule can look at it.
     Returns (committed tokens, per-call (k, a) list).  The first committed
     token of each call is the previous root's successor, so the returned
     stream starts after the root that was current on entry."""
     buf = CandidateBuffer()
-    cur = ReadCursor(radius)
+    cur = ReadCursor(radius) if cursor is None else cursor
     out, calls = [], []
     step = 0
     while len(out) < reply_len:

@@ -91,16 +91,28 @@ def attention(q, k_cache, v_cache, q_pos):
     q: [T, n_q, d] queries at positions q_pos [T];
     k_cache, v_cache: [n_kv, S, d], the entry at index j holds position j.
     Query head h reads KV head floor(h * n_kv / n_q); row t sees keys
-    j <= q_pos[t].  Returns [T, n_q, d]."""
+    j <= q_pos[t].  Returns [T, n_q, d].
+
+    The heads are independent; for large score matrices they are computed
+    on several threads (each head's arithmetic is the same either way, and
+    each writes only its own slice of the output)."""
     T, n_q, d = q.shape
     n_kv = k_cache.shape[0]
     out = np.zeros((T, n_q, d), dtype=F64)
     j = np.arange(k_cache.shape[1])
-    for h in range(n_q):
+
+    def head(h):
         g = h * n_kv // n_q
         s = (q[:, h, :] @ k_cache[g].T) / np.sqrt(F64(d))            # [T, S]
         s = np.where(j[None, :] <= np.asarray(q_pos)[:, None], s, -np.inf)
         out[:, h, :] = softmax(s) @ v_cache[g]
+
+    if T * k_cache.shape[1] < (1 << 20):
+        for h in range(n_q):
+            head(h)
+    else:
+        with ThreadPoolExecutor(min(n_q, os.cpu_count() or 1, 16)) as ex:
+            list(ex.map(head, range(n_q)))
     return out
 
 
@@ -137,9 +149,12 @@ def verify_block(target_tokens, cands, k):
 class OracleModel:
     """Target model state machine mirroring the C ABI calls.
 
-    weights: dict {(name, layer): array} with the tensors of
-    workload.gen.weight_spec (float32 arrays; bf16 models hold
-    bf16-representable values).  All arithmetic is float64.
+    weights: mapping {(name, layer): array} with the tensors of
+    workload.gen.weight_spec (float32 or float64 arrays; bf16 models hold
+    bf16-representable values).  Each is read once, when the model is
+    built, and held in float64 (a mapping that produces tensors on demand
+    keeps only one extra tensor alive at a time).  All arithmetic is
+    float64.
     """
 
     def __init__(self, shape, weights, capacity=None):

@@ -7,7 +7,6 @@ greedy decision differs has an oracle top-2 margin <= 0.05, in which case
 the oracle is teacher-forced onto the GPU's commit (the paper records such
 near-tied top-1 differences rather than hiding them, Appendix F.6).
 """
-import copy
 import os
 import sys
 
@@ -50,6 +49,41 @@ def make_pair(shape, seed=0, max_requests=1, max_kv_len=512, max_k=8, oracle=Tru
     return om, gpu
 
 
+class DeviceValues:
+    """Read-only mapping {(name, layer): float64 tensor} over the canonical
+    tensors in the C ABI's format (workload.gen.make_weights(fmt="device")):
+    bf16 bit patterns become their exact float64 values when read, so the
+    oracle and the GPU are built from the very same arrays."""
+
+    def __init__(self, shape, tensors):
+        self.w = gen.weights_dict(shape, tensors)
+
+    def __getitem__(self, key):
+        t = self.w[key]
+        return gen.bf16_bits_to_f64(t) if t.dtype == np.uint16 else np.asarray(t, dtype=np.float64)
+
+
+def full_pair(shape, seed=0, max_requests=1, max_kv_len=1024, max_k=8):
+    """(oracle, GPU model) of a full-size shape from one set of generated
+    weights: the GPU model is loaded first, then the oracle converts the
+    same arrays to float64 one tensor at a time."""
+    import time
+    from paper_2609_37617_amd import as2d
+    ensure_built()
+    t0 = time.time()
+    dev = gen.make_weights(shape, seed, fmt="device")
+    gpu = as2d.Model(shape, dev, max_requests=max_requests, max_kv_len=max_kv_len, max_k=max_k)
+    om = OracleModel(shape, DeviceValues(shape, dev), capacity=max_kv_len)
+    del dev
+    log(f"[{shape.name}] weights generated, loaded on the GPU and held by the oracle in {time.time() - t0:.1f}s")
+    return om, gpu
+
+
+def log(msg):
+    """Progress line (long full-depth tests print one per stage)."""
+    print(msg, flush=True)
+
+
 def prefix(shape, n_audio, n_instr, seed=0, req=0):
     return (gen.audio_embeddings(shape, n_audio, seed, req, fmt="oracle"),
             gen.audio_embeddings(shape, n_audio, seed, req, fmt="device"),
@@ -70,6 +104,8 @@ def oracle_prefill(om, audio, instr, chunk=2048):
         c1 = min(T, c0 + chunk)
         rows = np.array([c1 - c0 - 1]) if c1 == T else np.array([], dtype=np.int64)
         logits = om.forward(x[c0:c1], c0, logit_rows=rows)
+        if T > chunk:
+            log(f"  oracle prefill: rows {c0}..{c1 - 1} of {T}")
     om.last_logits = logits
     om.root = greedy(logits[0])
     om.kv_len = om.prefix_len = T
@@ -77,11 +113,14 @@ def oracle_prefill(om, audio, instr, chunk=2048):
 
 
 def snapshot(om):
-    return (copy.deepcopy(om.k_cache), copy.deepcopy(om.v_cache), om.kv_len, om.root)
+    """The oracle's decoding state.  Shallow: the oracle never writes into a
+    cache array (appending and truncating both make new arrays or views),
+    so holding the per-layer arrays keeps their contents."""
+    return (list(om.k_cache), list(om.v_cache), om.kv_len, om.root)
 
 
 def restore(om, snap):
-    om.k_cache, om.v_cache, om.kv_len, om.root = copy.deepcopy(snap[0]), copy.deepcopy(snap[1]), snap[2], snap[3]
+    om.k_cache, om.v_cache, om.kv_len, om.root = list(snap[0]), list(snap[1]), snap[2], snap[3]
 
 
 def teacher_force(om, snap, cands, a, corr):
@@ -111,13 +150,14 @@ def parity_round(om, gpu, req, cands, k, tol, stats, check_logits=True):
     ro = om.verify(cands, k)
     rg = gpu.verify(req, cands[:k], k)
     check_round(om, snap, ro, rg, gpu.row_tokens(req), gpu.logits(req) if check_logits else None,
-                cands, k, tol, stats)
+                cands, k, tol, stats, gpu.row_margins(req))
     return rg
 
 
-def check_round(om, snap, ro, rg, toks, lg, cands, k, tol, stats):
+def check_round(om, snap, ro, rg, toks, lg, cands, k, tol, stats, margins=None):
     """The near-tie protocol for one request's verify result rg (GPU row
-    tokens toks, logits lg or None) against the oracle's ro from state snap."""
+    tokens toks, logits lg or None, device top-2 margins or None) against
+    the oracle's ro from state snap."""
     if lg is not None:
         assert lg.shape == ro["logits"].shape
         err = float(np.max(np.abs(lg.astype(np.float64) - ro["logits"])))
@@ -125,6 +165,10 @@ def check_round(om, snap, ro, rg, toks, lg, cands, k, tol, stats):
         assert err <= tol, f"logit error {err} > {tol}"
         # the GPU's greedy tokens are the arg-max of its own logits (same precision)
         assert toks == [int(np.argmax(r)) for r in lg]
+        if margins is not None:
+            # the device's top-2 margin is that of its own logits, exactly
+            top = np.sort(lg, axis=1)
+            assert np.array_equal(margins, top[:, -1] - top[:, -2])
     stats.rounds += 1
     if (rg["accepted_len"], rg["correction_token"]) != (ro["accepted_len"], ro["correction_token"]):
         i = next(j for j in range(k + 1) if toks[j] != ro["tokens"][j])

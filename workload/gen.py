@@ -91,6 +91,24 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (b.astype(np.uint32) << 16).view(np.float32)
 
 
+def bf16_bits_to_f64(b: np.ndarray) -> np.ndarray:
+    """float64 array holding the values of bf16 bit patterns (exact), in row
+    blocks on several threads (the 7B-shaped matrices are large)."""
+    from concurrent.futures import ThreadPoolExecutor
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    out = np.empty(b.shape, dtype=np.float64)
+    flat_in, flat_out = b.reshape(-1), out.reshape(-1)
+    n = _threads()
+    edges = np.linspace(0, flat_in.size, n + 1).astype(np.int64)
+
+    def conv(i):
+        lo, hi = edges[i], edges[i + 1]
+        flat_out[lo:hi] = (flat_in[lo:hi].astype(np.uint32) << 16).view(np.float32)
+    with ThreadPoolExecutor(n) as ex:
+        list(ex.map(conv, range(n)))
+    return out
+
+
 def f32_to_bf16_bits(f: np.ndarray) -> np.ndarray:
     """Exact for float32 arrays whose values are bf16-representable."""
     u = np.ascontiguousarray(f, dtype=np.float32).view(np.uint32)
