@@ -56,6 +56,11 @@ def parse():
     ap.add_argument("--no-decoupled", action="store_true", help="skip the concurrent-drafter measurement")
     ap.add_argument("--no-width-profile", action="store_true",
                     help="skip the per-k step times (single-request workloads with a k sweep)")
+    ap.add_argument("--passes", type=int, default=5, help="whole-reply passes behind `value` (median)")
+    ap.add_argument("--no-configs", action="store_true", help="skip the 3B, long-audio and mixed-batch workloads")
+    ap.add_argument("--trace-window", action="store_true",
+                    help="profiling run: reference streams and every timed call at the workload's width, "
+                         "nothing else (no passes, extras or back-to-back GEMM timing)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a plain copy kernel "
                          "of known size, for scaling hardware byte counters)")
@@ -163,6 +168,191 @@ def cpu_baseline(shape, n_audio, n_instr, k, mean_committed, seed=0, min_seconds
             "step_seconds": t_step}
 
 
+class Runner:
+    """One library context with its requests prefilled: the greedy
+    reference stream of every request (committed by the GPU itself; by the
+    Proposition any proposal stream commits exactly it) and the seeded
+    corrupted candidates drawn from it.  A step is one verification call
+    over every request whose reply is not finished (one fused pass when
+    there are several)."""
+
+    def __init__(self, model, shape, reqs, seed, ref_width=1):
+        self.model, self.shape, self.reqs, self.seed = model, shape, reqs, seed
+        self.starts, self.refs, self.srcs = [], [], []
+        self.prefill_info = None
+        for i, r in enumerate(reqs):
+            audio = gen.audio_embeddings(shape, r.n_audio, seed, i, fmt="device")
+            instr = gen.instruction_tokens(shape, r.n_instr, seed, i)
+            t0 = time.perf_counter()
+            first, L = model.prefill(i, audio, instr)
+            dt = time.perf_counter() - t0
+            if self.prefill_info is None:
+                self.prefill_info = {"rows": L, "ms": round(dt * 1e3, 2), "rows_per_s": round(L / dt, 1)}
+            self.starts.append((L, first))
+        t0 = time.perf_counter()
+        self.refs = self._references(ref_width)
+        log(f"[bench] {len(reqs)} request(s) prefilled; reference streams in {time.perf_counter() - t0:.1f}s")
+        self.set_p(None)
+        self.done = [0] * len(reqs)
+
+    def _references(self, width):
+        """[first root, y_1, ..., y_N] per request, committed by the GPU in
+        fused passes over the unfinished requests; width - 1 zero tokens
+        are proposed per call (width 1: target-only steps)."""
+        refs = [[st[1]] for st in self.starts]
+        for i in range(len(self.reqs)):
+            self.model.rollback(i, *self.starts[i])
+        while True:
+            ids = [i for i, r in enumerate(self.reqs) if len(refs[i]) - 1 < r.reply_len]
+            if not ids:
+                break
+            # width > 1: every call at the full width (the stream may run a
+            # few tokens past the reply; it is cut below)
+            cands = [[0] * (width - 1 if width > 1 else 0) for i in ids]
+            outs = self.model.verify_batch(ids, cands)
+            for i, c, o in zip(ids, cands, outs):
+                refs[i] += c[:o["accepted_len"]] + [o["correction_token"]]
+        for i in range(len(self.reqs)):
+            refs[i] = refs[i][:self.reqs[i].reply_len + 1]
+            self.model.rollback(i, *self.starts[i])
+        return refs
+
+    def set_p(self, p):
+        """Candidate sources of corruption p (None: each request's own)."""
+        self.srcs = [gen.CandidateSource(self.refs[i], self.shape.vocab, r.p if p is None else p,
+                                         seed=self.seed, req=i) for i, r in enumerate(self.reqs)]
+
+    def restart(self):
+        for i in range(len(self.reqs)):
+            self.model.rollback(i, *self.starts[i])
+        self.done = [0] * len(self.reqs)
+
+    def finished(self):
+        return all(d >= r.reply_len for d, r in zip(self.done, self.reqs))
+
+    def step(self, k_force=None):
+        """One verification call; returns (tokens committed, rows, KV
+        positions attended before the call)."""
+        if self.finished():
+            self.restart()
+        ids, cands = [], []
+        for i, r in enumerate(self.reqs):
+            if self.done[i] >= r.reply_len:
+                continue
+            k = min(r.k if k_force is None else k_force, r.reply_len - self.done[i] - 1)
+            ids.append(i)
+            cands.append(self.srcs[i].block(self.done[i], k))
+        kv = sum(self.starts[i][0] + self.done[i] for i in ids)
+        m = self.model
+        outs = m.verify_batch(ids, cands) if len(ids) > 1 else [m.verify(ids[0], cands[0])]
+        got = 0
+        for i, c, o in zip(ids, cands, outs):
+            assert c[:o["accepted_len"]] == self.srcs[i].ref[self.done[i] + 1:self.done[i] + 1 + o["accepted_len"]].tolist()
+            self.done[i] += o["accepted_len"] + 1
+            got += o["accepted_len"] + 1
+        return got, sum(len(c) + 1 for c in cands), kv
+
+    def full_passes(self, n_passes):
+        """n_passes whole passes over every reply (from the end of the
+        prefix to the last token), each timed on its own."""
+        out = []
+        for _ in range(n_passes):
+            self.restart()
+            sync()
+            steps = tok = rows = kv = 0
+            t0 = time.perf_counter()
+            while not self.finished():
+                c, w, kk = self.step()
+                steps += 1
+                tok += c
+                rows += w
+                kv += kk
+            sync()
+            out.append({"s": time.perf_counter() - t0, "steps": steps, "tokens": tok, "rows": rows, "kv": kv})
+        self.restart()
+        return out
+
+    def near_ties(self, margin=0.05):
+        """One untimed pass counting verified rows whose device-side top-2
+        logit margin is at most `margin`."""
+        self.restart()
+        n = rows = 0
+        while not self.finished():
+            before = [d for d in self.done]
+            self.step()
+            for i, r in enumerate(self.reqs):
+                if self.done[i] != before[i]:
+                    mg = self.model.row_margins(i)
+                    n += int(np.sum(mg <= margin))
+                    rows += len(mg)
+        self.restart()
+        return {"rows": rows, "near_tie_rows": n, "margin": margin}
+
+
+_hip = None
+
+
+def sync():
+    global _hip
+    if _hip is None:
+        import ctypes
+        _hip = ctypes.CDLL("libamdhip64.so")
+    assert _hip.hipDeviceSynchronize() == 0
+
+
+def kv_bytes(shape, rows, kv_keys, elem):
+    """KV bytes of a pass: reads of the attended keys plus the appended rows."""
+    return elem * shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * (kv_keys + rows)
+
+
+def summarize(model, shape, passes):
+    """Whole-reply throughput from timed passes: median tokens/s and the
+    step's algorithmic bytes (float32 KV as stored, and with the KV counted
+    in bf16 as a bf16 cache would hold it) over the median step time."""
+    tps = sorted(p["tokens"] / p["s"] for p in passes)
+    med = passes[[p["tokens"] / p["s"] for p in passes].index(tps[len(tps) // 2])]
+    steps, s = med["steps"], med["s"]
+    rows, kv = med["rows"] / steps, med["kv"] / steps
+    b32 = model.step_bytes(int(round(rows)), int(round(kv)))
+    b16 = b32 - kv_bytes(shape, rows, kv, 4) + kv_bytes(shape, rows, kv, 2)
+    ms = s * 1e3 / steps
+    return {"tokens_per_s": round(tps[len(tps) // 2], 2), "passes": len(passes),
+            "tokens_per_s_min_max": [round(tps[0], 2), round(tps[-1], 2)],
+            "verify_steps_per_s": round(steps / s, 2), "ms_per_step": round(ms, 4),
+            "mean_committed_per_step": round(med["tokens"] / steps, 3), "mean_rows_per_step": round(rows, 2),
+            "step_bytes": int(b32), "step_gbps": round(b32 / ms / 1e6, 1),
+            "step_hbm_frac": round(b32 / ms / 1e6 / PEAK_HBM_GBPS, 4),
+            "step_bytes_bf16_kv": int(b16), "step_hbm_frac_bf16_kv": round(b16 / ms / 1e6 / PEAK_HBM_GBPS, 4)}
+
+
+def measure_config(index, shape_dev=None, seed=0, n_passes=3):
+    """Whole-reply throughput of workload `index` in a context of its own
+    (weights from shape_dev when given: the same model)."""
+    from paper_2609_37617_amd import as2d
+    wl = wc.workload(index)
+    shape, reqs = wl.shape, wl.requests
+    t0 = time.time()
+    dev = shape_dev if shape_dev is not None else gen.make_weights(shape, wl.seed, fmt="device")
+    max_k = max(max(r.k for r in reqs), 1)
+    max_kv = (max(r.n_audio + r.n_instr + r.reply_len for r in reqs) + max_k + 2 + 63) // 64 * 64
+    model = as2d.Model(shape, dev, max_requests=len(reqs), max_kv_len=max_kv, max_k=max_k)
+    del dev
+    run = Runner(model, shape, reqs, wl.seed)
+    for _ in range(3):
+        run.step()
+    res = summarize(model, shape, run.full_passes(n_passes))
+    res.update({"workload": wl.name, "layers": shape.n_layers, "requests": len(reqs),
+                "prefix": [r.n_audio + r.n_instr for r in reqs] if len(reqs) > 1 else reqs[0].n_audio + reqs[0].n_instr,
+                "reply_tokens": [r.reply_len for r in reqs] if len(reqs) > 1 else reqs[0].reply_len,
+                "k": [r.k for r in reqs] if len(reqs) > 1 else reqs[0].k,
+                "p": [round(r.p, 3) for r in reqs] if len(reqs) > 1 else reqs[0].p,
+                "prefill_first_request": run.prefill_info})
+    model.close()
+    log(f"[bench] {wl.name}: {res['tokens_per_s']} tok/s, {res['ms_per_step']} ms/step, "
+        f"{res['step_hbm_frac']:.1%} of peak ({time.time() - t0:.1f}s)")
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -182,81 +372,32 @@ def main():
     max_k = max(max(r.k for r in reqs), max(wl.k_sweep, default=0) if len(reqs) == 1 else 0, 1)
     max_kv = max(r.n_audio + r.n_instr + r.reply_len for r in reqs) + max_k + 2
     max_kv = (max_kv + 63) // 64 * 64
+    trace = args.trace_window
+    extras = not trace
     log(f"[bench] workload {wl.name}: {len(reqs)} request(s), shape {shape.name} L={shape.n_layers}")
     t0 = time.time()
     dev = gen.make_weights(shape, wl.seed, fmt="device")
     log(f"[bench] weights generated in {time.time() - t0:.1f}s")
     t0 = time.time()
     model = as2d.Model(shape, dev, max_requests=len(reqs), max_kv_len=max_kv, max_k=max_k)
-    del dev
+    keep_dev = extras and not args.no_configs and args.layers is None and wl.shape.name == wc.QWEN7B.name
+    if not keep_dev:
+        del dev
     log(f"[bench] weights loaded and packed in {time.time() - t0:.1f}s")
 
-    # prefill every request; reference streams from target-only decoding
-    srcs, starts = [], []
-    for i, r in enumerate(reqs):
-        audio = gen.audio_embeddings(shape, r.n_audio, wl.seed, i, fmt="device")
-        instr = gen.instruction_tokens(shape, r.n_instr, wl.seed, i)
-        t0 = time.time()
-        first, L = model.prefill(i, audio, instr)
-        prefill_s = time.time() - t0
-        y = [first] + [model.decode_one(i)["correction_token"] for _ in range(r.reply_len)]
-        model.rollback(i, L, first)
-        starts.append((L, first))
-        srcs.append(gen.CandidateSource(y, shape.vocab, r.p, seed=wl.seed, req=i))
-        log(f"[bench] request {i}: prefix {L} rows prefilled in {prefill_s * 1e3:.1f} ms, reference stream "
-            f"{r.reply_len} tokens ({time.time() - t0:.1f}s)")
-        prefill_info = {"rows": L, "ms": round(prefill_s * 1e3, 2), "rows_per_s": round(L / prefill_s, 1)}
-
-    done = [0] * len(reqs)        # committed tokens of the current reply pass
-
-    def restart():
-        """Every request back to the end of its prefix (start of its reply)."""
-        for i in range(len(reqs)):
-            model.rollback(i, *starts[i])
-            done[i] = 0
-
-    def step(k_force=None):
-        """One verification call over every request with reply left (one
-        fused pass for several requests); returns tokens committed."""
-        ids, cands = [], []
-        for i, r in enumerate(reqs):
-            if done[i] >= r.reply_len:
-                continue
-            k = min(r.k if k_force is None else k_force, r.reply_len - done[i] - 1)
-            ids.append(i)
-            cands.append(srcs[i].block(done[i], k))
-        if not ids:
-            restart()
-            return step(k_force)
-        outs = model.verify_batch(ids, cands) if len(ids) > 1 else [model.verify(ids[0], cands[0])]
-        got = 0
-        for i, c, o in zip(ids, cands, outs):
-            assert c[:o["accepted_len"]] == srcs[i].ref[done[i] + 1:done[i] + 1 + o["accepted_len"]].tolist()
-            done[i] += o["accepted_len"] + 1
-            got += o["accepted_len"] + 1
-        return got, sum(len(c) + 1 for c in cands), sum(model.state(i)[0] for i in ids)
+    # prefill every request; reference streams committed by the GPU (with
+    # --trace-window in passes of the timed width, so that a kernel trace of
+    # the run holds verification launches of that width only)
+    run = Runner(model, shape, reqs, wl.seed, ref_width=(reqs[0].k + 1) if trace else 1)
+    srcs, starts, prefill_info = run.srcs, run.starts, run.prefill_info
+    step, restart = run.step, run.restart
 
     if args.calib_copy_mib:
         copy_calibration(args.calib_copy_mib)
     for _ in range(args.warmup):
         step()
-    # one untimed pass over every reply: the workload's tokens per step,
-    # which a window of K steps only samples (acceptance varies along the
-    # stream with the corruption draws)
+    # the driver's window: K steps from the beginning of the replies
     restart()
-    pass_steps = pass_tokens = 0
-    while True:
-        pass_tokens += step()[0]
-        pass_steps += 1
-        if all(d >= r.reply_len for d, r in zip(done, reqs)):
-            break
-    # the timed window starts at the beginning of the replies
-    restart()
-    import ctypes
-    _hip = ctypes.CDLL("libamdhip64.so")
-
-    def sync():
-        assert _hip.hipDeviceSynchronize() == 0
     sync()
     committed = rows = kvsum = 0
     t0 = time.perf_counter()
@@ -272,13 +413,22 @@ def main():
     mean_kv = kvsum / args.steps
     step_bytes = model.step_bytes(int(round(mean_rows)), int(mean_kv))
     gbps = step_bytes / (elapsed / args.steps) / 1e9
-    log(f"[bench] {args.steps} steps in {elapsed:.3f}s: {ms:.3f} ms/step, {committed / elapsed:.1f} tok/s, "
+    log(f"[bench] {args.steps} steps in {elapsed:.3f}s: {ms:.3f} ms/step, {committed / elapsed:.1f} tok/s in the window, "
         f"{gbps:.0f} GB/s ({gbps / PEAK_HBM_GBPS:.1%} of peak)")
+
+    # the headline: whole replies, median of n passes
+    whole = ties = None
+    if extras:
+        whole = summarize(model, shape, run.full_passes(args.passes))
+        log(f"[bench] whole replies ({args.passes} passes): {whole['tokens_per_s']} tok/s, "
+            f"{whole['mean_committed_per_step']} tokens per step, {whole['ms_per_step']} ms/step")
+        ties = run.near_ties()
+        log(f"[bench] near ties (device top-2 margin <= 0.05): {ties}")
 
     # the same window through the persistent step kernel (one launch per
     # pass; opt-in, reported beside the headline, which is the graph mode)
     exec_modes = {"graph_ms_per_step": round(ms, 4)}
-    if model.exec_info()[1] > 0:
+    if extras and model.exec_info()[1] > 0:
         restart()
         model.set_exec_mode(as2d.EXEC_PERSISTENT)
         for _ in range(2):
@@ -294,9 +444,23 @@ def main():
         restart()
         log(f"[bench] persistent step kernel: {exec_modes['persistent_ms_per_step']:.3f} ms/step")
 
+    # p-sweep of the k = 8 workload: whole-reply throughput per corruption rate
+    p_sweep = None
+    if extras and len(reqs) == 1 and wl.p_sweep:
+        p_sweep = {}
+        for p in wl.p_sweep:
+            run.set_p(p)
+            for _ in range(2):
+                step()
+            p_sweep[str(p)] = summarize(model, shape, run.full_passes(3))
+        run.set_p(None)
+        restart()
+        log("[bench] p-sweep: " + ", ".join(f"p={p} {v['tokens_per_s']} tok/s ({v['mean_committed_per_step']}/step)"
+                                             for p, v in p_sweep.items()))
+
     roof = None
     kernel_ms = {}
-    if not args.no_kernel_timing:
+    if extras and not args.no_kernel_timing:
         model.set_timing(True)
         model.timing_reset()
         n_t = max(10, args.steps // 2)
@@ -320,6 +484,18 @@ def main():
                 "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic_from_profiles(),
                 "kernel": "gemm_gate_up", "rows": rows0, "bytes_per_launch": gu_bytes,
                 "avg_launch_us": round(gu_us, 2), "ms_per_step_with_events": round(t_evt, 3)}
+        # every verification GEMM at W = 1 and at the timed width
+        gemms = {}
+        H, F, V = shape.hidden, shape.ffn, shape.vocab
+        es = 2 if shape.dtype == wc.BF16 else 4
+        nbytes = {"gemm_qkv": es * H * shape.qkv_out, "gemm_o": es * H * shape.n_q_heads * shape.head_dim,
+                  "gemm_gate_up": es * 2 * F * H, "gemm_down": es * F * H, "gemm_lm_head": es * V * H}
+        for which, name in enumerate(nbytes):
+            for w in sorted({1, rows0}):
+                us = model.time_gemm(which, w, 4 * shape.n_layers if which < 4 else 8)
+                gemms[f"{name}_w{w}"] = {"us": round(us, 2), "gbps": round(nbytes[name] / us / 1e3, 1),
+                                         "frac": round(nbytes[name] / us / 1e3 / PEAK_HBM_GBPS, 4)}
+        roof["gemms_back_to_back"] = gemms
         log("[bench] per-kernel: " + ", ".join(f"{k} {v['avg_us']:.1f}us x{v['launches'] // n_t}"
                                                for k, v in kernel_ms.items()))
 
@@ -332,7 +508,7 @@ def main():
 
     # width-cost profile: step time per k (the paper's R(K) curve, one request)
     width = None
-    if not args.no_width_profile and len(reqs) == 1 and wl.k_sweep:
+    if extras and not args.no_width_profile and len(reqs) == 1 and wl.k_sweep:
         width = {}
         for kk in wl.k_sweep:
             for _ in range(2):
@@ -350,7 +526,7 @@ def main():
     # continuations at prefix offsets 0, 64 and 128 after prefill, 5 timed
     # calls per width and offset) and the offline budget choice from it
     vprof = budget_sel = None
-    if not args.no_width_profile and len(reqs) == 1:
+    if extras and not args.no_width_profile and len(reqs) == 1:
         from paper_2609_37617_amd import budget as bsel
         r0 = reqs[0]
         y = srcs[0].ref.tolist()                    # [first root, y_1, y_2, ...]
@@ -420,7 +596,7 @@ def main():
     # target-decoupled decoding with a drafter on the same GPU (3B- and 0.5B-shaped):
     # serial comparator and concurrent run, with the stage accounting
     decoupled = None
-    if not args.no_decoupled and len(reqs) == 1 and wl.shape.name == wc.QWEN7B.name and args.layers is None:
+    if extras and not args.no_decoupled and len(reqs) == 1 and wl.shape.name == wc.QWEN7B.name and args.layers is None:
         from paper_2609_37617_amd import overlap as ovl
         r0 = reqs[0]
         y = srcs[0].ref.tolist()
@@ -501,7 +677,7 @@ def main():
     # insertions, deletions): with the bounded realignment, and with the
     # search turned off (radius 0: every mismatch read as a substitution)
     aligned = None
-    if not args.no_align and len(reqs) == 1:
+    if extras and not args.no_align and len(reqs) == 1:
         r0 = reqs[0]
         edits = (0.2, 0.05, 0.05)
         draft = gen.edited_stream(srcs[0].ref[1:].tolist(), shape.vocab, *edits, seed=wl.seed)
@@ -527,16 +703,27 @@ def main():
         log(f"[bench] buffer decoding, edited draft: {aligned['with_alignment']} | radius 0: {aligned['without_search']}")
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if extras and not args.no_cpu_baseline:
         r0 = reqs[0]
         t0 = time.time()
-        cpu = cpu_baseline(shape, r0.n_audio, r0.n_instr, r0.k, committed / args.steps)
+        cpu = cpu_baseline(shape, r0.n_audio, r0.n_instr, r0.k, whole["mean_committed_per_step"])
         log(f"[bench] cpu baseline {cpu['value']:.3f} tok/s ({time.time() - t0:.1f}s)")
+
+    # the other workloads, each in a context of its own: the 3B shape, the
+    # long-audio prefix and the mixed batch (the same 7B weights)
+    configs = None
+    if keep_dev:
+        model.close()
+        configs = {}
+        for idx in (1, 3, 4):
+            same = wc.workload(idx).shape.name == shape.name
+            configs[wc.workload(idx).name] = measure_config(idx, dev if same else None, n_passes=3 if idx != 4 else 2)
+        del dev
 
     r0 = reqs[0]
     out = {
         "metric": METRIC,
-        "value": round(committed / elapsed, 2),
+        "value": whole["tokens_per_s"] if whole else round(committed / elapsed, 2),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -552,16 +739,22 @@ def main():
                    "requests": len(reqs), "prefix": r0.n_audio + r0.n_instr, "reply_tokens": r0.reply_len,
                    "k": r0.k, "p": r0.p},
         "verify_steps_per_s": round(args.steps / elapsed, 2),
-        "mean_committed_per_step": round(committed / args.steps, 3),
-        "full_pass": {"steps": pass_steps, "committed": pass_tokens,
-                      "mean_committed_per_step": round(pass_tokens / pass_steps, 3)},
+        "window": {"steps": args.steps, "committed": committed, "tokens_per_s": round(committed / elapsed, 2),
+                   "mean_committed_per_step": round(committed / args.steps, 3)},
+        "whole_replies": whole,
+        "near_ties": ties,
+        "trace_window": bool(trace),
         "step_hbm_bytes": step_bytes,
+        "step_hbm_bytes_bf16_kv": int(step_bytes - kv_bytes(shape, mean_rows, mean_kv, 4)
+                                      + kv_bytes(shape, mean_rows, mean_kv, 2)),
         "step_hbm_gbps": round(gbps, 1),
         "step_hbm_frac": round(gbps / PEAK_HBM_GBPS, 4),
         "roofline": roof,
         "cpu_baseline": cpu,
         "stream_ceiling_gbps": round(stream_gbps, 1),
         "exec_modes": exec_modes,
+        "p_sweep": p_sweep,
+        "configs": configs,
         "ms_per_step_by_k": width,
         "buffer_decoding": aligned,
         "prefill_first_request": prefill_info,
@@ -571,7 +764,8 @@ def main():
         "kernels": {k: round(v["avg_us"], 2) for k, v in kernel_ms.items()},
     }
     print(json.dumps(out), flush=True)
-    model.close()
+    if not keep_dev:
+        model.close()
 
 
 if __name__ == "__main__":
