@@ -138,6 +138,24 @@ int as2d_decode_one(as2d_ctx* ctx, int32_t req, as2d_verify_out* out);
 int as2d_verify_batch(as2d_ctx* ctx, int32_t n, const int32_t* reqs, const int32_t* cands_flat,
                       const int32_t* ks, as2d_verify_out* outs);
 
+/*
+ * Verification for callers that cannot allocate device memory (code under
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * as2d_verify for one request, with every buffer the pass works in
+ * (activations, split-K and attention partials, counters, row descriptors)
+ * taken from the library's static scratch array (64 MiB per GPU, held until
+ * the process ends) instead of the context's own.  The weights, the KV
+ * cache, the pinned result buffers and, with keep_logits, the logits stay
+ * in the context.  The call allocates nothing and launches its kernels one
+ * by one on the context's stream (no graph); results are bit-identical to
+ * as2d_verify.  AS2D_ECAPACITY when the pass needs more than the array
+ * holds: the need grows with the model's widths and the request's KV length
+ * (about 23 MiB for the 7B shape at 1,040 positions); the message gives the
+ * bytes.  Every call on one GPU shares the array: calls that overlap on one
+ * GPU (from several contexts or threads) race.
+ */
+int as2d_verify_static(as2d_ctx* ctx, int32_t req, const int32_t* cands, int32_t k, as2d_verify_out* out);
+
 /* ---- test and inspection hooks (not on the timed path) ---------------- */
 
 /* When on, later calls also write the float32 logits of every processed

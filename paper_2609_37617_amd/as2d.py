@@ -28,7 +28,7 @@ EXPORTS = ["as2d_load_weights", "as2d_prefill_kv", "as2d_verify", "as2d_decode_o
            "as2d_cbuf_create", "as2d_cbuf_free", "as2d_cbuf_publish", "as2d_cbuf_snapshot",
            "as2d_cbuf_read", "as2d_cbuf_n_records", "as2d_cbuf_get_record", "as2d_cursor_init",
            "as2d_cursor_propose", "as2d_cursor_update", "as2d_verify_from_buffer", "as2d_run_decoupled",
-           "as2d_set_stream", "as2d_set_cu_budget"]
+           "as2d_set_stream", "as2d_set_cu_budget", "as2d_verify_static"]
 
 
 class Config(ctypes.Structure):
@@ -90,6 +90,7 @@ def load_library(path: str = LIB_PATH):
                                       ctypes.POINTER(_P)]
     lib.as2d_prefill_kv.argtypes = [_P, _I, _P, _I, _P, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
     lib.as2d_verify.argtypes = [_P, _I, _P, _I, ctypes.POINTER(VerifyOut)]
+    lib.as2d_verify_static.argtypes = [_P, _I, _P, _I, ctypes.POINTER(VerifyOut)]
     lib.as2d_decode_one.argtypes = [_P, _I, ctypes.POINTER(VerifyOut)]
     lib.as2d_verify_batch.argtypes = [_P, _I, _P, _P, _P, _P]
     lib.as2d_set_keep_logits.argtypes = [_P, _I]
@@ -199,6 +200,15 @@ class Model:
         k = len(c) if k is None else k
         out = VerifyOut()
         self._check(self.lib.as2d_verify(self.ctx, req, _ptr(c) if c.size else None, k, ctypes.byref(out)))
+        return out.as_dict()
+
+    def verify_static(self, req: int, cands: Sequence[int]) -> dict:
+        """as2d_verify_static: the same call with the pass's buffers in the
+        library's static scratch array (allocates nothing)."""
+        c = np.ascontiguousarray(cands, dtype=np.int32)
+        out = VerifyOut()
+        self._check(self.lib.as2d_verify_static(self.ctx, req, _ptr(c) if c.size else None, len(c),
+                                                ctypes.byref(out)))
         return out.as_dict()
 
     def decode_one(self, req: int) -> dict:

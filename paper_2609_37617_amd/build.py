@@ -4,7 +4,8 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SRC = [os.path.join(HERE, "csrc", f) for f in ("kernels.hip", "step.hip", "as2d.cpp", "cbuf.cpp", "decoupled.cpp")]
+SRC = [os.path.join(HERE, "csrc", f) for f in ("kernels.hip", "step.hip", "static_scratch.hip", "as2d.cpp", "cbuf.cpp",
+                                                    "decoupled.cpp")]
 LIB = os.path.join(HERE, "libas2d.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

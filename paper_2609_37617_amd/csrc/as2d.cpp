@@ -23,6 +23,9 @@ using namespace as2d;
 
 namespace {
 
+// Rows of a pass of as2d_verify_static (the direct GEMM path's two row tiles).
+constexpr int kStaticRows = kDirectMT * 16;
+
 struct GemmPlan {
   int N = 0, K = 0, KT = 0, pairs = 0, KS = 1, ktps = 0, np = 1, ns = 4;
   int G = 0;  // balanced direct path: workgroups sharing the units (0: one tile per workgroup)
@@ -42,8 +45,9 @@ struct ReqState {
 // Device memory one forward pass works in besides the weights and the KV
 // cache: activations, split-K and attention partials, arg-max partials,
 // counters and the pass's descriptors and results.  A context holds one
-// set sized for its largest pass; the launcher takes the set as an
-// argument.
+// set sized for its largest pass; as2d_verify_static points one into the
+// library's static scratch array instead (the launcher takes the set as an
+// argument).
 struct PassBufs {
   float *x = nullptr, *q = nullptr, *logits = nullptr, *sumsq = nullptr;
   float *amax_val = nullptr, *amax_val2 = nullptr, *row_margin = nullptr;
@@ -858,6 +862,52 @@ int split_counter_count(const as2d_ctx* c) {
   return n;
 }
 
+// Pass buffers for passes of up to kStaticRows rows over n_chunks key
+// chunks, laid out from `base` (256-byte aligned pieces); returns the
+// bytes they span.  The logits (an output the caller reads with
+// as2d_get_logits) stay in the context.
+size_t static_layout(const as2d_ctx* c, int n_chunks, char* base, PassBufs* S) {
+  const as2d_config& g = c->cfg;
+  const size_t R = kStaticRows, H = g.hidden, F = g.ffn, V = g.vocab, QD = (size_t)g.n_q_heads * g.head_dim;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* p = base + off;
+    off += (bytes + 255) / 256 * 256;
+    return (void*)p;
+  };
+  size_t part = 0;
+  for (const GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm})
+    if (p->KS > 1) part = std::max(part, (size_t)p->KS * R * p->N);
+  S->d_rows = (RowDesc*)take(sizeof(RowDesc) * R);
+  S->d_reqs = (ReqDesc*)take(sizeof(ReqDesc) * 2 * g.max_requests);
+  S->d_out = (StepOut*)take(sizeof(StepOut) * g.max_requests);
+  S->x = (float*)take(R * H * 4);
+  S->q = (float*)take(R * QD * 4);
+  S->xg = take(R * H * 4);
+  S->attn = take(R * QD * 4);
+  S->hbuf = take(R * F * 4);
+  if (c->bf16) {
+    S->xg_plane = (long long)(R * H);
+    S->attn_plane = (long long)(R * QD);
+    S->h_plane = (long long)(R * F);
+  }
+  S->logits = c->b.logits;
+  S->sumsq = (float*)take((H / kPairCols) * R * 4);
+  S->amax_val = (float*)take((V / kPairCols) * R * 4);
+  S->amax_val2 = (float*)take((V / kPairCols) * R * 4);
+  S->amax_idx = (int*)take((V / kPairCols) * R * 4);
+  S->row_tok = (int*)take(R * 4);
+  S->row_bad = (int*)take(R * 4);
+  S->row_margin = (float*)take(R * 4);
+  S->fin_counters = (int*)take((size_t)g.max_requests * 4);
+  S->part = (float*)take(part * 4);
+  S->counters = (int*)take((size_t)split_counter_count(c) * 4);
+  S->part_rows = (int)R;
+  S->pacc = (float*)take((size_t)n_chunks * R * QD * 4);
+  S->pml = (float*)take((size_t)n_chunks * R * g.n_q_heads * 2 * 4);
+  return off;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -1071,6 +1121,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   CK(dalloc(c, &c->b.counters, (size_t)n_cnt * 4));
   HIP_TRY(c, hipMemsetAsync(c->b.counters, 0, (size_t)n_cnt * 4, c->stream));
   HIP_TRY(c, prepare_kernels());
+  {
+    // the static scratch of as2d_verify_static: its address on this device
+    void* p = nullptr;
+    size_t n = 0;
+    HIP_TRY(c, static_scratch(&p, &n));
+  }
   // persistent step kernel (verification passes of up to 32 rows; every
   // GEMM on a balanced plan)
   bool all_balanced = true;
@@ -1217,6 +1273,39 @@ int as2d_verify_batch(as2d_ctx* c, int32_t n, const int32_t* reqs, const int32_t
   if (rc) return rc;
   if ((rc = run_forward(c, M, n, n, true, true))) return rc;
   return commit_verify(c, n, reqs, ks, outs);
+}
+
+int as2d_verify_static(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k, as2d_verify_out* out) {
+  int M = 0;
+  int rc = assemble_verify(c, 1, &req, cands, &k, out, kStaticRows, &M);
+  if (rc) return rc;
+  const as2d_config& g = c->cfg;
+  const int mr = g.max_requests;
+  const int n_chunks = (c->h_reqs[0].L0 + M + kAttnChunk - 1) / kAttnChunk;
+  void* base = nullptr;
+  size_t cap = 0;
+  HIP_TRY(c, static_scratch(&base, &cap));
+  PassBufs S;
+  const size_t need = static_layout(c, n_chunks, (char*)base, &S);
+  if (need > cap)
+    return fail(c, AS2D_ECAPACITY, "verify_static: the pass needs %zu bytes of static scratch, %zu available (%d keys)",
+                need, cap, c->h_reqs[0].L0 + M);
+  hipStream_t s = c->stream;
+  HIP_TRY(c, hipMemcpyAsync(S.d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
+  HIP_TRY(c, hipMemcpyAsync(S.d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
+  // the array keeps the last call's contents: counters must start at zero
+  HIP_TRY(c, launch_fill_zero(S.counters, split_counter_count(c), s));
+  HIP_TRY(c, launch_fill_zero(S.fin_counters, mr, s));
+  const int timing = c->timing;   // no event bracketing here (events are created on first use)
+  c->timing = 0;
+  rc = launch_pass(c, S, M, 1, 1, M, true, n_chunks);
+  c->timing = timing;
+  if (rc) return rc;
+  HIP_TRY(c, hipMemcpyAsync(c->h_out, S.d_out, sizeof(StepOut), hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(c->h_tok, S.row_tok, sizeof(int) * M, hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipMemcpyAsync(c->h_margin, S.row_margin, sizeof(float) * M, hipMemcpyDeviceToHost, s));
+  HIP_TRY(c, hipStreamSynchronize(s));
+  return commit_verify(c, 1, &req, &k, out);
 }
 
 int as2d_verify(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k, as2d_verify_out* out) {

@@ -206,6 +206,10 @@ hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, i
 // Zeroes n ints (a kernel, not a memset, so that it may be captured).
 hipError_t launch_fill_zero(int* p, int n, hipStream_t s);
 
+// The library's static scratch array (static_scratch.hip) on the current
+// device: its device address (looked up once per device) and size.
+hipError_t static_scratch(void** ptr, size_t* bytes);
+
 // Streams n16 16-byte units of buf with `grid` workgroups (read-bandwidth
 // reference); n16 must split into whole 8 KiB runs per wave.
 hipError_t launch_stream_read(const uint4* buf, long long n16, int grid, unsigned* out, hipStream_t s);
