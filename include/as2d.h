@@ -20,9 +20,10 @@
  *   - All device memory (packed weights, KV cache slots, scratch) is owned
  *     by the library and released by as2d_free().
  *   - Number formats: weights are stored in cfg->dtype; the residual
- *     stream, KV cache, softmax and accumulators are float32, and bf16
- *     models multiply activations into the weights as bf16 (hi, lo) pairs,
- *     i.e. to about 17 significant bits.
+ *     stream, softmax and accumulators are float32, and bf16 models
+ *     multiply activations into the weights as bf16 (hi, lo) pairs, i.e.
+ *     to about 17 significant bits; their KV cache holds the keys and
+ *     values as such pairs too (4 bytes per element, as float32).
  *   - A context is used by one host thread at a time.
  *   - Token ids are int32 in [0, vocab).
  *
@@ -143,14 +144,14 @@ int as2d_verify_batch(as2d_ctx* ctx, int32_t n, const int32_t* reqs, const int32
  * graph capture, tight serving loops, harnesses that forbid allocation):
  * as2d_verify for one request, with every buffer the pass works in
  * (activations, split-K and attention partials, counters, row descriptors)
- * taken from the library's static scratch array (64 MiB per GPU, held until
+ * taken from the library's static scratch array (32 MiB per GPU, held until
  * the process ends) instead of the context's own.  The weights, the KV
  * cache, the pinned result buffers and, with keep_logits, the logits stay
  * in the context.  The call allocates nothing and launches its kernels one
  * by one on the context's stream (no graph); results are bit-identical to
  * as2d_verify.  AS2D_ECAPACITY when the pass needs more than the array
  * holds: the need grows with the model's widths and the request's KV length
- * (about 23 MiB for the 7B shape at 1,040 positions); the message gives the
+ * (about 10 MiB for the 7B shape at 1,040 positions); the message gives the
  * bytes.  Every call on one GPU shares the array: calls that overlap on one
  * GPU (from several contexts or threads) race.
  */
@@ -210,8 +211,10 @@ int as2d_rollback(as2d_ctx* ctx, int32_t req, int32_t kv_len, int32_t root);
 int as2d_get_state(as2d_ctx* ctx, int32_t req, int32_t* kv_len, int32_t* root, int32_t* committed);
 
 /* Copy positions 0..n_tok-1 of one layer's cache: host_k, host_v
- * [n_kv][n_tok][head_dim] float32 (K after rotation).  The cache is
- * float32 for every model dtype. */
+ * [n_kv][n_tok][head_dim] float32 (K after rotation).  A bf16 model's
+ * cache holds each value as a bf16 pair (hi, lo) with hi + lo equal to the
+ * float32 value to about 2^-17 relative (the operands the attention
+ * multiplies); that sum is returned.  Float32 models keep float32. */
 int as2d_read_kv(as2d_ctx* ctx, int32_t req, int32_t layer, void* host_k, void* host_v, int32_t n_tok);
 
 /* Rebind the context to another stream (hip_stream = NULL: a stream of its

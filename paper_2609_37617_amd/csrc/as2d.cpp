@@ -53,6 +53,7 @@ struct PassBufs {
   float *amax_val = nullptr, *amax_val2 = nullptr, *row_margin = nullptr;
   float *part = nullptr, *pacc = nullptr, *pml = nullptr;
   int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr, *row_bad = nullptr, *fin_counters = nullptr;
+  int* attn_cnt = nullptr;                                // finished attention blocks per (request, head)
   void *xg = nullptr, *attn = nullptr, *hbuf = nullptr;  // activation planes
   long long xg_plane = 0, attn_plane = 0, h_plane = 0;    // offset of the lo plane (bf16), elements
   int part_rows = 0;                                      // row stride of the attention partials
@@ -84,13 +85,14 @@ struct as2d_ctx {
   GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
 
   float *kc = nullptr, *vc = nullptr;  // float32 KV cache
-  long long slot_stride = 0, layer_stride = 0;
+  long long slot_stride = 0, layer_stride = 0;  // float32 units (a bf16 cache holds twice as many elements)
+  int kv_stride = 0;                             // positions per head in the cache: max_kv_len rounded up to 64
 
   PassBufs b;                 // the context's pass buffers
   float* rope_cs = nullptr;   // rotary table [max_kv_len][head_dim / 2][2]
   void* audio = nullptr;      // audio rows of the prefill being run
   size_t audio_cap = 0;
-  int n_chunks_cap = 0;
+  int n_blocks_cap = 0;   // 64-key attention blocks of a full slot
   int max_rows = 0;
 
   RowDesc* h_rows = nullptr;
@@ -344,10 +346,11 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M, const
 // Kernel launches of one forward pass over the rows and requests in the
 // device descriptors: n_att attention requests (d_reqs[0..n_att)), n_fin
 // finish requests (d_reqs[max_requests..)) covering fin_rows rows;
-// with_head = run the LM head and verification.  max_chunks bounds the
-// attention key chunks (chunks past a request's keys exit at once).
+// with_head = run the LM head and verification; prefill = a prefill pass
+// (one request, its rows in order).  max_blocks bounds the
+// attention key blocks of any request (it sizes the attention grid).
 int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int fin_rows, bool with_head,
-                int max_chunks) {
+                int max_blocks, bool prefill) {
   const as2d_config& g = c->cfg;
   hipStream_t s = c->stream;
   const bool bf = c->bf16;
@@ -372,7 +375,7 @@ int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int
       a.k_cache = kc;
       a.v_cache = vc;
       a.slot_stride = c->slot_stride;
-      a.kv_cap = g.max_kv_len;
+      a.kv_cap = c->kv_stride;
       a.n_q = g.n_q_heads;
       a.n_kv = g.n_kv_heads;
       a.head_dim = d;
@@ -386,7 +389,7 @@ int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int
       a.k_cache = kc;
       a.v_cache = vc;
       a.slot_stride = c->slot_stride;
-      a.kv_cap = g.max_kv_len;
+      a.kv_cap = c->kv_stride;
       a.rows = B.d_rows;
       a.reqs = B.d_reqs;
       a.n_q = g.n_q_heads;
@@ -399,9 +402,9 @@ int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int
       a.out = B.attn;
       a.out_plane = B.attn_plane;
       a.M = M;
-      a.row_groups = (M + kAttnRowGroup - 1) / kAttnRowGroup;   // a function of the graph key
+      a.attn_cnt = B.attn_cnt;
       Timed t(c, K_ATTN);
-      HIP_TRY(c, launch_attention(bf, a, n_att, max_chunks, s));
+      HIP_TRY(c, launch_attention(bf, a, n_att, max_blocks, prefill, s));
     }
     {
       GemmArgs a = base_args(c, c->p_o, w.o, M, &B);
@@ -490,7 +493,7 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     s.qkv.k_cache = kc;
     s.qkv.v_cache = vc;
     s.qkv.slot_stride = c->slot_stride;
-    s.qkv.kv_cap = g.max_kv_len;
+    s.qkv.kv_cap = c->kv_stride;
     s.qkv.n_q = nq;
     s.qkv.n_kv = nkv;
     s.qkv.head_dim = d;
@@ -502,7 +505,7 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     a.k_cache = kc;
     a.v_cache = vc;
     a.slot_stride = c->slot_stride;
-    a.kv_cap = g.max_kv_len;
+    a.kv_cap = c->kv_stride;
     a.rows = c->b.d_rows;
     a.reqs = c->b.d_reqs;
     a.n_q = nq;
@@ -513,7 +516,7 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     a.pml = c->b.pml;
     a.part_rows = c->b.part_rows;
     a.out = (char*)c->pattn + l * qs * 4;
-    a.row_groups = 1;
+    a.attn_cnt = c->b.attn_cnt;
     a.out_plane = c->bf16 ? (long long)qs : 0;
     a.M = M;
 
@@ -638,7 +641,7 @@ int graph_for(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows, bool persi
     hipGraph_t gr = nullptr;
     HIP_TRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
     int rc = persistent ? launch_persistent(c, M, n_att, n_fin, fin_rows)
-                        : launch_pass(c, c->b, M, n_att, n_fin, fin_rows, true, c->n_chunks_cap);
+                        : launch_pass(c, c->b, M, n_att, n_fin, fin_rows, true, c->n_blocks_cap, false);
     hipError_t e = hipStreamEndCapture(c->stream, &gr);
     if (rc) {
       if (gr) hipGraphDestroy(gr);
@@ -667,12 +670,12 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool v
   for (int r = 0; r < n_fin; ++r) fin_rows += c->h_reqs[mr + r].W;
   HIP_TRY(c, hipMemcpyAsync(c->b.d_rows, c->h_rows, sizeof(RowDesc) * M, hipMemcpyHostToDevice, s));
   HIP_TRY(c, hipMemcpyAsync(c->b.d_reqs, c->h_reqs, sizeof(ReqDesc) * 2 * mr, hipMemcpyHostToDevice, s));
-  int max_chunks = 1;
+  int max_blocks = 1;
   for (int r = 0; r < n_att; ++r) {
     const int nk = c->h_reqs[r].L0 + c->h_reqs[r].W;
-    max_chunks = std::max(max_chunks, (nk + kAttnChunk - 1) / kAttnChunk);
+    max_blocks = std::max(max_blocks, (nk + kAttnBlock - 1) / kAttnBlock);
   }
-  if (max_chunks > c->n_chunks_cap) return fail(c, AS2D_ECAPACITY, "attention chunks %d > %d", max_chunks, c->n_chunks_cap);
+  if (max_blocks > c->n_blocks_cap) return fail(c, AS2D_ECAPACITY, "attention blocks %d > %d", max_blocks, c->n_blocks_cap);
   const bool verify_pass = verify_call && with_head && n_fin == n_att;
   const bool persistent = verify_pass && c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && M <= kStepRows;
   const bool graph = verify_pass && c->exec_mode != AS2D_EXEC_EAGER && !c->timing;
@@ -684,7 +687,7 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool v
     HIP_TRY(c, hipGraphLaunch(ex, s));
   } else {
     int rc = persistent ? launch_persistent(c, M, n_att, n_fin, fin_rows)
-                        : launch_pass(c, c->b, M, n_att, n_fin, fin_rows, with_head, max_chunks);
+                        : launch_pass(c, c->b, M, n_att, n_fin, fin_rows, with_head, max_blocks, !verify_call);
     if (rc) return rc;
   }
   if (persistent) HIP_TRY(c, hipMemcpyAsync(&c->h_err, c->perr, sizeof(int), hipMemcpyDeviceToHost, s));
@@ -862,11 +865,11 @@ int split_counter_count(const as2d_ctx* c) {
   return n;
 }
 
-// Pass buffers for passes of up to kStaticRows rows over n_chunks key
-// chunks, laid out from `base` (256-byte aligned pieces); returns the
+// Pass buffers for passes of up to kStaticRows rows over n_blocks key
+// blocks, laid out from `base` (256-byte aligned pieces); returns the
 // bytes they span.  The logits (an output the caller reads with
 // as2d_get_logits) stay in the context.
-size_t static_layout(const as2d_ctx* c, int n_chunks, char* base, PassBufs* S) {
+size_t static_layout(const as2d_ctx* c, int n_blocks, char* base, PassBufs* S) {
   const as2d_config& g = c->cfg;
   const size_t R = kStaticRows, H = g.hidden, F = g.ffn, V = g.vocab, QD = (size_t)g.n_q_heads * g.head_dim;
   size_t off = 0;
@@ -903,8 +906,10 @@ size_t static_layout(const as2d_ctx* c, int n_chunks, char* base, PassBufs* S) {
   S->part = (float*)take(part * 4);
   S->counters = (int*)take((size_t)split_counter_count(c) * 4);
   S->part_rows = (int)R;
-  S->pacc = (float*)take((size_t)n_chunks * R * QD * 4);
-  S->pml = (float*)take((size_t)n_chunks * R * g.n_q_heads * 2 * 4);
+  const size_t spans = (n_blocks + kAttnSpan - 1) / kAttnSpan;
+  S->pacc = (float*)take(spans * R * QD * 4);
+  S->pml = (float*)take(spans * R * g.n_q_heads * 2 * 4);
+  S->attn_cnt = (int*)take((size_t)g.max_requests * g.n_q_heads * 4);
   return off;
 }
 
@@ -961,7 +966,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   if (((g.n_q_heads + 2 * g.n_kv_heads) * g.head_dim) % 128 || (g.n_q_heads * g.head_dim) % 128)
     return bad("attention widths must be multiples of 128");
   if (g.dtype != AS2D_F32 && g.dtype != AS2D_BF16) return bad("dtype must be AS2D_F32 or AS2D_BF16");
-  if (g.max_requests < 1 || g.max_kv_len < 2 || g.max_kv_len > kMaxChunks * kAttnChunk || g.max_k < 0 ||
+  if (g.max_requests < 1 || g.max_kv_len < 2 || g.max_kv_len > kMaxBlocks * kAttnBlock || g.max_k < 0 ||
       g.max_k > 31)
     return bad("capacity: max_requests >= 1, 2 <= max_kv_len <= 32768, 0 <= max_k <= 31");
   if (g.hidden > 8192) return bad("hidden must be <= 8192");
@@ -1082,7 +1087,8 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     int rc = 0;
 
   // KV cache: [slot][layer][kv_head][pos][d]
-  c->layer_stride = (long long)nkv * g.max_kv_len * d;
+  c->kv_stride = (g.max_kv_len + 63) / 64 * 64;
+  c->layer_stride = (long long)nkv * c->kv_stride * d;
   c->slot_stride = c->layer_stride * g.n_layers;
   const size_t kv_bytes = (size_t)c->slot_stride * g.max_requests * sizeof(float);
   CK(dalloc(c, &c->kc, kv_bytes));
@@ -1091,7 +1097,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   // activations and scratch, sized for the largest pass
   c->max_rows = kMaxRows;   // rows per pass (prefill chunks, fused batches)
   const int MR = kMaxRows;
-  c->n_chunks_cap = (g.max_kv_len + kAttnChunk - 1) / kAttnChunk;
+  c->n_blocks_cap = (g.max_kv_len + kAttnBlock - 1) / kAttnBlock;
   CK(dalloc(c, &c->b.x, (size_t)MR * H * 4));
   CK(dalloc(c, &c->b.q, (size_t)MR * nq * d * 4));
   // activation planes: two bf16 planes or one float32 plane, 4 bytes per element either way
@@ -1162,8 +1168,11 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
     }
   }
   c->b.part_rows = MR;
-  CK(dalloc(c, &c->b.pacc, (size_t)c->n_chunks_cap * MR * nq * d * 4));
-  CK(dalloc(c, &c->b.pml, (size_t)c->n_chunks_cap * MR * nq * 2 * 4));
+  const size_t spans_cap = (c->n_blocks_cap + kAttnSpan - 1) / kAttnSpan;
+  CK(dalloc(c, &c->b.pacc, spans_cap * MR * nq * d * 4));
+  CK(dalloc(c, &c->b.pml, spans_cap * MR * nq * 2 * 4));
+  CK(dalloc(c, &c->b.attn_cnt, (size_t)g.max_requests * nq * 4));
+  HIP_TRY(c, hipMemsetAsync(c->b.attn_cnt, 0, (size_t)g.max_requests * nq * 4, c->stream));
   CK(dalloc(c, &c->b.d_rows, sizeof(RowDesc) * MR));
   CK(dalloc(c, &c->b.d_reqs, sizeof(ReqDesc) * 2 * g.max_requests));
   CK(dalloc(c, &c->b.d_out, sizeof(StepOut) * g.max_requests));
@@ -1281,12 +1290,12 @@ int as2d_verify_static(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k
   if (rc) return rc;
   const as2d_config& g = c->cfg;
   const int mr = g.max_requests;
-  const int n_chunks = (c->h_reqs[0].L0 + M + kAttnChunk - 1) / kAttnChunk;
+  const int n_blocks = (c->h_reqs[0].L0 + M + kAttnBlock - 1) / kAttnBlock;
   void* base = nullptr;
   size_t cap = 0;
   HIP_TRY(c, static_scratch(&base, &cap));
   PassBufs S;
-  const size_t need = static_layout(c, n_chunks, (char*)base, &S);
+  const size_t need = static_layout(c, n_blocks, (char*)base, &S);
   if (need > cap)
     return fail(c, AS2D_ECAPACITY, "verify_static: the pass needs %zu bytes of static scratch, %zu available (%d keys)",
                 need, cap, c->h_reqs[0].L0 + M);
@@ -1296,9 +1305,10 @@ int as2d_verify_static(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k
   // the array keeps the last call's contents: counters must start at zero
   HIP_TRY(c, launch_fill_zero(S.counters, split_counter_count(c), s));
   HIP_TRY(c, launch_fill_zero(S.fin_counters, mr, s));
+  HIP_TRY(c, launch_fill_zero(S.attn_cnt, mr * g.n_q_heads, s));
   const int timing = c->timing;   // no event bracketing here (events are created on first use)
   c->timing = 0;
-  rc = launch_pass(c, S, M, 1, 1, M, true, n_chunks);
+  rc = launch_pass(c, S, M, 1, 1, M, true, n_blocks, false);
   c->timing = timing;
   if (rc) return rc;
   HIP_TRY(c, hipMemcpyAsync(c->h_out, S.d_out, sizeof(StepOut), hipMemcpyDeviceToHost, s));
@@ -1393,12 +1403,38 @@ int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* ho
   if (layer < 0 || layer >= g.n_layers || n_tok < 0 || n_tok > g.max_kv_len || !host_k || !host_v)
     return fail(c, AS2D_EINVAL, "read_kv: bad arguments");
   HIP_TRY(c, hipStreamSynchronize(c->stream));
-  const size_t row = (size_t)g.head_dim;
+  const size_t d = (size_t)g.head_dim, cap = (size_t)c->kv_stride;
+  float* ok = static_cast<float*>(host_k);
+  float* ov = static_cast<float*>(host_v);
+  // one head's cache region: cap * d floats of K (positions, then dimensions:
+  // bf16 (hi, lo) rows or float32 rows) and of V (dimensions, then positions:
+  // bf16 (hi, lo) planes or one float32 plane)
+  std::vector<float> kbuf(cap * d), vbuf(cap * d);
+  auto hi16 = [](const float* base, size_t i) {
+    uint16_t h;
+    memcpy(&h, reinterpret_cast<const char*>(base) + 2 * i, 2);
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+  };
   for (int h = 0; h < g.n_kv_heads; ++h) {
-    const size_t src = (size_t)req * c->slot_stride + (size_t)layer * c->layer_stride +
-                       (size_t)h * g.max_kv_len * g.head_dim;
-    HIP_TRY(c, hipMemcpy((float*)host_k + h * n_tok * row, c->kc + src, n_tok * row * 4, hipMemcpyDeviceToHost));
-    HIP_TRY(c, hipMemcpy((float*)host_v + h * n_tok * row, c->vc + src, n_tok * row * 4, hipMemcpyDeviceToHost));
+    const size_t src = (size_t)req * c->slot_stride + (size_t)layer * c->layer_stride + (size_t)h * cap * d;
+    HIP_TRY(c, hipMemcpy(kbuf.data(), c->kc + src, cap * d * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(c, hipMemcpy(vbuf.data(), c->vc + src, cap * d * 4, hipMemcpyDeviceToHost));
+    for (size_t t = 0; t < (size_t)n_tok; ++t)
+      for (size_t j = 0; j < d; ++j) {
+        float kv, vv;
+        if (c->bf16) {
+          kv = hi16(kbuf.data(), t * 2 * d + j) + hi16(kbuf.data(), t * 2 * d + d + j);
+          vv = hi16(vbuf.data(), j * cap + t) + hi16(vbuf.data(), (d + j) * cap + t);
+        } else {
+          kv = kbuf[t * d + j];
+          vv = vbuf[j * cap + t];
+        }
+        ok[((size_t)h * n_tok + t) * d + j] = kv;
+        ov[((size_t)h * n_tok + t) * d + j] = vv;
+      }
   }
   return AS2D_OK;
 }
@@ -1526,7 +1562,7 @@ int as2d_time_gemm(as2d_ctx* c, int32_t which, int32_t rows, int32_t reps, doubl
         a = base_args(c, c->p_qkv, w.qkv, rows);
         a.A = c->b.xg; a.a_plane = c->b.xg_plane; a.bias = w.bias; a.q_out = c->b.q;
         a.k_cache = c->kc + (size_t)l * c->layer_stride; a.v_cache = c->vc + (size_t)l * c->layer_stride;
-        a.slot_stride = c->slot_stride; a.kv_cap = g.max_kv_len; a.n_q = g.n_q_heads;
+        a.slot_stride = c->slot_stride; a.kv_cap = c->kv_stride; a.n_q = g.n_q_heads;
         a.n_kv = g.n_kv_heads; a.head_dim = g.head_dim; a.rope_cs = c->rope_cs;
         break;
       case 1:

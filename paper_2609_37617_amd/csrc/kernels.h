@@ -30,11 +30,12 @@ constexpr int kMaxMTiles = 9;           // up to 144 rows per forward pass
 constexpr int kMaxRows = kMaxMTiles * 16;
 constexpr int kDirectMT = 2;            // row tiles of the direct path (up to 32 rows)
 constexpr int kStepRows = kDirectMT * 16;  // rows of a persistent-kernel pass
-constexpr int kAttnChunk = 32;          // keys per attention split
-constexpr int kAttnRowGroup = 32;       // rows per attention workgroup (row groups)
+constexpr int kAttnBlock = 64;          // keys per attention block (absolute positions)
+constexpr int kAttnSpan = 2;            // blocks per attention span (the first merge level)
+constexpr int kAttnSpanKeys = kAttnSpan * kAttnBlock;
 constexpr int kMaxSplits = 16;          // largest k-split count of a GEMM
 constexpr int kMaxUnits = 24;           // (pair, split) units per workgroup, balanced direct path
-constexpr int kMaxChunks = 1024;        // attention chunks per row (positions < 32768)
+constexpr int kMaxBlocks = 512;         // attention blocks per row (positions < 32768)
 
 // Column order of a packed matrix (pack_kernel): which matrix row (output
 // column) sits at column 16 j + c of tile pair tp.
@@ -93,10 +94,10 @@ struct GemmArgs {
   const RowDesc* rows;
   const float* bias;     // EPI_QKV (may be null)
   float* q_out;          // EPI_QKV: [M][n_q*d]
-  float* k_cache;        // EPI_QKV: this layer's K cache, slot stride `slot_stride`
+  float* k_cache;        // EPI_QKV: this layer's K cache (layout: AttnArgs), slot stride `slot_stride`
   float* v_cache;
-  long long slot_stride; // elements between slots
-  int kv_cap;            // positions per slot
+  long long slot_stride; // float32 units between slots
+  int kv_cap;            // positions per head (a multiple of 64)
   int n_q, n_kv, head_dim;
   const float* rope_cs;  // [kv_cap][head_dim/2][2] (cos, sin)
   const float* x;        // EPI_RESID: residual [M][N] read
@@ -111,24 +112,31 @@ struct GemmArgs {
   int* amax_idx;         //   lowest column holding the largest value
 };
 
+// KV cache of one layer and slot, per KV head (kv_cap * d float32 units
+// each for K and for V):
+//   bf16 models: K [pos][2][d] bf16: the (hi, lo) pair of each value, hi row
+//   then lo row per position; V [2][d][pos] bf16: hi plane then lo plane,
+//   each dimension-major (a dimension's positions are contiguous);
+//   float32 models: K [pos][d], V [d][pos] float32.
+// hi = bf16(x) and lo = bf16(x - hi): the operands of the attention's
+// matrix-core products, stored once when the row is appended.
 struct AttnArgs {
   const float* q;        // [M][n_q*d]
-  const float* k_cache;  // this layer, float32 [slot][kv_head][pos][d]
+  const float* k_cache;  // this layer
   const float* v_cache;
-  long long slot_stride;
-  int kv_cap;
+  long long slot_stride; // float32 units between slots
+  int kv_cap;            // positions per head (a multiple of 64)
   const RowDesc* rows;
   const ReqDesc* reqs;
   int n_q, n_kv, head_dim;
   float scale;
-  float* pacc;           // [chunk][part_rows][n_q][d]
-  float* pml;            // [chunk][part_rows][n_q][2]
+  float* pacc;           // span states [span][part_rows][n_q][d]
+  float* pml;            // [span][part_rows][n_q][2]: running maximum and sum
   int part_rows;         // row stride of the partials (at least the pass's rows)
+  int* attn_cnt;         // finished spans per (request of the pass, head), zero between launches
   void* out;             // planes [kMaxRows][n_q*d]
   long long out_plane;
   int M;
-  int row_groups;        // attention chunk grid: z = request x row_groups + group of
-                         // kAttnRowGroup rows (at least ceil(rows of any request / kAttnRowGroup))
 };
 
 // Persistent step kernel (step.hip): one verification pass of up to 32 rows.
@@ -193,9 +201,11 @@ int step_ra_slice(bool bf16, int KS, int KT);
 hipError_t step_occupancy(bool bf16, int MT, int head_dim, int hidden, int sl, int* blocks_per_cu);
 hipError_t launch_step(bool bf16, int MT, int head_dim, int sl, const StepArgs& a, int grid, int n_counters,
                        hipStream_t s);
-// Attention over n_reqs requests; max_chunks bounds the 32-key chunks of
-// any request (the grid size).
-hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s);
+// Attention over n_reqs requests (attn.h).  Verification passes (rows of a
+// request <= 32): max_blocks bounds the 64-key blocks of any request and
+// sizes the grid (any value covers every cache length; the grid is at most
+// kAttnGrid workgroups).  prefill: one request of up to kMaxRows rows.
+hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_blocks, bool prefill, hipStream_t s);
 // n_rows = sum of the requests' W; counters: one per request, zero between launches.
 // Writes each verified row's greedy token, non-finite flag and top-2 margin.
 hipError_t launch_finish(const RowDesc* rows, const ReqDesc* reqs, int n_reqs, int n_rows,

@@ -9,7 +9,7 @@
 // bit for bit, the logits and cache rows of k + 1 sequential target-only
 // steps (the pathwise-equivalence requirement of Appendix C.4, met here
 // numerically and not only up to masks).
-#include "tiles.h"
+#include "attn.h"
 
 namespace as2d {
 
@@ -268,46 +268,121 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 }
 
 // ---------------------------------------------------------------------------
-// Block-causal grouped-query attention, split over the key axis.
+// Block-causal grouped-query attention (attn.h).
 //
-// Workgroup (chunk c, query head h, request r, row group) runs
-// attn_chunk_tile over keys [32 c, 32 c + 32) of the request's float32
-// cache slot, for the group's kAttnRowGroup rows, in batches of RB rows
-// per wave (kAttnBatch when a pass has more than one row group, else one);
-// the merge kernel, one workgroup per (head, row), combines a row's chunks
-// in ascending order (attn_merge_row).
+// Verification passes: work items (request, 128-key span, query head),
+// with the heads of a KV group adjacent and dealt so that consecutive items
+// run on one XCD (their keys and values are read from memory once and from
+// that XCD's L2 for the group's other heads).  A fixed grid of workgroups
+// takes the items in turn, so the grid does not depend on the cache
+// length.  An item merges its span's blocks and stores the span state; the
+// last item of a (request, head) to finish (agent-scope counter) merges
+// every row of the request over its spans and writes the attention output.
+//
+// Prefill passes (one request, up to 144 rows): one workgroup per (query
+// head, 32 rows) walks the spans in ascending order and merges them as it
+// goes, with the same arithmetic, so no partials go through memory.
 
-template <int D, int RB>
-__global__ __launch_bounds__(256, 4) void attn_chunk_kernel(const AttnArgs p) {
+constexpr int kAttnGrid = 768;   // workgroups of the verification kernel (3 per compute unit)
+
+template <bool BF, int D, int RT>
+__global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int n_reqs) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int rg = blockIdx.z % p.row_groups;
-  const ReqDesc rq = p.reqs[blockIdx.z / p.row_groups];
-  const int r_lo = rg * kAttnRowGroup, r_hi = min(rq.W, r_lo + kAttnRowGroup);
-  // no row of the group reaches this chunk's first key
-  if (r_lo >= r_hi || (int)blockIdx.x * kAttnChunk > rq.L0 + r_hi - 1) return;
-  attn_chunk_tile<D, false, kAttnRowGroup / 4, RB>(p, blockIdx.x, blockIdx.y, rq, smem, r_lo, r_hi);
+  __shared__ int s_last;
+  constexpr int KS = D / AttnFmt<BF>::KE;
+  const int G = gridDim.x;
+  int total = 0;
+  for (int r = 0; r < n_reqs; ++r) {
+    const ReqDesc rq = load_invariant(p.reqs + r);
+    total += p.n_q * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
+  }
+  for (int t = xcd_contiguous(blockIdx.x, G); t < total; t += G) {
+    // item t: request r, span sp, head h (the heads of a KV group are adjacent)
+    int r = 0, u = t, ns = 0;
+    ReqDesc rq;
+    for (;; ++r) {
+      rq = load_invariant(p.reqs + r);
+      ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
+      if (u < p.n_q * ns || r == n_reqs - 1) break;
+      u -= p.n_q * ns;
+    }
+    const int sp = u / p.n_q, h = u - sp * p.n_q;
+    // every load of the item in flight at once: the span's keys and
+    // values, then the queries
+    int b0, b1;
+    attn_span_range(rq, sp, b0, b1);
+    AttnRaw<BF, D> raw[kAttnSpan];
+#pragma unroll
+    for (int j = 0; j < kAttnSpan; ++j) attn_fetch<BF, D>(p, rq, h, min(b0 + j, b1 - 1), raw[j]);
+    Op2 q[RT][KS];
+    attn_load_q<BF, D, RT>(p, rq, h, q);
+    AttnState<RT, D / 64> state;
+#pragma unroll
+    for (int j = 0; j < kAttnSpan; ++j)
+      if (b0 + j < b1) attn_span_block<BF, D, RT>(p, rq, b0 + j, b0, q, raw[j], smem, state);
+    attn_store_span<D, RT>(p, rq, h, sp, state);
+    wait_vmem();
+    __syncthreads();   // every wave's span stores are performed
+    if (threadIdx.x == 0) s_last = counter_add(&p.attn_cnt[r * p.n_q + h], 1) == ns - 1;
+    __syncthreads();
+    if (s_last) {
+      if (threadIdx.x == 0) st<true>(&p.attn_cnt[r * p.n_q + h], 0);   // ready for the next launch
+      for (int i = threadIdx.x >> 4; i < rq.W; i += 16) attn_merge_row<BF, D, false>(p, rq, i, h);
+    }
+    __syncthreads();   // s_last is reused by the next item
+  }
 }
 
 template <bool BF, int D>
-__global__ __launch_bounds__(D) void attn_merge_kernel(const AttnArgs p) {
-  __shared__ float sm[kMaxChunks], sl[kMaxChunks];
-  attn_merge_row<BF, D, false>(p, blockIdx.y, blockIdx.x, 0, sm, sl, [] { __syncthreads(); });
+__global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  constexpr int RT = 2;
+  constexpr int KS = D / AttnFmt<BF>::KE;
+  constexpr int DTW = D / 64;
+  const int h = blockIdx.x, r0 = blockIdx.y * 16 * RT;
+  const ReqDesc full = load_invariant(p.reqs);
+  if (r0 >= full.W) return;
+  // this workgroup's rows as a request of their own: same positions
+  const ReqDesc rq{full.row_start + r0, min(full.W - r0, 16 * RT), full.L0 + r0, full.slot};
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  Op2 q[RT][KS];
+  attn_load_q<BF, D, RT>(p, rq, h, q);
+  AttnState<RT, DTW> all;
+  const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
+  for (int sp = 0; sp < ns; ++sp) {
+    AttnState<RT, DTW> state;
+    attn_span<BF, D, RT>(p, rq, h, sp, q, smem, state);
+    attn_state_merge<RT, DTW>(all, state.M, state.L, state.A, sp == 0, [&](int rt, int i) {
+      return rq.L0 + min(16 * rt + 4 * (lane >> 4) + i, rq.W - 1) >= sp * kAttnSpanKeys;
+    });
+  }
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * rt + 4 * (lane >> 4) + i;
+      if (r < rq.W)
+#pragma unroll
+        for (int t = 0; t < DTW; ++t)
+          store_act<BF, false>(p.out, p.out_plane,
+                               frag_index<BF>(rq.row_start + r, h * D + 16 * (wave * DTW + t) + (lane & 15), p.n_q * D),
+                               all.A[rt][t][i] / all.L[rt][i]);
+    }
 }
 
 template <bool BF, int D>
-static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
-  if (max_chunks > kMaxChunks) return hipErrorInvalidValue;
-  // Workgroups are dealt to the 8 XCDs round-robin by linear index; with
-  // the chunk dimension a multiple of 8, every head of chunk c runs on the
-  // same XCD, so the query heads of a KV group share that chunk's keys and
-  // values in one L2 (extra chunks exit at once).
-  if (a.row_groups < 1) return hipErrorInvalidValue;
-  const dim3 grid((max_chunks + 7) / 8 * 8, a.n_q, n_reqs * a.row_groups);
-  if (a.row_groups > 1) attn_chunk_kernel<D, kAttnBatch><<<grid, 256, attn_lds_bytes<D, kAttnBatch>(), s>>>(a);
-  else attn_chunk_kernel<D, 1><<<grid, 256, attn_lds_bytes<D>(), s>>>(a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  attn_merge_kernel<BF, D><<<dim3(a.n_q, a.M), D, 0, s>>>(a);
+static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_blocks, bool prefill, hipStream_t s) {
+  if (max_blocks > kMaxBlocks || n_reqs < 1) return hipErrorInvalidValue;
+  if (prefill) {
+    if (n_reqs != 1) return hipErrorInvalidValue;
+    attn_prefill_kernel<BF, D><<<dim3(a.n_q, (a.M + 31) / 32), 256, attn_block_lds_bytes<BF, D, 2>(), s>>>(a);
+    return hipGetLastError();
+  }
+  // rows per request: at most 32 (two row tiles) on this path
+  const long long items = (long long)n_reqs * a.n_q * ((max_blocks + kAttnSpan - 1) / kAttnSpan);
+  const int grid = (int)std::min<long long>(kAttnGrid, (items + 7) / 8 * 8);
+  if (a.M > 16) attn_verify_kernel<BF, D, 2><<<grid, 256, attn_block_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
+  else attn_verify_kernel<BF, D, 1><<<grid, 256, attn_block_lds_bytes<BF, D, 1>(), s>>>(a, n_reqs);
   return hipGetLastError();
 }
 
@@ -352,11 +427,11 @@ hipError_t prepare_kernels() {
   return e;
 }
 
-hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_chunks, hipStream_t s) {
-  if (a.head_dim == 128) return bf16 ? attn_dispatch<true, 128>(a, n_reqs, max_chunks, s)
-                                     : attn_dispatch<false, 128>(a, n_reqs, max_chunks, s);
-  if (a.head_dim == 64) return bf16 ? attn_dispatch<true, 64>(a, n_reqs, max_chunks, s)
-                                    : attn_dispatch<false, 64>(a, n_reqs, max_chunks, s);
+hipError_t launch_attention(bool bf16, const AttnArgs& a, int n_reqs, int max_blocks, bool prefill, hipStream_t s) {
+  if (a.head_dim == 128) return bf16 ? attn_dispatch<true, 128>(a, n_reqs, max_blocks, prefill, s)
+                                     : attn_dispatch<false, 128>(a, n_reqs, max_blocks, prefill, s);
+  if (a.head_dim == 64) return bf16 ? attn_dispatch<true, 64>(a, n_reqs, max_blocks, prefill, s)
+                                    : attn_dispatch<false, 64>(a, n_reqs, max_blocks, prefill, s);
   return hipErrorInvalidValue;
 }
 

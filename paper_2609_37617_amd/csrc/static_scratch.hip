@@ -17,7 +17,7 @@
 
 namespace as2d {
 
-constexpr size_t kStaticScratchBytes = 64ull << 20;
+constexpr size_t kStaticScratchBytes = 32ull << 20;
 
 static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 

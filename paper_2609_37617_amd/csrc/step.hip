@@ -9,8 +9,8 @@
 // depend on activations), then waits until the producing phase's
 // completion counter reaches its target, so weight streaming continues
 // across phase boundaries instead of stopping at a kernel boundary.
-// Attention tiles are dealt round-robin, the next tile's keys and values
-// loaded while the current one runs.
+// Attention spans (attn.h) are dealt round-robin and store their states;
+// a second phase merges every (row, head) over its spans.
 //
 // Cross-workgroup data is written with write-through (agent-scope) stores
 // and every activation buffer is written once per launch (per-layer
@@ -20,7 +20,7 @@
 //
 // Tiles are the same units with the same arithmetic as the per-operation
 // kernels (tiles.h), so results match those kernels bit for bit.
-#include "tiles.h"
+#include "attn.h"
 
 namespace as2d {
 
@@ -118,13 +118,14 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
   }
 
   stamp(a, 0, 2);
-  // attention tiles of this pass: n_q heads x chunks of each request
-  int n_chunk_tiles = 0;
+  // attention items of this pass: (request, 128-key span, query head)
+  int n_items = 0;
   for (int r = 0; r < a.n_reqs; ++r) {
     const ReqDesc rq = load_invariant(a.reqs + r);
-    n_chunk_tiles += a.n_q * ((rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk);
+    n_items += a.n_q * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
   }
-  constexpr int kMergeGroups = 256 / D;  // (row, head) merges per workgroup pass
+  constexpr int KS = D / AttnFmt<BF>::KE;
+  const int quarter = tid >> 4;
 
   for (int l = 0; l < L; ++l) {
     const StepLayer* ly = a.layers + l;
@@ -133,75 +134,60 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
     gemm_phase<BF, MT, SL, A_NORM, EPI_QKV>(load_invariant(&ly->qkv), M, prev, prev_target, &a.phase_cnt[ph_layer(l, 0)], a, smem,
                                              s_scale, s_flags);
 
-    // attention chunks
+    // attention spans: the items of the per-operation kernel, dealt
+    // round-robin; each stores its span state
     stamp(a, ph_layer(l, 1), 0);
-    // tile t: request, head and chunk
-    auto tile_of = [&](int t, ReqDesc& rq, int& h, int& c) {
-      int r = 0, u = t;
-      for (;; ++r) {
-        rq = load_invariant(a.reqs + r);
-        const int n = a.n_q * ((rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk);
-        if (u < n || r == a.n_reqs - 1) break;
-        u -= n;
-      }
-      const int nch = (rq.L0 + rq.W + kAttnChunk - 1) / kAttnChunk;
-      h = u / nch;
-      c = u - h * nch;
-    };
-    if ((int)blockIdx.x < n_chunk_tiles) {
-      // one tile per workgroup; the next tile's keys and values are
-      // requested while the current tile's rows run
+    if ((int)blockIdx.x < n_items) {
       wait_count(&a.phase_cnt[ph_layer(l, 0)], a.done_qkv, a.err, a.spin_limit);
       stamp(a, ph_layer(l, 1), 1);
       const AttnArgs at = load_invariant(&ly->attn);
-      ReqDesc rq, rq2;
-      int h, c, h2 = 0, c2 = 0;
-      tile_of(blockIdx.x, rq, h, c);
-      AttnKV<D> cur, nxt;
-      attn_load_kv<D>(at, c, h, rq, cur);
       int mine = 0;
-      for (int t = blockIdx.x; t < n_chunk_tiles; t += G) {
-        const bool more = t + G < n_chunk_tiles;
-        if (more) tile_of(t + G, rq2, h2, c2);
-        attn_tile_kv<D, true, kStepRows / 4, 1>(at, c, h, rq, smem, cur, [&] {
-          if (more) attn_load_kv<D>(at, c2, h2, rq2, nxt);
-        });
-        lds_sync();   // the next tile overwrites the chunk in LDS
+      for (int t = blockIdx.x; t < n_items; t += G) {
+        int r = 0, u = t, ns = 0;
+        ReqDesc rq;
+        for (;; ++r) {
+          rq = load_invariant(a.reqs + r);
+          ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
+          if (u < a.n_q * ns || r == a.n_reqs - 1) break;
+          u -= a.n_q * ns;
+        }
+        const int sp = u / a.n_q, h = u - sp * a.n_q;
+        Op2 q[2][KS];
+        attn_load_q<BF, D, 2>(at, rq, h, q);
+        AttnState<2, D / 64> sst;
+        attn_span<BF, D, 2>(at, rq, h, sp, q, smem, sst);
+        attn_store_span<D, 2>(at, rq, h, sp, sst);
         ++mine;
-        cur = nxt;
-        rq = rq2;
-        h = h2;
-        c = c2;
       }
-      // one signal for all this workgroup's tiles, once their stores are done
+      // one signal for all this workgroup's items, once their stores are done
       wait_vmem();
       __syncthreads();
       if (tid == 0) counter_add(&a.phase_cnt[ph_layer(l, 1)], mine);
     }
     stamp(a, ph_layer(l, 1), 2);
 
-    // merge of every (row, head): kMergeGroups per workgroup pass
+    // merge of every (row, head), one per quarter wave, spans in ascending order
     const int n_merge = M * a.n_q;
     stamp(a, ph_layer(l, 2), 0);
-    bool waited = false;
-    for (int t0 = blockIdx.x * kMergeGroups; t0 < n_merge; t0 += G * kMergeGroups) {
-      if (!waited) {
-        wait_count(&a.phase_cnt[ph_layer(l, 1)], n_chunk_tiles, a.err, a.spin_limit);
-        stamp(a, ph_layer(l, 2), 1);
-        waited = true;
-      }
-      const int grp = tid / D;
-      const int t = t0 + grp;
-      float* sm = reinterpret_cast<float*>(smem) + grp * 2 * kMaxChunks;
+    if ((int)blockIdx.x * 16 < n_merge) {
+      wait_count(&a.phase_cnt[ph_layer(l, 1)], n_items, a.err, a.spin_limit);
+      stamp(a, ph_layer(l, 2), 1);
       const AttnArgs at = load_invariant(&ly->attn);
-      if (t < n_merge)
-        attn_merge_row<BF, D, true>(at, t / a.n_q, t % a.n_q, grp * D, sm, sm + kMaxChunks,
-                                    [] { __syncthreads(); }, true);
-      else
-        attn_merge_row<BF, D, true>(at, 0, 0, grp * D, sm, sm + kMaxChunks, [] { __syncthreads(); },
-                                    false);
+      int mine = 0;
+      for (int t0 = blockIdx.x * 16; t0 < n_merge; t0 += G * 16) {
+        const int t = t0 + quarter;
+        if (t < n_merge) {
+          const int m = t / a.n_q, h = t - m * a.n_q;
+          int r = 0;
+          ReqDesc rq = load_invariant(a.reqs);
+          while (r < a.n_reqs - 1 && m >= rq.row_start + rq.W) rq = load_invariant(a.reqs + ++r);
+          attn_merge_row<BF, D, true>(at, rq, m - rq.row_start, h);
+        }
+        mine += min(16, n_merge - t0);
+      }
+      wait_vmem();
       __syncthreads();
-      if (tid == 0) counter_add(&a.phase_cnt[ph_layer(l, 2)], min(kMergeGroups, n_merge - t0));
+      if (tid == 0) counter_add(&a.phase_cnt[ph_layer(l, 2)], mine);
     }
     stamp(a, ph_layer(l, 2), 2);
 
@@ -278,9 +264,9 @@ int step_lds_bytes(int MT, int head_dim, int hidden) {
   // hidden <= 8192
   int b = kRangeMinLds;                                 // one workgroup per compute unit
   b = max(b, gemm_range_lds_bytes(MT, kMaxUnits));
-  b = max(b, head_dim == 128 ? attn_lds_bytes<128>() : attn_lds_bytes<64>());
+  b = max(b, head_dim == 128 ? attn_block_lds_bytes<true, 128, 2>() : attn_block_lds_bytes<true, 64, 2>());
+  b = max(b, head_dim == 128 ? attn_block_lds_bytes<false, 128, 2>() : attn_block_lds_bytes<false, 64, 2>());
   b = max(b, hidden * 4);                               // embedding row
-  b = max(b, (256 / head_dim) * 2 * kMaxChunks * 4);    // merge scratch
   return b;
 }
 

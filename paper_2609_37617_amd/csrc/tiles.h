@@ -137,12 +137,30 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& p, float* F, int f
         if (head < p.n_q) {
           st<COH>(p.q_out + (size_t)m * p.n_q * d + n, v);
         } else {
+          // K: [pos][(hi, lo)][d] (bf16) or [pos][d] (float32), see AttnArgs
           const int kvh = head - p.n_q;
-          st<COH>(p.k_cache + (size_t)rd.slot * p.slot_stride + ((size_t)kvh * p.kv_cap + rd.pos) * d + dd, v);
+          float* kb = p.k_cache + (size_t)rd.slot * p.slot_stride + (size_t)kvh * p.kv_cap * d;
+          if constexpr (BF) {
+            uint16_t* k16 = reinterpret_cast<uint16_t*>(kb) + (size_t)rd.pos * 2 * d + dd;
+            const uint16_t hi = f2bf(v);
+            st<COH>(k16, hi);
+            st<COH>(k16 + d, f2bf(v - bf2f(hi)));
+          } else {
+            st<COH>(kb + (size_t)rd.pos * d + dd, v);
+          }
         }
       } else {
+        // V: [(hi, lo)][d][pos] (bf16) or [d][pos] (float32), see AttnArgs
         const int kvh = head - p.n_q - p.n_kv;
-        st<COH>(p.v_cache + (size_t)rd.slot * p.slot_stride + ((size_t)kvh * p.kv_cap + rd.pos) * d + dd, v);
+        float* vb = p.v_cache + (size_t)rd.slot * p.slot_stride + (size_t)kvh * p.kv_cap * d;
+        if constexpr (BF) {
+          uint16_t* v16 = reinterpret_cast<uint16_t*>(vb) + (size_t)dd * p.kv_cap + rd.pos;
+          const uint16_t hi = f2bf(v);
+          st<COH>(v16, hi);
+          st<COH>(v16 + (size_t)d * p.kv_cap, f2bf(v - bf2f(hi)));
+        } else {
+          st<COH>(vb + (size_t)dd * p.kv_cap + rd.pos, v);
+        }
       }
     }
   } else {  // EPI_ARGMAX (identity column order: column = token id)
@@ -1065,272 +1083,6 @@ __device__ bool gemm_tile_staged(const GemmArgs& p, int M, int group, int split,
     }
   }
   return true;
-}
-
-// ---------------------------------------------------------------------------
-// Attention over one 32-key chunk c of request r for query head h.  The
-// chunk's keys and values (float32) are staged in LDS; each wave takes the
-// request's rows in turn, kAttnBatch rows at a time (all its rows' queries
-// are loaded into registers first).  For a row at position pos >= 32 c,
-// lane pairs (j, j + 32) each take half of the dot product of key j (keys
-// j <= pos), the wave forms the chunk's softmax statistics (max m, sum l
-// of exp(s - m)) and each lane the unnormalised output
-// sum_j exp(s_j - m) v_j of its dimensions.  A row's chunks are combined
-// in ascending order by attn_merge_row.  Both sums run in ascending order
-// as single fused multiply-adds; their operands are read from LDS first,
-// each key and value element once for a batch of RB rows (RB > 1 for tiles
-// of many rows: a batch costs less than its rows one by one, but more than
-// one row).  256 threads; smem: attn_lds_bytes<D, RB>().
-
-constexpr int kAttnBatch = 2;   // rows a wave takes together in tiles of many rows
-
-template <int D, int RB = 1> __host__ __device__ constexpr int attn_lds_bytes() {
-  return (2 * kAttnChunk * (D + 1) + 4 * RB * (D + kAttnChunk)) * 4;
-}
-
-// The chunk's keys and values in registers: thread x holds float4 number
-// t * 256 + x of each (row-major [key][D]); elements past the request's
-// keys hold unused values.
-template <int D> struct AttnKV {
-  static constexpr int V4 = kAttnChunk * D / 4 / 256;
-  float4 k[V4], v[V4];
-};
-
-template <int D>
-__device__ __forceinline__ void attn_load_kv(const AttnArgs& p, int c, int h, const ReqDesc& rq, AttnKV<D>& r) {
-  constexpr int C = kAttnChunk;
-  const int key0 = c * C;
-  const int nk = min(C, rq.L0 + rq.W - key0);
-  const int g = h * p.n_kv / p.n_q;
-  const float* kb = p.k_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
-  const float* vb = p.v_cache + (size_t)rq.slot * p.slot_stride + ((size_t)g * p.kv_cap + key0) * D;
-  // elements past the request's keys read the last key's instead (in the
-  // slot; unused): no branch around the loads, so the waits stay exact
-#pragma unroll
-  for (int t = 0; t < AttnKV<D>::V4; ++t) {
-    const int f = min((t * 256 + (int)threadIdx.x) * 4, nk * D - 4);   // element index in the chunk
-    r.k[t] = ldg(reinterpret_cast<const float4*>(kb + f));
-    r.v[t] = ldg(reinterpret_cast<const float4*>(vb + f));
-  }
-}
-
-// Up to RB rows of a chunk tile, by one wave: the queries are in qw (LDS,
-// RB x D floats), the chunk's keys and values in Ks / Vs (row stride
-// D + 1), pw is RB x C floats of LDS scratch; stores each of the first nb
-// rows' partial output and (m, l).  Every row's sums take the same
-// operands in the same order whatever the batch.
-template <int D, bool COH, int RB>
-__device__ __forceinline__ void attn_rows(const AttnArgs& p, int c, int h, int key0, int nk, const int (&pos)[RB],
-                                          const int (&row)[RB], int nb, const float* Ks, const float* Vs,
-                                          const float* qw, float* pw) {
-  constexpr int C = kAttnChunk;
-  constexpr int RS = D + 1;
-  constexpr int QL = D / 64;
-  constexpr int DH = D / 2;
-  const int lane = threadIdx.x & 63;
-  const int j = lane & (C - 1), half = lane >> 5;
-  float a[RB];
-#pragma unroll
-  for (int r = 0; r < RB; ++r) a[r] = 0.0f;
-  if (j < nk) {
-    // in blocks of B elements: each block's keys are read once, then for
-    // each row its query elements and its multiply-adds in order (one row:
-    // blocks of 32, fewer LDS round trips; batches: 16, fewer registers)
-    constexpr int B = RB == 1 ? 32 : 16;
-#pragma unroll
-    for (int b0 = 0; b0 < DH; b0 += B) {
-      const float* kr = Ks + j * RS + half * DH + b0;
-      float kk[B];
-#pragma unroll
-      for (int dd = 0; dd < B; ++dd) kk[dd] = kr[dd];
-#pragma unroll
-      for (int r = 0; r < RB; ++r) {
-        const float4* qh = reinterpret_cast<const float4*>(qw + r * D + half * DH + b0);
-        float qq[B];
-#pragma unroll
-        for (int d4 = 0; d4 < B / 4; ++d4) {
-          const float4 q4 = qh[d4];
-          qq[4 * d4] = q4.x; qq[4 * d4 + 1] = q4.y; qq[4 * d4 + 2] = q4.z; qq[4 * d4 + 3] = q4.w;
-        }
-#pragma unroll
-        for (int dd = 0; dd < B; ++dd) a[r] = __builtin_fmaf(qq[dd], kk[dd], a[r]);
-      }
-    }
-  }
-  float mx[RB], l[RB];
-#pragma unroll
-  for (int r = 0; r < RB; ++r) {
-    const float ar = a[r] + __shfl_xor(a[r], 32);  // both halves: same sum (commutative)
-    const bool valid = j < nk && key0 + j <= pos[r];
-    const float s = valid ? ar * p.scale : -INFINITY;
-    mx[r] = wave_max(s);
-    const float pj = valid ? expf(s - mx[r]) : 0.0f;
-    l[r] = wave_sum(half == 0 ? pj : 0.0f);
-    if (half == 0) pw[r * C + j] = pj;
-  }
-  __builtin_amdgcn_wave_barrier();
-#pragma unroll
-  for (int t = 0; t < QL; ++t) {
-    const int dd = t * 64 + lane;
-    float o[RB];
-#pragma unroll
-    for (int r = 0; r < RB; ++r) o[r] = 0.0f;
-    // keys in blocks of KB: each block's values are read once, then for
-    // each row its weights and its multiply-adds in key order
-    constexpr int KB = RB == 1 ? C : 16;
-#pragma unroll
-    for (int j0 = 0; j0 < C; j0 += KB) {
-      float vv[KB];
-#pragma unroll
-      for (int jj = 0; jj < KB; ++jj) vv[jj] = Vs[(j0 + jj) * RS + dd];   // rows >= nk: read, never used
-#pragma unroll
-      for (int r = 0; r < RB; ++r) {
-        float pv[KB];
-#pragma unroll
-        for (int j4 = 0; j4 < KB / 4; ++j4) {
-          const float4 p4 = reinterpret_cast<const float4*>(pw + r * C + j0)[j4];
-          pv[4 * j4] = p4.x; pv[4 * j4 + 1] = p4.y; pv[4 * j4 + 2] = p4.z; pv[4 * j4 + 3] = p4.w;
-        }
-#pragma unroll
-        for (int jj = 0; jj < KB; ++jj) o[r] = j0 + jj < nk ? __builtin_fmaf(pv[jj], vv[jj], o[r]) : o[r];
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < RB; ++r)
-      if (r < nb) st<COH>(p.pacc + (((size_t)c * p.part_rows + row[r]) * p.n_q + h) * D + dd, o[r]);
-  }
-  // (m, l): every lane stores, even lanes m and odd lanes l, one store
-  // with no branch around it
-#pragma unroll
-  for (int r = 0; r < RB; ++r)
-    if (r < nb) st<COH>(p.pml + (((size_t)c * p.part_rows + row[r]) * p.n_q + h) * 2 + (lane & 1), lane & 1 ? l[r] : mx[r]);
-}
-
-// The tile from keys and values already in registers; `pre` runs once the
-// registers are in LDS and the first query is requested (the persistent
-// kernel loads the next tile's keys and values there).
-// Rows [r_lo, r_hi) of the request (all by default), r_hi - r_lo <= 4 RPW
-// (checked by the callers' hosts).
-template <int D, bool COH, int RPW, int RB, class Pre>
-__device__ __forceinline__ void attn_tile_kv(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem,
-                                             const AttnKV<D>& r, Pre&& pre, int r_lo = 0, int r_hi = -1) {
-  constexpr int C = kAttnChunk;
-  static_assert(RPW % RB == 0, "rows per wave in whole batches");
-  constexpr int RS = D + 1;                   // odd LDS row stride (floats)
-  constexpr int QL = D / 64;                  // query elements per lane
-  float* Ks = reinterpret_cast<float*>(smem);
-  float* Vs = Ks + C * RS;
-  float* qs = Vs + C * RS;
-  float* ps = qs + 4 * RB * D;
-
-  const int key0 = c * C;
-  const int nk = min(C, rq.L0 + rq.W - key0);
-  const int qcols = p.n_q * D;
-#pragma unroll
-  for (int t = 0; t < AttnKV<D>::V4; ++t) {   // rows >= nk: unused values
-    const int f = (t * 256 + threadIdx.x) * 4;
-    const int j = f / D, dd = f - j * D;
-    float* kd = Ks + j * RS + dd;
-    float* vd = Vs + j * RS + dd;
-    kd[0] = r.k[t].x; kd[1] = r.k[t].y; kd[2] = r.k[t].z; kd[3] = r.k[t].w;
-    vd[0] = r.v[t].x; vd[1] = r.v[t].y; vd[2] = r.v[t].z; vd[3] = r.v[t].w;
-  }
-
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float* qw = qs + wave * RB * D;
-  float* pw = ps + wave * RB * C;
-  // rows [r_lo, r_hi) of the request (all by default); the first row of
-  // this wave at or after the chunk start
-  if (r_hi < 0) r_hi = rq.W;
-  int i = r_lo + wave;
-  while (i < r_hi && rq.L0 + i < key0) i += 4;
-  // the queries of all this wave's rows (at most RPW) are loaded first, so
-  // no load follows a store and the row loop never waits for its stores;
-  // row min(ii, r_hi - 1) keeps the loads free of branches (rows past the
-  // end are loaded, never used)
-  auto qrow = [&](int ii) { return p.q + (size_t)(rq.row_start + min(ii, r_hi - 1)) * qcols + h * D + lane; };
-  float qa[RPW][QL];
-#pragma unroll
-  for (int k = 0; k < RPW; ++k)
-#pragma unroll
-    for (int t = 0; t < QL; ++t) qa[k][t] = ldg(qrow(i + 4 * k) + t * 64);
-  pre();
-  __syncthreads();
-#pragma unroll
-  for (int k0 = 0; k0 < RPW; k0 += RB) {
-    if (i + 4 * k0 >= r_hi) break;
-    const int nb = min(RB, (r_hi - 1 - (i + 4 * k0)) / 4 + 1);   // rows of this batch
-    int pos[RB], row[RB];
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-      pos[b] = rq.L0 + i + 4 * (k0 + b);
-      row[b] = rq.row_start + i + 4 * (k0 + b);
-#pragma unroll
-      for (int t = 0; t < QL; ++t) qw[b * D + t * 64 + lane] = qa[k0 + b][t];
-    }
-    __builtin_amdgcn_wave_barrier();
-    attn_rows<D, COH, RB>(p, c, h, key0, nk, pos, row, nb, Ks, Vs, qw, pw);
-    __builtin_amdgcn_wave_barrier();
-  }
-}
-
-template <int D, bool COH, int RPW, int RB>
-__device__ __forceinline__ void attn_chunk_tile(const AttnArgs& p, int c, int h, const ReqDesc& rq, unsigned char* smem,
-                                                int r_lo = 0, int r_hi = -1) {
-  AttnKV<D> r;
-  attn_load_kv<D>(p, c, h, rq, r);
-  attn_tile_kv<D, COH, RPW, RB>(p, c, h, rq, smem, r, [] {}, r_lo, r_hi);
-}
-
-// Merge of row `row`'s chunks for head h by D threads starting at thread t0:
-// chunk weights w_c = exp(m_c - max m) go through LDS (sm, sl: kMaxChunks
-// floats each); each thread then sums its dimension over the chunks in
-// ascending order, L = sum_c l_c w_c and a = sum_c acc_c w_c, out = a / L.
-// The first kB chunks' partial sums are loaded before the statistics are
-// combined, so a row of up to kB chunks costs one round trip to memory.
-// `sync` synchronises the threads that share it; with valid = false the
-// threads only join those syncs.
-
-template <bool BF, int D, bool COH, class Sync>
-__device__ __forceinline__ void attn_merge_row(const AttnArgs& p, int row, int h, int t0, float* sm, float* sl, Sync&& sync,
-                               bool valid = true) {
-  constexpr int kB = 32;
-  const int dd = threadIdx.x - t0;
-  const RowDesc rd = load_invariant(p.rows + row);
-  const int nc = valid ? rd.pos / kAttnChunk + 1 : 0;
-  auto ld = [](const float* q) { if constexpr (COH) return ld_coherent(q); else return ldg(q); };
-  auto acc_at = [&](int c) { return p.pacc + (((size_t)c * p.part_rows + row) * p.n_q + h) * D + dd; };
-  // loads past the row's chunks read its last chunk (unused): no branch
-  // around them, so the waits stay exact
-  const int cl = max(nc, 1) - 1;
-  float v[kB];
-#pragma unroll
-  for (int b = 0; b < kB; ++b) v[b] = ld(acc_at(min(b, cl)));
-  for (int c = dd; c < nc; c += D) {
-    const size_t o = ((size_t)c * p.part_rows + row) * p.n_q + h;
-    sm[c] = ld(p.pml + o * 2);
-    sl[c] = ld(p.pml + o * 2 + 1);
-  }
-  sync();
-  float mx = -INFINITY;
-  for (int c = 0; c < nc; ++c) mx = fmaxf(mx, sm[c]);
-  sync();
-  for (int c = dd; c < nc; c += D) sm[c] = expf(sm[c] - mx);
-  sync();
-  float L = 0.0f, a = 0.0f;
-  for (int c0 = 0; c0 < nc; c0 += kB) {
-    if (c0 > 0) {
-#pragma unroll
-      for (int b = 0; b < kB; ++b) v[b] = ld(acc_at(min(c0 + b, cl)));
-    }
-#pragma unroll
-    for (int b = 0; b < kB; ++b)
-      if (c0 + b < nc) {
-        L += sl[c0 + b] * sm[c0 + b];
-        a += v[b] * sm[c0 + b];
-      }
-  }
-  if (valid) store_act<BF, COH>(p.out, p.out_plane, frag_index<BF>(row, h * D + dd, p.n_q * D), a / L);
 }
 
 // ---------------------------------------------------------------------------

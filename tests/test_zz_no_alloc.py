@@ -44,8 +44,8 @@ def test_static_verify_equals_verify(shape):
 def test_static_verify_refuses_a_pass_beyond_the_array():
     from paper_2609_37617_amd import as2d
     shape = QWEN7B.with_layers(1)
-    _, gpu = make_pair(shape, seed=0, max_requests=1, max_kv_len=6016, max_k=8, oracle=False)
-    _, a_dev, instr = prefix(shape, 5900, 32, seed=2)
+    _, gpu = make_pair(shape, seed=0, max_requests=1, max_kv_len=16064, max_k=8, oracle=False)
+    _, a_dev, instr = prefix(shape, 16000, 32, seed=2)     # 126 spans of 128 keys: about 36 MiB in all
     first, L = gpu.prefill(0, a_dev, instr)
     with pytest.raises(as2d.As2dError) as e:
         gpu.verify_static(0, [1, 2, 3])
