@@ -376,13 +376,13 @@ def main():
     extras = not trace
     log(f"[bench] workload {wl.name}: {len(reqs)} request(s), shape {shape.name} L={shape.n_layers}")
     t0 = time.time()
-    dev = gen.make_weights(shape, wl.seed, fmt="device")
+    weights = gen.make_weights(shape, wl.seed, fmt="device")
     log(f"[bench] weights generated in {time.time() - t0:.1f}s")
     t0 = time.time()
-    model = as2d.Model(shape, dev, max_requests=len(reqs), max_kv_len=max_kv, max_k=max_k)
+    model = as2d.Model(shape, weights, max_requests=len(reqs), max_kv_len=max_kv, max_k=max_k)
     keep_dev = extras and not args.no_configs and args.layers is None and wl.shape.name == wc.QWEN7B.name
     if not keep_dev:
-        del dev
+        del weights
     log(f"[bench] weights loaded and packed in {time.time() - t0:.1f}s")
 
     # prefill every request; reference streams committed by the GPU (with
@@ -721,8 +721,9 @@ def main():
         configs = {}
         for idx in (1, 3, 4):
             same = wc.workload(idx).shape.name == shape.name
-            configs[wc.workload(idx).name] = measure_config(idx, dev if same else None, n_passes=3 if idx != 4 else 2)
-        del dev
+            configs[wc.workload(idx).name] = measure_config(idx, weights if same else None,
+                                                            n_passes=3 if idx != 4 else 2)
+        del weights
 
     r0 = reqs[0]
     out = {
