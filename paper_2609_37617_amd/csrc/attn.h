@@ -469,20 +469,29 @@ template <bool BF, int D, bool OUT_COH>
 __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, const ReqDesc& rq, int r, int h) {
   constexpr int DQ = D / 16;   // dimensions per lane
   constexpr int kB = 8;        // spans whose loads are in flight together
+  static_assert(DQ % 4 == 0, "whole 16-byte reads per lane");
   const int ql = threadIdx.x & 15;
   const int row = rq.row_start + r;
   const int ns = (rq.L0 + r) / kAttnSpanKeys + 1;
   auto at = [&](int sp) { return ((size_t)sp * p.part_rows + row) * p.n_q + h; };
+  const __amdgpu_buffer_rsrc_t racc = coherent_rsrc(p.pacc), rml = coherent_rsrc(p.pml);
   float M = 0.f, L = 0.f, A[DQ];
   for (int s0 = 0; s0 < ns; s0 += kB) {
     float ms[kB], ls[kB], as[kB][DQ];
 #pragma unroll
     for (int u = 0; u < kB; ++u) {
       const size_t o = at(min(s0 + u, ns - 1));   // past the last span: read it again, unused
-      ms[u] = ld_coherent(p.pml + o * 2);
-      ls[u] = ld_coherent(p.pml + o * 2 + 1);
+      const float2 ml = ld_coherent2(rml, (uint32_t)(o * 2 * sizeof(float)));
+      ms[u] = ml.x;
+      ls[u] = ml.y;
 #pragma unroll
-      for (int t = 0; t < DQ; ++t) as[u][t] = ld_coherent(p.pacc + o * D + DQ * ql + t);
+      for (int t = 0; t < DQ; t += 4) {
+        const float4 a = ld_coherent4(racc, (uint32_t)((o * D + DQ * ql + t) * sizeof(float)));
+        as[u][t] = a.x;
+        as[u][t + 1] = a.y;
+        as[u][t + 2] = a.z;
+        as[u][t + 3] = a.w;
+      }
     }
 #pragma unroll
     for (int u = 0; u < kB; ++u) {
@@ -499,9 +508,10 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, const ReqDesc&
       }
     }
   }
+  float o[DQ];
 #pragma unroll
-  for (int t = 0; t < DQ; ++t)
-    store_act<BF, OUT_COH>(p.out, p.out_plane, frag_index<BF>(row, h * D + DQ * ql + t, p.n_q * D), A[t] / L);
+  for (int t = 0; t < DQ; ++t) o[t] = A[t] / L;
+  store_act_run<BF, OUT_COH, DQ>(p.out, p.out_plane, frag_index<BF>(row, h * D + DQ * ql, p.n_q * D), o);
 }
 
 }  // namespace as2d

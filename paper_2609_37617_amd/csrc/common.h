@@ -63,6 +63,24 @@ template <typename V> __device__ __forceinline__ V ld_coherent(const V* p) {
   return __hip_atomic_load(gmem(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Wider reads with the cache policy of ld_coherent (sc1: past this XCD's
+// L2), through a raw buffer descriptor of the allocation's base: 8 or 16
+// bytes at byte offset `off` (< 2^31, aligned to the access size).  For a
+// lane that reads several consecutive floats another workgroup of the same
+// launch stored with agent-scope stores.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+constexpr int kCPolSC1 = 16;   // cache-policy bits of the buffer instructions: sc1
+__device__ __forceinline__ float4 ld_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCPolSC1);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
+__device__ __forceinline__ float2 ld_coherent2(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kCPolSC1);
+  return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
+}
+
 // Index of element (m, k) of an activation operand with K columns in MFMA
 // fragment order: one block of 16 rows x KE elements (one k-step of one
 // 16-row tile, 1 KiB) after another, tiles outer, k-steps inner; inside a
@@ -91,6 +109,48 @@ template <bool BF, bool COH> __device__ __forceinline__ void store_act(void* bas
     st<COH>(b + i + plane, f2bf(v - bf2f(hi)));
   } else {
     st<COH>(static_cast<float*>(base) + i, v);
+  }
+}
+
+// N consecutive elements v[0..N) at elements i .. i + N - 1 of the
+// activation planes, which the caller guarantees lie in one k-step block
+// (so they are contiguous in memory) with i a multiple of N (N = 4 or 8).
+template <bool BF, bool COH, int N>
+__device__ __forceinline__ void store_act_run(void* base, long long plane, size_t i, const float* v) {
+  static_assert(N == 4 || N == 8, "run of 4 or 8 elements");
+  if constexpr (BF) {
+    uint32_t hw[N / 2], lw[N / 2];
+#pragma unroll
+    for (int t = 0; t < N / 2; ++t) {
+      const uint16_t h0 = f2bf(v[2 * t]), h1 = f2bf(v[2 * t + 1]);
+      hw[t] = h0 | ((uint32_t)h1 << 16);
+      lw[t] = f2bf(v[2 * t] - bf2f(h0)) | ((uint32_t)f2bf(v[2 * t + 1] - bf2f(h1)) << 16);
+    }
+    uint32_t* hp = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(base) + i);
+    uint32_t* lp = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(base) + i + plane);
+    if constexpr (COH) {
+#pragma unroll
+      for (int t = 0; t < N / 2; ++t) {
+        st<true>(hp + t, hw[t]);
+        st<true>(lp + t, lw[t]);
+      }
+    } else if constexpr (N == 8) {
+      *gmem(reinterpret_cast<u32x4*>(hp)) = u32x4{hw[0], hw[1], hw[2], hw[3]};
+      *gmem(reinterpret_cast<u32x4*>(lp)) = u32x4{lw[0], lw[1], lw[2], lw[3]};
+    } else {
+      typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+      *gmem(reinterpret_cast<u32x2*>(hp)) = u32x2{hw[0], hw[1]};
+      *gmem(reinterpret_cast<u32x2*>(lp)) = u32x2{lw[0], lw[1]};
+    }
+  } else {
+    float* fp = static_cast<float*>(base) + i;
+    if constexpr (COH) {
+#pragma unroll
+      for (int t = 0; t < N; ++t) st<true>(fp + t, v[t]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < N; t += 4) *gmem(reinterpret_cast<f4*>(fp + t)) = f4{v[t], v[t + 1], v[t + 2], v[t + 3]};
+    }
   }
 }
 
