@@ -1427,7 +1427,7 @@ int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* ho
         float kv, vv;
         if (c->bf16) {
           kv = hi16(kbuf.data(), t * 2 * d + j) + hi16(kbuf.data(), t * 2 * d + d + j);
-          vv = hi16(vbuf.data(), j * cap + t) + hi16(vbuf.data(), (d + j) * cap + t);
+          vv = hi16(vbuf.data(), j * cap + v_col(t)) + hi16(vbuf.data(), (d + j) * cap + v_col(t));
         } else {
           kv = kbuf[t * d + j];
           vv = vbuf[j * cap + t];

@@ -3,29 +3,31 @@
 // persistent step kernel (step.hip).
 //
 // Arithmetic of one row (position pos) and query head h, reading KV head
-// g = floor(h n_kv / n_q).  Keys are taken in blocks of kAttnBlock = 64 at
-// absolute positions; block b holds keys [64 b, 64 b + 64) up to pos:
+// g = floor(h n_kv / n_q).  Keys are taken in spans of kAttnSpanKeys = 128 at
+// absolute positions, and a span in four chunks of kAttnChunk = 32 keys (one
+// per wave); chunk c of span sp holds keys [128 sp + 32 c, 128 sp + 32 c + 32)
+// up to pos:
 //   s_j   = (q . k_j) * scale, a matrix-core product: for bf16 models q and
 //           k are split into bf16 pairs (hi = bf16(x), lo = bf16(x - hi))
-//           and s = q_hi k_hi + q_hi k_lo + q_lo k_hi over four 32-wide
-//           k-steps; float32 models use float32 products;
-//   m_b   = max_j s_j (per 16-key tile, then the four tiles);
-//   p_j   = exp(s_j - m_b), 0 for keys after pos;
-//   l_b   = sum_j p_j: per 16-key tile in a fixed butterfly, the four tile
-//           sums added in order;
-//   acc_b = sum_j p_j v_j, a matrix-core product of the (hi, lo) splits of
-//           p and v (p_hi v_hi + p_hi v_lo + p_lo v_hi, 32-key steps).
+//           and s = q_hi k_hi + q_hi k_lo + q_lo k_hi over 32-wide k-steps;
+//           float32 models use float32 products;
+//   m_c   = max_j s_j over the chunk;
+//   p_j   = exp(s_j - m_c), 0 for keys after pos;
+//   l_c   = sum_j p_j: a lane's keys of each 16-key tile in order, the two
+//           tiles in order, then across lanes in a fixed butterfly;
+//   acc_c = sum_j p_j v_j, a matrix-core product of the (hi, lo) splits of
+//           p and v (p_hi v_hi + p_hi v_lo + p_lo v_hi) over the chunk.
 // s is formed transposed (keys on the matrix-core rows), so each lane holds
-// four consecutive keys of one query row; the sums over keys run in a fixed
-// pattern (a lane's four keys in order, then across lanes in a fixed
-// butterfly, then the four 16-key tiles in order).
+// four consecutive keys of one query row per 16-key tile, and p stays in the
+// registers that feed the p v product (bf16: the k-slice of lane group q is
+// keys 4q .. 4q + 3 of the chunk's first tile and of its second tile, and v
+// is read in that order).
 // Merging a partial (m, l, acc) into a running state (M, L, A):
 //   M' = max(M, m), a = exp(M - M'), c = exp(m - M'),
 //   L = fma(L, a, l c), A = fma(A, a, acc c), M = M'.
-// Two levels: the blocks of each span of kAttnSpan = 2 blocks (128 keys,
-// absolute) are merged in ascending order, starting from the span's first
-// block; the spans' states are then merged in ascending order, starting
-// from span 0.  The output is A / L.
+// Two levels: the four chunks of a span are merged in ascending order,
+// starting from the first; the spans' states are then merged in ascending
+// order, starting from span 0.  The output is A / L.
 //
 // Every quantity of a row depends only on that row's query and the keys
 // and values (matrix-core rows are independent), so a row gets the same
@@ -37,19 +39,21 @@
 
 namespace as2d {
 
+constexpr int kAttnChunk = kAttnSpanKeys / kWaves;   // keys of one wave's chunk of a span
+
 template <bool BF> struct AttnFmt {
   static constexpr int PER = BF ? 8 : 4;                  // elements per lane per k-step
   static constexpr int KE = 4 * PER;                      // k-step
   static constexpr int PARTS = BF ? 2 : 1;                // hi, lo planes
-  static constexpr int VS = kAttnBlock + (BF ? 8 : 4);    // LDS row stride of V^T and P, elements
-  static constexpr int ES = BF ? 2 : 4;                   // bytes per LDS element
+  static constexpr int KSV = kAttnChunk / KE;             // k-steps of p v over a chunk
 };
+static_assert(kAttnChunk == 32, "two 16-key tiles per chunk");
 
-// LDS of a block tile for RT row tiles: P [PARTS][16 RT][VS] and the
-// per-wave row statistics [2][4][16 RT] floats.
-template <bool BF, int D, int RT> __host__ __device__ constexpr int attn_block_lds_bytes() {
-  using F = AttnFmt<BF>;
-  return F::PARTS * 16 * RT * F::VS * F::ES + 2 * 4 * 16 * RT * 4;
+// LDS of one span for RT row tiles: every wave's chunk sums acc_c
+// [wave][rt][dimension tile][lane] (16 bytes per lane) and chunk statistics
+// m_c, l_c [wave][16 RT] each.
+template <bool BF, int D, int RT> __host__ __device__ constexpr int attn_span_lds_bytes() {
+  return kWaves * RT * (D / 16) * 64 * 16 + 2 * kWaves * 16 * RT * 4;
 }
 
 // A matrix-core operand of one k-step (16 bytes per lane and part).
@@ -91,16 +95,6 @@ template <bool BF> __device__ __forceinline__ f4 mma3(const Op2& a, const Op2& b
     acc = mma_step<false>(a.h, b.h, acc);
   }
   return acc;
-}
-
-// Reduction over the 16 lanes of a DPP row (the lanes that hold the same
-// four rows of a matrix-core tile): each step combines the same two values
-// on both partner lanes, so all 16 lanes end with the same bits.
-template <class Op> __device__ __forceinline__ float row16_reduce(float v, Op op) {
-  v = op(v, dpp_get<kDppXor1>(v));
-  v = op(v, dpp_get<kDppXor2>(v));
-  v = op(v, dpp_get<kDppHalfMirror>(v));
-  return op(v, dpp_get<kDppMirror>(v));
 }
 
 // Combination with the partner lane l ^ 16 (SWAP32 false) or l ^ 32 (true)
@@ -169,19 +163,21 @@ __device__ __forceinline__ void attn_load_q(const AttnArgs& p, const ReqDesc& rq
   }
 }
 
-// One block's keys and values as loaded from the cache (layout: AttnArgs),
-// already the matrix-core operands: lane l of wave w holds the k-step
-// slices of key 16 w + l % 16 (for s, rows of the transposed product) and,
-// for each of its dimension tiles t, dimension 16 (w DTW + t) + l % 16 at
-// keys KE ks + PER (l / 16) + e (for p v).  Keys past the request's: K
-// reads its last key (a branch-free load, never used), V elements are set
-// to zero (their p is 0, and 0 times a stale value must stay 0).
+// One wave's chunk of keys and values as loaded from the cache (layout:
+// AttnArgs), already the matrix-core operands.  k[kt]: the k-step slices of
+// key 16 kt + l % 16 of the chunk (rows of the transposed product s).
+// v[t][j]: dimension 16 t + l % 16 at the keys of k-step j of p v (bf16:
+// keys 4 (l / 16) .. + 3 of both tiles; float32: keys 16 j + 4 (l / 16)
+// .. + 3), in one 16-byte read per part (the V layout, AttnArgs).  Keys
+// past the request's: K reads its last key (a branch-free load, never
+// used), V elements are zero (their p is 0, and 0 times a stale value must
+// stay 0); a chunk that starts past the last key reads no V.
 template <bool BF, int D> struct AttnRaw {
-  static constexpr int KS = D / AttnFmt<BF>::KE;
-  static constexpr int KSV = kAttnBlock / AttnFmt<BF>::KE;
-  static constexpr int DTW = D / 64;
-  Op2 k[KS];
-  Op2 v[DTW][KSV];
+  static constexpr int KS = D / AttnFmt<BF>::KE;   // k-steps of q . k
+  static constexpr int DT = D / 16;                // dimension tiles
+  static constexpr int KSV = AttnFmt<BF>::KSV;
+  Op2 k[2][KS];
+  Op2 v[DT][KSV];
 };
 
 // Zeroes the elements e of a 16-byte operand (bf16: 8, float32: 4) whose
@@ -200,164 +196,69 @@ template <bool BF> __device__ __forceinline__ uint4 keep_first(uint4 x, int n) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// Wave w's chunk of span sp.  Reads stay inside the slot's rows: K rows up
+// to the last key, V rows only for a chunk that starts at or before it (the
+// row stride is a multiple of 64, so such a chunk ends inside the row).
 template <bool BF, int D>
-__device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq, int h, int b, AttnRaw<BF, D>& r) {
+__device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq, int h, int sp, AttnRaw<BF, D>& r) {
   using F = AttnFmt<BF>;
   using Raw = AttnRaw<BF, D>;
   using T = typename ET<BF>::T;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int lg = lane >> 4, lr = lane & 15;
-  const int key0 = b * kAttnBlock;
-  const int last = rq.L0 + rq.W - 1;          // last key of the request in this pass
+  const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;   // first key of the chunk
+  const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
   const int g = h * p.n_kv / p.n_q;
   const size_t head = (size_t)rq.slot * p.slot_stride + (size_t)g * p.kv_cap * D;   // float32 units
   const T* kb = reinterpret_cast<const T*>(p.k_cache + head);
   const T* vb = reinterpret_cast<const T*>(p.v_cache + head);
-  const T* kr = kb + (size_t)min(key0 + 16 * wave + lr, last) * F::PARTS * D + F::PER * lg;
 #pragma unroll
-  for (int ks = 0; ks < Raw::KS; ++ks) {
-    r.k[ks].h = ldg(reinterpret_cast<const uint4*>(kr + F::KE * ks));
-    r.k[ks].l = BF ? ldg(reinterpret_cast<const uint4*>(kr + D + F::KE * ks)) : r.k[ks].h;
-  }
-  const bool tail = key0 + kAttnBlock > last + 1;   // the block holds keys past the request's
+  for (int kt = 0; kt < 2; ++kt) {
+    const T* kr = kb + (size_t)min(kc + 16 * kt + lr, last) * F::PARTS * D + F::PER * lg;
 #pragma unroll
-  for (int t = 0; t < Raw::DTW; ++t) {
-    const T* vr = vb + (size_t)(16 * (wave * Raw::DTW + t) + lr) * p.kv_cap + key0 + F::PER * lg;
-#pragma unroll
-    for (int ks = 0; ks < Raw::KSV; ++ks) {
-      Op2 o;
-      o.h = ldg(reinterpret_cast<const uint4*>(vr + F::KE * ks));
-      o.l = BF ? ldg(reinterpret_cast<const uint4*>(vr + (size_t)D * p.kv_cap + F::KE * ks)) : o.h;
-      if (tail) {
-        const int n = min(max(last + 1 - (key0 + F::KE * ks + F::PER * lg), 0), F::PER);
-        o.h = keep_first<BF>(o.h, n);
-        o.l = keep_first<BF>(o.l, n);
-      }
-      r.v[t][ks] = o;
+    for (int ks = 0; ks < Raw::KS; ++ks) {
+      r.k[kt][ks].h = ldg(reinterpret_cast<const uint4*>(kr + F::KE * ks));
+      r.k[kt][ks].l = BF ? ldg(reinterpret_cast<const uint4*>(kr + D + F::KE * ks)) : r.k[kt][ks].h;
     }
   }
-}
-
-// One block of keys (block b) of request rq, rows of row tiles rt < RT
-// (queries q; keys and values of the query head's KV head as fetched in
-// raw): the block statistics of every row and acc_b of this wave's
-// dimension tiles.  256 threads, 4 waves: wave w forms s for keys
-// [16 w, 16 w + 16) of the block and acc_b for dimension tiles
-// [w DTW, (w + 1) DTW).  On return, for lane l and i < 4, row
-// 16 rt + 4 (l / 16) + i has statistics m[rt][i], l[rt][i] (m = -inf, l = 0
-// when the block starts after the row's position) and acc[rt][t] holds
-// acc_b of that row at dimension 16 (w DTW + t) + l % 16.  smem:
-// attn_block_lds_bytes<BF, D, RT>(), not in use on entry (the caller
-// synchronises the workgroup between blocks).
-template <bool BF, int D, int RT> struct AttnBlockOut {
-  static constexpr int DTW = D / 64;   // dimension tiles per wave
-  f4 acc[RT][DTW];
-  float m[RT][4], l[RT][4];
-};
-
-template <bool BF, int D, int RT>
-__device__ __forceinline__ void attn_block(const AttnArgs& p, const ReqDesc& rq, int b,
-                                           const Op2 (&q)[RT][D / AttnFmt<BF>::KE], const AttnRaw<BF, D>& raw,
-                                           unsigned char* smem, AttnBlockOut<BF, D, RT>& out) {
-#pragma clang fp contract(off)
-  using F = AttnFmt<BF>;
-  using T = typename ET<BF>::T;
-  constexpr int KS = D / F::KE;              // k-steps of q . k
-  constexpr int KSV = kAttnBlock / F::KE;    // k-steps of p v
-  constexpr int DTW = D / 64;
-  constexpr int R = 16 * RT;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int lg = lane >> 4, lr = lane & 15;
-  T* PB = reinterpret_cast<T*>(smem);                                  // [PARTS][R][VS]
-  float* smax = reinterpret_cast<float*>(PB + F::PARTS * R * F::VS);   // [4][R]
-  float* ssum = smax + 4 * R;                                          // [4][R]
-  const int key0 = b * kAttnBlock;
-
-  // s transposed for this wave's 16 keys: lane l holds keys 16 w + 4 (l / 16) + i
-  // of query row 16 rt + l % 16
-  float s[RT][4];
-  {
+  if (kc > last) {   // no key of the chunk is in the request
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < Raw::DT; ++t)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = mma3<BF>(raw.k[ks], q[rt][ks], acc);
-      const int pos = rq.L0 + min(16 * rt + lr, rq.W - 1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) s[rt][i] = key0 + 16 * wave + 4 * lg + i <= pos ? acc[i] * p.scale : -INFINITY;
-    }
+      for (int j = 0; j < Raw::KSV; ++j) r.v[t][j] = Op2{make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+    return;
   }
-  // block maximum per row: a lane's four keys, the four lanes of the row,
-  // then the four waves in order
+  const bool tail = kc + kAttnChunk > last + 1;   // the chunk holds keys past the request's
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    float mx = fmaxf(fmaxf(fmaxf(s[rt][0], s[rt][1]), s[rt][2]), s[rt][3]);
-    mx = swap_combine<false>(mx, FMax{});
-    mx = swap_combine<true>(mx, FMax{});
-    if (lg == 0) smax[wave * R + 16 * rt + lr] = mx;
-  }
-  __syncthreads();
-  // p = exp(s - m_b) into LDS (row-major, (hi, lo)); its per-row sums
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = 16 * rt + lr;
-    const float mb = fmaxf(fmaxf(fmaxf(smax[r], smax[R + r]), smax[2 * R + r]), smax[3 * R + r]);
-    float pj[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pj[i] = mb == -INFINITY ? 0.0f : expf(s[rt][i] - mb);
-    float sm = ((pj[0] + pj[1]) + pj[2]) + pj[3];
-    sm = swap_combine<false>(sm, FAdd{});
-    sm = swap_combine<true>(sm, FAdd{});
-    if (lg == 0) ssum[wave * R + r] = sm;
-    const int c = 16 * wave + 4 * lg;
+  for (int t = 0; t < Raw::DT; ++t) {
+    const T* vr = vb + (size_t)(16 * t + lr) * p.kv_cap + kc;
     if constexpr (BF) {
-      uint32_t hw[2], lw[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const uint16_t h0 = f2bf(pj[2 * t]), h1 = f2bf(pj[2 * t + 1]);
-        hw[t] = h0 | ((uint32_t)h1 << 16);
-        lw[t] = f2bf(pj[2 * t] - bf2f(h0)) | ((uint32_t)f2bf(pj[2 * t + 1] - bf2f(h1)) << 16);
+      // keys 4 lg .. 4 lg + 3 of the first tile, then of the second: columns
+      // 8 lg .. 8 lg + 7 of the chunk (v_col)
+      uint4 oh = ldg(reinterpret_cast<const uint4*>(vr + 8 * lg));
+      uint4 ol = ldg(reinterpret_cast<const uint4*>(vr + (size_t)D * p.kv_cap + 8 * lg));
+      if (tail) {
+        const int n0 = min(max(last + 1 - (kc + 4 * lg), 0), 4);
+        const int n1 = min(max(last + 1 - (kc + 16 + 4 * lg), 0), 4);
+        const uint4 a = keep_first<true>(make_uint4(oh.x, oh.y, 0, 0), n0), b = keep_first<true>(make_uint4(oh.z, oh.w, 0, 0), n1);
+        const uint4 c = keep_first<true>(make_uint4(ol.x, ol.y, 0, 0), n0), d = keep_first<true>(make_uint4(ol.z, ol.w, 0, 0), n1);
+        oh = make_uint4(a.x, a.y, b.x, b.y);
+        ol = make_uint4(c.x, c.y, d.x, d.y);
       }
-      *reinterpret_cast<uint2*>(PB + r * F::VS + c) = make_uint2(hw[0], hw[1]);
-      *reinterpret_cast<uint2*>(PB + (R + r) * F::VS + c) = make_uint2(lw[0], lw[1]);
+      r.v[t][0] = Op2{oh, ol};
     } else {
-      *reinterpret_cast<float4*>(PB + r * F::VS + c) = make_float4(pj[0], pj[1], pj[2], pj[3]);
-    }
-  }
-  __syncthreads();   // ssum and P
-  // the statistics of this lane's output rows 16 rt + 4 (l / 16) + i
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 16 * rt + 4 * lg + i;
-      out.m[rt][i] = fmaxf(fmaxf(fmaxf(smax[r], smax[R + r]), smax[2 * R + r]), smax[3 * R + r]);
-      out.l[rt][i] = ((ssum[r] + ssum[R + r]) + ssum[2 * R + r]) + ssum[3 * R + r];
-    }
-  // acc_b = P V for this wave's dimension tiles
-#pragma unroll
-  for (int t = 0; t < DTW; ++t) {
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      f4 acc = f4{0.f, 0.f, 0.f, 0.f};
-      const int r = 16 * rt + lr;
-#pragma unroll
-      for (int ks = 0; ks < KSV; ++ks) {
-        const int c = F::KE * ks + F::PER * lg;
-        Op2 a;
-        a.h = *reinterpret_cast<const uint4*>(PB + r * F::VS + c);
-        a.l = a.h;
-        if constexpr (BF) a.l = *reinterpret_cast<const uint4*>(PB + (R + r) * F::VS + c);
-        acc = mma3<BF>(a, raw.v[t][ks], acc);
+      for (int j = 0; j < Raw::KSV; ++j) {
+        uint4 o = ldg(reinterpret_cast<const uint4*>(vr + 16 * j + 4 * lg));
+        if (tail) o = keep_first<false>(o, min(max(last + 1 - (kc + 16 * j + 4 * lg), 0), 4));
+        r.v[t][j] = Op2{o, o};
       }
-      out.acc[rt][t] = acc;
     }
   }
 }
 
 // Running attention state of this lane's rows (16 rt + 4 (lane / 16) + i)
-// and dimensions (16 (w DTW + t) + lane % 16), in the layout of
-// AttnBlockOut.
+// and dimensions (16 (w DTW + t) + lane % 16).
 template <int RT, int DTW> struct AttnState {
   float M[RT][4], L[RT][4], A[RT][DTW][4];
 };
@@ -386,55 +287,123 @@ __device__ __forceinline__ void attn_state_merge(AttnState<RT, DTW>& st, const f
     }
 }
 
-// Block b of span sp (first block b0) merged into st; rows before the
-// block's first key are left as they are.  Synchronises the workgroup
-// afterwards (the next block overwrites LDS).
+// The state of span sp for rows of row tiles rt < RT (queries q; this
+// wave's chunk of keys and values in raw), in the layout of AttnState: for
+// lane l and i < 4, row 16 rt + 4 (l / 16) + i, dimensions 16 (w DTW + t) +
+// l % 16.  Rows whose position is before the span's first key get no
+// meaningful state (they are never stored or merged).  256 threads, 4 waves;
+// smem: attn_span_lds_bytes<BF, D, RT>(), not in use on entry (the caller
+// synchronises the workgroup before it is written again).
 template <bool BF, int D, int RT>
-__device__ __forceinline__ void attn_span_block(const AttnArgs& p, const ReqDesc& rq, int b, int b0,
+__device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc& rq, int sp,
                                                 const Op2 (&q)[RT][D / AttnFmt<BF>::KE], const AttnRaw<BF, D>& raw,
                                                 unsigned char* smem, AttnState<RT, D / 64>& st) {
-  constexpr int DTW = D / 64;
-  const int lane = threadIdx.x & 63;
-  AttnBlockOut<BF, D, RT> o;
-  attn_block<BF, D, RT>(p, rq, b, q, raw, smem, o);
-  float acc[RT][DTW][4];
+#pragma clang fp contract(off)
+  using Raw = AttnRaw<BF, D>;
+  constexpr int KS = Raw::KS, DT = Raw::DT, DTW = D / 64, R = 16 * RT;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lg = lane >> 4, lr = lane & 15;
+  const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;
+  f4* SA = reinterpret_cast<f4*>(smem);                                 // [wave][rt][t][lane]
+  float* SM = reinterpret_cast<float*>(SA + kWaves * RT * DT * 64);   // [wave][R]
+  float* SL = SM + kWaves * R;                                          // [wave][R]
+
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
+  for (int rt = 0; rt < RT; ++rt) {
+    // s transposed: lane l holds keys kc + 16 kt + 4 (l / 16) + i of row 16 rt + l % 16
+    const int pos = rq.L0 + min(16 * rt + lr, rq.W - 1);
+    float s[2][4];
 #pragma unroll
-    for (int t = 0; t < DTW; ++t)
+    for (int kt = 0; kt < 2; ++kt) {
+      f4 acc = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[rt][t][i] = o.acc[rt][t][i];
-  attn_state_merge<RT, DTW>(st, o.m, o.l, acc, b == b0, [&](int rt, int i) {
-    return rq.L0 + min(16 * rt + 4 * (lane >> 4) + i, rq.W - 1) >= b * kAttnBlock;
-  });
+      for (int ks = 0; ks < KS; ++ks) acc = mma3<BF>(raw.k[kt][ks], q[rt][ks], acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[kt][i] = kc + 16 * kt + 4 * lg + i <= pos ? acc[i] * p.scale : -INFINITY;
+    }
+    float mx = s[0][0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e >> 2][e & 3]);
+    mx = swap_combine<false>(mx, FMax{});
+    mx = swap_combine<true>(mx, FMax{});
+    float pj[2][4];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pj[kt][i] = mx == -INFINITY ? 0.0f : expf(s[kt][i] - mx);
+    float sm = (((pj[0][0] + pj[0][1]) + pj[0][2]) + pj[0][3]) + (((pj[1][0] + pj[1][1]) + pj[1][2]) + pj[1][3]);
+    sm = swap_combine<false>(sm, FAdd{});
+    sm = swap_combine<true>(sm, FAdd{});
+    if (lg == 0) {
+      SM[wave * R + 16 * rt + lr] = mx;
+      SL[wave * R + 16 * rt + lr] = sm;
+    }
+    // acc_c = p v for every dimension tile, p straight from registers
+    f4* sa = SA + (size_t)(wave * RT + rt) * DT * 64 + lane;
+    if constexpr (BF) {
+      uint32_t hw[4], lw[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {   // elements 2 w, 2 w + 1: tile w / 2, keys 2 (w % 2), 2 (w % 2) + 1
+        const float v0 = pj[w >> 1][2 * (w & 1)], v1 = pj[w >> 1][2 * (w & 1) + 1];
+        const uint16_t h0 = f2bf(v0), h1 = f2bf(v1);
+        hw[w] = h0 | ((uint32_t)h1 << 16);
+        lw[w] = f2bf(v0 - bf2f(h0)) | ((uint32_t)f2bf(v1 - bf2f(h1)) << 16);
+      }
+      const Op2 a{make_uint4(hw[0], hw[1], hw[2], hw[3]), make_uint4(lw[0], lw[1], lw[2], lw[3])};
+#pragma unroll
+      for (int t = 0; t < DT; ++t) sa[t * 64] = mma3<BF>(a, raw.v[t][0], f4{0.f, 0.f, 0.f, 0.f});
+    } else {
+#pragma unroll
+      for (int t = 0; t < DT; ++t) {
+        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+          const uint4 a = make_uint4(__float_as_uint(pj[kt][0]), __float_as_uint(pj[kt][1]), __float_as_uint(pj[kt][2]),
+                                     __float_as_uint(pj[kt][3]));
+          acc = mma_step<false>(a, raw.v[t][kt].h, acc);
+        }
+        sa[t * 64] = acc;
+      }
+    }
+  }
   __syncthreads();
+  // the four chunks merged in order, for this wave's dimension tiles
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    MergeCoef k[kWaves - 1][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 16 * rt + 4 * lg + i;
+      float M = SM[r], L = SL[r];
+#pragma unroll
+      for (int c = 1; c < kWaves; ++c) k[c - 1][i] = attn_merge_coef(M, L, SM[c * R + r], SL[c * R + r]);
+      st.M[rt][i] = M;
+      st.L[rt][i] = L;
+    }
+#pragma unroll
+    for (int tw = 0; tw < DTW; ++tw) {
+      const int t = wave * DTW + tw;
+      f4 A = SA[(size_t)(0 * RT + rt) * DT * 64 + t * 64 + lane];
+#pragma unroll
+      for (int c = 1; c < kWaves; ++c) {
+        const f4 a = SA[(size_t)(c * RT + rt) * DT * 64 + t * 64 + lane];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) A[i] = attn_merge_acc(A[i], a[i], k[c - 1][i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st.A[rt][tw][i] = A[i];
+    }
+  }
 }
 
-// Blocks [b0, b1) of span sp = b0 / kAttnSpan.
-__device__ __forceinline__ void attn_span_range(const ReqDesc& rq, int sp, int& b0, int& b1) {
-  b0 = sp * kAttnSpan;
-  b1 = min(b0 + kAttnSpan, (rq.L0 + rq.W - 1) / kAttnBlock + 1);
-}
-
-// Span `sp` of request rq for head h: its blocks merged in ascending order
-// into st (a row's state starts at the span's first block).  The next
-// block's keys and values are requested while the current one is computed.
+// Span sp of request rq for head h: fetch, then attn_span_state.
 template <bool BF, int D, int RT>
 __device__ __forceinline__ void attn_span(const AttnArgs& p, const ReqDesc& rq, int h, int sp,
                                           const Op2 (&q)[RT][D / AttnFmt<BF>::KE], unsigned char* smem,
                                           AttnState<RT, D / 64>& st) {
-  int b0, b1;
-  attn_span_range(rq, sp, b0, b1);
-  // two buffers taken in turn: block b + 1 is requested before block b runs
-  AttnRaw<BF, D> r0, r1;
-  attn_fetch<BF, D>(p, rq, h, b0, r0);
-  for (int b = b0; b < b1; b += 2) {
-    if (b + 1 < b1) attn_fetch<BF, D>(p, rq, h, b + 1, r1);
-    attn_span_block<BF, D, RT>(p, rq, b, b0, q, r0, smem, st);
-    if (b + 1 >= b1) break;
-    if (b + 2 < b1) attn_fetch<BF, D>(p, rq, h, b + 2, r0);
-    attn_span_block<BF, D, RT>(p, rq, b + 1, b0, q, r1, smem, st);
-  }
+  AttnRaw<BF, D> raw;
+  attn_fetch<BF, D>(p, rq, h, sp, raw);
+  attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, st);
 }
 
 // Stores the span state of the rows of the request that reach span sp:

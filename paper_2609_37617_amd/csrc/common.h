@@ -11,6 +11,7 @@ namespace as2d {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
 // element formats
@@ -138,7 +139,6 @@ __device__ __forceinline__ void store_act_run(void* base, long long plane, size_
       *gmem(reinterpret_cast<u32x4*>(hp)) = u32x4{hw[0], hw[1], hw[2], hw[3]};
       *gmem(reinterpret_cast<u32x4*>(lp)) = u32x4{lw[0], lw[1], lw[2], lw[3]};
     } else {
-      typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
       *gmem(reinterpret_cast<u32x2*>(hp)) = u32x2{hw[0], hw[1]};
       *gmem(reinterpret_cast<u32x2*>(lp)) = u32x2{lw[0], lw[1]};
     }

@@ -115,11 +115,20 @@ struct GemmArgs {
 // KV cache of one layer and slot, per KV head (kv_cap * d float32 units
 // each for K and for V):
 //   bf16 models: K [pos][2][d] bf16: the (hi, lo) pair of each value, hi row
-//   then lo row per position; V [2][d][pos] bf16: hi plane then lo plane,
-//   each dimension-major (a dimension's positions are contiguous);
+//   then lo row per position; V [2][d][col] bf16: hi plane then lo plane,
+//   each dimension-major, position pos at column v_col(pos) (the keys of
+//   each aligned group of 32 reordered so that the eight keys one lane group
+//   multiplies in p v are adjacent);
 //   float32 models: K [pos][d], V [d][pos] float32.
 // hi = bf16(x) and lo = bf16(x - hi): the operands of the attention's
 // matrix-core products, stored once when the row is appended.
+//
+// v_col: within a group of 32, key 16 t + 4 g + e (t < 2, g < 4, e < 4)
+// sits at 8 g + 4 t + e.
+__host__ __device__ inline int v_col(int pos) {
+  return (pos & ~31) | (((pos >> 2) & 3) << 3) | (((pos >> 4) & 1) << 2) | (pos & 3);
+}
+
 struct AttnArgs {
   const float* q;        // [M][n_q*d]
   const float* k_cache;  // this layer

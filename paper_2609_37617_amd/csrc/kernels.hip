@@ -307,19 +307,14 @@ __global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int 
       u -= p.n_q * ns;
     }
     const int sp = u / p.n_q, h = u - sp * p.n_q;
-    // every load of the item in flight at once: the span's keys and
-    // values, then the queries
-    int b0, b1;
-    attn_span_range(rq, sp, b0, b1);
-    AttnRaw<BF, D> raw[kAttnSpan];
-#pragma unroll
-    for (int j = 0; j < kAttnSpan; ++j) attn_fetch<BF, D>(p, rq, h, min(b0 + j, b1 - 1), raw[j]);
+    // every load of the item in flight at once: this wave's chunk of keys
+    // and values, then the queries
+    AttnRaw<BF, D> raw;
+    attn_fetch<BF, D>(p, rq, h, sp, raw);
     Op2 q[RT][KS];
     attn_load_q<BF, D, RT>(p, rq, h, q);
     AttnState<RT, D / 64> state;
-#pragma unroll
-    for (int j = 0; j < kAttnSpan; ++j)
-      if (b0 + j < b1) attn_span_block<BF, D, RT>(p, rq, b0 + j, b0, q, raw[j], smem, state);
+    attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, state);
     attn_store_span<D, RT>(p, rq, h, sp, state);
     wait_vmem();
     __syncthreads();   // every wave's span stores are performed
@@ -333,10 +328,12 @@ __global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int 
   }
 }
 
+constexpr int kAttnPrefillRT = 1;   // row tiles per prefill workgroup
+
 template <bool BF, int D>
 __global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  constexpr int RT = 2;
+  constexpr int RT = kAttnPrefillRT;   // one row tile: two chunk buffers stay in registers
   constexpr int KS = D / AttnFmt<BF>::KE;
   constexpr int DTW = D / 64;
   const int h = blockIdx.x, r0 = blockIdx.y * 16 * RT;
@@ -349,12 +346,23 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
   attn_load_q<BF, D, RT>(p, rq, h, q);
   AttnState<RT, DTW> all;
   const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
-  for (int sp = 0; sp < ns; ++sp) {
+  // two chunk buffers taken in turn: span sp + 1 is requested before span sp runs
+  AttnRaw<BF, D> ka, kb;
+  attn_fetch<BF, D>(p, rq, h, 0, ka);
+  auto run = [&](int sp, const AttnRaw<BF, D>& raw) {
     AttnState<RT, DTW> state;
-    attn_span<BF, D, RT>(p, rq, h, sp, q, smem, state);
+    attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, state);
     attn_state_merge<RT, DTW>(all, state.M, state.L, state.A, sp == 0, [&](int rt, int i) {
       return rq.L0 + min(16 * rt + 4 * (lane >> 4) + i, rq.W - 1) >= sp * kAttnSpanKeys;
     });
+    __syncthreads();   // the next span writes the LDS again
+  };
+  for (int sp = 0; sp < ns; sp += 2) {
+    if (sp + 1 < ns) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);
+    run(sp, ka);
+    if (sp + 1 >= ns) break;
+    if (sp + 2 < ns) attn_fetch<BF, D>(p, rq, h, sp + 2, ka);
+    run(sp + 1, kb);
   }
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
@@ -375,14 +383,15 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_blocks, b
   if (max_blocks > kMaxBlocks || n_reqs < 1) return hipErrorInvalidValue;
   if (prefill) {
     if (n_reqs != 1) return hipErrorInvalidValue;
-    attn_prefill_kernel<BF, D><<<dim3(a.n_q, (a.M + 31) / 32), 256, attn_block_lds_bytes<BF, D, 2>(), s>>>(a);
+    constexpr int R = 16 * kAttnPrefillRT;
+    attn_prefill_kernel<BF, D><<<dim3(a.n_q, (a.M + R - 1) / R), 256, attn_span_lds_bytes<BF, D, kAttnPrefillRT>(), s>>>(a);
     return hipGetLastError();
   }
   // rows per request: at most 32 (two row tiles) on this path
   const long long items = (long long)n_reqs * a.n_q * ((max_blocks + kAttnSpan - 1) / kAttnSpan);
   const int grid = (int)std::min<long long>(kAttnGrid, (items + 7) / 8 * 8);
-  if (a.M > 16) attn_verify_kernel<BF, D, 2><<<grid, 256, attn_block_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
-  else attn_verify_kernel<BF, D, 1><<<grid, 256, attn_block_lds_bytes<BF, D, 1>(), s>>>(a, n_reqs);
+  if (a.M > 16) attn_verify_kernel<BF, D, 2><<<grid, 256, attn_span_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
+  else attn_verify_kernel<BF, D, 1><<<grid, 256, attn_span_lds_bytes<BF, D, 1>(), s>>>(a, n_reqs);
   return hipGetLastError();
 }
 
@@ -414,8 +423,25 @@ static hipError_t prepare_staged() {
   return e;
 }
 
+// Attention kernels: two row tiles of 128 dimensions exchange 64 KiB of
+// chunk sums plus their statistics.
+template <bool BF, int D>
+static hipError_t prepare_attention() {
+  auto allow = [](const void* k, int bytes) { return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, bytes); };
+  hipError_t e = allow(reinterpret_cast<const void*>(&attn_verify_kernel<BF, D, 1>), attn_span_lds_bytes<BF, D, 1>());
+  if (e == hipSuccess)
+    e = allow(reinterpret_cast<const void*>(&attn_verify_kernel<BF, D, 2>), attn_span_lds_bytes<BF, D, 2>());
+  if (e == hipSuccess)
+    e = allow(reinterpret_cast<const void*>(&attn_prefill_kernel<BF, D>), attn_span_lds_bytes<BF, D, kAttnPrefillRT>());
+  return e;
+}
+
 hipError_t prepare_kernels() {
   hipError_t e = prepare_step_kernels();
+  if (e == hipSuccess) e = prepare_attention<true, 128>();
+  if (e == hipSuccess) e = prepare_attention<true, 64>();
+  if (e == hipSuccess) e = prepare_attention<false, 128>();
+  if (e == hipSuccess) e = prepare_attention<false, 64>();
 #define AS2D_P(bf, am, ep) \
   if (e == hipSuccess) e = prepare_range<bf, am, ep>(); \
   if (e == hipSuccess) e = prepare_staged<bf, am, ep>();

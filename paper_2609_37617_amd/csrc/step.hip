@@ -157,6 +157,7 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
         AttnState<2, D / 64> sst;
         attn_span<BF, D, 2>(at, rq, h, sp, q, smem, sst);
         attn_store_span<D, 2>(at, rq, h, sp, sst);
+        __syncthreads();   // the next item writes the LDS again
         ++mine;
       }
       // one signal for all this workgroup's items, once their stores are done
@@ -264,8 +265,8 @@ int step_lds_bytes(int MT, int head_dim, int hidden) {
   // hidden <= 8192
   int b = kRangeMinLds;                                 // one workgroup per compute unit
   b = max(b, gemm_range_lds_bytes(MT, kMaxUnits));
-  b = max(b, head_dim == 128 ? attn_block_lds_bytes<true, 128, 2>() : attn_block_lds_bytes<true, 64, 2>());
-  b = max(b, head_dim == 128 ? attn_block_lds_bytes<false, 128, 2>() : attn_block_lds_bytes<false, 64, 2>());
+  b = max(b, head_dim == 128 ? attn_span_lds_bytes<true, 128, 2>() : attn_span_lds_bytes<true, 64, 2>());
+  b = max(b, head_dim == 128 ? attn_span_lds_bytes<false, 128, 2>() : attn_span_lds_bytes<false, 64, 2>());
   b = max(b, hidden * 4);                               // embedding row
   return b;
 }
