@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--trace-window", action="store_true",
                     help="profiling run: reference streams and every timed call at the workload's width, "
                          "nothing else (no passes, extras or back-to-back GEMM timing)")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the vendor library's bf16 GEMM (torch.nn.functional.linear, i.e. "
+                         "hipBLASLt/rocBLAS) on the verification GEMM shapes at W = 1 and the timed width")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device-to-device copy of this many MiB (a plain copy kernel "
                          "of known size, for scaling hardware byte counters)")
@@ -115,6 +118,33 @@ def copy_calibration(mib):
     hip.hipFree(src)
     hip.hipFree(dst)
     log(f"[bench] calibration copy: {mib} MiB read + {mib} MiB written")
+
+
+def library_gemm_us(n, k, rows, reps=40):
+    """The vendor library's bf16 product y = x W^T (x [rows, k], W [n, k],
+    float32 accumulation, bf16 output) through torch, back to back over
+    enough weight copies that no launch finds its matrix in the 256 MB
+    memory-side cache: the comparison for a matrix-core GEMM at small
+    widths (a GEMV-style kernel at rows = 1)."""
+    import torch
+    import torch.nn.functional as F
+    dev = torch.device("cuda", 0)
+    copies = max(1, -(-(600 << 20) // (2 * n * k)))
+    ws = [torch.randn(n, k, device=dev, dtype=torch.bfloat16) for _ in range(copies)]
+    x = torch.randn(rows, k, device=dev, dtype=torch.bfloat16)
+    for w in ws:
+        F.linear(x, w)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(reps):
+        F.linear(x, ws[i % copies])
+    e1.record()
+    e1.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    del ws, x
+    torch.cuda.empty_cache()
+    return us
 
 
 def cpu_baseline(shape, n_audio, n_instr, k, mean_committed, seed=0, min_seconds=10.0, max_reps=400):
@@ -712,6 +742,19 @@ def main():
                                          "frac": round(nbytes[name] / us / 1e3 / PEAK_HBM_GBPS, 4)}
         roof["gemms_back_to_back"] = gemms
         log("[bench] GEMMs back to back: " + ", ".join(f"{k} {v['us']}us {v['frac']:.0%}" for k, v in gemms.items()))
+        if args.library_gemm and shape.dtype == wc.BF16:
+            shapes = {"gemm_qkv": shape.qkv_out, "gemm_o": H, "gemm_gate_up": 2 * F, "gemm_down": H,
+                      "gemm_lm_head": V}
+            kdim = {"gemm_qkv": H, "gemm_o": shape.n_q_heads * shape.head_dim, "gemm_gate_up": H,
+                    "gemm_down": F, "gemm_lm_head": H}
+            lib = {}
+            for name, n in shapes.items():
+                for w in sorted({1, roof["rows"]}):
+                    us = library_gemm_us(n, kdim[name], w)
+                    lib[f"{name}_w{w}"] = {"us": round(us, 2), "frac": round(nbytes[name] / us / 1e3 / PEAK_HBM_GBPS, 4)}
+            roof["library_gemm_back_to_back"] = lib
+            log("[bench] library bf16 GEMM back to back: "
+                + ", ".join(f"{k} {v['us']}us {v['frac']:.0%}" for k, v in lib.items()))
 
     # the other workloads, each in a context of its own: the 3B shape, the
     # long-audio prefix and the mixed batch (the same 7B weights)
