@@ -366,7 +366,7 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
       }
     }
   }
-  __syncthreads();
+  lds_sync();   // LDS only: global loads in flight (the next span's) stay in flight
   // the four chunks merged in order, for this wave's dimension tiles
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
@@ -445,37 +445,52 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, const ReqDesc&
   auto at = [&](int sp) { return ((size_t)sp * p.part_rows + row) * p.n_q + h; };
   const __amdgpu_buffer_rsrc_t racc = coherent_rsrc(p.pacc), rml = coherent_rsrc(p.pml);
   float M = 0.f, L = 0.f, A[DQ];
-  for (int s0 = 0; s0 < ns; s0 += kB) {
-    float ms[kB], ls[kB], as[kB][DQ];
+  // batches of kB spans; the next batch is requested before the current one
+  // is merged (past the last span: the last one again, unused)
+  struct Batch {
+    float m[kB], l[kB], a[kB][DQ];
+  };
+  auto load = [&](int s0, Batch& b) {
 #pragma unroll
     for (int u = 0; u < kB; ++u) {
-      const size_t o = at(min(s0 + u, ns - 1));   // past the last span: read it again, unused
+      const size_t o = at(min(s0 + u, ns - 1));
       const float2 ml = ld_coherent2(rml, (uint32_t)(o * 2 * sizeof(float)));
-      ms[u] = ml.x;
-      ls[u] = ml.y;
+      b.m[u] = ml.x;
+      b.l[u] = ml.y;
 #pragma unroll
       for (int t = 0; t < DQ; t += 4) {
         const float4 a = ld_coherent4(racc, (uint32_t)((o * D + DQ * ql + t) * sizeof(float)));
-        as[u][t] = a.x;
-        as[u][t + 1] = a.y;
-        as[u][t + 2] = a.z;
-        as[u][t + 3] = a.w;
+        b.a[u][t] = a.x;
+        b.a[u][t + 1] = a.y;
+        b.a[u][t + 2] = a.z;
+        b.a[u][t + 3] = a.w;
       }
     }
+  };
+  auto merge = [&](int s0, const Batch& b) {
 #pragma unroll
     for (int u = 0; u < kB; ++u) {
       if (s0 + u >= ns) break;
       if (s0 + u == 0) {
-        M = ms[u];
-        L = ls[u];
+        M = b.m[u];
+        L = b.l[u];
 #pragma unroll
-        for (int t = 0; t < DQ; ++t) A[t] = as[u][t];
+        for (int t = 0; t < DQ; ++t) A[t] = b.a[u][t];
       } else {
-        const MergeCoef k = attn_merge_coef(M, L, ms[u], ls[u]);
+        const MergeCoef k = attn_merge_coef(M, L, b.m[u], b.l[u]);
 #pragma unroll
-        for (int t = 0; t < DQ; ++t) A[t] = attn_merge_acc(A[t], as[u][t], k);
+        for (int t = 0; t < DQ; ++t) A[t] = attn_merge_acc(A[t], b.a[u][t], k);
       }
     }
+  };
+  Batch b0, b1;
+  load(0, b0);
+  for (int s0 = 0; s0 < ns; s0 += 2 * kB) {
+    if (s0 + kB < ns) load(s0 + kB, b1);
+    merge(s0, b0);
+    if (s0 + kB >= ns) break;
+    if (s0 + 2 * kB < ns) load(s0 + 2 * kB, b0);
+    merge(s0 + kB, b1);
   }
   float o[DQ];
 #pragma unroll

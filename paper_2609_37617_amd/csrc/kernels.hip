@@ -283,7 +283,7 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // head, 32 rows) walks the spans in ascending order and merges them as it
 // goes, with the same arithmetic, so no partials go through memory.
 
-constexpr int kAttnGrid = 768;   // workgroups of the verification kernel (3 per compute unit)
+constexpr int kAttnGrid = 256;   // workgroups of the verification kernel (one per compute unit: its registers allow no more)
 
 template <bool BF, int D, int RT>
 __global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int n_reqs) {
@@ -291,34 +291,65 @@ __global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int 
   __shared__ int s_last;
   constexpr int KS = D / AttnFmt<BF>::KE;
   const int G = gridDim.x;
-  int total = 0;
-  for (int r = 0; r < n_reqs; ++r) {
-    const ReqDesc rq = load_invariant(p.reqs + r);
-    total += p.n_q * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
-  }
+  // a workgroup item is a run of up to R consecutive spans of one (request,
+  // head): the least R whose items fit the grid (one span each while they
+  // do; long caches take several per workgroup, the next span's keys and
+  // values requested while the current one runs)
+  int ns_max = 1;
+  auto n_items = [&](int R) {
+    int n = 0;
+    for (int r = 0; r < n_reqs; ++r) {
+      const ReqDesc rq = load_invariant(p.reqs + r);
+      const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
+      ns_max = max(ns_max, ns);
+      n += p.n_q * ((ns + R - 1) / R);
+    }
+    return n;
+  };
+  int R = 1, total = n_items(1);
+  while (total > G && R < ns_max) total = n_items(++R);
   for (int t = xcd_contiguous(blockIdx.x, G); t < total; t += G) {
-    // item t: request r, span sp, head h (the heads of a KV group are adjacent)
-    int r = 0, u = t, ns = 0;
+    // item t: request r, run j, head h (the heads of a KV group are adjacent)
+    int r = 0, u = t, ns = 0, nr = 0;
     ReqDesc rq;
     for (;; ++r) {
       rq = load_invariant(p.reqs + r);
       ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
-      if (u < p.n_q * ns || r == n_reqs - 1) break;
-      u -= p.n_q * ns;
+      nr = (ns + R - 1) / R;
+      if (u < p.n_q * nr || r == n_reqs - 1) break;
+      u -= p.n_q * nr;
     }
-    const int sp = u / p.n_q, h = u - sp * p.n_q;
-    // every load of the item in flight at once: this wave's chunk of keys
-    // and values, then the queries
-    AttnRaw<BF, D> raw;
-    attn_fetch<BF, D>(p, rq, h, sp, raw);
+    const int j = u / p.n_q, h = u - j * p.n_q;
+    const int sp0 = j * R, sp1 = min(sp0 + R, ns);
+    // the first span's keys and values, then the queries, all in flight at once
+    AttnRaw<BF, D> ka, kb;
+    attn_fetch<BF, D>(p, rq, h, sp0, ka);
     Op2 q[RT][KS];
     attn_load_q<BF, D, RT>(p, rq, h, q);
-    AttnState<RT, D / 64> state;
-    attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, state);
-    attn_store_span<D, RT>(p, rq, h, sp, state);
+    auto run = [&](int sp, const AttnRaw<BF, D>& raw) {
+      AttnState<RT, D / 64> state;
+      attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, state);
+      attn_store_span<D, RT>(p, rq, h, sp, state);
+      lds_sync();   // the next span writes the LDS again (the prefetch stays in flight)
+    };
+    if constexpr (RT == 1) {   // two chunk buffers taken in turn
+      for (int sp = sp0; sp < sp1; sp += 2) {
+        if (sp + 1 < sp1) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);
+        run(sp, ka);
+        if (sp + 1 >= sp1) break;
+        if (sp + 2 < sp1) attn_fetch<BF, D>(p, rq, h, sp + 2, ka);
+        run(sp + 1, kb);
+      }
+    } else {   // two row tiles: one buffer (two would not fit the registers)
+      for (int sp = sp0; sp < sp1; ++sp) {
+        if (sp > sp0) attn_fetch<BF, D>(p, rq, h, sp, ka);
+        run(sp, ka);
+      }
+    }
     wait_vmem();
     __syncthreads();   // every wave's span stores are performed
-    if (threadIdx.x == 0) s_last = counter_add(&p.attn_cnt[r * p.n_q + h], 1) == ns - 1;
+    const int done = sp1 - sp0;
+    if (threadIdx.x == 0) s_last = counter_add(&p.attn_cnt[r * p.n_q + h], done) == ns - done;
     __syncthreads();
     if (s_last) {
       if (threadIdx.x == 0) st<true>(&p.attn_cnt[r * p.n_q + h], 0);   // ready for the next launch
@@ -355,7 +386,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
     attn_state_merge<RT, DTW>(all, state.M, state.L, state.A, sp == 0, [&](int rt, int i) {
       return rq.L0 + min(16 * rt + 4 * (lane >> 4) + i, rq.W - 1) >= sp * kAttnSpanKeys;
     });
-    __syncthreads();   // the next span writes the LDS again
+    lds_sync();   // the next span writes the LDS again (the prefetch stays in flight)
   };
   for (int sp = 0; sp < ns; sp += 2) {
     if (sp + 1 < ns) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);

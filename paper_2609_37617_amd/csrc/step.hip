@@ -157,7 +157,7 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
         AttnState<2, D / 64> sst;
         attn_span<BF, D, 2>(at, rq, h, sp, q, smem, sst);
         attn_store_span<D, 2>(at, rq, h, sp, sst);
-        __syncthreads();   // the next item writes the LDS again
+        lds_sync();   // the next item writes the LDS again
         ++mine;
       }
       // one signal for all this workgroup's items, once their stores are done
