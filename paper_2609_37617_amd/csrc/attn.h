@@ -170,7 +170,8 @@ __device__ __forceinline__ void attn_load_q(const AttnArgs& p, const ReqDesc& rq
 // keys 4 (l / 16) .. + 3 of both tiles; float32: keys 16 j + 4 (l / 16)
 // .. + 3), in one 16-byte read per part (the V layout, AttnArgs).  Keys
 // past the request's: K reads its last key (a branch-free load, never
-// used), V elements are zero (their p is 0, and 0 times a stale value must
+// used); V is read as stored and its elements are set to zero where p v
+// takes them (attn_v_operand: their p is 0, and 0 times a stale value must
 // stay 0); a chunk that starts past the last key reads no V.
 template <bool BF, int D> struct AttnRaw {
   static constexpr int KS = D / AttnFmt<BF>::KE;   // k-steps of q . k
@@ -228,33 +229,45 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
       for (int j = 0; j < Raw::KSV; ++j) r.v[t][j] = Op2{make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
     return;
   }
-  const bool tail = kc + kAttnChunk > last + 1;   // the chunk holds keys past the request's
 #pragma unroll
   for (int t = 0; t < Raw::DT; ++t) {
     const T* vr = vb + (size_t)(16 * t + lr) * p.kv_cap + kc;
     if constexpr (BF) {
       // keys 4 lg .. 4 lg + 3 of the first tile, then of the second: columns
       // 8 lg .. 8 lg + 7 of the chunk (v_col)
-      uint4 oh = ldg(reinterpret_cast<const uint4*>(vr + 8 * lg));
-      uint4 ol = ldg(reinterpret_cast<const uint4*>(vr + (size_t)D * p.kv_cap + 8 * lg));
-      if (tail) {
-        const int n0 = min(max(last + 1 - (kc + 4 * lg), 0), 4);
-        const int n1 = min(max(last + 1 - (kc + 16 + 4 * lg), 0), 4);
-        const uint4 a = keep_first<true>(make_uint4(oh.x, oh.y, 0, 0), n0), b = keep_first<true>(make_uint4(oh.z, oh.w, 0, 0), n1);
-        const uint4 c = keep_first<true>(make_uint4(ol.x, ol.y, 0, 0), n0), d = keep_first<true>(make_uint4(ol.z, ol.w, 0, 0), n1);
-        oh = make_uint4(a.x, a.y, b.x, b.y);
-        ol = make_uint4(c.x, c.y, d.x, d.y);
-      }
-      r.v[t][0] = Op2{oh, ol};
+      r.v[t][0] = Op2{ldg(reinterpret_cast<const uint4*>(vr + 8 * lg)),
+                      ldg(reinterpret_cast<const uint4*>(vr + (size_t)D * p.kv_cap + 8 * lg))};
     } else {
 #pragma unroll
       for (int j = 0; j < Raw::KSV; ++j) {
-        uint4 o = ldg(reinterpret_cast<const uint4*>(vr + 16 * j + 4 * lg));
-        if (tail) o = keep_first<false>(o, min(max(last + 1 - (kc + 16 * j + 4 * lg), 0), 4));
+        const uint4 o = ldg(reinterpret_cast<const uint4*>(vr + 16 * j + 4 * lg));
         r.v[t][j] = Op2{o, o};
       }
     }
   }
+}
+
+// The V operand of dimension tile t and k-step j as p v takes it: elements
+// of keys past the request's last key set to zero (a chunk past the last
+// key was not read).  Done here rather than at the load, so that no wait
+// for the data sits between the requests of the next chunk.
+template <bool BF, int D>
+__device__ __forceinline__ Op2 attn_v_operand(const AttnRaw<BF, D>& r, int t, int j, int kc, int last) {
+  const int lg = (threadIdx.x & 63) >> 4;
+  Op2 o = r.v[t][j];
+  if (kc + kAttnChunk <= last + 1) return o;   // every key of the chunk is in the request
+  if constexpr (BF) {
+    const int n0 = min(max(last + 1 - (kc + 4 * lg), 0), 4);
+    const int n1 = min(max(last + 1 - (kc + 16 + 4 * lg), 0), 4);
+    const uint4 a = keep_first<true>(make_uint4(o.h.x, o.h.y, 0, 0), n0), b = keep_first<true>(make_uint4(o.h.z, o.h.w, 0, 0), n1);
+    const uint4 c = keep_first<true>(make_uint4(o.l.x, o.l.y, 0, 0), n0), d = keep_first<true>(make_uint4(o.l.z, o.l.w, 0, 0), n1);
+    o.h = make_uint4(a.x, a.y, b.x, b.y);
+    o.l = make_uint4(c.x, c.y, d.x, d.y);
+  } else {
+    o.h = keep_first<false>(o.h, min(max(last + 1 - (kc + 16 * j + 4 * lg), 0), 4));
+    o.l = o.h;
+  }
+  return o;
 }
 
 // Running attention state of this lane's rows (16 rt + 4 (lane / 16) + i)
@@ -304,6 +317,7 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lg = lane >> 4, lr = lane & 15;
   const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;
+  const int last = rq.L0 + rq.W - 1;   // last key of the request in this pass
   f4* SA = reinterpret_cast<f4*>(smem);                                 // [wave][rt][t][lane]
   float* SM = reinterpret_cast<float*>(SA + kWaves * RT * DT * 64);   // [wave][R]
   float* SL = SM + kWaves * R;                                          // [wave][R]
@@ -351,7 +365,7 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
       }
       const Op2 a{make_uint4(hw[0], hw[1], hw[2], hw[3]), make_uint4(lw[0], lw[1], lw[2], lw[3])};
 #pragma unroll
-      for (int t = 0; t < DT; ++t) sa[t * 64] = mma3<BF>(a, raw.v[t][0], f4{0.f, 0.f, 0.f, 0.f});
+      for (int t = 0; t < DT; ++t) sa[t * 64] = mma3<BF>(a, attn_v_operand<BF, D>(raw, t, 0, kc, last), f4{0.f, 0.f, 0.f, 0.f});
     } else {
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
@@ -360,7 +374,7 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
         for (int kt = 0; kt < 2; ++kt) {
           const uint4 a = make_uint4(__float_as_uint(pj[kt][0]), __float_as_uint(pj[kt][1]), __float_as_uint(pj[kt][2]),
                                      __float_as_uint(pj[kt][3]));
-          acc = mma_step<false>(a, raw.v[t][kt].h, acc);
+          acc = mma_step<false>(a, attn_v_operand<BF, D>(raw, t, kt, kc, last).h, acc);
         }
         sa[t * 64] = acc;
       }

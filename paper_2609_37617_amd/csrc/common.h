@@ -172,6 +172,12 @@ template <class T> __device__ __forceinline__ T load_invariant(const T* p) {
 }
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// The same wait through the compiler's own instruction (s_waitcnt vmcnt(0),
+// expcnt and lgkmcnt left alone), so that its wait placement knows that every
+// earlier vector memory operation has completed: a loop can then hold a
+// second set of loads in flight without the counter's 63-entry limit making
+// the compiler wait for everything.
+__device__ __forceinline__ void wait_vmem_counted() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Agent-scope counter increment; returns the previous value.
 __device__ __forceinline__ int counter_add(int* c, int v) {

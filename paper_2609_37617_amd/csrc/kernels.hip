@@ -332,11 +332,13 @@ __global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int 
       attn_store_span<D, RT>(p, rq, h, sp, state);
       lds_sync();   // the next span writes the LDS again (the prefetch stays in flight)
     };
-    if constexpr (RT == 1) {   // two chunk buffers taken in turn
+    if constexpr (RT == 1) {   // two chunk buffers taken in turn (as in attn_prefill_kernel)
       for (int sp = sp0; sp < sp1; sp += 2) {
+        wait_vmem_counted();
         if (sp + 1 < sp1) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);
         run(sp, ka);
         if (sp + 1 >= sp1) break;
+        wait_vmem_counted();
         if (sp + 2 < sp1) attn_fetch<BF, D>(p, rq, h, sp + 2, ka);
         run(sp + 1, kb);
       }
@@ -388,10 +390,14 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
     });
     lds_sync();   // the next span writes the LDS again (the prefetch stays in flight)
   };
+  // (each buffer's reads complete before the other's are issued: 32 reads
+  // per lane and span, so two spans would exceed what the wave can count)
   for (int sp = 0; sp < ns; sp += 2) {
+    wait_vmem_counted();
     if (sp + 1 < ns) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);
     run(sp, ka);
     if (sp + 1 >= ns) break;
+    wait_vmem_counted();
     if (sp + 2 < ns) attn_fetch<BF, D>(p, rq, h, sp + 2, ka);
     run(sp + 1, kb);
   }
