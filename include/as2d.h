@@ -186,7 +186,8 @@ int as2d_get_row_margins(as2d_ctx* ctx, int32_t req, float* host, int32_t max_ro
  *                         captured into a graph; larger passes use
  *                         AS2D_EXEC_GRAPH.
  * as2d_get_exec_info reports the mode and the persistent kernel's grid
- * (0 when the device cannot hold it; it then falls back to graphs). */
+ * (0 when the device, or the compute-unit budget, cannot hold it;
+ * verification passes then run as AS2D_EXEC_GRAPH). */
 enum { AS2D_EXEC_EAGER = 0, AS2D_EXEC_GRAPH = 1, AS2D_EXEC_PERSISTENT = 2 };
 int as2d_set_exec_mode(as2d_ctx* ctx, int32_t mode);
 int as2d_get_exec_info(as2d_ctx* ctx, int32_t* mode, int32_t* persistent_grid);
@@ -226,9 +227,12 @@ int as2d_set_stream(as2d_ctx* ctx, void* hip_stream);
 /* Size the balanced GEMM grids (and the persistent kernel's) for `cus`
  * compute units (1 .. the device's; 0 restores all of them): each such
  * GEMM then runs cus workgroups of one CU each, leaving the other CUs to
- * work on other streams (a drafter beside the target).  Split counts, and
- * so every result, are unchanged.  Waits for the stream and drops cached
- * graphs and per-pass argument arrays. */
+ * work on other streams (a drafter beside the target).  A GEMM with more
+ * than 24 (tile pair, k-split) units per workgroup at that grid keeps the
+ * grid that gives it 24; if one does, the persistent kernel (one
+ * workgroup per budgeted CU) is not used and as2d_get_exec_info reports
+ * grid 0.  Split counts, and so every result, are unchanged.  Waits for
+ * the stream and drops cached graphs and per-pass argument arrays. */
 int as2d_set_cu_budget(as2d_ctx* ctx, int32_t cus);
 /* Mark a slot free (its state is discarded). */
 int as2d_release_request(as2d_ctx* ctx, int32_t req);

@@ -111,6 +111,7 @@ struct as2d_ctx {
 
   // persistent step kernel: per-layer activation buffers and counters
   bool pers_ok = false;
+  bool pers_fit = true;          // every balanced plan's grid fits the persistent grid
   int pers_grid[3] = {0, 0, 0};  // by M-tile count 1, 2: one workgroup per usable CU
   int pers_sl = 0;               // register-resident slice length of the gate/up plan (0: none)
   float *px = nullptr, *psumsq = nullptr, *pq = nullptr;
@@ -677,7 +678,7 @@ int run_forward(as2d_ctx* c, int M, int n_att, int n_fin, bool with_head, bool v
   }
   if (max_blocks > c->n_blocks_cap) return fail(c, AS2D_ECAPACITY, "attention blocks %d > %d", max_blocks, c->n_blocks_cap);
   const bool verify_pass = verify_call && with_head && n_fin == n_att;
-  const bool persistent = verify_pass && c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && M <= kStepRows;
+  const bool persistent = verify_pass && c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && c->pers_fit && M <= kStepRows;
   const bool graph = verify_pass && c->exec_mode != AS2D_EXEC_EAGER && !c->timing;
   if (persistent && !step_layers_for(c, M)) return fail(c, AS2D_ENOMEM, "persistent step arguments");
   if (graph) {
@@ -713,7 +714,7 @@ int as2d_prepare_graphs(as2d_ctx* c, int32_t max_rows) {
   if (c->exec_mode == AS2D_EXEC_EAGER || c->timing) return AS2D_OK;   // no graphs in these modes
   max_rows = std::min(max_rows, c->cfg.max_k + 1);
   for (int M = 1; M <= max_rows; ++M) {
-    const bool persistent = c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && M <= kStepRows;
+    const bool persistent = c->exec_mode == AS2D_EXEC_PERSISTENT && c->pers_ok && c->pers_fit && M <= kStepRows;
     if (persistent && !step_layers_for(c, M)) return fail(c, AS2D_ENOMEM, "persistent step arguments");
     hipGraphExec_t ex = nullptr;
     const int rc = graph_for(c, M, 1, 1, M, persistent, &ex);
@@ -759,7 +760,15 @@ int set_grids(as2d_ctx* c, int cus) {
   HIP_TRY(c, hipGetDevice(&dev));
   HIP_TRY(c, hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev));
   const int n = cus > 0 ? std::min(cus, dev_cus) : dev_cus;
-  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) set_grid(*p, n);
+  // a plan whose units would exceed kMaxUnits per workgroup on n keeps a
+  // wider grid; the persistent kernel, one workgroup per CU of the budget,
+  // then cannot hold that phase and verification passes use graphs
+  int widest = 0;
+  for (GemmPlan* p : {&c->p_qkv, &c->p_o, &c->p_gu, &c->p_down, &c->p_lm}) {
+    set_grid(*p, n);
+    widest = std::max(widest, p->G);
+  }
+  c->pers_fit = widest <= n;
   if (c->pers_ok)
     for (int mt = 1; mt <= 2; ++mt) c->pers_grid[mt] = n;
   return AS2D_OK;
@@ -1487,7 +1496,7 @@ int as2d_set_exec_mode(as2d_ctx* c, int32_t mode) {
 int as2d_get_exec_info(as2d_ctx* c, int32_t* mode, int32_t* persistent_grid) {
   if (!c) return AS2D_EINVAL;
   if (mode) *mode = c->exec_mode;
-  if (persistent_grid) *persistent_grid = c->pers_ok ? c->pers_grid[1] : 0;
+  if (persistent_grid) *persistent_grid = c->pers_ok && c->pers_fit ? c->pers_grid[1] : 0;
   return AS2D_OK;
 }
 
@@ -1495,7 +1504,11 @@ int as2d_set_step_trace(as2d_ctx* c, int32_t on) {
   if (!c) return AS2D_EINVAL;
   if (!c->pers_ok) return fail(c, AS2D_ESTATE, "no persistent step kernel on this device");
   if (on && !c->ptrace) {
-    const size_t n = (size_t)std::max(c->pers_grid[1], c->pers_grid[2]) * c->n_phase * 3;
+    // sized for the whole device: a later compute-unit budget can widen the grid
+    int dev = 0, dev_cus = 0;
+    HIP_TRY(c, hipGetDevice(&dev));
+    HIP_TRY(c, hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev));
+    const size_t n = (size_t)std::max({c->pers_grid[1], c->pers_grid[2], dev_cus}) * c->n_phase * 3;
     int rc = dalloc(c, &c->ptrace, n * sizeof(long long));
     if (rc) return rc;
     HIP_TRY(c, hipMemset(c->ptrace, 0, n * sizeof(long long)));

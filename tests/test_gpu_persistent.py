@@ -60,3 +60,34 @@ def test_persistent_equals_graph(model, ks):
         gpu.set_exec_mode(as2d.EXEC_GRAPH)
         gpu.decode_one(0)                     # other work between replays
         gpu.rollback(0, *states[0])
+
+
+def test_persistent_after_cu_budget_equals_graph(model):
+    """A compute-unit budget rebuilds the persistent kernel's grid and its
+    per-layer argument arrays.  On 224 CUs the persistent pass runs on 224
+    workgroups; on 128 the LM head's 4,752 tile pairs need 198 workgroups of
+    24 units, more than the budget, so persistent mode runs the graph path
+    (reported grid 0).  Either way, and after the budget is lifted again,
+    the result is the whole-device graph's bit for bit."""
+    as2d, gpu, states = model
+    rng = np.random.default_rng(11)
+    reqs = [0, 1]
+    cands = [[int(t) for t in rng.integers(0, SHAPE.vocab, k)] for k in (8, 5)]
+    gpu.set_exec_mode(as2d.EXEC_GRAPH)
+    ref = run(gpu, reqs, cands, states)
+    try:
+        for cus, grid in ((224, 224), (128, 0), (0, None)):
+            gpu.set_cu_budget(cus)
+            print(f"persistent after cu budget {cus}", flush=True)
+            if grid is not None:
+                assert gpu.exec_info()[1] == grid
+            for mode in (as2d.EXEC_PERSISTENT, as2d.EXEC_EAGER):
+                gpu.set_exec_mode(mode)
+                got = run(gpu, reqs, cands, states)
+                for (o, lg, kv), (ro, rlg, rkv) in zip(got, ref):
+                    assert o == ro, (cus, mode)
+                    assert np.array_equal(lg, rlg), (cus, mode)
+                    assert np.array_equal(kv[0], rkv[0]) and np.array_equal(kv[1], rkv[1]), (cus, mode)
+    finally:
+        gpu.set_cu_budget(0)
+        gpu.set_exec_mode(as2d.EXEC_GRAPH)
