@@ -53,10 +53,10 @@ struct PassBufs {
   float *amax_val = nullptr, *amax_val2 = nullptr, *row_margin = nullptr;
   float *part = nullptr, *pacc = nullptr, *pml = nullptr;
   int *amax_idx = nullptr, *counters = nullptr, *row_tok = nullptr, *row_bad = nullptr, *fin_counters = nullptr;
-  int* attn_cnt = nullptr;                                // finished attention blocks per (request, head)
   void *xg = nullptr, *attn = nullptr, *hbuf = nullptr;  // activation planes
   long long xg_plane = 0, attn_plane = 0, h_plane = 0;    // offset of the lo plane (bf16), elements
-  int part_rows = 0;                                      // row stride of the attention partials
+  int part_spans = 0;                                     // span stride of the attention states
+  int* attn_cnt = nullptr;                                // finished spans per (request, KV head, row block)
   RowDesc* d_rows = nullptr;
   ReqDesc* d_reqs = nullptr;  // [2 * max_requests]: attention requests, then finish requests
   StepOut* d_out = nullptr;
@@ -112,6 +112,7 @@ struct as2d_ctx {
   // persistent step kernel: per-layer activation buffers and counters
   bool pers_ok = false;
   bool pers_fit = true;          // every balanced plan's grid fits the persistent grid
+  int attn_rt = 0;               // row tiles per attention block (0: chosen per pass)
   int pers_grid[3] = {0, 0, 0};  // by M-tile count 1, 2: one workgroup per usable CU
   int pers_sl = 0;               // register-resident slice length of the gate/up plan (0: none)
   float *px = nullptr, *psumsq = nullptr, *pq = nullptr;
@@ -399,11 +400,14 @@ int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int
       a.scale = 1.0f / std::sqrt((float)d);
       a.pacc = B.pacc;
       a.pml = B.pml;
-      a.part_rows = B.part_rows;
+      a.part_spans = B.part_spans;
+      // caches of up to 16 spans: the span kernel merges (no second launch)
+      a.merge_last = B.part_spans <= 16;
+      a.attn_cnt = B.attn_cnt;
       a.out = B.attn;
       a.out_plane = B.attn_plane;
       a.M = M;
-      a.attn_cnt = B.attn_cnt;
+      a.attn_rt = c->attn_rt;
       Timed t(c, K_ATTN);
       HIP_TRY(c, launch_attention(bf, a, n_att, max_blocks, prefill, s));
     }
@@ -515,9 +519,8 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     a.scale = 1.0f / std::sqrt((float)d);
     a.pacc = c->b.pacc;
     a.pml = c->b.pml;
-    a.part_rows = c->b.part_rows;
+    a.part_spans = c->b.part_spans;
     a.out = (char*)c->pattn + l * qs * 4;
-    a.attn_cnt = c->b.attn_cnt;
     a.out_plane = c->bf16 ? (long long)qs : 0;
     a.M = M;
 
@@ -914,11 +917,11 @@ size_t static_layout(const as2d_ctx* c, int n_blocks, char* base, PassBufs* S) {
   S->fin_counters = (int*)take((size_t)g.max_requests * 4);
   S->part = (float*)take(part * 4);
   S->counters = (int*)take((size_t)split_counter_count(c) * 4);
-  S->part_rows = (int)R;
+  S->part_spans = (int)((n_blocks + kAttnSpan - 1) / kAttnSpan);
   const size_t spans = (n_blocks + kAttnSpan - 1) / kAttnSpan;
   S->pacc = (float*)take(spans * R * QD * 4);
   S->pml = (float*)take(spans * R * g.n_q_heads * 2 * 4);
-  S->attn_cnt = (int*)take((size_t)g.max_requests * g.n_q_heads * 4);
+  S->attn_cnt = (int*)take((size_t)g.max_requests * g.n_q_heads * 2 * 4);
   return off;
 }
 
@@ -1176,12 +1179,12 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
       c->pers_ok = true;
     }
   }
-  c->b.part_rows = MR;
+  c->b.part_spans = (int)((c->n_blocks_cap + kAttnSpan - 1) / kAttnSpan);
   const size_t spans_cap = (c->n_blocks_cap + kAttnSpan - 1) / kAttnSpan;
   CK(dalloc(c, &c->b.pacc, spans_cap * MR * nq * d * 4));
   CK(dalloc(c, &c->b.pml, spans_cap * MR * nq * 2 * 4));
-  CK(dalloc(c, &c->b.attn_cnt, (size_t)g.max_requests * nq * 4));
-  HIP_TRY(c, hipMemsetAsync(c->b.attn_cnt, 0, (size_t)g.max_requests * nq * 4, c->stream));
+  CK(dalloc(c, &c->b.attn_cnt, (size_t)g.max_requests * nq * 2 * 4));
+  HIP_TRY(c, hipMemsetAsync(c->b.attn_cnt, 0, (size_t)g.max_requests * nq * 2 * 4, c->stream));
   CK(dalloc(c, &c->b.d_rows, sizeof(RowDesc) * MR));
   CK(dalloc(c, &c->b.d_reqs, sizeof(ReqDesc) * 2 * g.max_requests));
   CK(dalloc(c, &c->b.d_out, sizeof(StepOut) * g.max_requests));
@@ -1209,6 +1212,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   memset(c->h_reqs, 0, sizeof(ReqDesc) * 2 * g.max_requests);
   c->reqs.assign(g.max_requests, ReqState());
   c->exec_mode = env_int("AS2D_EXEC_MODE", AS2D_EXEC_GRAPH);
+  c->attn_rt = env_int("AS2D_ATTN_RT", 0);
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return AS2D_OK;
   }();
@@ -1314,7 +1318,7 @@ int as2d_verify_static(as2d_ctx* c, int32_t req, const int32_t* cands, int32_t k
   // the array keeps the last call's contents: counters must start at zero
   HIP_TRY(c, launch_fill_zero(S.counters, split_counter_count(c), s));
   HIP_TRY(c, launch_fill_zero(S.fin_counters, mr, s));
-  HIP_TRY(c, launch_fill_zero(S.attn_cnt, mr * g.n_q_heads, s));
+  HIP_TRY(c, launch_fill_zero(S.attn_cnt, mr * g.n_q_heads * 2, s));
   const int timing = c->timing;   // no event bracketing here (events are created on first use)
   c->timing = 0;
   rc = launch_pass(c, S, M, 1, 1, M, true, n_blocks, false);
@@ -1436,10 +1440,11 @@ int as2d_read_kv(as2d_ctx* c, int32_t req, int32_t layer, void* host_k, void* ho
         float kv, vv;
         if (c->bf16) {
           kv = hi16(kbuf.data(), t * 2 * d + j) + hi16(kbuf.data(), t * 2 * d + d + j);
-          vv = hi16(vbuf.data(), j * cap + v_col(t)) + hi16(vbuf.data(), (d + j) * cap + v_col(t));
+          vv = hi16(vbuf.data(), v_elem((int)t, 0, (int)j, (int)d, true)) +
+               hi16(vbuf.data(), v_elem((int)t, 1, (int)j, (int)d, true));
         } else {
           kv = kbuf[t * d + j];
-          vv = vbuf[j * cap + t];
+          vv = vbuf[v_elem((int)t, 0, (int)j, (int)d, false)];
         }
         ok[((size_t)h * n_tok + t) * d + j] = kv;
         ov[((size_t)h * n_tok + t) * d + j] = vv;

@@ -140,19 +140,34 @@ __device__ __forceinline__ float attn_merge_acc(float A, float acc, MergeCoef k)
   return __builtin_fmaf(A, k.a, acc * k.c);
 }
 
-// The operands of one request's queries for head h: this lane's share of
-// every k-step of row tiles rt < RT (rows 16 rt + lane % 16 of the request;
-// rows past W read row W - 1, whose results are never used).
+// The query rows of an attention block.  Block row rr (0 .. 16 RT) is the
+// linear row u = u0 + rr of the query heads h0, h0 + 1, .. that share one KV
+// head, u = (h - h0) W + i for request row i; rows past the n = heads x W of
+// those heads repeat the last one (computed, never stored).  A block of one
+// head: h0 = h, n = W, u0 = 0.  Each row's arithmetic is the same in any
+// block.
+struct AttnRows {
+  int h0, W, n, u0;
+  __device__ int lin(int rr) const { return min(u0 + rr, n - 1); }
+  __device__ int head(int rr) const { return h0 + lin(rr) / W; }
+  __device__ int row(int rr) const { return lin(rr) % W; }
+  __device__ bool valid(int rr) const { return u0 + rr < n; }
+};
+__device__ __forceinline__ AttnRows attn_rows_of_head(int h, int W) { return AttnRows{h, W, W, 0}; }
+
+// The operands of a block's queries: this lane's share of every k-step of
+// row tiles rt < RT (block row 16 rt + lane % 16).
 template <bool BF, int D, int RT>
-__device__ __forceinline__ void attn_load_q(const AttnArgs& p, const ReqDesc& rq, int h, Op2 (&q)[RT][D / AttnFmt<BF>::KE]) {
+__device__ __forceinline__ void attn_load_q(const AttnArgs& p, const ReqDesc& rq, const AttnRows& rows,
+                                            Op2 (&q)[RT][D / AttnFmt<BF>::KE]) {
   using F = AttnFmt<BF>;
   const int lane = threadIdx.x & 63;
   const int qcols = p.n_q * D;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    const int r = min(16 * rt + (lane & 15), rq.W - 1);
-    const float4* base =
-        reinterpret_cast<const float4*>(p.q + (size_t)(rq.row_start + r) * qcols + h * D + F::PER * (lane >> 4));
+    const int rr = 16 * rt + (lane & 15);
+    const float4* base = reinterpret_cast<const float4*>(p.q + (size_t)(rq.row_start + rows.row(rr)) * qcols +
+                                                         rows.head(rr) * D + F::PER * (lane >> 4));
 #pragma unroll
     for (int ks = 0; ks < D / F::KE; ++ks) {
       float4 v[2];
@@ -197,11 +212,12 @@ template <bool BF> __device__ __forceinline__ uint4 keep_first(uint4 x, int n) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Wave w's chunk of span sp.  Reads stay inside the slot's rows: K rows up
-// to the last key, V rows only for a chunk that starts at or before it (the
-// row stride is a multiple of 64, so such a chunk ends inside the row).
+// Wave w's chunk of span sp of KV head g.  Reads stay inside the slot's
+// rows: K rows up to the last key, V rows only for a chunk that starts at or
+// before it (the row stride is a multiple of 64, so such a chunk ends inside
+// the row).
 template <bool BF, int D>
-__device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq, int h, int sp, AttnRaw<BF, D>& r) {
+__device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq, int g, int sp, AttnRaw<BF, D>& r) {
   using F = AttnFmt<BF>;
   using Raw = AttnRaw<BF, D>;
   using T = typename ET<BF>::T;
@@ -209,7 +225,6 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
   const int lg = lane >> 4, lr = lane & 15;
   const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;   // first key of the chunk
   const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
-  const int g = h * p.n_kv / p.n_q;
   const size_t head = (size_t)rq.slot * p.slot_stride + (size_t)g * p.kv_cap * D;   // float32 units
   const T* kb = reinterpret_cast<const T*>(p.k_cache + head);
   const T* vb = reinterpret_cast<const T*>(p.v_cache + head);
@@ -229,14 +244,16 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
       for (int j = 0; j < Raw::KSV; ++j) r.v[t][j] = Op2{make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
     return;
   }
+  // the chunk's V block (v_elem): [parts][D][32]
+  const T* vc = vb + (size_t)(kc >> 5) * F::PARTS * D * 32;
 #pragma unroll
   for (int t = 0; t < Raw::DT; ++t) {
-    const T* vr = vb + (size_t)(16 * t + lr) * p.kv_cap + kc;
+    const T* vr = vc + (16 * t + lr) * 32;
     if constexpr (BF) {
       // keys 4 lg .. 4 lg + 3 of the first tile, then of the second: columns
-      // 8 lg .. 8 lg + 7 of the chunk (v_col)
+      // 8 lg .. 8 lg + 7 of the block (v_col)
       r.v[t][0] = Op2{ldg(reinterpret_cast<const uint4*>(vr + 8 * lg)),
-                      ldg(reinterpret_cast<const uint4*>(vr + (size_t)D * p.kv_cap + 8 * lg))};
+                      ldg(reinterpret_cast<const uint4*>(vr + D * 32 + 8 * lg))};
     } else {
 #pragma unroll
       for (int j = 0; j < Raw::KSV; ++j) {
@@ -300,17 +317,19 @@ __device__ __forceinline__ void attn_state_merge(AttnState<RT, DTW>& st, const f
     }
 }
 
-// The state of span sp for rows of row tiles rt < RT (queries q; this
-// wave's chunk of keys and values in raw), in the layout of AttnState: for
-// lane l and i < 4, row 16 rt + 4 (l / 16) + i, dimensions 16 (w DTW + t) +
-// l % 16.  Rows whose position is before the span's first key get no
-// meaningful state (they are never stored or merged).  256 threads, 4 waves;
+// The state of span sp for the block rows of row tiles rt < RT (queries q;
+// this wave's chunk of keys and values in raw), in the layout of AttnState:
+// for lane l and i < 4, block row 16 rt + 4 (l / 16) + i, dimensions
+// 16 (w DTW + t) + l % 16.  Rows whose position is before the span's first
+// key get no meaningful state (they are never stored or merged).  256 threads, 4 waves;
 // smem: attn_span_lds_bytes<BF, D, RT>(), not in use on entry (the caller
-// synchronises the workgroup before it is written again).
+// synchronises the workgroup before it is written again).  Two steps:
+// attn_span_chunks (each wave's chunk sums into the LDS; q and raw are not
+// needed after it) and attn_merge_chunks.
 template <bool BF, int D, int RT>
-__device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc& rq, int sp,
-                                                const Op2 (&q)[RT][D / AttnFmt<BF>::KE], const AttnRaw<BF, D>& raw,
-                                                unsigned char* smem, AttnState<RT, D / 64>& st) {
+__device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDesc& rq, const AttnRows& rows, int sp,
+                                                 const Op2 (&q)[RT][D / AttnFmt<BF>::KE], const AttnRaw<BF, D>& raw,
+                                                 unsigned char* smem) {
 #pragma clang fp contract(off)
   using Raw = AttnRaw<BF, D>;
   constexpr int KS = Raw::KS, DT = Raw::DT, DTW = D / 64, R = 16 * RT;
@@ -322,29 +341,33 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
   float* SM = reinterpret_cast<float*>(SA + kWaves * RT * DT * 64);   // [wave][R]
   float* SL = SM + kWaves * R;                                          // [wave][R]
 
+  // s of every row tile first, so that the keys are free before p v
+  float s[RT][2][4];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
-    // s transposed: lane l holds keys kc + 16 kt + 4 (l / 16) + i of row 16 rt + l % 16
-    const int pos = rq.L0 + min(16 * rt + lr, rq.W - 1);
-    float s[2][4];
+    // s transposed: lane l holds keys kc + 16 kt + 4 (l / 16) + i of block row 16 rt + l % 16
+    const int pos = rq.L0 + rows.row(16 * rt + lr);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       f4 acc = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) acc = mma3<BF>(raw.k[kt][ks], q[rt][ks], acc);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) s[kt][i] = kc + 16 * kt + 4 * lg + i <= pos ? acc[i] * p.scale : -INFINITY;
+      for (int i = 0; i < 4; ++i) s[rt][kt][i] = kc + 16 * kt + 4 * lg + i <= pos ? acc[i] * p.scale : -INFINITY;
     }
-    float mx = s[0][0];
+  }
 #pragma unroll
-    for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[e >> 2][e & 3]);
+  for (int rt = 0; rt < RT; ++rt) {
+    float mx = s[rt][0][0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) mx = fmaxf(mx, s[rt][e >> 2][e & 3]);
     mx = swap_combine<false>(mx, FMax{});
     mx = swap_combine<true>(mx, FMax{});
     float pj[2][4];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pj[kt][i] = mx == -INFINITY ? 0.0f : expf(s[kt][i] - mx);
+      for (int i = 0; i < 4; ++i) pj[kt][i] = mx == -INFINITY ? 0.0f : expf(s[rt][kt][i] - mx);
     float sm = (((pj[0][0] + pj[0][1]) + pj[0][2]) + pj[0][3]) + (((pj[1][0] + pj[1][1]) + pj[1][2]) + pj[1][3]);
     sm = swap_combine<false>(sm, FAdd{});
     sm = swap_combine<true>(sm, FAdd{});
@@ -380,6 +403,16 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
       }
     }
   }
+}
+
+template <bool BF, int D, int RT>
+__device__ __forceinline__ void attn_merge_chunks(unsigned char* smem, AttnState<RT, D / 64>& st) {
+#pragma clang fp contract(off)
+  constexpr int DT = D / 16, DTW = D / 64, R = 16 * RT;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lg = lane >> 4;
+  const f4* SA = reinterpret_cast<const f4*>(smem);                          // [wave][rt][t][lane]
+  const float* SM = reinterpret_cast<const float*>(SA + kWaves * RT * DT * 64);   // [wave][R]
+  const float* SL = SM + kWaves * R;                                              // [wave][R]
   lds_sync();   // LDS only: global loads in flight (the next span's) stay in flight
   // the four chunks merged in order, for this wave's dimension tiles
 #pragma unroll
@@ -410,20 +443,31 @@ __device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc
   }
 }
 
-// Span sp of request rq for head h: fetch, then attn_span_state.
 template <bool BF, int D, int RT>
-__device__ __forceinline__ void attn_span(const AttnArgs& p, const ReqDesc& rq, int h, int sp,
+__device__ __forceinline__ void attn_span_state(const AttnArgs& p, const ReqDesc& rq, const AttnRows& rows, int sp,
+                                                const Op2 (&q)[RT][D / AttnFmt<BF>::KE], const AttnRaw<BF, D>& raw,
+                                                unsigned char* smem, AttnState<RT, D / 64>& st) {
+  attn_span_chunks<BF, D, RT>(p, rq, rows, sp, q, raw, smem);
+  attn_merge_chunks<BF, D, RT>(smem, st);
+}
+
+// KV head of the query heads of a block.
+__device__ __forceinline__ int attn_kv_head(const AttnArgs& p, const AttnRows& rows) { return rows.h0 * p.n_kv / p.n_q; }
+
+// Span sp of request rq for a block's rows: fetch, then attn_span_state.
+template <bool BF, int D, int RT>
+__device__ __forceinline__ void attn_span(const AttnArgs& p, const ReqDesc& rq, const AttnRows& rows, int sp,
                                           const Op2 (&q)[RT][D / AttnFmt<BF>::KE], unsigned char* smem,
                                           AttnState<RT, D / 64>& st) {
   AttnRaw<BF, D> raw;
-  attn_fetch<BF, D>(p, rq, h, sp, raw);
-  attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, st);
+  attn_fetch<BF, D>(p, rq, attn_kv_head(p, rows), sp, raw);
+  attn_span_state<BF, D, RT>(p, rq, rows, sp, q, raw, smem, st);
 }
 
-// Stores the span state of the rows of the request that reach span sp:
-// pacc[sp][row][h][D] (A), pml[sp][row][h][2] (M, L), agent-scope stores.
+// Stores the span state of the block's rows that reach span sp:
+// pacc[row][h][sp][D] (A), pml[row][h][sp][2] (M, L), agent-scope stores.
 template <int D, int RT>
-__device__ __forceinline__ void attn_store_span(const AttnArgs& p, const ReqDesc& rq, int h, int sp,
+__device__ __forceinline__ void attn_store_span(const AttnArgs& p, const ReqDesc& rq, const AttnRows& rows, int sp,
                                                 const AttnState<RT, D / 64>& st) {
   constexpr int DTW = D / 64;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -431,9 +475,10 @@ __device__ __forceinline__ void attn_store_span(const AttnArgs& p, const ReqDesc
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = 16 * rt + 4 * (lane >> 4) + i;
-      if (r < rq.W && rq.L0 + r >= sp * kAttnSpanKeys) {
-        const size_t o = ((size_t)sp * p.part_rows + rq.row_start + r) * p.n_q + h;
+      const int rr = 16 * rt + 4 * (lane >> 4) + i;
+      const int r = rows.row(rr);
+      if (rows.valid(rr) && rq.L0 + r >= sp * kAttnSpanKeys) {
+        const size_t o = ((size_t)(rq.row_start + r) * p.n_q + rows.head(rr)) * p.part_spans + sp;
 #pragma unroll
         for (int t = 0; t < DTW; ++t)
           store_partial(p.pacc + o * D + 16 * (wave * DTW + t) + (lane & 15), st.A[rt][t][i]);
@@ -456,7 +501,7 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, const ReqDesc&
   const int ql = threadIdx.x & 15;
   const int row = rq.row_start + r;
   const int ns = (rq.L0 + r) / kAttnSpanKeys + 1;
-  auto at = [&](int sp) { return ((size_t)sp * p.part_rows + row) * p.n_q + h; };
+  auto at = [&](int sp) { return ((size_t)row * p.n_q + h) * p.part_spans + sp; };
   const __amdgpu_buffer_rsrc_t racc = coherent_rsrc(p.pacc), rml = coherent_rsrc(p.pml);
   float M = 0.f, L = 0.f, A[DQ];
   // batches of kB spans; the next batch is requested before the current one
@@ -510,6 +555,92 @@ __device__ __forceinline__ void attn_merge_row(const AttnArgs& p, const ReqDesc&
 #pragma unroll
   for (int t = 0; t < DQ; ++t) o[t] = A[t] / L;
   store_act_run<BF, OUT_COH, DQ>(p.out, p.out_plane, frag_index<BF>(row, h * D + DQ * ql, p.n_q * D), o);
+}
+
+// Row i of request rq, head h, by one wave: the same fold as attn_merge_row
+// (span states in ascending order from span 0), with lane l holding
+// dimensions [DL l, DL l + DL), DL = D / 64.  The states come in batches of
+// kB spans, the next batch requested before the current one is folded; the
+// fold's coefficients of a batch are computed one span per lane: the
+// running maximum before span s is the maximum of m over spans 0 .. s - 1,
+// which a prefix scan gives exactly (fmax rounds nothing).  The states were
+// stored by an earlier kernel; the output planes are read by a later one.
+template <bool BF, int D>
+__device__ __forceinline__ void attn_merge_wave(const AttnArgs& p, const ReqDesc& rq, int i, int h) {
+#pragma clang fp contract(off)
+  constexpr int DL = D / 64;   // dimensions per lane
+  constexpr int kB = 16;       // spans per batch
+  static_assert(DL == 1 || DL == 2, "64 or 128 dimensions");
+  const int lane = threadIdx.x & 63, bl = lane & (kB - 1);
+  const int row = rq.row_start + i;
+  const int ns = (rq.L0 + i) / kAttnSpanKeys + 1;
+  auto at = [&](int sp) { return ((size_t)row * p.n_q + h) * p.part_spans + sp; };
+  struct Batch {
+    float m, l, a[kB][DL];
+  };
+  // past the last span: the last one again, unused
+  auto load = [&](int s0, Batch& b) {
+    const float2 ml = ldg(reinterpret_cast<const float2*>(p.pml + at(min(s0 + bl, ns - 1)) * 2));
+    b.m = ml.x;
+    b.l = ml.y;
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+      const float* src = p.pacc + at(min(s0 + u, ns - 1)) * D + DL * lane;
+      if constexpr (DL == 2) {
+        const float2 v = ldg(reinterpret_cast<const float2*>(src));
+        b.a[u][0] = v.x;
+        b.a[u][1] = v.y;
+      } else {
+        b.a[u][0] = ldg(src);
+      }
+    }
+  };
+  float M = -INFINITY, L = 0.f, A[DL];
+  auto merge = [&](int s0, const Batch& b) {
+    // lane u: the running maximum after span s0 + u (mx) and before it (mb)
+    float mx = s0 + bl < ns ? b.m : -INFINITY;
+#pragma unroll
+    for (int d = 1; d < kB; d <<= 1) {
+      const float o = __shfl_up(mx, d, kB);
+      if (bl >= d) mx = fmaxf(mx, o);
+    }
+    mx = fmaxf(M, mx);
+    float mb = __shfl_up(mx, 1, kB);
+    if (bl == 0) mb = M;
+    const float ca = expf(mb - mx), cc = expf(b.m - mx);
+#pragma unroll
+    for (int u = 0; u < kB; ++u) {
+      if (s0 + u < ns) {
+        const float lu = lane_value(b.l, u);
+        if (s0 + u == 0) {
+          L = lu;
+#pragma unroll
+          for (int t = 0; t < DL; ++t) A[t] = b.a[u][t];
+        } else {
+          const float ka = lane_value(ca, u), kc = lane_value(cc, u);
+          L = __builtin_fmaf(L, ka, lu * kc);
+#pragma unroll
+          for (int t = 0; t < DL; ++t) A[t] = __builtin_fmaf(A[t], ka, b.a[u][t] * kc);
+        }
+      }
+    }
+    M = lane_value(mx, min(ns - s0, kB) - 1);
+  };
+  Batch b0, b1;
+  load(0, b0);
+  for (int s0 = 0; s0 < ns; s0 += 2 * kB) {
+    if (s0 + kB < ns) load(s0 + kB, b1);
+    merge(s0, b0);
+    if (s0 + kB >= ns) break;
+    if (s0 + 2 * kB < ns) load(s0 + 2 * kB, b0);
+    merge(s0 + kB, b1);
+  }
+  float o[DL];
+#pragma unroll
+  for (int t = 0; t < DL; ++t) o[t] = A[t] / L;
+  const size_t e = frag_index<BF>(row, h * D + DL * lane, p.n_q * D);
+  if constexpr (DL == 2) store_act_run<BF, false, 2>(p.out, p.out_plane, e, o);
+  else store_act<BF, false>(p.out, p.out_plane, e, o[0]);
 }
 
 }  // namespace as2d

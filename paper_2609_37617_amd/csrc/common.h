@@ -9,6 +9,7 @@
 namespace as2d {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
@@ -45,6 +46,10 @@ __device__ __forceinline__ uint4 ldg(const uint4* p) {
 __device__ __forceinline__ float4 ldg(const float4* p) {
   const f4 v = *gmem(reinterpret_cast<const f4*>(p));
   return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float2 ldg(const float2* p) {
+  const f2 v = *gmem(reinterpret_cast<const f2*>(p));
+  return make_float2(v.x, v.y);
 }
 template <class V> __device__ __forceinline__ V ldg(const V* p) { return *gmem(p); }
 
@@ -118,7 +123,7 @@ template <bool BF, bool COH> __device__ __forceinline__ void store_act(void* bas
 // (so they are contiguous in memory) with i a multiple of N (N = 4 or 8).
 template <bool BF, bool COH, int N>
 __device__ __forceinline__ void store_act_run(void* base, long long plane, size_t i, const float* v) {
-  static_assert(N == 4 || N == 8, "run of 4 or 8 elements");
+  static_assert(N == 2 || N == 4 || N == 8, "run of 2, 4 or 8 elements");
   if constexpr (BF) {
     uint32_t hw[N / 2], lw[N / 2];
 #pragma unroll
@@ -138,6 +143,9 @@ __device__ __forceinline__ void store_act_run(void* base, long long plane, size_
     } else if constexpr (N == 8) {
       *gmem(reinterpret_cast<u32x4*>(hp)) = u32x4{hw[0], hw[1], hw[2], hw[3]};
       *gmem(reinterpret_cast<u32x4*>(lp)) = u32x4{lw[0], lw[1], lw[2], lw[3]};
+    } else if constexpr (N == 2) {
+      *gmem(hp) = hw[0];
+      *gmem(lp) = lw[0];
     } else {
       *gmem(reinterpret_cast<u32x2*>(hp)) = u32x2{hw[0], hw[1]};
       *gmem(reinterpret_cast<u32x2*>(lp)) = u32x2{lw[0], lw[1]};
@@ -147,6 +155,8 @@ __device__ __forceinline__ void store_act_run(void* base, long long plane, size_
     if constexpr (COH) {
 #pragma unroll
       for (int t = 0; t < N; ++t) st<true>(fp + t, v[t]);
+    } else if constexpr (N == 2) {
+      *gmem(reinterpret_cast<f2*>(fp)) = f2{v[0], v[1]};
     } else {
 #pragma unroll
       for (int t = 0; t < N; t += 4) *gmem(reinterpret_cast<f4*>(fp + t)) = f4{v[t], v[t + 1], v[t + 2], v[t + 3]};

@@ -114,12 +114,14 @@ struct GemmArgs {
 
 // KV cache of one layer and slot, per KV head (kv_cap * d float32 units
 // each for K and for V):
-//   bf16 models: K [pos][2][d] bf16: the (hi, lo) pair of each value, hi row
-//   then lo row per position; V [2][d][col] bf16: hi plane then lo plane,
-//   each dimension-major, position pos at column v_col(pos) (the keys of
-//   each aligned group of 32 reordered so that the eight keys one lane group
-//   multiplies in p v are adjacent);
-//   float32 models: K [pos][d], V [d][pos] float32.
+//   K, bf16 models: [pos][2][d] bf16, the (hi, lo) pair of each value, hi
+//   row then lo row per position; float32 models: [pos][d] float32.
+//   V: blocks of 32 positions; block pos / 32 holds [parts][d][32] elements
+//   (v_elem), so that the values of one 32-key chunk are one contiguous
+//   run of d x 128 bytes: bf16 models hold the hi plane then
+//   the lo plane, the keys of the block reordered (v_col) so that the eight
+//   keys one lane group multiplies in p v are adjacent; float32 models hold
+//   one float32 plane in key order.
 // hi = bf16(x) and lo = bf16(x - hi): the operands of the attention's
 // matrix-core products, stored once when the row is appended.
 //
@@ -127,6 +129,13 @@ struct GemmArgs {
 // sits at 8 g + 4 t + e.
 __host__ __device__ inline int v_col(int pos) {
   return (pos & ~31) | (((pos >> 2) & 3) << 3) | (((pos >> 4) & 1) << 2) | (pos & 3);
+}
+// Element index (bf16 or float32 units) of V value (pos, part, dimension
+// dd) of one KV head with d dimensions.
+__host__ __device__ inline size_t v_elem(int pos, int part, int dd, int d, bool bf16) {
+  const int parts = bf16 ? 2 : 1;
+  const int col = bf16 ? (v_col(pos) & 31) : (pos & 31);
+  return ((size_t)(pos >> 5) * parts + part) * d * 32 + (size_t)dd * 32 + col;
 }
 
 struct AttnArgs {
@@ -139,13 +148,15 @@ struct AttnArgs {
   const ReqDesc* reqs;
   int n_q, n_kv, head_dim;
   float scale;
-  float* pacc;           // span states [span][part_rows][n_q][d]
-  float* pml;            // [span][part_rows][n_q][2]: running maximum and sum
-  int part_rows;         // row stride of the partials (at least the pass's rows)
-  int* attn_cnt;         // finished spans per (request of the pass, head), zero between launches
+  float* pacc;           // span states [row][n_q][part_spans][d]
+  float* pml;            // [row][n_q][part_spans][2]: running maximum and sum
+  int part_spans;        // spans per (row, head) in the state arrays
+  int* attn_cnt;         // merge_last: finished spans per (request, KV head, block of 2 heads' rows), zero between launches
+  int merge_last;        // 1: the last item of a block merges its rows (no merge kernel)
   void* out;             // planes [kMaxRows][n_q*d]
   long long out_plane;
   int M;
+  int attn_rt;           // row tiles per block of the verification kernel (0: chosen from M)
 };
 
 // Persistent step kernel (step.hip): one verification pass of up to 32 rows.

@@ -270,31 +270,34 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // ---------------------------------------------------------------------------
 // Block-causal grouped-query attention (attn.h).
 //
-// Verification passes: work items (request, 128-key span, query head),
-// with the heads of a KV group adjacent and dealt so that consecutive items
-// run on one XCD (their keys and values are read from memory once and from
-// that XCD's L2 for the group's other heads).  A fixed grid of workgroups
-// takes the items in turn, so the grid does not depend on the cache
-// length.  An item merges its span's blocks and stores the span state; the
-// last item of a (request, head) to finish (agent-scope counter) merges
-// every row of the request over its spans and writes the attention output.
+// Verification passes.  attn_group_kernel: work items (request, run of
+// 128-key spans, KV head, row block), a row block being up to 16 RT rows of
+// the query heads that share the KV head (their rows of the request, head by
+// head), so each span's keys and values are read once per block; the blocks
+// of one (run, KV head) are adjacent and dealt to one XCD.  A fixed grid of
+// workgroups takes the items in turn, so the grid does not depend on the
+// cache length; each item stores its rows' span states.  The states of a
+// row are folded in order, for caches of up to 16 spans by the last item of
+// the block to finish (one quarter wave per row and head), else by
+// attn_merge_kernel (one wave per row and head).
 //
 // Prefill passes (one request, up to 144 rows): one workgroup per (query
-// head, 32 rows) walks the spans in ascending order and merges them as it
+// head, 16 rows) walks the spans in ascending order and merges them as it
 // goes, with the same arithmetic, so no partials go through memory.
 
-constexpr int kAttnGrid = 256;   // workgroups of the verification kernel (one per compute unit: its registers allow no more)
+constexpr int kAttnGrid = 256;   // workgroups of the span kernel (one per compute unit: its LDS allows no more)
 
+// The items of a launch with blocks of RT row tiles.
 template <bool BF, int D, int RT>
-__global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int n_reqs) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  __shared__ int s_last;
+__device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, unsigned char* smem) {
   constexpr int KS = D / AttnFmt<BF>::KE;
+  constexpr int BR = 16 * RT;   // rows of a block
   const int G = gridDim.x;
-  // a workgroup item is a run of up to R consecutive spans of one (request,
-  // head): the least R whose items fit the grid (one span each while they
-  // do; long caches take several per workgroup, the next span's keys and
-  // values requested while the current one runs)
+  const int hpg = p.n_q / p.n_kv;   // query heads per KV head
+  auto blocks = [&](const ReqDesc& rq) { return (hpg * rq.W + BR - 1) / BR; };
+  // an item covers a run of up to R consecutive spans: the least R whose
+  // items fit the grid (one span each while they do; long caches take
+  // several per workgroup)
   int ns_max = 1;
   auto n_items = [&](int R) {
     int n = 0;
@@ -302,63 +305,110 @@ __global__ __launch_bounds__(256) void attn_verify_kernel(const AttnArgs p, int 
       const ReqDesc rq = load_invariant(p.reqs + r);
       const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
       ns_max = max(ns_max, ns);
-      n += p.n_q * ((ns + R - 1) / R);
+      n += p.n_kv * blocks(rq) * ((ns + R - 1) / R);
     }
     return n;
   };
   int R = 1, total = n_items(1);
   while (total > G && R < ns_max) total = n_items(++R);
   for (int t = xcd_contiguous(blockIdx.x, G); t < total; t += G) {
-    // item t: request r, run j, head h (the heads of a KV group are adjacent)
-    int r = 0, u = t, ns = 0, nr = 0;
+    // item t: request r, then run j, KV head g, row block b
+    int r = 0, u = t, ns = 0, nb = 0;
     ReqDesc rq;
     for (;; ++r) {
       rq = load_invariant(p.reqs + r);
       ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
-      nr = (ns + R - 1) / R;
-      if (u < p.n_q * nr || r == n_reqs - 1) break;
-      u -= p.n_q * nr;
+      nb = blocks(rq);
+      const int n = p.n_kv * nb * ((ns + R - 1) / R);
+      if (u < n || r == n_reqs - 1) break;
+      u -= n;
     }
-    const int j = u / p.n_q, h = u - j * p.n_q;
+    const int j = u / (p.n_kv * nb);
+    const int v = u - j * p.n_kv * nb;
+    const int g = v / nb, b = v - g * nb;
+    const AttnRows rows{g * hpg, rq.W, hpg * rq.W, b * BR};
     const int sp0 = j * R, sp1 = min(sp0 + R, ns);
     // the first span's keys and values, then the queries, all in flight at once
-    AttnRaw<BF, D> ka, kb;
-    attn_fetch<BF, D>(p, rq, h, sp0, ka);
+    AttnRaw<BF, D> ka;
+    attn_fetch<BF, D>(p, rq, g, sp0, ka);
     Op2 q[RT][KS];
-    attn_load_q<BF, D, RT>(p, rq, h, q);
+    attn_load_q<BF, D, RT>(p, rq, rows, q);
     auto run = [&](int sp, const AttnRaw<BF, D>& raw) {
       AttnState<RT, D / 64> state;
-      attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, state);
-      attn_store_span<D, RT>(p, rq, h, sp, state);
-      lds_sync();   // the next span writes the LDS again (the prefetch stays in flight)
+      attn_span_state<BF, D, RT>(p, rq, rows, sp, q, raw, smem, state);
+      attn_store_span<D, RT>(p, rq, rows, sp, state);
+      lds_sync();   // the LDS is written again next (a prefetch stays in flight)
     };
     if constexpr (RT == 1) {   // two chunk buffers taken in turn (as in attn_prefill_kernel)
+      AttnRaw<BF, D> kb;
       for (int sp = sp0; sp < sp1; sp += 2) {
         wait_vmem_counted();
-        if (sp + 1 < sp1) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);
+        if (sp + 1 < sp1) attn_fetch<BF, D>(p, rq, g, sp + 1, kb);
         run(sp, ka);
         if (sp + 1 >= sp1) break;
         wait_vmem_counted();
-        if (sp + 2 < sp1) attn_fetch<BF, D>(p, rq, h, sp + 2, ka);
+        if (sp + 2 < sp1) attn_fetch<BF, D>(p, rq, g, sp + 2, ka);
         run(sp + 1, kb);
       }
     } else {   // two row tiles: one buffer (two would not fit the registers)
       for (int sp = sp0; sp < sp1; ++sp) {
-        if (sp > sp0) attn_fetch<BF, D>(p, rq, h, sp, ka);
+        if (sp > sp0) attn_fetch<BF, D>(p, rq, g, sp, ka);
         run(sp, ka);
       }
     }
-    wait_vmem();
-    __syncthreads();   // every wave's span stores are performed
-    const int done = sp1 - sp0;
-    if (threadIdx.x == 0) s_last = counter_add(&p.attn_cnt[r * p.n_q + h], done) == ns - done;
-    __syncthreads();
-    if (s_last) {
-      if (threadIdx.x == 0) st<true>(&p.attn_cnt[r * p.n_q + h], 0);   // ready for the next launch
-      for (int i = threadIdx.x >> 4; i < rq.W; i += 16) attn_merge_row<BF, D, false>(p, rq, i, h);
+    if (p.merge_last) {
+      // the last item of the block to finish (agent-scope counter) merges
+      // its rows, one quarter wave per (row, head)
+      __shared__ int s_last;
+      wait_vmem();
+      __syncthreads();   // every wave's span stores are performed
+      const int done = sp1 - sp0;
+      int* cnt = p.attn_cnt + (r * p.n_kv + g) * 2 * hpg + b;
+      if (threadIdx.x == 0) s_last = counter_add(cnt, done) == ns - done;
+      __syncthreads();
+      if (s_last) {
+        if (threadIdx.x == 0) st<true>(cnt, 0);   // ready for the next launch
+        const int nv = min(BR, rows.n - rows.u0);
+        for (int k = threadIdx.x >> 4; k < nv; k += 16) attn_merge_row<BF, D, false>(p, rq, rows.row(k), rows.head(k));
+      }
+      __syncthreads();   // s_last is reused by the next item
     }
-    __syncthreads();   // s_last is reused by the next item
   }
+}
+
+// Blocks of one row tile while each (span, KV head, block) can have a
+// workgroup of its own, else of two (half the reads of the keys and values
+// per row, runs of spans per workgroup); an attn_rt of 1 or 2 fixes it.
+template <bool BF, int D>
+__global__ __launch_bounds__(256) void attn_group_kernel(const AttnArgs p, int n_reqs) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  int rt = p.attn_rt;
+  if (rt != 1 && rt != 2) {
+    const int hpg = p.n_q / p.n_kv;
+    int n = 0;
+    for (int r = 0; r < n_reqs; ++r) {
+      const ReqDesc rq = load_invariant(p.reqs + r);
+      n += p.n_kv * ((hpg * rq.W + 15) / 16) * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
+    }
+    rt = n <= (int)gridDim.x ? 1 : 2;
+  }
+  if (rt == 1) attn_group_items<BF, D, 1>(p, n_reqs, smem);
+  else attn_group_items<BF, D, 2>(p, n_reqs, smem);
+}
+
+// One wave per (request row, query head), heads of a row adjacent.
+template <bool BF, int D>
+__global__ __launch_bounds__(64) void attn_merge_kernel(const AttnArgs p, int n_reqs) {
+  int u = blockIdx.x;
+  ReqDesc rq;
+  for (int r = 0;; ++r) {
+    if (r == n_reqs) return;
+    rq = load_invariant(p.reqs + r);
+    if (u < rq.W * p.n_q) break;
+    u -= rq.W * p.n_q;
+  }
+  const int i = u / p.n_q;
+  attn_merge_wave<BF, D>(p, rq, i, u - i * p.n_q);
 }
 
 constexpr int kAttnPrefillRT = 1;   // row tiles per prefill workgroup
@@ -375,16 +425,18 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
   // this workgroup's rows as a request of their own: same positions
   const ReqDesc rq{full.row_start + r0, min(full.W - r0, 16 * RT), full.L0 + r0, full.slot};
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const AttnRows rows = attn_rows_of_head(h, rq.W);
+  const int g = attn_kv_head(p, rows);
   Op2 q[RT][KS];
-  attn_load_q<BF, D, RT>(p, rq, h, q);
+  attn_load_q<BF, D, RT>(p, rq, rows, q);
   AttnState<RT, DTW> all;
   const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
   // two chunk buffers taken in turn: span sp + 1 is requested before span sp runs
   AttnRaw<BF, D> ka, kb;
-  attn_fetch<BF, D>(p, rq, h, 0, ka);
+  attn_fetch<BF, D>(p, rq, g, 0, ka);
   auto run = [&](int sp, const AttnRaw<BF, D>& raw) {
     AttnState<RT, DTW> state;
-    attn_span_state<BF, D, RT>(p, rq, sp, q, raw, smem, state);
+    attn_span_state<BF, D, RT>(p, rq, rows, sp, q, raw, smem, state);
     attn_state_merge<RT, DTW>(all, state.M, state.L, state.A, sp == 0, [&](int rt, int i) {
       return rq.L0 + min(16 * rt + 4 * (lane >> 4) + i, rq.W - 1) >= sp * kAttnSpanKeys;
     });
@@ -394,11 +446,11 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
   // per lane and span, so two spans would exceed what the wave can count)
   for (int sp = 0; sp < ns; sp += 2) {
     wait_vmem_counted();
-    if (sp + 1 < ns) attn_fetch<BF, D>(p, rq, h, sp + 1, kb);
+    if (sp + 1 < ns) attn_fetch<BF, D>(p, rq, g, sp + 1, kb);
     run(sp, ka);
     if (sp + 1 >= ns) break;
     wait_vmem_counted();
-    if (sp + 2 < ns) attn_fetch<BF, D>(p, rq, h, sp + 2, ka);
+    if (sp + 2 < ns) attn_fetch<BF, D>(p, rq, g, sp + 2, ka);
     run(sp + 1, kb);
   }
 #pragma unroll
@@ -424,11 +476,17 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_blocks, b
     attn_prefill_kernel<BF, D><<<dim3(a.n_q, (a.M + R - 1) / R), 256, attn_span_lds_bytes<BF, D, kAttnPrefillRT>(), s>>>(a);
     return hipGetLastError();
   }
-  // rows per request: at most 32 (two row tiles) on this path
-  const long long items = (long long)n_reqs * a.n_q * ((max_blocks + kAttnSpan - 1) / kAttnSpan);
+  // items of one-tile blocks at the slot capacity, from the most rows a
+  // request of the pass can have (so that one captured graph serves every
+  // pass of M rows and n_reqs requests)
+  const int hpg = a.n_q / a.n_kv;
+  const long long rows = (long long)hpg * (a.M - n_reqs + 1);
+  const long long items = (long long)n_reqs * a.n_kv * ((rows + 15) / 16) * ((max_blocks + kAttnSpan - 1) / kAttnSpan);
   const int grid = (int)std::min<long long>(kAttnGrid, (items + 7) / 8 * 8);
-  if (a.M > 16) attn_verify_kernel<BF, D, 2><<<grid, 256, attn_span_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
-  else attn_verify_kernel<BF, D, 1><<<grid, 256, attn_span_lds_bytes<BF, D, 1>(), s>>>(a, n_reqs);
+  attn_group_kernel<BF, D><<<grid, 256, attn_span_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.merge_last) return e;
+  attn_merge_kernel<BF, D><<<a.M * a.n_q, 64, 0, s>>>(a, n_reqs);
   return hipGetLastError();
 }
 
@@ -465,9 +523,7 @@ static hipError_t prepare_staged() {
 template <bool BF, int D>
 static hipError_t prepare_attention() {
   auto allow = [](const void* k, int bytes) { return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, bytes); };
-  hipError_t e = allow(reinterpret_cast<const void*>(&attn_verify_kernel<BF, D, 1>), attn_span_lds_bytes<BF, D, 1>());
-  if (e == hipSuccess)
-    e = allow(reinterpret_cast<const void*>(&attn_verify_kernel<BF, D, 2>), attn_span_lds_bytes<BF, D, 2>());
+  hipError_t e = allow(reinterpret_cast<const void*>(&attn_group_kernel<BF, D>), attn_span_lds_bytes<BF, D, 2>());
   if (e == hipSuccess)
     e = allow(reinterpret_cast<const void*>(&attn_prefill_kernel<BF, D>), attn_span_lds_bytes<BF, D, kAttnPrefillRT>());
   return e;

@@ -152,11 +152,12 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
           u -= a.n_q * ns;
         }
         const int sp = u / a.n_q, h = u - sp * a.n_q;
+        const AttnRows rows = attn_rows_of_head(h, rq.W);
         Op2 q[2][KS];
-        attn_load_q<BF, D, 2>(at, rq, h, q);
+        attn_load_q<BF, D, 2>(at, rq, rows, q);
         AttnState<2, D / 64> sst;
-        attn_span<BF, D, 2>(at, rq, h, sp, q, smem, sst);
-        attn_store_span<D, 2>(at, rq, h, sp, sst);
+        attn_span<BF, D, 2>(at, rq, rows, sp, q, smem, sst);
+        attn_store_span<D, 2>(at, rq, rows, sp, sst);
         lds_sync();   // the next item writes the LDS again
         ++mine;
       }

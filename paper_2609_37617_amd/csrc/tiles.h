@@ -150,16 +150,16 @@ __device__ __forceinline__ void epilogue_rows(const GemmArgs& p, float* F, int f
           }
         }
       } else {
-        // V: [(hi, lo)][d][v_col(pos)] (bf16) or [d][pos] (float32), see AttnArgs
+        // V: blocks of 32 positions (v_elem, see AttnArgs)
         const int kvh = head - p.n_q - p.n_kv;
         float* vb = p.v_cache + (size_t)rd.slot * p.slot_stride + (size_t)kvh * p.kv_cap * d;
         if constexpr (BF) {
-          uint16_t* v16 = reinterpret_cast<uint16_t*>(vb) + (size_t)dd * p.kv_cap + v_col(rd.pos);
+          uint16_t* v16 = reinterpret_cast<uint16_t*>(vb);
           const uint16_t hi = f2bf(v);
-          st<COH>(v16, hi);
-          st<COH>(v16 + (size_t)d * p.kv_cap, f2bf(v - bf2f(hi)));
+          st<COH>(v16 + v_elem(rd.pos, 0, dd, d, true), hi);
+          st<COH>(v16 + v_elem(rd.pos, 1, dd, d, true), f2bf(v - bf2f(hi)));
         } else {
-          st<COH>(vb + (size_t)dd * p.kv_cap + rd.pos, v);
+          st<COH>(vb + v_elem(rd.pos, 0, dd, d, false), v);
         }
       }
     }
