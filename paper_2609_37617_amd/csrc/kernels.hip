@@ -339,16 +339,18 @@ __device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, 
       attn_store_span<D, RT>(p, rq, rows, sp, state);
       lds_sync();   // the LDS is written again next (a prefetch stays in flight)
     };
-    if constexpr (RT == 1) {   // two chunk buffers taken in turn (as in attn_prefill_kernel)
+    if constexpr (RT == 1) {
+      // two chunk buffers taken in turn, a buffer refilled right after its
+      // span's state is stored: the wait for a buffer's data (inserted by
+      // the compiler) then leaves the later span's stores in flight
       AttnRaw<BF, D> kb;
+      if (sp0 + 1 < sp1) attn_fetch<BF, D>(p, rq, g, sp0 + 1, kb);
       for (int sp = sp0; sp < sp1; sp += 2) {
-        wait_vmem_counted();
-        if (sp + 1 < sp1) attn_fetch<BF, D>(p, rq, g, sp + 1, kb);
         run(sp, ka);
-        if (sp + 1 >= sp1) break;
-        wait_vmem_counted();
         if (sp + 2 < sp1) attn_fetch<BF, D>(p, rq, g, sp + 2, ka);
+        if (sp + 1 >= sp1) break;
         run(sp + 1, kb);
+        if (sp + 3 < sp1) attn_fetch<BF, D>(p, rq, g, sp + 3, kb);
       }
     } else {   // two row tiles: one buffer (two would not fit the registers)
       for (int sp = sp0; sp < sp1; ++sp) {
