@@ -379,20 +379,24 @@ __device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, 
 }
 
 // Blocks of one row tile while each (span, KV head, block) can have a
-// workgroup of its own, else of two (half the reads of the keys and values
-// per row, runs of spans per workgroup); an attn_rt of 1 or 2 fixes it.
+// workgroup of its own, or while two-tile blocks would not cut the items by
+// a third (requests of few rows: the second tile would be padding); else
+// of two (half the reads of the keys and values per row, fewer runs of
+// spans per workgroup).  An attn_rt of 1 or 2 fixes it.
 template <bool BF, int D>
 __global__ __launch_bounds__(256) void attn_group_kernel(const AttnArgs p, int n_reqs) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   int rt = p.attn_rt;
   if (rt != 1 && rt != 2) {
     const int hpg = p.n_q / p.n_kv;
-    int n = 0;
+    int n1 = 0, n2 = 0;   // items with one-tile and two-tile blocks, one span each
     for (int r = 0; r < n_reqs; ++r) {
       const ReqDesc rq = load_invariant(p.reqs + r);
-      n += p.n_kv * ((hpg * rq.W + 15) / 16) * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
+      const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
+      n1 += p.n_kv * ((hpg * rq.W + 15) / 16) * ns;
+      n2 += p.n_kv * ((hpg * rq.W + 31) / 32) * ns;
     }
-    rt = n <= (int)gridDim.x ? 1 : 2;
+    rt = n1 <= (int)gridDim.x || 2 * n1 < 3 * n2 ? 1 : 2;
   }
   if (rt == 1) attn_group_items<BF, D, 1>(p, n_reqs, smem);
   else attn_group_items<BF, D, 2>(p, n_reqs, smem);
