@@ -119,7 +119,7 @@ struct as2d_ctx {
   void *pxg = nullptr, *pattn = nullptr, *ph = nullptr;
   int *psplit = nullptr, *pphase = nullptr, *perr = nullptr;
   int split_stride = 0;  // counters per (layer, GEMM)
-  int rg_grid = 448;     // staged GEMMs: least grid for row groups of 2-3 tiles
+  int rg_grid = 700;     // staged GEMMs: least grid for row groups of 2-3 tiles
   int n_phase = 0;
   std::map<int, StepLayer*> step_layers;  // by M: device array of per-layer arguments
   int cu_budget = 0;                      // as2d_set_cu_budget (0: all compute units)
@@ -1018,7 +1018,7 @@ int as2d_load_weights(const as2d_config* cfg, const void* const* host, int32_t n
   const int target = env_int("AS2D_TARGET_WGS", 256);
   const int ks_qkv = env_int("AS2D_KS_QKV", 0), ks_o = env_int("AS2D_KS_O", 0), ks_gu = env_int("AS2D_KS_GU", 0);
   const int ks_down = env_int("AS2D_KS_DOWN", 0), ks_lm = env_int("AS2D_KS_LM", 0);
-  c->rg_grid = env_int("AS2D_RG_GRID", 448);
+  c->rg_grid = env_int("AS2D_RG_GRID", 700);
   c->p_qkv = make_plan(qkv_n, H, KE, target, ks_qkv);
   c->p_o = make_plan(H, nq * d, KE, target, ks_o);
   c->p_gu = make_plan(2 * F, H, KE, target, ks_gu);

@@ -1,7 +1,8 @@
 """Prefill through the staged GEMMs gives the same bits whatever the row
 grouping: groups of 3 row tiles with two tile pairs per wave on every
-matrix, the default mix (3 tiles for gate/up, 2 for QKV, 1 for O and down),
-and single-tile groups everywhere.  Row grouping only changes which
+matrix, a mix of 3 tiles for gate/up, 2 for QKV and 1 for O and down, the
+default (3 tiles for gate/up, 1 elsewhere), and single-tile groups
+everywhere.  Row grouping only changes which
 workgroup computes which rows, never the order of a sum.  7B shape, two
 layers (the second layer's KV depends on every GEMM of the first), the
 782-row prefix (passes of 144 rows and one of 62); compares both layers'
@@ -15,9 +16,9 @@ from workload import QWEN7B, gen
 pytestmark = pytest.mark.gpu
 
 SHAPE = QWEN7B.with_layers(2)
-# least grid for row groups of 2-3 tiles: 0 -> always 3 tiles; 448 -> the
-# library's default; 1e5 -> always 1 tile
-SETTINGS = (0, 448, 100000)
+# least grid for row groups of 2-3 tiles: 0 -> always 3 tiles; 448 -> groups
+# of 2 for QKV; 700 -> the library's default; 1e5 -> always 1 tile
+SETTINGS = (0, 448, 700, 100000)
 
 
 @pytest.fixture(scope="module")
