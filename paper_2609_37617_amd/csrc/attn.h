@@ -216,8 +216,9 @@ template <bool BF> __device__ __forceinline__ uint4 keep_first(uint4 x, int n) {
 // rows: K rows up to the last key, V rows only for a chunk that starts at or
 // before it (the row stride is a multiple of 64, so such a chunk ends inside
 // the row).
+// The keys (attn_fetch_k) and the values (attn_fetch_v) of the chunk.
 template <bool BF, int D>
-__device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq, int g, int sp, AttnRaw<BF, D>& r) {
+__device__ __forceinline__ void attn_fetch_k(const AttnArgs& p, const ReqDesc& rq, int g, int sp, AttnRaw<BF, D>& r) {
   using F = AttnFmt<BF>;
   using Raw = AttnRaw<BF, D>;
   using T = typename ET<BF>::T;
@@ -227,7 +228,6 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
   const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
   const size_t head = (size_t)rq.slot * p.slot_stride + (size_t)g * p.kv_cap * D;   // float32 units
   const T* kb = reinterpret_cast<const T*>(p.k_cache + head);
-  const T* vb = reinterpret_cast<const T*>(p.v_cache + head);
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     const T* kr = kb + (size_t)min(kc + 16 * kt + lr, last) * F::PARTS * D + F::PER * lg;
@@ -237,6 +237,18 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
       r.k[kt][ks].l = BF ? ldg(reinterpret_cast<const uint4*>(kr + D + F::KE * ks)) : r.k[kt][ks].h;
     }
   }
+}
+template <bool BF, int D>
+__device__ __forceinline__ void attn_fetch_v(const AttnArgs& p, const ReqDesc& rq, int g, int sp, AttnRaw<BF, D>& r) {
+  using F = AttnFmt<BF>;
+  using Raw = AttnRaw<BF, D>;
+  using T = typename ET<BF>::T;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int lg = lane >> 4, lr = lane & 15;
+  const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;   // first key of the chunk
+  const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
+  const size_t head = (size_t)rq.slot * p.slot_stride + (size_t)g * p.kv_cap * D;   // float32 units
+  const T* vb = reinterpret_cast<const T*>(p.v_cache + head);
   if (kc > last) {   // no key of the chunk is in the request
 #pragma unroll
     for (int t = 0; t < Raw::DT; ++t)
@@ -262,6 +274,11 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
       }
     }
   }
+}
+template <bool BF, int D>
+__device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq, int g, int sp, AttnRaw<BF, D>& r) {
+  attn_fetch_k<BF, D>(p, rq, g, sp, r);
+  attn_fetch_v<BF, D>(p, rq, g, sp, r);
 }
 
 // The V operand of dimension tile t and k-step j as p v takes it: elements
@@ -326,10 +343,13 @@ __device__ __forceinline__ void attn_state_merge(AttnState<RT, DTW>& st, const f
 // synchronises the workgroup before it is written again).  Two steps:
 // attn_span_chunks (each wave's chunk sums into the LDS; q and raw are not
 // needed after it) and attn_merge_chunks.
-template <bool BF, int D, int RT>
+struct NoOp {
+  __device__ void operator()() const {}
+};
+template <bool BF, int D, int RT, class PreV = NoOp>
 __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDesc& rq, const AttnRows& rows, int sp,
                                                  const Op2 (&q)[RT][D / AttnFmt<BF>::KE], const AttnRaw<BF, D>& raw,
-                                                 unsigned char* smem) {
+                                                 unsigned char* smem, PreV pre_v = PreV{}) {
 #pragma clang fp contract(off)
   using Raw = AttnRaw<BF, D>;
   constexpr int KS = Raw::KS, DT = Raw::DT, DTW = D / 64, R = 16 * RT;
@@ -356,6 +376,7 @@ __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDes
       for (int i = 0; i < 4; ++i) s[rt][kt][i] = kc + 16 * kt + 4 * lg + i <= pos ? acc[i] * p.scale : -INFINITY;
     }
   }
+  pre_v();   // a caller that fetches the values only now (the keys' registers are free)
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     float mx = s[rt][0][0];

@@ -287,9 +287,12 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 
 constexpr int kAttnGrid = 256;   // workgroups of the span kernel (one per compute unit: its LDS allows no more)
 
-// The items of a launch with blocks of RT row tiles.
-template <bool BF, int D, int RT>
+// The items of a launch with blocks of RT row tiles.  LOWREG (RT = 1): a
+// workgroup within half the register file (two per compute unit), one span
+// buffer, the values fetched once the span's scores are formed.
+template <bool BF, int D, int RT, bool LOWREG = false>
 __device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, unsigned char* smem) {
+  static_assert(!LOWREG || RT == 1, "one row tile");
   constexpr int KS = D / AttnFmt<BF>::KE;
   constexpr int BR = 16 * RT;   // rows of a block
   const int G = gridDim.x;
@@ -330,7 +333,8 @@ __device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, 
     const int sp0 = j * R, sp1 = min(sp0 + R, ns);
     // the first span's keys and values, then the queries, all in flight at once
     AttnRaw<BF, D> ka;
-    attn_fetch<BF, D>(p, rq, g, sp0, ka);
+    if constexpr (LOWREG) attn_fetch_k<BF, D>(p, rq, g, sp0, ka);
+    else attn_fetch<BF, D>(p, rq, g, sp0, ka);
     Op2 q[RT][KS];
     attn_load_q<BF, D, RT>(p, rq, rows, q);
     auto run = [&](int sp, const AttnRaw<BF, D>& raw) {
@@ -339,7 +343,16 @@ __device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, 
       attn_store_span<D, RT>(p, rq, rows, sp, state);
       lds_sync();   // the LDS is written again next (a prefetch stays in flight)
     };
-    if constexpr (RT == 1) {
+    if constexpr (LOWREG) {
+      for (int sp = sp0; sp < sp1; ++sp) {
+        if (sp > sp0) attn_fetch_k<BF, D>(p, rq, g, sp, ka);
+        AttnState<1, D / 64> state;
+        attn_span_chunks<BF, D, 1>(p, rq, rows, sp, q, ka, smem, [&] { attn_fetch_v<BF, D>(p, rq, g, sp, ka); });
+        attn_merge_chunks<BF, D, 1>(smem, state);
+        attn_store_span<D, 1>(p, rq, rows, sp, state);
+        lds_sync();   // the LDS is written again next
+      }
+    } else if constexpr (RT == 1) {
       // two chunk buffers taken in turn, a buffer refilled right after its
       // span's state is stored: the wait for a buffer's data (inserted by
       // the compiler) then leaves the later span's stores in flight
@@ -400,6 +413,14 @@ __global__ __launch_bounds__(256) void attn_group_kernel(const AttnArgs p, int n
   }
   if (rt == 1) attn_group_items<BF, D, 1>(p, n_reqs, smem);
   else attn_group_items<BF, D, 2>(p, n_reqs, smem);
+}
+
+// Slots whose one-tile items outnumber the compute units: one-tile blocks
+// on two workgroups per compute unit, each overlapping the other's waits.
+template <bool BF, int D>
+__global__ __launch_bounds__(256, 2) void attn_group2_kernel(const AttnArgs p, int n_reqs) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  attn_group_items<BF, D, 1, true>(p, n_reqs, smem);
 }
 
 // One wave per (request row, query head), heads of a row adjacent.
@@ -488,8 +509,13 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_blocks, b
   const int hpg = a.n_q / a.n_kv;
   const long long rows = (long long)hpg * (a.M - n_reqs + 1);
   const long long items = (long long)n_reqs * a.n_kv * ((rows + 15) / 16) * ((max_blocks + kAttnSpan - 1) / kAttnSpan);
-  const int grid = (int)std::min<long long>(kAttnGrid, (items + 7) / 8 * 8);
-  attn_group_kernel<BF, D><<<grid, 256, attn_span_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
+  if (items > kAttnGrid && a.attn_rt == 0) {
+    const int grid2 = (int)std::min<long long>(2 * kAttnGrid, (items + 7) / 8 * 8);
+    attn_group2_kernel<BF, D><<<grid2, 256, attn_span_lds_bytes<BF, D, 1>(), s>>>(a, n_reqs);
+  } else {
+    const int grid = (int)std::min<long long>(kAttnGrid, (items + 7) / 8 * 8);
+    attn_group_kernel<BF, D><<<grid, 256, attn_span_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
+  }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.merge_last) return e;
   attn_merge_kernel<BF, D><<<a.M * a.n_q, 64, 0, s>>>(a, n_reqs);
