@@ -344,10 +344,14 @@ __device__ __forceinline__ void attn_group_items(const AttnArgs& p, int n_reqs, 
       lds_sync();   // the LDS is written again next (a prefetch stays in flight)
     };
     if constexpr (LOWREG) {
+      // once a span's scores are formed its keys' registers take the next
+      // span's keys, requested right after the span's values
       for (int sp = sp0; sp < sp1; ++sp) {
-        if (sp > sp0) attn_fetch_k<BF, D>(p, rq, g, sp, ka);
         AttnState<1, D / 64> state;
-        attn_span_chunks<BF, D, 1>(p, rq, rows, sp, q, ka, smem, [&] { attn_fetch_v<BF, D>(p, rq, g, sp, ka); });
+        attn_span_chunks<BF, D, 1>(p, rq, rows, sp, q, ka, smem, [&] {
+          attn_fetch_v<BF, D>(p, rq, g, sp, ka);
+          if (sp + 1 < sp1) attn_fetch_k<BF, D>(p, rq, g, sp + 1, ka);
+        });
         attn_merge_chunks<BF, D, 1>(smem, state);
         attn_store_span<D, 1>(p, rq, rows, sp, state);
         lds_sync();   // the LDS is written again next
