@@ -224,10 +224,12 @@ int as2d_read_kv(as2d_ctx* ctx, int32_t req, int32_t layer, void* host_k, void* 
  * as2d_load_weights refuses one the same way.  Results do not depend on
  * the stream. */
 int as2d_set_stream(as2d_ctx* ctx, void* hip_stream);
-/* Size the balanced GEMM grids (and the persistent kernel's) for `cus`
- * compute units (1 .. the device's; 0 restores all of them): each such
- * GEMM then runs cus workgroups of one CU each, leaving the other CUs to
- * work on other streams (a drafter beside the target).  A GEMM with more
+/* Size the balanced GEMM grids (and the persistent kernel's and the
+ * verification attention's) for `cus` compute units (1 .. the device's;
+ * 0 restores all of them): each such GEMM then runs cus workgroups of one
+ * CU each, and the attention at most cus (two per CU for long caches),
+ * leaving the other CUs to work on other streams (a drafter beside the
+ * target); prefill kernels still size their grids by the rows.  A GEMM with more
  * than 24 (tile pair, k-split) units per workgroup at that grid keeps the
  * grid that gives it 24; if one does, the persistent kernel (one
  * workgroup per budgeted CU) is not used and as2d_get_exec_info reports

@@ -123,6 +123,7 @@ struct as2d_ctx {
   int n_phase = 0;
   std::map<int, StepLayer*> step_layers;  // by M: device array of per-layer arguments
   int cu_budget = 0;                      // as2d_set_cu_budget (0: all compute units)
+  int grid_cus = 0;                       // compute units the grids are sized for
   int h_err = 0;
   long long* ptrace = nullptr;  // persistent-kernel timeline (as2d_set_step_trace)
   int trace_on = 0;
@@ -408,6 +409,7 @@ int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int
       a.out_plane = B.attn_plane;
       a.M = M;
       a.attn_rt = c->attn_rt;
+      a.cus = c->grid_cus;
       Timed t(c, K_ATTN);
       HIP_TRY(c, launch_attention(bf, a, n_att, max_blocks, prefill, s));
     }
@@ -763,6 +765,7 @@ int set_grids(as2d_ctx* c, int cus) {
   HIP_TRY(c, hipGetDevice(&dev));
   HIP_TRY(c, hipDeviceGetAttribute(&dev_cus, hipDeviceAttributeMultiprocessorCount, dev));
   const int n = cus > 0 ? std::min(cus, dev_cus) : dev_cus;
+  c->grid_cus = n;
   // a plan whose units would exceed kMaxUnits per workgroup on n keeps a
   // wider grid; the persistent kernel, one workgroup per CU of the budget,
   // then cannot hold that phase and verification passes use graphs

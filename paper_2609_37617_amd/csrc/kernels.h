@@ -156,7 +156,8 @@ struct AttnArgs {
   void* out;             // planes [kMaxRows][n_q*d]
   long long out_plane;
   int M;
-  int attn_rt;           // row tiles per block of the verification kernel (0: chosen from M)
+  int attn_rt;           // row tiles per block of the verification kernel (0: chosen per launch)
+  int cus;               // compute units the verification kernels may fill (the CU budget)
 };
 
 // Persistent step kernel (step.hip): one verification pass of up to 32 rows.

@@ -285,7 +285,7 @@ hipError_t launch_gemm(bool bf16, int amode, int epi, const GemmArgs& a, hipStre
 // head, 16 rows) walks the spans in ascending order and merges them as it
 // goes, with the same arithmetic, so no partials go through memory.
 
-constexpr int kAttnGrid = 256;   // workgroups of the span kernel (one per compute unit: its LDS allows no more)
+constexpr int kAttnGrid = 256;   // compute units the span kernels fill at most (attn_group_kernel: one workgroup each)
 
 // The items of a launch with blocks of RT row tiles.  LOWREG (RT = 1): a
 // workgroup within half the register file (two per compute unit), one span
@@ -513,11 +513,12 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_blocks, b
   const int hpg = a.n_q / a.n_kv;
   const long long rows = (long long)hpg * (a.M - n_reqs + 1);
   const long long items = (long long)n_reqs * a.n_kv * ((rows + 15) / 16) * ((max_blocks + kAttnSpan - 1) / kAttnSpan);
-  if (items > kAttnGrid && a.attn_rt == 0) {
-    const int grid2 = (int)std::min<long long>(2 * kAttnGrid, (items + 7) / 8 * 8);
+  const int cus = a.cus > 0 ? std::min(a.cus, kAttnGrid) : kAttnGrid;
+  if (items > cus && a.attn_rt == 0) {
+    const int grid2 = (int)std::min<long long>(2 * cus, (items + 7) / 8 * 8);
     attn_group2_kernel<BF, D><<<grid2, 256, attn_span_lds_bytes<BF, D, 1>(), s>>>(a, n_reqs);
   } else {
-    const int grid = (int)std::min<long long>(kAttnGrid, (items + 7) / 8 * 8);
+    const int grid = (int)std::min<long long>(cus, (items + 7) / 8 * 8);
     attn_group_kernel<BF, D><<<grid, 256, attn_span_lds_bytes<BF, D, 2>(), s>>>(a, n_reqs);
   }
   const hipError_t e = hipGetLastError();
