@@ -151,7 +151,9 @@ struct AttnArgs {
   float* pacc;           // span states [row][n_q][part_spans][d]
   float* pml;            // [row][n_q][part_spans][2]: running maximum and sum
   int part_spans;        // spans per (row, head) in the state arrays
-  int* attn_cnt;         // merge_last: finished spans per (request, KV head, block of 2 heads' rows), zero between launches
+  int* attn_cnt;         // merge_last: finished spans per (request, KV head, row block), zero between
+                         // launches; [request][KV head][2 n_q / n_kv]: a request has at most 32 rows
+                         // (max_k <= 31), so a KV head's rows fill at most that many 16-row blocks
   int merge_last;        // 1: the last item of a block merges its rows (no merge kernel)
   void* out;             // planes [kMaxRows][n_q*d]
   long long out_plane;
