@@ -597,6 +597,7 @@ int launch_persistent(as2d_ctx* c, int M, int n_att, int n_fin, int fin_rows) {
   a.reqs = c->b.d_reqs;
   a.n_reqs = n_att;
   a.n_q = g.n_q_heads;
+  a.n_kv = g.n_kv_heads;
   a.fin_reqs = c->b.d_reqs + g.max_requests;
   a.n_fin = n_fin;
   a.fin_rows = fin_rows;

@@ -184,7 +184,7 @@ struct StepArgs {
   long long xg0_plane;
   const ReqDesc* reqs;       // attention requests
   int n_reqs;
-  int n_q;
+  int n_q, n_kv;
   const ReqDesc* fin_reqs;   // verified requests and their rows
   int n_fin;
   int fin_rows;

@@ -119,10 +119,13 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
 
   stamp(a, 0, 2);
   // attention items of this pass: (request, 128-key span, query head)
+  // attention items: (request, span, KV head, 16-row block of the rows of
+  // the query heads that share the KV head), as in the per-operation kernel
+  const int hpg = a.n_q / a.n_kv;
   int n_items = 0;
   for (int r = 0; r < a.n_reqs; ++r) {
     const ReqDesc rq = load_invariant(a.reqs + r);
-    n_items += a.n_q * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
+    n_items += a.n_kv * ((hpg * rq.W + 15) / 16) * ((rq.L0 + rq.W - 1) / kAttnSpanKeys + 1);
   }
   constexpr int KS = D / AttnFmt<BF>::KE;
   const int quarter = tid >> 4;
@@ -134,8 +137,8 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
     gemm_phase<BF, MT, SL, A_NORM, EPI_QKV>(load_invariant(&ly->qkv), M, prev, prev_target, &a.phase_cnt[ph_layer(l, 0)], a, smem,
                                              s_scale, s_flags);
 
-    // attention spans: the items of the per-operation kernel, dealt
-    // round-robin; each stores its span state
+    // attention spans, dealt round-robin; each item stores its rows' span
+    // states
     stamp(a, ph_layer(l, 1), 0);
     if ((int)blockIdx.x < n_items) {
       wait_count(&a.phase_cnt[ph_layer(l, 0)], a.done_qkv, a.err, a.spin_limit);
@@ -143,21 +146,24 @@ __global__ __launch_bounds__(256, 1) void step_kernel(const StepArgs a) {
       const AttnArgs at = load_invariant(&ly->attn);
       int mine = 0;
       for (int t = blockIdx.x; t < n_items; t += G) {
-        int r = 0, u = t, ns = 0;
+        int r = 0, u = t, ns = 0, nb = 0;
         ReqDesc rq;
         for (;; ++r) {
           rq = load_invariant(a.reqs + r);
           ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
-          if (u < a.n_q * ns || r == a.n_reqs - 1) break;
-          u -= a.n_q * ns;
+          nb = (hpg * rq.W + 15) / 16;
+          if (u < a.n_kv * nb * ns || r == a.n_reqs - 1) break;
+          u -= a.n_kv * nb * ns;
         }
-        const int sp = u / a.n_q, h = u - sp * a.n_q;
-        const AttnRows rows = attn_rows_of_head(h, rq.W);
-        Op2 q[2][KS];
-        attn_load_q<BF, D, 2>(at, rq, rows, q);
-        AttnState<2, D / 64> sst;
-        attn_span<BF, D, 2>(at, rq, rows, sp, q, smem, sst);
-        attn_store_span<D, 2>(at, rq, rows, sp, sst);
+        const int sp = u / (a.n_kv * nb);
+        const int v = u - sp * a.n_kv * nb;
+        const int g = v / nb, b = v - g * nb;
+        const AttnRows rows{g * hpg, rq.W, hpg * rq.W, 16 * b};
+        Op2 q[1][KS];
+        attn_load_q<BF, D, 1>(at, rq, rows, q);
+        AttnState<1, D / 64> sst;
+        attn_span<BF, D, 1>(at, rq, rows, sp, q, smem, sst);
+        attn_store_span<D, 1>(at, rq, rows, sp, sst);
         lds_sync();   // the next item writes the LDS again
         ++mine;
       }
