@@ -346,6 +346,10 @@ GemmArgs base_args(as2d_ctx* c, const GemmPlan& pl, const uint4* W, int M, const
   return a;
 }
 
+// Attention score scale: log2(e) / sqrt(d), rounded once to float32 (the
+// kernels take base-2 exponentials of the scores).
+float attn_scale(int d) { return (float)(1.4426950408889634 / std::sqrt((double)d)); }
+
 // Kernel launches of one forward pass over the rows and requests in the
 // device descriptors: n_att attention requests (d_reqs[0..n_att)), n_fin
 // finish requests (d_reqs[max_requests..)) covering fin_rows rows;
@@ -398,7 +402,7 @@ int launch_pass(as2d_ctx* c, const PassBufs& B, int M, int n_att, int n_fin, int
       a.n_q = g.n_q_heads;
       a.n_kv = g.n_kv_heads;
       a.head_dim = d;
-      a.scale = 1.0f / std::sqrt((float)d);
+      a.scale = attn_scale(d);
       a.pacc = B.pacc;
       a.pml = B.pml;
       a.part_spans = B.part_spans;
@@ -518,7 +522,7 @@ StepLayer* step_layers_for(as2d_ctx* c, int M) {
     a.n_q = nq;
     a.n_kv = nkv;
     a.head_dim = d;
-    a.scale = 1.0f / std::sqrt((float)d);
+    a.scale = attn_scale(d);
     a.pacc = c->b.pacc;
     a.pml = c->b.pml;
     a.part_spans = c->b.part_spans;

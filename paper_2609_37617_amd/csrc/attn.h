@@ -10,9 +10,12 @@
 //   s_j   = (q . k_j) * scale, a matrix-core product: for bf16 models q and
 //           k are split into bf16 pairs (hi = bf16(x), lo = bf16(x - hi))
 //           and s = q_hi k_hi + q_hi k_lo + q_lo k_hi over 32-wide k-steps;
-//           float32 models use float32 products;
+//           float32 models use float32 products; scale = log2(e) / sqrt(d)
+//           (rounded once to float32), so scores are in base-2 units;
 //   m_c   = max_j s_j over the chunk;
-//   p_j   = exp(s_j - m_c), 0 for keys after pos;
+//   p_j   = 2^(s_j - m_c), 0 for keys after pos (the hardware base-2
+//           exponential, exp2 below: the same softmax as exp of the
+//           natural-unit scores);
 //   l_c   = sum_j p_j: a lane's keys of each 16-key tile in order, the two
 //           tiles in order, then across lanes in a fixed butterfly;
 //   acc_c = sum_j p_j v_j, a matrix-core product of the (hi, lo) splits of
@@ -23,7 +26,7 @@
 // keys 4q .. 4q + 3 of the chunk's first tile and of its second tile, and v
 // is read in that order).
 // Merging a partial (m, l, acc) into a running state (M, L, A):
-//   M' = max(M, m), a = exp(M - M'), c = exp(m - M'),
+//   M' = max(M, m), a = exp2(M - M'), c = exp2(m - M'),
 //   L = fma(L, a, l c), A = fma(A, a, acc c), M = M'.
 // Two levels: the four chunks of a span are merged in ascending order,
 // starting from the first; the spans' states are then merged in ascending
@@ -40,6 +43,9 @@
 namespace as2d {
 
 constexpr int kAttnChunk = kAttnSpanKeys / kWaves;   // keys of one wave's chunk of a span
+
+// 2^x by the hardware instruction (0 for x = -inf).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 template <bool BF> struct AttnFmt {
   static constexpr int PER = BF ? 8 : 4;                  // elements per lane per k-step
@@ -130,7 +136,7 @@ struct MergeCoef {
 __device__ __forceinline__ MergeCoef attn_merge_coef(float& M, float& L, float m, float l) {
 #pragma clang fp contract(off)
   const float Mn = fmaxf(M, m);
-  const MergeCoef k{expf(M - Mn), expf(m - Mn)};
+  const MergeCoef k{exp2_hw(M - Mn), exp2_hw(m - Mn)};
   L = __builtin_fmaf(L, k.a, l * k.c);
   M = Mn;
   return k;
@@ -388,7 +394,7 @@ __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDes
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pj[kt][i] = mx == -INFINITY ? 0.0f : expf(s[rt][kt][i] - mx);
+      for (int i = 0; i < 4; ++i) pj[kt][i] = mx == -INFINITY ? 0.0f : exp2_hw(s[rt][kt][i] - mx);
     float sm = (((pj[0][0] + pj[0][1]) + pj[0][2]) + pj[0][3]) + (((pj[1][0] + pj[1][1]) + pj[1][2]) + pj[1][3]);
     sm = swap_combine<false>(sm, FAdd{});
     sm = swap_combine<true>(sm, FAdd{});
@@ -628,7 +634,7 @@ __device__ __forceinline__ void attn_merge_wave(const AttnArgs& p, const ReqDesc
     mx = fmaxf(M, mx);
     float mb = __shfl_up(mx, 1, kB);
     if (bl == 0) mb = M;
-    const float ca = expf(mb - mx), cc = expf(b.m - mx);
+    const float ca = exp2_hw(mb - mx), cc = exp2_hw(b.m - mx);
 #pragma unroll
     for (int u = 0; u < kB; ++u) {
       if (s0 + u < ns) {

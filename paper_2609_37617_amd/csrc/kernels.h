@@ -147,7 +147,7 @@ struct AttnArgs {
   const RowDesc* rows;
   const ReqDesc* reqs;
   int n_q, n_kv, head_dim;
-  float scale;
+  float scale;           // log2(e) / sqrt(head_dim): scores in base-2 units
   float* pacc;           // span states [row][n_q][part_spans][d]
   float* pml;            // [row][n_q][part_spans][2]: running maximum and sum
   int part_spans;        // spans per (row, head) in the state arrays
