@@ -55,6 +55,10 @@ template <bool BF> struct AttnFmt {
 };
 static_assert(kAttnChunk == 32, "two 16-key tiles per chunk");
 
+// Wave of a span group: four waves take a span's four chunks (a workgroup
+// of eight waves runs two spans at once, one per group of four).
+__device__ __forceinline__ int attn_wave() { return (threadIdx.x >> 6) & (kWaves - 1); }
+
 // LDS of one span for RT row tiles: every wave's chunk sums acc_c
 // [wave][rt][dimension tile][lane] (16 bytes per lane) and chunk statistics
 // m_c, l_c [wave][16 RT] each.
@@ -228,7 +232,7 @@ __device__ __forceinline__ void attn_fetch_k(const AttnArgs& p, const ReqDesc& r
   using F = AttnFmt<BF>;
   using Raw = AttnRaw<BF, D>;
   using T = typename ET<BF>::T;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = attn_wave(), lane = threadIdx.x & 63;
   const int lg = lane >> 4, lr = lane & 15;
   const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;   // first key of the chunk
   const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
@@ -249,7 +253,7 @@ __device__ __forceinline__ void attn_fetch_v(const AttnArgs& p, const ReqDesc& r
   using F = AttnFmt<BF>;
   using Raw = AttnRaw<BF, D>;
   using T = typename ET<BF>::T;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = attn_wave(), lane = threadIdx.x & 63;
   const int lg = lane >> 4, lr = lane & 15;
   const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;   // first key of the chunk
   const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
@@ -344,7 +348,8 @@ __device__ __forceinline__ void attn_state_merge(AttnState<RT, DTW>& st, const f
 // this wave's chunk of keys and values in raw), in the layout of AttnState:
 // for lane l and i < 4, block row 16 rt + 4 (l / 16) + i, dimensions
 // 16 (w DTW + t) + l % 16.  Rows whose position is before the span's first
-// key get no meaningful state (they are never stored or merged).  256 threads, 4 waves;
+// key get no meaningful state (they are never stored or merged).  Four waves
+// (a span group, attn_wave);
 // smem: attn_span_lds_bytes<BF, D, RT>(), not in use on entry (the caller
 // synchronises the workgroup before it is written again).  Two steps:
 // attn_span_chunks (each wave's chunk sums into the LDS; q and raw are not
@@ -359,7 +364,7 @@ __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDes
 #pragma clang fp contract(off)
   using Raw = AttnRaw<BF, D>;
   constexpr int KS = Raw::KS, DT = Raw::DT, DTW = D / 64, R = 16 * RT;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wave = attn_wave(), lane = threadIdx.x & 63;
   const int lg = lane >> 4, lr = lane & 15;
   const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;
   const int last = rq.L0 + rq.W - 1;   // last key of the request in this pass
@@ -436,7 +441,7 @@ template <bool BF, int D, int RT>
 __device__ __forceinline__ void attn_merge_chunks(unsigned char* smem, AttnState<RT, D / 64>& st) {
 #pragma clang fp contract(off)
   constexpr int DT = D / 16, DTW = D / 64, R = 16 * RT;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, lg = lane >> 4;
+  const int wave = attn_wave(), lane = threadIdx.x & 63, lg = lane >> 4;
   const f4* SA = reinterpret_cast<const f4*>(smem);                          // [wave][rt][t][lane]
   const float* SM = reinterpret_cast<const float*>(SA + kWaves * RT * DT * 64);   // [wave][R]
   const float* SL = SM + kWaves * R;                                              // [wave][R]

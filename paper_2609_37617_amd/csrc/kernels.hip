@@ -442,60 +442,89 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(const AttnArgs p, int n_
   attn_merge_wave<BF, D>(p, rq, i, u - i * p.n_q);
 }
 
-constexpr int kAttnPrefillRT = 1;   // row tiles per prefill workgroup
+// Prefill attention: one workgroup per (query head, 16-row tile) runs
+// the tile's spans two at a time with eight waves, group 0 (waves 0-3) on
+// spans 0, 2, 4, ..., group 1 on spans 1, 3, 5, ...,
+// each group on its own LDS span buffer and with one chunk buffer in
+// registers (a span's keys give way to the next span's once its scores
+// are formed), so that two waves share each SIMD.  The running state
+// stays in group 0, which merges the spans in order: its own span, then
+// group 1's state handed over through the LDS; the same arithmetic as one
+// span at a time.  Group 1 runs the last span again when the count is odd
+// (its state is not merged) so that both groups reach the same barriers.
+template <bool BF, int D> __host__ __device__ constexpr int attn_prefill_lds_bytes() {
+  return 2 * attn_span_lds_bytes<BF, D, 1>() + kWaves * (2 + D / 64) * 64 * 16;
+}
 
 template <bool BF, int D>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(const AttnArgs p) {
+__global__ __launch_bounds__(512) void attn_prefill_kernel(const AttnArgs p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  constexpr int RT = kAttnPrefillRT;   // one row tile: two chunk buffers stay in registers
   constexpr int KS = D / AttnFmt<BF>::KE;
   constexpr int DTW = D / 64;
-  const int h = blockIdx.x, r0 = blockIdx.y * 16 * RT;
+  const int h = blockIdx.x, r0 = blockIdx.y * 16;
   const ReqDesc full = load_invariant(p.reqs);
   if (r0 >= full.W) return;
-  // this workgroup's rows as a request of their own: same positions
-  const ReqDesc rq{full.row_start + r0, min(full.W - r0, 16 * RT), full.L0 + r0, full.slot};
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const ReqDesc rq{full.row_start + r0, min(full.W - r0, 16), full.L0 + r0, full.slot};
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 8, wave = attn_wave();
+  unsigned char* mine = smem + grp * attn_span_lds_bytes<BF, D, 1>();
+  // group 1's span state for group 0: [wave][M, L, A tiles][lane]
+  f4* X = reinterpret_cast<f4*>(smem + 2 * attn_span_lds_bytes<BF, D, 1>()) + wave * (2 + DTW) * 64 + lane;
   const AttnRows rows = attn_rows_of_head(h, rq.W);
   const int g = attn_kv_head(p, rows);
-  Op2 q[RT][KS];
-  attn_load_q<BF, D, RT>(p, rq, rows, q);
-  AttnState<RT, DTW> all;
   const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
-  // two chunk buffers taken in turn: span sp + 1 is requested before span sp runs
-  AttnRaw<BF, D> ka, kb;
-  attn_fetch<BF, D>(p, rq, g, 0, ka);
-  auto run = [&](int sp, const AttnRaw<BF, D>& raw) {
-    AttnState<RT, DTW> state;
-    attn_span_state<BF, D, RT>(p, rq, rows, sp, q, raw, smem, state);
-    attn_state_merge<RT, DTW>(all, state.M, state.L, state.A, sp == 0, [&](int rt, int i) {
-      return rq.L0 + min(16 * rt + 4 * (lane >> 4) + i, rq.W - 1) >= sp * kAttnSpanKeys;
-    });
-    lds_sync();   // the next span writes the LDS again (the prefetch stays in flight)
+  const auto span_of = [&](int j) { return min(j + grp, ns - 1); };
+  AttnRaw<BF, D> raw;
+  attn_fetch_k<BF, D>(p, rq, g, span_of(0), raw);
+  Op2 q[1][KS];
+  attn_load_q<BF, D, 1>(p, rq, rows, q);
+  AttnState<1, DTW> all;
+  const auto take = [&](int sp) {
+    return [&, sp](int, int i) { return rq.L0 + min(4 * (lane >> 4) + i, rq.W - 1) >= sp * kAttnSpanKeys; };
   };
-  // (each buffer's reads complete before the other's are issued: 32 reads
-  // per lane and span, so two spans would exceed what the wave can count)
-  for (int sp = 0; sp < ns; sp += 2) {
-    wait_vmem_counted();
-    if (sp + 1 < ns) attn_fetch<BF, D>(p, rq, g, sp + 1, kb);
-    run(sp, ka);
-    if (sp + 1 >= ns) break;
-    wait_vmem_counted();
-    if (sp + 2 < ns) attn_fetch<BF, D>(p, rq, g, sp + 2, ka);
-    run(sp + 1, kb);
-  }
+  for (int j = 0; j < ns; j += 2) {
+    const int sp = span_of(j);
+    AttnState<1, DTW> st;
+    attn_span_chunks<BF, D, 1>(p, rq, rows, sp, q, raw, mine, [&] {
+      attn_fetch_v<BF, D>(p, rq, g, sp, raw);
+      if (j + 2 < ns) attn_fetch_k<BF, D>(p, rq, g, span_of(j + 2), raw);
+    });
+    attn_merge_chunks<BF, D, 1>(mine, st);
+    if (grp) {
+      X[0] = f4{st.M[0][0], st.M[0][1], st.M[0][2], st.M[0][3]};
+      X[64] = f4{st.L[0][0], st.L[0][1], st.L[0][2], st.L[0][3]};
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 16 * rt + 4 * (lane >> 4) + i;
-      if (r < rq.W)
-#pragma unroll
-        for (int t = 0; t < DTW; ++t)
-          store_act<BF, false>(p.out, p.out_plane,
-                               frag_index<BF>(rq.row_start + r, h * D + 16 * (wave * DTW + t) + (lane & 15), p.n_q * D),
-                               all.A[rt][t][i] / all.L[rt][i]);
+      for (int t = 0; t < DTW; ++t) X[(2 + t) * 64] = f4{st.A[0][t][0], st.A[0][t][1], st.A[0][t][2], st.A[0][t][3]};
+    } else {
+      attn_state_merge<1, DTW>(all, st.M, st.L, st.A, j == 0, take(j));
     }
+    lds_sync();   // group 1's state is in the LDS; the span buffers are free
+    if (!grp && j + 1 < ns) {
+      const f4 m = X[0], l = X[64];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        st.M[0][i] = m[i];
+        st.L[0][i] = l[i];
+      }
+#pragma unroll
+      for (int t = 0; t < DTW; ++t) {
+        const f4 a = X[(2 + t) * 64];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st.A[0][t][i] = a[i];
+      }
+      attn_state_merge<1, DTW>(all, st.M, st.L, st.A, false, take(j + 1));
+    }
+  }
+  if (grp) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * (lane >> 4) + i;
+    if (r < rq.W)
+#pragma unroll
+      for (int t = 0; t < DTW; ++t)
+        store_act<BF, false>(p.out, p.out_plane,
+                             frag_index<BF>(rq.row_start + r, h * D + 16 * (wave * DTW + t) + (lane & 15), p.n_q * D),
+                             all.A[0][t][i] / all.L[0][i]);
+  }
 }
 
 template <bool BF, int D>
@@ -503,8 +532,7 @@ static hipError_t attn_dispatch(const AttnArgs& a, int n_reqs, int max_blocks, b
   if (max_blocks > kMaxBlocks || n_reqs < 1) return hipErrorInvalidValue;
   if (prefill) {
     if (n_reqs != 1) return hipErrorInvalidValue;
-    constexpr int R = 16 * kAttnPrefillRT;
-    attn_prefill_kernel<BF, D><<<dim3(a.n_q, (a.M + R - 1) / R), 256, attn_span_lds_bytes<BF, D, kAttnPrefillRT>(), s>>>(a);
+    attn_prefill_kernel<BF, D><<<dim3(a.n_q, (a.M + 15) / 16), 512, attn_prefill_lds_bytes<BF, D>(), s>>>(a);
     return hipGetLastError();
   }
   // items of one-tile blocks at the slot capacity, from the most rows a
@@ -556,13 +584,14 @@ static hipError_t prepare_staged() {
 }
 
 // Attention kernels: two row tiles of 128 dimensions exchange 64 KiB of
-// chunk sums plus their statistics.
+// chunk sums plus their statistics; the prefill kernel's two span groups
+// 81 KiB with the handed-over states.
 template <bool BF, int D>
 static hipError_t prepare_attention() {
   auto allow = [](const void* k, int bytes) { return hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, bytes); };
   hipError_t e = allow(reinterpret_cast<const void*>(&attn_group_kernel<BF, D>), attn_span_lds_bytes<BF, D, 2>());
   if (e == hipSuccess)
-    e = allow(reinterpret_cast<const void*>(&attn_prefill_kernel<BF, D>), attn_span_lds_bytes<BF, D, kAttnPrefillRT>());
+    e = allow(reinterpret_cast<const void*>(&attn_prefill_kernel<BF, D>), attn_prefill_lds_bytes<BF, D>());
   return e;
 }
 
