@@ -446,8 +446,9 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(const AttnArgs p, int n_
 // the tile's spans two at a time with eight waves, group 0 (waves 0-3) on
 // spans 0, 2, 4, ..., group 1 on spans 1, 3, 5, ...,
 // each group on its own LDS span buffer and with one chunk buffer in
-// registers (a span's keys give way to the next span's once its scores
-// are formed), so that two waves share each SIMD.  The running state
+// registers (a span's keys give way to the group's next span's keys once
+// its scores are formed, its values to the next values once its products
+// are), so that two waves share each SIMD.  The running state
 // stays in group 0, which merges the spans in order: its own span, then
 // group 1's state handed over through the LDS; the same arithmetic as one
 // span at a time.  Group 1 runs the last span again when the count is odd
@@ -474,7 +475,7 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(const AttnArgs p) {
   const int ns = (rq.L0 + rq.W - 1) / kAttnSpanKeys + 1;
   const auto span_of = [&](int j) { return min(j + grp, ns - 1); };
   AttnRaw<BF, D> raw;
-  attn_fetch_k<BF, D>(p, rq, g, span_of(0), raw);
+  attn_fetch<BF, D>(p, rq, g, span_of(0), raw);
   Op2 q[1][KS];
   attn_load_q<BF, D, 1>(p, rq, rows, q);
   AttnState<1, DTW> all;
@@ -485,9 +486,9 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(const AttnArgs p) {
     const int sp = span_of(j);
     AttnState<1, DTW> st;
     attn_span_chunks<BF, D, 1>(p, rq, rows, sp, q, raw, mine, [&] {
-      attn_fetch_v<BF, D>(p, rq, g, sp, raw);
       if (j + 2 < ns) attn_fetch_k<BF, D>(p, rq, g, span_of(j + 2), raw);
     });
+    if (j + 2 < ns) attn_fetch_v<BF, D>(p, rq, g, span_of(j + 2), raw);
     attn_merge_chunks<BF, D, 1>(mine, st);
     if (grp) {
       X[0] = f4{st.M[0][0], st.M[0][1], st.M[0][2], st.M[0][3]};
