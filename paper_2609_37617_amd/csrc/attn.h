@@ -57,7 +57,7 @@ static_assert(kAttnChunk == 32, "two 16-key tiles per chunk");
 
 // Wave of a span group: four waves take a span's four chunks (a workgroup
 // of eight waves runs two spans at once, one per group of four).
-__device__ __forceinline__ int attn_wave() { return (threadIdx.x >> 6) & (kWaves - 1); }
+__device__ __forceinline__ int attn_wave() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & (kWaves - 1); }
 
 // LDS of one span for RT row tiles: every wave's chunk sums acc_c
 // [wave][rt][dimension tile][lane] (16 bytes per lane) and chunk statistics
@@ -368,6 +368,9 @@ __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDes
   const int lg = lane >> 4, lr = lane & 15;
   const int kc = sp * kAttnSpanKeys + kAttnChunk * wave;
   const int last = rq.L0 + rq.W - 1;   // last key of the request in this pass
+  // every key of the chunk is in the request (wave-uniform): p v takes the
+  // values as loaded, without the masking path's copies
+  const bool whole = kc + kAttnChunk <= last + 1;
   f4* SA = reinterpret_cast<f4*>(smem);                                 // [wave][rt][t][lane]
   float* SM = reinterpret_cast<float*>(SA + kWaves * RT * DT * 64);   // [wave][R]
   float* SL = SM + kWaves * R;                                          // [wave][R]
@@ -419,8 +422,13 @@ __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDes
         lw[w] = f2bf(v0 - bf2f(h0)) | ((uint32_t)f2bf(v1 - bf2f(h1)) << 16);
       }
       const Op2 a{make_uint4(hw[0], hw[1], hw[2], hw[3]), make_uint4(lw[0], lw[1], lw[2], lw[3])};
+      if (whole) {
 #pragma unroll
-      for (int t = 0; t < DT; ++t) sa[t * 64] = mma3<BF>(a, attn_v_operand<BF, D>(raw, t, 0, kc, last), f4{0.f, 0.f, 0.f, 0.f});
+        for (int t = 0; t < DT; ++t) sa[t * 64] = mma3<BF>(a, raw.v[t][0], f4{0.f, 0.f, 0.f, 0.f});
+      } else {
+#pragma unroll
+        for (int t = 0; t < DT; ++t) sa[t * 64] = mma3<BF>(a, attn_v_operand<BF, D>(raw, t, 0, kc, last), f4{0.f, 0.f, 0.f, 0.f});
+      }
     } else {
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
@@ -429,7 +437,7 @@ __device__ __forceinline__ void attn_span_chunks(const AttnArgs& p, const ReqDes
         for (int kt = 0; kt < 2; ++kt) {
           const uint4 a = make_uint4(__float_as_uint(pj[kt][0]), __float_as_uint(pj[kt][1]), __float_as_uint(pj[kt][2]),
                                      __float_as_uint(pj[kt][3]));
-          acc = mma_step<false>(a, attn_v_operand<BF, D>(raw, t, kt, kc, last).h, acc);
+          acc = mma_step<false>(a, whole ? raw.v[t][kt].h : attn_v_operand<BF, D>(raw, t, kt, kc, last).h, acc);
         }
         sa[t * 64] = acc;
       }
