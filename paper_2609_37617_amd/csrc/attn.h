@@ -197,7 +197,8 @@ __device__ __forceinline__ void attn_load_q(const AttnArgs& p, const ReqDesc& rq
 // past the request's: K reads its last key (a branch-free load, never
 // used); V is read as stored and its elements are set to zero where p v
 // takes them (attn_v_operand: their p is 0, and 0 times a stale value must
-// stay 0); a chunk that starts past the last key reads no V.
+// stay 0); a chunk that starts past the last key reads the last key's V
+// block, all of it set to zero there.
 template <bool BF, int D> struct AttnRaw {
   static constexpr int KS = D / AttnFmt<BF>::KE;   // k-steps of q . k
   static constexpr int DT = D / 16;                // dimension tiles
@@ -223,9 +224,8 @@ template <bool BF> __device__ __forceinline__ uint4 keep_first(uint4 x, int n) {
 }
 
 // Wave w's chunk of span sp of KV head g.  Reads stay inside the slot's
-// rows: K rows up to the last key, V rows only for a chunk that starts at or
-// before it (the row stride is a multiple of 64, so such a chunk ends inside
-// the row).
+// rows: K rows up to the last key, V blocks up to the last key's (the row
+// stride is a multiple of 64, so a block ends inside the row).
 // The keys (attn_fetch_k) and the values (attn_fetch_v) of the chunk.
 template <bool BF, int D>
 __device__ __forceinline__ void attn_fetch_k(const AttnArgs& p, const ReqDesc& rq, int g, int sp, AttnRaw<BF, D>& r) {
@@ -259,15 +259,10 @@ __device__ __forceinline__ void attn_fetch_v(const AttnArgs& p, const ReqDesc& r
   const int last = rq.L0 + rq.W - 1;                       // last key of the request in this pass
   const size_t head = (size_t)rq.slot * p.slot_stride + (size_t)g * p.kv_cap * D;   // float32 units
   const T* vb = reinterpret_cast<const T*>(p.v_cache + head);
-  if (kc > last) {   // no key of the chunk is in the request
-#pragma unroll
-    for (int t = 0; t < Raw::DT; ++t)
-#pragma unroll
-      for (int j = 0; j < Raw::KSV; ++j) r.v[t][j] = Op2{make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
-    return;
-  }
-  // the chunk's V block (v_elem): [parts][D][32]
-  const T* vc = vb + (size_t)(kc >> 5) * F::PARTS * D * 32;
+  // the chunk's V block (v_elem): [parts][D][32]; a chunk past the last key
+  // reads the last key's block instead (a branch-free load whose elements
+  // attn_v_operand all sets to zero)
+  const T* vc = vb + (size_t)(min(kc, last) >> 5) * F::PARTS * D * 32;
 #pragma unroll
   for (int t = 0; t < Raw::DT; ++t) {
     const T* vr = vc + (16 * t + lr) * 32;
@@ -293,7 +288,7 @@ __device__ __forceinline__ void attn_fetch(const AttnArgs& p, const ReqDesc& rq,
 
 // The V operand of dimension tile t and k-step j as p v takes it: elements
 // of keys past the request's last key set to zero (a chunk past the last
-// key was not read).  Done here rather than at the load, so that no wait
+// key holds the last key's block: all of it).  Done here rather than at the load, so that no wait
 // for the data sits between the requests of the next chunk.
 template <bool BF, int D>
 __device__ __forceinline__ Op2 attn_v_operand(const AttnRaw<BF, D>& r, int t, int j, int kc, int last) {
